@@ -1,0 +1,253 @@
+"""Refresh-step benchmark on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--cfg 4] [--no-cpu]
+
+One step is the whole refresh step of one layer: the scoring pass
+(conduit_score), reweighting and global top-k (conduit_select_topk), the cache
+merge (conduit_scatter_kv) and the refresh attention of the selected rows
+(conduit_refresh_attn), all through the C ABI.  Inputs are synthetic (seeded
+generator), already resident in HBM.  Before each timed step a 512 MB scrub
+buffer is written so the caches start cold; after it, the merged cache is
+restored from a pristine copy.  Both happen outside the per-step HIP events.
+
+Prints one JSON line.  `value` is visual tokens scored and refreshed per
+second for the layer (N_vis / step time).  `roofline` covers the refresh
+attention (the dominant call): algorithmic FLOPs 4 * H_q * d * sum_i (p_i + 1)
+over its event-timed duration, against the bf16 dense MFMA peak.
+`cpu_baseline` times the float64 CPU oracle on a bounded sample of the same
+step on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "visual tokens scored+refreshed/s per layer; refresh-step ms @16k tokens, 10%"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cfg", type=int, default=4, help="workload id (4 = 16k tokens, 10%%)")
+    ap.add_argument("--budget", default="10%")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-scrub", action="store_true")
+    ap.add_argument("--cpu-row-stride", type=int, default=8,
+                    help="CPU baseline refreshes every n-th selected row and scales by n")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_05821_amd import api, workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.config(args.cfg, n_layers=1)
+    k = w.budgets[args.budget]
+    t_gen = time.time()
+    L = w.layer(0)
+    t_gen = time.time() - t_gen
+
+    def up(x):
+        if x.dtype == np.uint16:
+            return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(x).to(dev)
+
+    kc, vc, q = up(L["k"]), up(L["v"]), up(L["q"])
+    k_pristine, v_pristine = kc.clone(), vc.clone()
+    img = api.ImageTable(w.img_pos, w.img_off)
+    step = api.RefreshStep([{"k": kc, "v": vc, "q": q}], w.n_q_heads, w.q_pos0, img, k, lam=1.0,
+                           device=dev)
+    kv = step.kvs[0]
+
+    # Selection once (untimed) to gather the fresh rows the recompute would produce.
+    step.score_and_select()
+    torch.cuda.synchronize()
+    idx0 = step.idx[:k].clone()
+    idx_np = idx0.cpu().numpy()
+    fresh = {"k_new": up(np.ascontiguousarray(L["k_star"][idx_np])),
+             "v_new": up(np.ascontiguousarray(L["v_star"][idx_np])),
+             "q_sel": up(np.ascontiguousarray(L["q_star"][idx_np]))}
+    pos_np = step.pos[:k].cpu().numpy().astype(np.int64)
+    q_sel_np = np.ascontiguousarray(L["q_star"][idx_np])
+    del L["q_star"]
+
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    pos = step.pos[:k]
+    out, lse = step.out[0][:k], step.lse[0][:k]
+
+    def one_step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score)
+        if ev:
+            ev[1].record(stream)
+        api.conduit_select_topk(step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos,
+                                mask_out=step.mask, shat_out=step.shat, c_out=step.c)
+        if ev:
+            ev[2].record(stream)
+        api.conduit_scatter_kv(kv, pos, fresh["k_new"], fresh["v_new"])
+        if ev:
+            ev[3].record(stream)
+        api.conduit_refresh_attn(kv, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh)
+        if ev:
+            ev[4].record(stream)
+
+    def restore():
+        kc.copy_(k_pristine)
+        vc.copy_(v_pristine)
+
+    for _ in range(args.warmup):
+        one_step()
+        restore()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        if not args.no_scrub:
+            scrub.fill_(i & 0xFF)
+        one_step(events[i])
+        restore()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+
+    per = {"score": [], "select": [], "scatter": [], "refresh": [], "step": []}
+    for ev in events:
+        per["score"].append(ev[0].elapsed_time(ev[1]))
+        per["select"].append(ev[1].elapsed_time(ev[2]))
+        per["scatter"].append(ev[2].elapsed_time(ev[3]))
+        per["refresh"].append(ev[3].elapsed_time(ev[4]))
+        per["step"].append(ev[0].elapsed_time(ev[4]))
+    ms_step = statistics.mean(per["step"])
+    ms = {key: statistics.mean(v) for key, v in per.items()}
+    med = {key: statistics.median(v) for key, v in per.items()}
+
+    # Selection must be the same every step (deterministic).
+    assert torch.equal(step.idx[:k], idx0), "selection changed between steps"
+
+    # Algorithmic work.
+    H, d, hkv = w.n_q_heads, w.head_dim, w.n_kv_heads
+    refresh_flops = 4.0 * H * d * float(np.sum(pos_np + 1))
+    refresh_exps = H * float(np.sum(pos_np + 1))
+    e = 2  # bf16 bytes
+    score_bytes = (w.n_q * H * d * e + w.n_ctx * hkv * d * e + w.n_vis * hkv * d * e
+                   + w.n_vis * 4 * 4)
+    score_flops = 2.0 * d * H * sum(w.q_pos0 + i + 1 for i in range(w.n_q)) + \
+        2.0 * d * H * w.n_q * w.n_vis
+    scatter_bytes = 2 * 2 * k * hkv * d * e
+    refresh_tflops = refresh_flops / (ms["refresh"] * 1e-3) / 1e12
+
+    result = {
+        "metric": METRIC,
+        "value": w.n_vis / (ms_step * 1e-3),
+        "unit": "visual tokens/s per layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded generator; no dataset or weights)",
+        "config": {
+            "workload": w.name + f", budget {args.budget} (k={k}), one layer",
+            "cfg": args.cfg, "n_vis": w.n_vis, "n_ctx": w.n_ctx, "n_images": w.n_images,
+            "n_q": w.n_q, "n_q_heads": H, "n_kv_heads": hkv, "head_dim": d, "k": k,
+            "lambda": 1.0, "norm": "causal_row", "cold_cache_scrub": not args.no_scrub,
+        },
+        "roofline": {
+            "kernel": "refresh attention (conduit_refresh_attn: MFMA attention + split merge)",
+            "bound": "mfma",
+            "achieved": refresh_tflops,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": refresh_tflops / PEAK_BF16_TFLOPS,
+            "traffic": None,
+            "algorithmic_flops": refresh_flops,
+            "avg_ms": ms["refresh"],
+        },
+        "per_call_ms_mean": ms,
+        "per_call_ms_median": med,
+        "score": {
+            "algorithmic_bytes": score_bytes, "algorithmic_flops": score_flops,
+            "gbs": score_bytes / (ms["score"] * 1e-3) / 1e9,
+            "hbm_frac": score_bytes / (ms["score"] * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "mfma_frac": score_flops / (ms["score"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        },
+        "scatter_gbs": scatter_bytes / (ms["scatter"] * 1e-3) / 1e9,
+        "refresh_exps_per_s": refresh_exps / (ms["refresh"] * 1e-3),
+        "wall_ms_per_step_incl_scrub_restore": t_wall / args.steps * 1e3,
+        "gen_s": t_gen,
+    }
+
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(w, L, q_sel_np, idx_np, pos_np, k,
+                                              args.cpu_row_stride)
+    print(json.dumps(result))
+
+
+def cpu_baseline(w, L, q_sel, idx, pos, k, stride):
+    """The float64 oracle on this host: full scoring, reweighting, top-k and
+    merge of the layer, and the refresh attention of every `stride`-th selected
+    row, scaled by `stride` (rows are spread evenly over the positions)."""
+    import threadpoolctl
+
+    from oracle import conduit_oracle as O
+
+    info = threadpoolctl.threadpool_info()
+    blas_threads = max([i.get("num_threads", 1) for i in info] or [1])
+    cores = len(os.sched_getaffinity(0))
+    layer = {"q": L["q"], "k": L["k"], "v": L["v"]}
+    t0 = time.perf_counter()
+    O.select([layer], w.q_pos0, w.img_pos, w.img_off, k, lam=1.0)
+    t1 = time.perf_counter()
+    rows = list(range(0, k, stride))
+    t2 = time.perf_counter()
+    O.refresh_layer(L["k"], L["v"], pos, L["k_star"][idx], L["v_star"][idx], q_sel, rows=rows)
+    t3 = time.perf_counter()
+    t_step = (t1 - t0) + (t3 - t2) * (k / len(rows))
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": w.n_vis / t_step, "unit": "visual tokens/s per layer", "cores": blas_threads,
+            "kind": "oracle",
+            "sample": f"one layer of the same workload: full scoring pass, reweighting, top-k and "
+                      f"merge ({t1 - t0:.2f} s), refresh attention of {len(rows)} of {k} selected "
+                      f"rows (every {stride}th, {t3 - t2:.2f} s) scaled x{k / len(rows):.2f}; "
+                      f"float64 numpy",
+            "seconds_per_step": t_step, "host_cpus": cores, "blas_threads": blas_threads,
+            "cpu_model": cpu_model}
+
+
+if __name__ == "__main__":
+    main()

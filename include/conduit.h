@@ -1,0 +1,211 @@
+/*
+ * conduit.h - C ABI of the Conduit refresh step for reused visual KV caches
+ * (gfx950 / MI355X).
+ *
+ * The paper's refresh step, per request:
+ *   1. budget          k = floor(r * N_vis) over visual tokens only
+ *                      (Sec. 3.1 Eq. 2; Algorithm 1 first step and k = 0 exit);
+ *   2. scoring pass    per scored layer: softmax attention of the span queries
+ *                      over the cached keys, head- and query-mean over the
+ *                      visual columns (Sec. 3.3 Eq. 6), times the cached value
+ *                      norm (Eq. 7), accumulated over layers  -> conduit_score;
+ *   3. reweighting     image means g_j, coefficients c_j (Sec. 3.4 Eq. 8-9),
+ *                      composite score (Sec. 3.5 Eq. 10) and one global top-k
+ *                      (Eq. 11)                              -> conduit_select_topk;
+ *   4. recompute       per layer: the selected rows' fresh K/V are written
+ *                      into the cache, all other visual rows are reused
+ *                      (Sec. 3; Sec. 4.1 cache-reuse protocol)
+ *                                                            -> conduit_scatter_kv;
+ *                      then each selected row attends causally over the
+ *                      merged fresh/stale prefix             -> conduit_refresh_attn.
+ *
+ * Conventions shared by every entry point:
+ *   - Tensors are caller-owned DEVICE memory unless marked HOST.  The library
+ *     allocates nothing: scratch comes in through (ws, ws_bytes), sized by the
+ *     matching *_workspace_bytes query.  No state is kept apart from a
+ *     thread-local error string, so calls on different streams may run
+ *     concurrently as long as they do not share output or workspace memory.
+ *   - Every call only enqueues work on `stream` (a hipStream_t; NULL is the
+ *     default stream) and never synchronises.  Device faults surface at the
+ *     caller's next synchronisation.
+ *   - Every argument is checked on the host before anything is enqueued.  A
+ *     non-OK status means nothing was enqueued and no output was touched;
+ *     conduit_last_error() then describes the problem.  With no usable GPU a
+ *     valid call returns CONDUIT_ERR_HIP.
+ *   - Caches are token-major: element (token t, KV head h, dim e) sits at
+ *     base[t * stride + h * head_dim + e].  Queries and outputs are dense
+ *     [rows][n_q_heads][head_dim].  bf16 is IEEE binary32's top 16 bits.
+ *     Device pointers must be 16-byte aligned and strides a multiple of
+ *     16 bytes.
+ *   - Query head h reads KV head h / (n_q_heads / n_kv_heads).
+ *   - Supported: head_dim 64 or 128; CONDUIT_BF16 (MFMA kernels, fp32
+ *     accumulation) or CONDUIT_F32 (fp32 throughout).
+ *   - Results are bitwise reproducible run to run (no floating-point atomics).
+ */
+#ifndef CONDUIT_H
+#define CONDUIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CONDUIT_OK = 0,
+  CONDUIT_ERR_INVALID_ARG = 1,   /* bad pointer, size, range or layout          */
+  CONDUIT_ERR_UNSUPPORTED = 2,   /* valid but no kernel (head_dim, dtype, ...)  */
+  CONDUIT_ERR_WORKSPACE = 3,     /* ws_bytes below the *_workspace_bytes query  */
+  CONDUIT_ERR_HIP = 4            /* a HIP runtime call or launch failed         */
+} conduit_status;
+
+typedef enum { CONDUIT_F32 = 0, CONDUIT_BF16 = 1 } conduit_dtype;
+
+/* Domain of the scoring softmax (Eq. 6).  CAUSAL_ROW: each span token's full
+ * causal row (changed prefix, separators, every image's cached visual keys and
+ * span keys up to itself), then the visual columns are kept; this is the
+ * attention the model itself computes for the span.  VISUAL_ONLY: renormalised
+ * over the visual keys alone. */
+typedef enum { CONDUIT_NORM_CAUSAL_ROW = 0, CONDUIT_NORM_VISUAL_ONLY = 1 } conduit_norm;
+
+#define CONDUIT_MAX_IMAGES 256
+
+/* One layer's KV cache. */
+typedef struct {
+  void *k;                /* device [n_ctx][n_kv_heads][head_dim], dtype         */
+  void *v;                /* device, same layout                                 */
+  int64_t k_stride;       /* elements between consecutive tokens of k,
+                             >= n_kv_heads * head_dim                            */
+  int64_t v_stride;       /* same for v                                          */
+  int32_t n_ctx;          /* tokens in the cache (sequence positions 0..n_ctx-1) */
+  int32_t n_q_heads;      /* H_q; a multiple of n_kv_heads                       */
+  int32_t n_kv_heads;     /* H_kv                                                */
+  int32_t head_dim;       /* 64 or 128                                           */
+  int32_t dtype;          /* conduit_dtype                                       */
+} conduit_kv;
+
+/* The visual-token sets of Eq. 1: K images, each one contiguous run of
+ * sequence positions, in ascending order and not overlapping.  Visual token t
+ * (0 <= t < n_vis) is numbered image by image; image j holds tokens
+ * img_off[j] .. img_off[j+1]-1 at positions img_pos[j] .. img_pos[j]+n_j-1.
+ * HOST memory, read during the call only. */
+typedef struct {
+  int32_t n_images;       /* 1 .. CONDUIT_MAX_IMAGES                            */
+  int32_t n_vis;          /* == img_off[n_images]                               */
+  const int32_t *img_pos; /* HOST [n_images]                                    */
+  const int32_t *img_off; /* HOST [n_images + 1], img_off[0] = 0, strictly increasing */
+} conduit_images;
+
+/* Eq. 2: k = floor(r_num * n_vis / r_den), in exact integer arithmetic.
+ * Returns -1 if n_vis < 0, r_den <= 0, r_num < 0 or r_num > r_den. */
+int64_t conduit_budget(int64_t n_vis, int64_t r_num, int64_t r_den);
+
+/* ------------------------------------------------------------------------ *
+ * Scoring pass for one scored layer (Sec. 3.3 Eq. 6-7; the scoring loop of
+ * Algorithm 1; App. A.2 scoring forward pass).
+ *
+ * q        device [n_q][n_q_heads][head_dim], kv->dtype: the span queries; span
+ *          token i sits at position q_pos0 + i and sees keys 0 .. q_pos0 + i.
+ *          Requires q_pos0 + n_q <= kv->n_ctx and every image before q_pos0.
+ * scale    logit scale (1/sqrt(head_dim) for standard attention), > 0.
+ * row_lse_in   nullable device [n_q][n_q_heads] fp32: natural-log log-sum-exp of
+ *          each span row over the `norm` domain, e.g. from the model's own
+ *          attention of the span.  When given, the row-statistics pass is
+ *          skipped.
+ * row_lse_out  nullable device [n_q][n_q_heads] fp32: the row log-sum-exp.
+ * s_acc, a_acc device [n_vis] fp32, in/out.  With accumulate = 0 they are
+ *          overwritten with a_t * ||V_t|| and a_t; with accumulate = 1 these are
+ *          added to the current contents.  Calling once per scored layer in
+ *          layer order gives sum_l a_t^(l) ||V_t^(l)|| and sum_l a_t^(l).
+ * a_out, vnorm_out  nullable device [n_vis] fp32: this layer's a_t and ||V_t||
+ *          (the norm of the n_kv_heads * head_dim concatenated cached value).
+ * ws       device workspace of at least conduit_score_workspace_bytes(...).
+ * ------------------------------------------------------------------------ */
+size_t conduit_score_workspace_bytes(const conduit_kv *kv, int32_t n_q, const conduit_images *img);
+
+conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
+                             const conduit_images *img, conduit_norm norm, float scale,
+                             const float *row_lse_in, float *row_lse_out,
+                             float *s_acc, float *a_acc, int32_t accumulate,
+                             float *a_out, float *vnorm_out,
+                             void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Image reweighting and global top-k (Sec. 3.4 Eq. 8-9, Sec. 3.5 Eq. 10-11,
+ * the tail of Algorithm 1).
+ *
+ * s_acc, a_acc  device [n_vis] fp32: the layer sums produced by conduit_score.
+ * n_layers      |L| >= 1, the number of layers accumulated.
+ * lambda        reweighting strength in [0, 1] (1 in the paper's main setting).
+ *               c_j = (1 - lambda) + lambda * g_j / g_bar, exactly 1 when
+ *               g_j = g_bar (so always with one image) or when g_bar = 0.
+ * k             budget, 0 <= k <= n_vis.  Ties in the composite score go to
+ *               the lower visual index.  k = 0 only clears mask_out.
+ * idx_out       device [k] int32: selected visual indices, ascending.
+ * pos_out       device [k] int32: their sequence positions, ascending.
+ * mask_out      nullable device [n_vis] uint8: the refresh mask M.
+ * shat_out      nullable device [n_vis] fp32: composite scores
+ *               s_hat_t = (s_acc_t / n_layers) * c_pi(t).
+ * c_out         nullable device [n_images] fp32: the coefficients c_j.
+ * ------------------------------------------------------------------------ */
+size_t conduit_select_workspace_bytes(int32_t n_vis, int32_t n_images);
+
+conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32_t n_layers,
+                                   const conduit_images *img, float lambda, int32_t k,
+                                   int32_t *idx_out, int32_t *pos_out, uint8_t *mask_out,
+                                   float *shat_out, float *c_out,
+                                   void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Cache merge for one layer (Sec. 3: selected rows are recomputed, all other
+ * cached visual entries are reused).  For each i < k, row pos[i] of kv->k and
+ * kv->v is replaced by row i of k_new / v_new, in place.
+ *
+ * pos           device [k] int32, strictly ascending, each < kv->n_ctx
+ *               (device-side precondition, not checked on the device).
+ * k_new, v_new  device [k][n_kv_heads][head_dim] dense, kv->dtype.
+ * k_old_out, v_old_out  nullable device [k][n_kv_heads][head_dim]: receive the
+ *               replaced (stale) rows, so the merge can be undone.
+ * k = 0 enqueues nothing and leaves the cache untouched.
+ * ------------------------------------------------------------------------ */
+conduit_status conduit_scatter_kv(const conduit_kv *kv, const int32_t *pos, int32_t k,
+                                  const void *k_new, const void *v_new,
+                                  void *k_old_out, void *v_old_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Refresh attention for one layer: causal attention of the selected rows over
+ * the merged cache (the selective recompute of Sec. 3 and Sec. 4.1).  Row i
+ * sits at position pos[i] and attends to keys 0 .. pos[i] of kv (already
+ * merged by conduit_scatter_kv on the same stream), itself included.
+ *
+ * q_sel   device [k][n_q_heads][head_dim], kv->dtype: fresh queries, row i for
+ *         pos[i].
+ * pos     device [k] int32, ascending, each < kv->n_ctx (device-side
+ *         precondition).
+ * o_out   device [k][n_q_heads][head_dim], kv->dtype (bf16 rounded to nearest
+ *         even from fp32 accumulation).
+ * lse_out nullable device [k][n_q_heads] fp32: natural-log log-sum-exp.
+ * k = 0 enqueues nothing.
+ * ------------------------------------------------------------------------ */
+size_t conduit_refresh_workspace_bytes(const conduit_kv *kv, int32_t k);
+
+conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, const int32_t *pos,
+                                    int32_t k, float scale, void *o_out, float *lse_out,
+                                    void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Status name, e.g. "CONDUIT_ERR_INVALID_ARG". */
+const char *conduit_status_str(conduit_status status);
+
+/* Detail for the calling thread's last non-OK return ("" if none). */
+const char *conduit_last_error(void);
+
+/* Library version string. */
+const char *conduit_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONDUIT_H */

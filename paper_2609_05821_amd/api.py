@@ -1,0 +1,296 @@
+"""ctypes binding of libconduit (include/conduit.h) over torch device tensors.
+
+Argument marshalling only: every step of the refresh step runs in the HIP
+library.  torch provides device memory and the current stream; no torch
+compute is used on the path.  If the library is missing, the first call raises
+ConduitError (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libconduit.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
+F32, BF16 = 0, 1
+NORM_CAUSAL_ROW, NORM_VISUAL_ONLY = 0, 1
+MAX_IMAGES = 256
+
+EXPORTS = [
+    "conduit_budget", "conduit_score_workspace_bytes", "conduit_score",
+    "conduit_select_workspace_bytes", "conduit_select_topk", "conduit_scatter_kv",
+    "conduit_refresh_workspace_bytes", "conduit_refresh_attn", "conduit_status_str",
+    "conduit_last_error", "conduit_version",
+]
+
+
+class ConduitError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        super().__init__(f"{_status_name(status)}: {detail}")
+
+
+class KV(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("k_stride", ctypes.c_int64),
+                ("v_stride", ctypes.c_int64), ("n_ctx", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class Images(ctypes.Structure):
+    _fields_ = [("n_images", ctypes.c_int32), ("n_vis", ctypes.c_int32),
+                ("img_pos", ctypes.POINTER(ctypes.c_int32)),
+                ("img_off", ctypes.POINTER(ctypes.c_int32))]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libconduit.so (built in-tree by __graft_entry__.build())."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ConduitError(ERR_HIP, f"{LIB_PATH} is not built (run __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, f32, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                 ctypes.c_size_t)
+        pkv, pimg = ctypes.POINTER(KV), ctypes.POINTER(Images)
+        L.conduit_budget.argtypes = [i64, i64, i64]
+        L.conduit_budget.restype = i64
+        L.conduit_score_workspace_bytes.argtypes = [pkv, i32, pimg]
+        L.conduit_score_workspace_bytes.restype = sz
+        L.conduit_score.argtypes = [pkv, vp, i32, i32, pimg, ctypes.c_int, f32, vp, vp, vp, vp, i32,
+                                    vp, vp, vp, sz, vp]
+        L.conduit_score.restype = ctypes.c_int
+        L.conduit_select_workspace_bytes.argtypes = [i32, i32]
+        L.conduit_select_workspace_bytes.restype = sz
+        L.conduit_select_topk.argtypes = [vp, vp, i32, pimg, f32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.conduit_select_topk.restype = ctypes.c_int
+        L.conduit_scatter_kv.argtypes = [pkv, vp, i32, vp, vp, vp, vp, vp]
+        L.conduit_scatter_kv.restype = ctypes.c_int
+        L.conduit_refresh_workspace_bytes.argtypes = [pkv, i32]
+        L.conduit_refresh_workspace_bytes.restype = sz
+        L.conduit_refresh_attn.argtypes = [pkv, vp, vp, i32, f32, vp, vp, vp, sz, vp]
+        L.conduit_refresh_attn.restype = ctypes.c_int
+        L.conduit_status_str.argtypes = [ctypes.c_int]
+        L.conduit_status_str.restype = ctypes.c_char_p
+        L.conduit_last_error.argtypes = []
+        L.conduit_last_error.restype = ctypes.c_char_p
+        L.conduit_version.argtypes = []
+        L.conduit_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _status_name(status: int) -> str:
+    try:
+        return lib().conduit_status_str(status).decode()
+    except Exception:  # noqa: BLE001 - naming must never mask the real error
+        return f"status {status}"
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        raise ConduitError(status, lib().conduit_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise ConduitError(ERR_UNSUPPORTED, f"cache dtype {t.dtype} (bfloat16 or float32)")
+
+
+def kv_desc(k: torch.Tensor, v: torch.Tensor, n_q_heads: int) -> KV:
+    """Descriptor of one layer's cache: k, v are [n_ctx, H_kv, d] device tensors
+    whose last two dims are dense (any token stride)."""
+    for t in (k, v):
+        if t.dim() != 3 or t.stride(2) != 1 or t.stride(1) != t.shape[2]:
+            raise ConduitError(ERR_INVALID_ARG, "cache tensors must be [n_ctx, H_kv, d], rows dense")
+    if k.shape != v.shape or k.dtype != v.dtype:
+        raise ConduitError(ERR_INVALID_ARG, "k and v must match in shape and dtype")
+    n_ctx, hkv, d = k.shape
+    return KV(k.data_ptr(), v.data_ptr(), k.stride(0), v.stride(0), n_ctx, n_q_heads, hkv, d,
+              _dtype_code(k))
+
+
+class ImageTable:
+    """Host image table (Eq. 1) kept alive for the duration of calls."""
+
+    def __init__(self, img_pos: Sequence[int], img_off: Sequence[int]):
+        self.pos = np.ascontiguousarray(img_pos, dtype=np.int32)
+        self.off = np.ascontiguousarray(img_off, dtype=np.int32)
+        self.desc = Images(len(self.pos), int(self.off[-1]) if len(self.off) else 0,
+                           self.pos.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                           self.off.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
+
+    @property
+    def n_vis(self) -> int:
+        return int(self.desc.n_vis)
+
+    @property
+    def n_images(self) -> int:
+        return int(self.desc.n_images)
+
+
+def _workspace(nbytes: int, device, ws: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return ws
+    if ws is not None and ws.numel() * ws.element_size() >= nbytes:
+        return ws
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def _nbytes(t: Optional[torch.Tensor]) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+# ---------------------------------------------------------------------------
+# The four entry points
+# ---------------------------------------------------------------------------
+
+def conduit_budget(n_vis: int, r_num: int, r_den: int) -> int:
+    return int(lib().conduit_budget(n_vis, r_num, r_den))
+
+
+def score_workspace_bytes(kv: KV, n_q: int, img: ImageTable) -> int:
+    return int(lib().conduit_score_workspace_bytes(ctypes.byref(kv), n_q, ctypes.byref(img.desc)))
+
+
+def conduit_score(kv: KV, q: torch.Tensor, q_pos0: int, img: ImageTable, s_acc: torch.Tensor,
+                  a_acc: torch.Tensor, accumulate: bool = False, norm: int = NORM_CAUSAL_ROW,
+                  scale: Optional[float] = None, row_lse_in: Optional[torch.Tensor] = None,
+                  row_lse_out: Optional[torch.Tensor] = None, a_out: Optional[torch.Tensor] = None,
+                  vnorm_out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                  stream=None) -> None:
+    """Scoring pass of one layer (Eq. 6-7); see conduit_score in conduit.h."""
+    n_q = q.shape[0]
+    if scale is None:
+        scale = 1.0 / math.sqrt(kv.head_dim)
+    ws = _workspace(score_workspace_bytes(kv, n_q, img), q.device, ws)
+    _check(lib().conduit_score(ctypes.byref(kv), q.data_ptr(), n_q, q_pos0, ctypes.byref(img.desc),
+                               norm, scale, _ptr(row_lse_in), _ptr(row_lse_out), s_acc.data_ptr(),
+                               a_acc.data_ptr(), int(accumulate), _ptr(a_out), _ptr(vnorm_out),
+                               _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def conduit_select_topk(s_acc: torch.Tensor, a_acc: torch.Tensor, n_layers: int, img: ImageTable,
+                        lam: float, k: int, idx_out: torch.Tensor, pos_out: torch.Tensor,
+                        mask_out: Optional[torch.Tensor] = None,
+                        shat_out: Optional[torch.Tensor] = None,
+                        c_out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                        stream=None) -> None:
+    """Reweighting and global top-k (Eq. 8-11); see conduit_select_topk."""
+    need = 0 if shat_out is not None else int(
+        lib().conduit_select_workspace_bytes(img.n_vis, img.n_images))
+    ws = _workspace(need, s_acc.device, ws)
+    _check(lib().conduit_select_topk(s_acc.data_ptr(), a_acc.data_ptr(), n_layers,
+                                     ctypes.byref(img.desc), lam, k, _ptr(idx_out), _ptr(pos_out),
+                                     _ptr(mask_out), _ptr(shat_out), _ptr(c_out), _ptr(ws),
+                                     _nbytes(ws), _stream(stream)))
+
+
+def conduit_scatter_kv(kv: KV, pos: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                       k_old_out: Optional[torch.Tensor] = None,
+                       v_old_out: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Cache merge of one layer; see conduit_scatter_kv."""
+    _check(lib().conduit_scatter_kv(ctypes.byref(kv), pos.data_ptr(), pos.numel(),
+                                    _ptr(k_new), _ptr(v_new), _ptr(k_old_out), _ptr(v_old_out),
+                                    _stream(stream)))
+
+
+def refresh_workspace_bytes(kv: KV, k: int) -> int:
+    return int(lib().conduit_refresh_workspace_bytes(ctypes.byref(kv), k))
+
+
+def conduit_refresh_attn(kv: KV, q_sel: torch.Tensor, pos: torch.Tensor, o_out: torch.Tensor,
+                         lse_out: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                         ws: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Refresh attention of the selected rows over the merged cache."""
+    k = pos.numel()
+    if scale is None:
+        scale = 1.0 / math.sqrt(kv.head_dim)
+    ws = _workspace(refresh_workspace_bytes(kv, k), q_sel.device, ws)
+    _check(lib().conduit_refresh_attn(ctypes.byref(kv), q_sel.data_ptr(), pos.data_ptr(), k,
+                                      scale, o_out.data_ptr(), _ptr(lse_out), _ptr(ws), _nbytes(ws),
+                                      _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# A whole refresh step over preallocated buffers
+# ---------------------------------------------------------------------------
+
+class RefreshStep:
+    """Buffers and calls for one refresh step: score every layer, select once,
+    then merge and refresh every layer (the order of Algorithm 1 followed by
+    the selective recompute).
+
+    layers: list of dicts of device tensors {"k", "v", "q"} per scored layer
+    (k, v [n_ctx, H_kv, d]; q [n_q, H_q, d]).  Fresh rows for the selection
+    are passed to `refresh` as {"k_new", "v_new", "q_sel"} per layer.
+    """
+
+    def __init__(self, layers, n_q_heads: int, q_pos0: int, img: ImageTable, k: int,
+                 lam: float = 1.0, norm: int = NORM_CAUSAL_ROW, device="cuda"):
+        self.layers = layers
+        self.kvs = [kv_desc(L["k"], L["v"], n_q_heads) for L in layers]
+        self.q_pos0, self.img, self.k, self.lam, self.norm = q_pos0, img, k, lam, norm
+        self.n_q = layers[0]["q"].shape[0]
+        nv = img.n_vis
+        f32 = dict(dtype=torch.float32, device=device)
+        self.s_acc = torch.zeros(nv, **f32)
+        self.a_acc = torch.zeros(nv, **f32)
+        self.shat = torch.zeros(nv, **f32)
+        self.c = torch.zeros(img.n_images, **f32)
+        self.idx = torch.zeros(max(k, 1), dtype=torch.int32, device=device)
+        self.pos = torch.zeros(max(k, 1), dtype=torch.int32, device=device)
+        self.mask = torch.zeros(nv, dtype=torch.uint8, device=device)
+        ws_bytes = max(score_workspace_bytes(kv, self.n_q, img) for kv in self.kvs)
+        self.ws_score = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=device)
+        rb = max(refresh_workspace_bytes(kv, k) for kv in self.kvs) if k > 0 else 0
+        self.ws_refresh = torch.empty(max(rb, 1), dtype=torch.uint8, device=device)
+        L0 = layers[0]
+        self.out = [torch.empty((max(k, 1), n_q_heads, L0["k"].shape[2]), dtype=L0["k"].dtype,
+                                device=device) for _ in layers]
+        self.lse = [torch.empty((max(k, 1), n_q_heads), **f32) for _ in layers]
+
+    def score_and_select(self, stream=None):
+        if self.k == 0:
+            conduit_select_topk(self.s_acc, self.a_acc, len(self.layers), self.img, self.lam, 0,
+                                self.idx, self.pos, mask_out=self.mask, stream=stream)
+            return
+        for li, (L, kv) in enumerate(zip(self.layers, self.kvs)):
+            conduit_score(kv, L["q"], self.q_pos0, self.img, self.s_acc, self.a_acc,
+                          accumulate=li > 0, norm=self.norm, ws=self.ws_score, stream=stream)
+        conduit_select_topk(self.s_acc, self.a_acc, len(self.layers), self.img, self.lam, self.k,
+                            self.idx, self.pos, mask_out=self.mask, shat_out=self.shat,
+                            c_out=self.c, stream=stream)
+
+    def refresh(self, fresh, stream=None, k_old=None, v_old=None):
+        if self.k == 0:
+            return
+        pos = self.pos[: self.k]
+        for li, (kv, F) in enumerate(zip(self.kvs, fresh)):
+            conduit_scatter_kv(kv, pos, F["k_new"], F["v_new"],
+                               None if k_old is None else k_old[li],
+                               None if v_old is None else v_old[li], stream=stream)
+            conduit_refresh_attn(kv, F["q_sel"], pos, self.out[li][: self.k],
+                                 lse_out=self.lse[li][: self.k], ws=self.ws_refresh, stream=stream)

@@ -1,0 +1,461 @@
+// Host side of the C ABI declared in include/conduit.h: argument checks,
+// workspace layout, and the launch sequence of each entry point.  Every check
+// runs before the first HIP call, so a rejected call enqueues nothing.
+#include "conduit.h"
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "common.h"
+
+using namespace conduit;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+conduit_status fail(conduit_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+conduit_status hip_fail(hipError_t e, const char *what) {
+  return fail(CONDUIT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+conduit_status ok() {
+  g_last_error.clear();
+  return CONDUIT_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int esize(int32_t dtype) { return dtype == CONDUIT_BF16 ? 2 : 4; }
+
+conduit_status check_kv(const conduit_kv *kv) {
+  if (!kv) return fail(CONDUIT_ERR_INVALID_ARG, "kv is NULL");
+  if (kv->dtype != CONDUIT_F32 && kv->dtype != CONDUIT_BF16)
+    return fail(CONDUIT_ERR_INVALID_ARG, "kv->dtype %d is not a conduit_dtype", kv->dtype);
+  if (!kv->k || !kv->v) return fail(CONDUIT_ERR_INVALID_ARG, "kv->k or kv->v is NULL");
+  if (!aligned16(kv->k) || !aligned16(kv->v))
+    return fail(CONDUIT_ERR_INVALID_ARG, "kv->k and kv->v must be 16-byte aligned");
+  if (kv->n_ctx < 1) return fail(CONDUIT_ERR_INVALID_ARG, "kv->n_ctx = %d < 1", kv->n_ctx);
+  if (kv->n_kv_heads < 1 || kv->n_q_heads < 1)
+    return fail(CONDUIT_ERR_INVALID_ARG, "head counts must be >= 1");
+  if (kv->n_q_heads % kv->n_kv_heads != 0)
+    return fail(CONDUIT_ERR_INVALID_ARG, "n_q_heads %d is not a multiple of n_kv_heads %d",
+                kv->n_q_heads, kv->n_kv_heads);
+  if (kv->head_dim != 64 && kv->head_dim != 128)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", kv->head_dim);
+  const int64_t row = (int64_t)kv->n_kv_heads * kv->head_dim;
+  if (kv->k_stride < row || kv->v_stride < row)
+    return fail(CONDUIT_ERR_INVALID_ARG, "token strides (%lld, %lld) below a row of %lld elements",
+                (long long)kv->k_stride, (long long)kv->v_stride, (long long)row);
+  if ((kv->k_stride * esize(kv->dtype)) % 16 || (kv->v_stride * esize(kv->dtype)) % 16)
+    return fail(CONDUIT_ERR_INVALID_ARG, "token strides must be multiples of 16 bytes");
+  return CONDUIT_OK;
+}
+
+// The image table; `limit` is the first position that may not hold visual tokens.
+conduit_status check_images(const conduit_images *img, int64_t limit, ImageTable *tbl) {
+  if (!img) return fail(CONDUIT_ERR_INVALID_ARG, "img is NULL");
+  if (img->n_images < 1) return fail(CONDUIT_ERR_INVALID_ARG, "n_images = %d < 1", img->n_images);
+  if (img->n_images > CONDUIT_MAX_IMAGES)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "n_images = %d > %d", img->n_images, CONDUIT_MAX_IMAGES);
+  if (!img->img_pos || !img->img_off) return fail(CONDUIT_ERR_INVALID_ARG, "image arrays are NULL");
+  const int K = img->n_images;
+  if (img->img_off[0] != 0) return fail(CONDUIT_ERR_INVALID_ARG, "img_off[0] must be 0");
+  int64_t prev_end = 0;
+  for (int j = 0; j < K; ++j) {
+    const int64_t n_j = (int64_t)img->img_off[j + 1] - img->img_off[j];
+    if (n_j < 1) return fail(CONDUIT_ERR_INVALID_ARG, "image %d is empty or img_off decreases", j);
+    if (img->img_pos[j] < prev_end)
+      return fail(CONDUIT_ERR_INVALID_ARG, "image %d at position %d overlaps or is out of order", j,
+                  img->img_pos[j]);
+    prev_end = (int64_t)img->img_pos[j] + n_j;
+    if (prev_end > limit)
+      return fail(CONDUIT_ERR_INVALID_ARG, "image %d ends at %lld, beyond %lld", j, (long long)prev_end,
+                  (long long)limit);
+  }
+  if (img->n_vis != img->img_off[K])
+    return fail(CONDUIT_ERR_INVALID_ARG, "n_vis %d != img_off[n_images] %d", img->n_vis, img->img_off[K]);
+  if (tbl) {
+    memset(tbl, 0, sizeof(*tbl));
+    tbl->n_images = K;
+    tbl->n_vis = img->n_vis;
+    for (int j = 0; j < K; ++j) tbl->pos[j] = img->img_pos[j];
+    for (int j = 0; j <= K; ++j) tbl->off[j] = img->img_off[j];
+  }
+  return CONDUIT_OK;
+}
+
+// Key-split size for the attention kernel: enough workgroups to fill the
+// chip, each split a whole number of 64-key tiles.
+int32_t attn_chunk(int64_t n_rows, int32_t group, int32_t n_kv_heads, int64_t key_span,
+                   int64_t target_blocks, int64_t min_chunk) {
+  const int64_t pair_blocks = (n_rows * group + kAttnPairsPerBlock - 1) / kAttnPairsPerBlock;
+  const int64_t base = pair_blocks * n_kv_heads;
+  int64_t splits = (target_blocks + base - 1) / base;
+  if (splits < 1) splits = 1;
+  int64_t chunk = (key_span + splits - 1) / splits;
+  chunk = align_up(chunk < min_chunk ? min_chunk : chunk, kAttnKeyTile);
+  return (int32_t)chunk;
+}
+
+struct ScoreLayout {
+  size_t vis_pos, key_ok, row_b, part_m, part_l, colsum, vsq, total;
+  int32_t chunk, n_split;
+};
+
+ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis, int32_t key_span) {
+  ScoreLayout L{};
+  const int64_t rows = (int64_t)n_q * kv->n_q_heads;
+  const bool bf16 = kv->dtype == CONDUIT_BF16;
+  L.chunk = attn_chunk(n_q, kv->n_q_heads / kv->n_kv_heads, kv->n_kv_heads, key_span, 512, 64);
+  L.n_split = (key_span + L.chunk - 1) / L.chunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
+  L.vis_pos = take((size_t)n_vis * 4);
+  L.key_ok = take((size_t)kv->n_ctx);
+  L.row_b = take((size_t)rows * 4);
+  L.part_m = take(bf16 ? (size_t)L.n_split * rows * 4 : 0);
+  L.part_l = take(bf16 ? (size_t)L.n_split * rows * 4 : 0);
+  L.colsum = take((size_t)kv->n_kv_heads * n_vis * 4);
+  L.vsq = take((size_t)kv->n_kv_heads * n_vis * 4);
+  L.total = off;
+  return L;
+}
+
+struct RefreshLayout {
+  size_t part_m, part_l, part_o, total;
+  int32_t chunk, n_split;
+};
+
+RefreshLayout refresh_layout(const conduit_kv *kv, int32_t k) {
+  RefreshLayout L{};
+  if (kv->dtype != CONDUIT_BF16 || k <= 0) return L;
+  const int64_t rows = (int64_t)k * kv->n_q_heads;
+  L.chunk = attn_chunk(k, kv->n_q_heads / kv->n_kv_heads, kv->n_kv_heads, kv->n_ctx, 1024, 256);
+  L.n_split = (kv->n_ctx + L.chunk - 1) / L.chunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
+  L.part_m = take((size_t)L.n_split * rows * 4);
+  L.part_l = take((size_t)L.n_split * rows * 4);
+  L.part_o = take((size_t)L.n_split * rows * kv->head_dim * 4);
+  L.total = off;
+  return L;
+}
+
+conduit_status check_ws(const void *ws, size_t ws_bytes, size_t need) {
+  if (ws_bytes < need)
+    return fail(CONDUIT_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+  if (need > 0 && (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)))
+    return fail(CONDUIT_ERR_INVALID_ARG, "workspace must be non-NULL and 256-byte aligned");
+  return CONDUIT_OK;
+}
+
+char *at(void *ws, size_t off) { return static_cast<char *>(ws) + off; }
+
+}  // namespace
+
+extern "C" {
+
+int64_t conduit_budget(int64_t n_vis, int64_t r_num, int64_t r_den) {
+  if (n_vis < 0 || r_den <= 0 || r_num < 0 || r_num > r_den) return -1;
+  return (int64_t)(((__int128)r_num * n_vis) / r_den);
+}
+
+size_t conduit_score_workspace_bytes(const conduit_kv *kv, int32_t n_q, const conduit_images *img) {
+  if (!kv || !img || n_q < 1 || kv->n_kv_heads < 1 || kv->n_q_heads < kv->n_kv_heads || img->n_vis < 1)
+    return 0;
+  return score_layout(kv, n_q, img->n_vis, kv->n_ctx).total;
+}
+
+conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
+                             const conduit_images *img, conduit_norm norm, float scale,
+                             const float *row_lse_in, float *row_lse_out, float *s_acc, float *a_acc,
+                             int32_t accumulate, float *a_out, float *vnorm_out, void *ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  conduit_status st = check_kv(kv);
+  if (st) return st;
+  if (!q || !aligned16(q)) return fail(CONDUIT_ERR_INVALID_ARG, "q must be non-NULL and 16-byte aligned");
+  if (n_q < 1) return fail(CONDUIT_ERR_INVALID_ARG, "n_q = %d < 1", n_q);
+  if (q_pos0 < 0 || (int64_t)q_pos0 + n_q > kv->n_ctx)
+    return fail(CONDUIT_ERR_INVALID_ARG, "span [%d, %lld) outside the cache of %d tokens", q_pos0,
+                (long long)q_pos0 + n_q, kv->n_ctx);
+  if (norm != CONDUIT_NORM_CAUSAL_ROW && norm != CONDUIT_NORM_VISUAL_ONLY)
+    return fail(CONDUIT_ERR_INVALID_ARG, "norm %d is not a conduit_norm", (int)norm);
+  if (!(scale > 0.f) || scale == __builtin_inff()) return fail(CONDUIT_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (!s_acc || !a_acc) return fail(CONDUIT_ERR_INVALID_ARG, "s_acc and a_acc are required");
+  if (accumulate != 0 && accumulate != 1) return fail(CONDUIT_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  ImageTable tbl;
+  st = check_images(img, q_pos0, &tbl);
+  if (st) return st;
+  const ScoreLayout L = score_layout(kv, n_q, img->n_vis, kv->n_ctx);
+  st = check_ws(ws, ws_bytes, L.total);
+  if (st) return st;
+
+  const bool bf16 = kv->dtype == CONDUIT_BF16;
+  const int D = kv->head_dim;
+  const float scale_log2 = scale * kLog2e;
+  int32_t *vis_pos = reinterpret_cast<int32_t *>(at(ws, L.vis_pos));
+  uint8_t *key_ok = reinterpret_cast<uint8_t *>(at(ws, L.key_ok));
+  float *row_b = reinterpret_cast<float *>(at(ws, L.row_b));
+  const bool vis_only = norm == CONDUIT_NORM_VISUAL_ONLY;
+
+  hipError_t e = launch_build_maps(tbl, kv->n_ctx, vis_pos, vis_only ? key_ok : nullptr, stream);
+  if (e != hipSuccess) return hip_fail(e, "build_maps");
+
+  if (row_lse_in) {
+    e = launch_lse_to_b(row_lse_in, row_b, n_q * kv->n_q_heads, stream);
+    if (e != hipSuccess) return hip_fail(e, "lse_to_b");
+    if (row_lse_out) {
+      e = hipMemcpyAsync(row_lse_out, row_lse_in, (size_t)n_q * kv->n_q_heads * 4, hipMemcpyDeviceToDevice,
+                         stream);
+      if (e != hipSuccess) return hip_fail(e, "copy row_lse");
+    }
+  } else {
+    AttnParams ap{};
+    ap.k = kv->k;
+    ap.v = kv->v;
+    ap.k_stride = kv->k_stride;
+    ap.v_stride = kv->v_stride;
+    ap.n_kv_heads = kv->n_kv_heads;
+    ap.group = kv->n_q_heads / kv->n_kv_heads;
+    ap.n_q_heads = kv->n_q_heads;
+    ap.n_ctx = kv->n_ctx;
+    ap.q = q;
+    ap.n_rows = n_q;
+    ap.row_pos = nullptr;
+    ap.q_pos0 = q_pos0;
+    ap.key_ok = vis_only ? key_ok : nullptr;
+    ap.scale_log2 = scale_log2;
+    ap.chunk = L.chunk;
+    ap.n_split = L.n_split;
+    ap.part_m = reinterpret_cast<float *>(at(ws, L.part_m));
+    ap.part_l = reinterpret_cast<float *>(at(ws, L.part_l));
+    ap.part_o = nullptr;
+    CombineParams cp{};
+    cp.n_rows = n_q;
+    cp.n_q_heads = kv->n_q_heads;
+    cp.row_pos = nullptr;
+    cp.q_pos0 = q_pos0;
+    cp.chunk = L.chunk;
+    cp.part_m = ap.part_m;
+    cp.part_l = ap.part_l;
+    cp.part_o = nullptr;
+    cp.row_b = row_b;
+    cp.lse_out = row_lse_out;
+    if (bf16) {
+      e = launch_attn(ap, D, true, false, stream);
+      if (e != hipSuccess) return hip_fail(e, "row statistics");
+      e = launch_combine(cp, D, stream);
+      if (e != hipSuccess) return hip_fail(e, "row statistics merge");
+    } else {
+      e = launch_attn_f32(ap, cp, D, false, stream);
+      if (e != hipSuccess) return hip_fail(e, "row statistics");
+    }
+  }
+
+  ColsumParams cs{};
+  cs.k = kv->k;
+  cs.v = kv->v;
+  cs.k_stride = kv->k_stride;
+  cs.v_stride = kv->v_stride;
+  cs.n_kv_heads = kv->n_kv_heads;
+  cs.group = kv->n_q_heads / kv->n_kv_heads;
+  cs.n_q_heads = kv->n_q_heads;
+  cs.q = q;
+  cs.n_q = n_q;
+  cs.row_b = row_b;
+  cs.vis_pos = vis_pos;
+  cs.n_vis = img->n_vis;
+  cs.scale_log2 = scale_log2;
+  cs.colsum_part = reinterpret_cast<float *>(at(ws, L.colsum));
+  cs.vsq_part = reinterpret_cast<float *>(at(ws, L.vsq));
+  e = launch_colsum(cs, D, bf16, stream);
+  if (e != hipSuccess) return hip_fail(e, "column sums");
+
+  FinalizeParams fp{};
+  fp.colsum_part = cs.colsum_part;
+  fp.vsq_part = cs.vsq_part;
+  fp.n_kv_heads = kv->n_kv_heads;
+  fp.n_vis = img->n_vis;
+  fp.n_rows_f = (float)((int64_t)n_q * kv->n_q_heads);
+  fp.accumulate = accumulate;
+  fp.s_acc = s_acc;
+  fp.a_acc = a_acc;
+  fp.a_out = a_out;
+  fp.vnorm_out = vnorm_out;
+  e = launch_finalize(fp, stream);
+  if (e != hipSuccess) return hip_fail(e, "finalize");
+  return ok();
+}
+
+size_t conduit_select_workspace_bytes(int32_t n_vis, int32_t n_images) {
+  (void)n_images;
+  if (n_vis < 1) return 0;
+  return align_up((size_t)n_vis * 4, 256);
+}
+
+conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32_t n_layers,
+                                   const conduit_images *img, float lambda, int32_t k, int32_t *idx_out,
+                                   int32_t *pos_out, uint8_t *mask_out, float *shat_out, float *c_out, void *ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+  if (!s_acc || !a_acc) return fail(CONDUIT_ERR_INVALID_ARG, "s_acc and a_acc are required");
+  if (n_layers < 1) return fail(CONDUIT_ERR_INVALID_ARG, "n_layers = %d < 1", n_layers);
+  if (!(lambda >= 0.f && lambda <= 1.f)) return fail(CONDUIT_ERR_INVALID_ARG, "lambda must lie in [0, 1]");
+  conduit_status st = check_images(img, INT32_MAX, nullptr);
+  if (st) return st;
+  ImageTable tbl;
+  check_images(img, INT32_MAX, &tbl);
+  if (k < 0 || k > img->n_vis) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_vis = %d]", k, img->n_vis);
+  if (k > 0 && (!idx_out || !pos_out)) return fail(CONDUIT_ERR_INVALID_ARG, "idx_out and pos_out are required");
+  const size_t need = shat_out ? 0 : conduit_select_workspace_bytes(img->n_vis, img->n_images);
+  if (k > 0) {
+    st = check_ws(ws, ws_bytes, need);
+    if (st) return st;
+  }
+  hipError_t e;
+  if (k == 0) {  // Algorithm 1 early exit: the all-zero mask
+    if (mask_out) {
+      e = launch_clear_u8(mask_out, img->n_vis, stream);
+      if (e != hipSuccess) return hip_fail(e, "clear mask");
+    }
+    return ok();
+  }
+  SelectParams sp{};
+  sp.s_acc = s_acc;
+  sp.a_acc = a_acc;
+  sp.n_layers = n_layers;
+  sp.lambda = lambda;
+  sp.k = k;
+  sp.idx_out = idx_out;
+  sp.pos_out = pos_out;
+  sp.mask_out = mask_out;
+  sp.shat = shat_out ? shat_out : static_cast<float *>(ws);
+  sp.c_out = c_out;
+  e = launch_select(sp, tbl, stream);
+  if (e != hipSuccess) return hip_fail(e, "select");
+  return ok();
+}
+
+conduit_status conduit_scatter_kv(const conduit_kv *kv, const int32_t *pos, int32_t k, const void *k_new,
+                                  const void *v_new, void *k_old_out, void *v_old_out, hipStream_t stream) {
+  conduit_status st = check_kv(kv);
+  if (st) return st;
+  if (k < 0 || k > kv->n_ctx) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_ctx]", k);
+  if (k == 0) return ok();
+  if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
+  if (!k_new || !v_new || !aligned16(k_new) || !aligned16(v_new))
+    return fail(CONDUIT_ERR_INVALID_ARG, "k_new and v_new must be non-NULL and 16-byte aligned");
+  if ((k_old_out && !aligned16(k_old_out)) || (v_old_out && !aligned16(v_old_out)))
+    return fail(CONDUIT_ERR_INVALID_ARG, "k_old_out and v_old_out must be 16-byte aligned");
+  ScatterParams sp{};
+  sp.k = kv->k;
+  sp.v = kv->v;
+  sp.k_stride_bytes = kv->k_stride * esize(kv->dtype);
+  sp.v_stride_bytes = kv->v_stride * esize(kv->dtype);
+  sp.row_bytes = kv->n_kv_heads * kv->head_dim * esize(kv->dtype);
+  sp.pos = pos;
+  sp.n_rows = k;
+  sp.k_new = k_new;
+  sp.v_new = v_new;
+  sp.k_old = k_old_out;
+  sp.v_old = v_old_out;
+  hipError_t e = launch_scatter(sp, stream);
+  if (e != hipSuccess) return hip_fail(e, "scatter");
+  return ok();
+}
+
+size_t conduit_refresh_workspace_bytes(const conduit_kv *kv, int32_t k) {
+  if (!kv || k < 1 || kv->n_kv_heads < 1 || kv->n_q_heads < kv->n_kv_heads || kv->n_ctx < 1) return 0;
+  if (kv->head_dim != 64 && kv->head_dim != 128) return 0;
+  return refresh_layout(kv, k).total;
+}
+
+conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, const int32_t *pos, int32_t k,
+                                    float scale, void *o_out, float *lse_out, void *ws, size_t ws_bytes,
+                                    hipStream_t stream) {
+  conduit_status st = check_kv(kv);
+  if (st) return st;
+  if (k < 0 || k > kv->n_ctx) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_ctx]", k);
+  if (!(scale > 0.f) || scale == __builtin_inff()) return fail(CONDUIT_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (k == 0) return ok();
+  if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
+  if (!q_sel || !aligned16(q_sel) || !o_out || !aligned16(o_out))
+    return fail(CONDUIT_ERR_INVALID_ARG, "q_sel and o_out must be non-NULL and 16-byte aligned");
+  const RefreshLayout L = refresh_layout(kv, k);
+  st = check_ws(ws, ws_bytes, L.total);
+  if (st) return st;
+
+  AttnParams ap{};
+  ap.k = kv->k;
+  ap.v = kv->v;
+  ap.k_stride = kv->k_stride;
+  ap.v_stride = kv->v_stride;
+  ap.n_kv_heads = kv->n_kv_heads;
+  ap.group = kv->n_q_heads / kv->n_kv_heads;
+  ap.n_q_heads = kv->n_q_heads;
+  ap.n_ctx = kv->n_ctx;
+  ap.q = q_sel;
+  ap.n_rows = k;
+  ap.row_pos = pos;
+  ap.q_pos0 = 0;
+  ap.key_ok = nullptr;
+  ap.scale_log2 = scale * kLog2e;
+  ap.chunk = L.chunk;
+  ap.n_split = L.n_split;
+  CombineParams cp{};
+  cp.n_rows = k;
+  cp.n_q_heads = kv->n_q_heads;
+  cp.row_pos = pos;
+  cp.chunk = L.chunk;
+  cp.lse_out = lse_out;
+  cp.o_out = o_out;
+  cp.o_bf16 = kv->dtype == CONDUIT_BF16;
+  hipError_t e;
+  if (kv->dtype == CONDUIT_BF16) {
+    ap.part_m = reinterpret_cast<float *>(at(ws, L.part_m));
+    ap.part_l = reinterpret_cast<float *>(at(ws, L.part_l));
+    ap.part_o = reinterpret_cast<float *>(at(ws, L.part_o));
+    cp.part_m = ap.part_m;
+    cp.part_l = ap.part_l;
+    cp.part_o = ap.part_o;
+    e = launch_attn(ap, kv->head_dim, true, true, stream);
+    if (e != hipSuccess) return hip_fail(e, "refresh attention");
+    e = launch_combine(cp, kv->head_dim, stream);
+    if (e != hipSuccess) return hip_fail(e, "refresh merge");
+  } else {
+    e = launch_attn_f32(ap, cp, kv->head_dim, true, stream);
+    if (e != hipSuccess) return hip_fail(e, "refresh attention");
+  }
+  return ok();
+}
+
+const char *conduit_status_str(conduit_status status) {
+  switch (status) {
+    case CONDUIT_OK: return "CONDUIT_OK";
+    case CONDUIT_ERR_INVALID_ARG: return "CONDUIT_ERR_INVALID_ARG";
+    case CONDUIT_ERR_UNSUPPORTED: return "CONDUIT_ERR_UNSUPPORTED";
+    case CONDUIT_ERR_WORKSPACE: return "CONDUIT_ERR_WORKSPACE";
+    case CONDUIT_ERR_HIP: return "CONDUIT_ERR_HIP";
+  }
+  return "CONDUIT_ERR_UNKNOWN";
+}
+
+const char *conduit_last_error(void) { return g_last_error.c_str(); }
+
+const char *conduit_version(void) { return "conduit-gfx950 0.1.0"; }
+
+}  // extern "C"

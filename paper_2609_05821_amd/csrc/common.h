@@ -1,0 +1,181 @@
+// Internal declarations shared by the HIP kernels and the host layer of
+// libconduit (gfx950 only).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace conduit {
+
+typedef uint16_t u16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kMaxImages = 256;
+
+// Image table passed by value in kernel arguments (2 KB).
+struct ImageTable {
+  int32_t n_images;
+  int32_t n_vis;
+  int32_t pos[kMaxImages];      // first sequence position of image j
+  int32_t off[kMaxImages + 1];  // visual-index offsets
+};
+
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ float bf16_to_f32(u16 b) {
+  return __builtin_bit_cast(float, static_cast<uint32_t>(b) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ u16 f32_to_bf16(float f) {
+  return __builtin_bit_cast(u16, static_cast<__bf16>(f));
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// Kernel parameter blocks
+// ---------------------------------------------------------------------------
+
+// Causal attention of a set of query rows against one layer's cache.  Used for
+// the row statistics of the scoring pass (no values) and for the refresh
+// attention of the selected rows (with values).
+struct AttnParams {
+  const void *k;
+  const void *v;
+  int64_t k_stride;         // elements between tokens
+  int64_t v_stride;
+  int32_t n_kv_heads;
+  int32_t group;            // n_q_heads / n_kv_heads
+  int32_t n_q_heads;
+  int32_t n_ctx;
+  const void *q;            // [n_rows][n_q_heads][D]
+  int32_t n_rows;
+  const int32_t *row_pos;   // nullable: row r sits at q_pos0 + r
+  int32_t q_pos0;
+  const uint8_t *key_ok;    // nullable: key-domain filter (visual-only scoring)
+  float scale_log2;         // logit scale * log2(e)
+  int32_t chunk;            // keys per split (multiple of the key tile)
+  int32_t n_split;
+  float *part_m;            // [n_split][n_rows * n_q_heads]
+  float *part_l;
+  float *part_o;            // [n_split][n_rows * n_q_heads][D] (values only)
+};
+
+// Merge of split partials into final outputs.
+struct CombineParams {
+  int32_t n_rows;
+  int32_t n_q_heads;
+  const int32_t *row_pos;   // nullable: q_pos0 + r
+  int32_t q_pos0;
+  int32_t chunk;
+  const float *part_m;
+  const float *part_l;
+  const float *part_o;      // nullable (statistics only)
+  float *row_b;             // nullable [n_rows * H_q]: log2-domain log-sum-exp
+  float *lse_out;           // nullable [n_rows * H_q]: natural-log log-sum-exp
+  void *o_out;              // nullable [n_rows][H_q][D]
+  int32_t o_bf16;           // output element type
+};
+
+struct ColsumParams {
+  const void *k;
+  const void *v;
+  int64_t k_stride;
+  int64_t v_stride;
+  int32_t n_kv_heads;
+  int32_t group;
+  int32_t n_q_heads;
+  const void *q;            // [n_q][n_q_heads][D]
+  int32_t n_q;
+  const float *row_b;       // [n_q * n_q_heads] log2-domain log-sum-exp
+  const int32_t *vis_pos;   // [n_vis] sequence position of each visual token
+  int32_t n_vis;
+  float scale_log2;
+  float *colsum_part;       // [n_kv_heads][n_vis]
+  float *vsq_part;          // [n_kv_heads][n_vis]
+};
+
+struct FinalizeParams {
+  const float *colsum_part;
+  const float *vsq_part;
+  int32_t n_kv_heads;
+  int32_t n_vis;
+  float n_rows_f;           // n_q * n_q_heads, as float
+  int32_t accumulate;
+  float *s_acc;
+  float *a_acc;
+  float *a_out;             // nullable
+  float *vnorm_out;         // nullable
+};
+
+struct SelectParams {
+  const float *s_acc;
+  const float *a_acc;
+  int32_t n_layers;
+  float lambda;
+  int32_t k;
+  int32_t *idx_out;
+  int32_t *pos_out;
+  uint8_t *mask_out;        // nullable
+  float *shat;              // [n_vis]: caller's shat_out or workspace
+  float *c_out;             // nullable
+};
+
+struct ScatterParams {
+  void *k;
+  void *v;
+  int64_t k_stride_bytes;
+  int64_t v_stride_bytes;
+  int32_t row_bytes;        // n_kv_heads * head_dim * element size
+  const int32_t *pos;
+  int32_t n_rows;
+  const void *k_new;
+  const void *v_new;
+  void *k_old;              // nullable
+  void *v_old;              // nullable
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (host side, defined next to their kernels).  Each returns the
+// status of the launch.
+// ---------------------------------------------------------------------------
+hipError_t launch_build_maps(const ImageTable &tbl, int32_t n_ctx, int32_t *vis_pos,
+                             uint8_t *key_ok, hipStream_t s);
+hipError_t launch_attn(const AttnParams &p, int head_dim, bool bf16, bool with_values,
+                       hipStream_t s);
+hipError_t launch_combine(const CombineParams &p, int head_dim, hipStream_t s);
+hipError_t launch_attn_f32(const AttnParams &p, const CombineParams &out, int head_dim,
+                           bool with_values, hipStream_t s);
+hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, hipStream_t s);
+hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, hipStream_t s);
+hipError_t launch_finalize(const FinalizeParams &p, hipStream_t s);
+hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream_t s);
+hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s);
+hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
+
+// Tiling shared by the host layer (workspace sizing) and the kernels.
+constexpr int kAttnPairsPerBlock = 256;  // (row, head) pairs per workgroup
+constexpr int kAttnKeyTile = 64;         // keys per LDS tile
+constexpr int kColsumKeysPerBlock = 256; // visual keys per workgroup
+
+}  // namespace conduit

@@ -1,0 +1,43 @@
+// Cache merge for the selective recompute, gfx950: the selected rows take
+// their recomputed K/V, every other row is reused in place (Sec. 3).  One
+// wave per selected row moves 16-byte chunks of K and V; when asked, the
+// stale rows are copied out first so the merge can be undone.
+#include "common.h"
+
+namespace conduit {
+namespace {
+
+__global__ __launch_bounds__(256) void scatter_kernel(ScatterParams p) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= p.n_rows) return;
+  const int64_t pos = p.pos[row];
+  const int nch = p.row_bytes / 16;
+  char *kdst = static_cast<char *>(p.k) + pos * p.k_stride_bytes;
+  char *vdst = static_cast<char *>(p.v) + pos * p.v_stride_bytes;
+  const char *ksrc = static_cast<const char *>(p.k_new) + (int64_t)row * p.row_bytes;
+  const char *vsrc = static_cast<const char *>(p.v_new) + (int64_t)row * p.row_bytes;
+  for (int c = lane; c < nch; c += 64) {
+    const uint4 kn = reinterpret_cast<const uint4 *>(ksrc)[c];
+    const uint4 vn = reinterpret_cast<const uint4 *>(vsrc)[c];
+    if (p.k_old) {
+      reinterpret_cast<uint4 *>(static_cast<char *>(p.k_old) + (int64_t)row * p.row_bytes)[c] =
+          reinterpret_cast<const uint4 *>(kdst)[c];
+    }
+    if (p.v_old) {
+      reinterpret_cast<uint4 *>(static_cast<char *>(p.v_old) + (int64_t)row * p.row_bytes)[c] =
+          reinterpret_cast<const uint4 *>(vdst)[c];
+    }
+    reinterpret_cast<uint4 *>(kdst)[c] = kn;
+    reinterpret_cast<uint4 *>(vdst)[c] = vn;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_scatter(const ScatterParams &p, hipStream_t s) {
+  scatter_kernel<<<(p.n_rows + 3) / 4, 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace conduit

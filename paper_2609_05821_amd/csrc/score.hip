@@ -1,0 +1,222 @@
+// Scoring pass kernels, gfx950 (Sec. 3.3 Eq. 6-7; Algorithm 1 scoring loop).
+//
+// Once every span row's log-sum-exp b_r (log2 domain) is known, the visual
+// column sums of Eq. 6 are  sum_r 2^(c * <q_r, k_t> - b_r)  with
+// c = scale * log2(e).  A workgroup owns 256 visual keys of one KV head and
+// streams all (span token, grouped head) rows of that head past them:
+// S = Q K^T with v_mfma_f32_32x32x16_bf16 puts one key column in each lane
+// (16 rows per lane), so the column sums accumulate in-lane.  The same
+// workgroup reads its keys' V rows once for the value-norm proxy (the norm of
+// the concatenated cached heads), so the cache is read once per layer.
+// Per-KV-head partials are reduced in a fixed order by the finalize kernel,
+// which also applies the 1/(n_q H_q) mean and accumulates the layer into
+// s = sum_l a v and A = sum_l a (Eq. 7).
+#include "common.h"
+
+namespace conduit {
+namespace {
+
+constexpr float kInf = __builtin_inff();
+
+// Visual index <-> sequence position maps from the image table.
+__global__ void build_maps_kernel(ImageTable tbl, int n_ctx, int32_t *vis_pos, uint8_t *key_ok) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n_ctx) return;
+  int lo = 0, hi = tbl.n_images - 1;  // last image with pos[j] <= p
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (tbl.pos[mid] <= p) lo = mid; else hi = mid - 1;
+  }
+  const int j = lo;
+  const int n_j = tbl.off[j + 1] - tbl.off[j];
+  const bool vis = p >= tbl.pos[j] && p < tbl.pos[j] + n_j;
+  if (vis) vis_pos[tbl.off[j] + (p - tbl.pos[j])] = p;
+  if (key_ok) key_ok[p] = vis ? 1 : 0;
+}
+
+constexpr int kColsumThreads = 512;   // 8 waves x 32 keys
+
+template <int D>
+__global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParams p) {
+  constexpr int KS = D / 16;
+  constexpr int QCH = 32 * D / 8;       // 16-byte chunks in a 32-row Q block
+  __shared__ u16 qs[2][32][D + 8];
+  __shared__ float bs[2][32];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 31, half = lane >> 5;
+  const int kvh = blockIdx.y;
+  const int G = p.group;
+  const int n_pair = p.n_q * G;
+  const int nblk = (n_pair + 31) / 32;
+  const u16 *Kg = static_cast<const u16 *>(p.k);
+  const u16 *Vg = static_cast<const u16 *>(p.v);
+  const u16 *Qg = static_cast<const u16 *>(p.q);
+
+  // This lane's key column, held as the B operand for every row block.
+  const int t = blockIdx.x * kColsumKeysPerBlock + wave * 32 + col;
+  const bool tvalid = t < p.n_vis;
+  bf16x8 kreg[KS];
+  {
+    const u16 *krow = Kg + (int64_t)(tvalid ? p.vis_pos[t] : 0) * p.k_stride + kvh * D + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      kreg[ks] = as_bf16x8(tvalid ? *reinterpret_cast<const uint4 *>(krow + ks * 16) : make_uint4(0, 0, 0, 0));
+  }
+
+  // Cooperative load of row block `blk` (32 (span token, head) rows).
+  auto load_q = [&](int blk, uint4 &qv, float &bv) {
+    if (tid < QCH) {
+      const int row = tid / (D / 8), dc = tid % (D / 8);
+      const int pr = blk * 32 + row;
+      qv = make_uint4(0, 0, 0, 0);
+      if (pr < n_pair) {
+        const int i = pr / G, hq = kvh * G + pr % G;
+        qv = *reinterpret_cast<const uint4 *>(Qg + ((int64_t)i * p.n_q_heads + hq) * D + dc * 8);
+      }
+    }
+    if (tid < 32) {
+      const int pr = blk * 32 + tid;
+      bv = kInf;  // padding rows contribute 2^-inf = 0
+      if (pr < n_pair) bv = p.row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
+    }
+  };
+  auto store_q = [&](int buf, const uint4 &qv, float bv) {
+    if (tid < QCH) *reinterpret_cast<uint4 *>(&qs[buf][tid / (D / 8)][(tid % (D / 8)) * 8]) = qv;
+    if (tid < 32) bs[buf][tid] = bv;
+  };
+
+  uint4 qv = make_uint4(0, 0, 0, 0);
+  float bv = kInf;
+  load_q(0, qv, bv);
+  store_q(0, qv, bv);
+  __syncthreads();
+
+  float colsum = 0.f;
+  for (int blk = 0; blk < nblk; ++blk) {
+    const int buf = blk & 1;
+    if (blk + 1 < nblk) load_q(blk + 1, qv, bv);
+    f32x16 acc = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4 *>(&qs[buf][col][ks * 16 + 8 * half]));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kreg[ks], acc, 0, 0, 0);
+    }
+    // lane (col, half), register v holds row 8*(v/4) + 4*half + v%4
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 b = *reinterpret_cast<const f32x4 *>(&bs[buf][8 * g + 4 * half]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) colsum += fast_exp2(fmaf(acc[4 * g + i], p.scale_log2, -b[i]));
+    }
+    if (blk + 1 < nblk) store_q(buf ^ 1, qv, bv);
+    __syncthreads();
+  }
+  colsum += __shfl_xor(colsum, 32, 64);
+  if (half == 0 && tvalid) p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
+
+  // Value-norm proxy: this head's share of ||V_t||^2, two threads per key.
+  {
+    const int kk = tid >> 1, part = tid & 1;
+    const int tv = blockIdx.x * kColsumKeysPerBlock + kk;
+    float sq = 0.f;
+    if (tv < p.n_vis) {
+      const u16 *vrow = Vg + (int64_t)p.vis_pos[tv] * p.v_stride + kvh * D + part * (D / 2);
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c) {
+        const uint4 w = *reinterpret_cast<const uint4 *>(vrow + c * 8);
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __builtin_bit_cast(float, ws[e] << 16);
+          const float hi = __builtin_bit_cast(float, ws[e] & 0xffff0000u);
+          sq = fmaf(lo, lo, sq);
+          sq = fmaf(hi, hi, sq);
+        }
+      }
+    }
+    sq += __shfl_xor(sq, 1, 64);
+    if (part == 0 && tv < p.n_vis) p.vsq_part[(int64_t)kvh * p.n_vis + tv] = sq;
+  }
+}
+
+// fp32 path: one thread per (visual key, KV head).
+template <int D>
+__global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p) {
+  const int t = blockIdx.x * 64 + threadIdx.x;
+  const int kvh = blockIdx.y;
+  if (t >= p.n_vis) return;
+  const float *Kg = static_cast<const float *>(p.k);
+  const float *Vg = static_cast<const float *>(p.v);
+  const float *Qg = static_cast<const float *>(p.q);
+  const int64_t pos = p.vis_pos[t];
+  float kr[D];
+#pragma unroll
+  for (int e = 0; e < D; ++e) kr[e] = Kg[pos * p.k_stride + kvh * D + e];
+  float colsum = 0.f;
+  const int n_pair = p.n_q * p.group;
+  for (int pr = 0; pr < n_pair; ++pr) {
+    const int i = pr / p.group, hq = kvh * p.group + pr % p.group;
+    const float *q = Qg + ((int64_t)i * p.n_q_heads + hq) * D;
+    float dot = 0.f;
+#pragma unroll
+    for (int e = 0; e < D; ++e) dot = fmaf(q[e], kr[e], dot);
+    colsum += fast_exp2(fmaf(dot, p.scale_log2, -p.row_b[(int64_t)i * p.n_q_heads + hq]));
+  }
+  float sq = 0.f;
+  const float *vr = Vg + pos * p.v_stride + kvh * D;
+#pragma unroll 8
+  for (int e = 0; e < D; ++e) sq = fmaf(vr[e], vr[e], sq);
+  p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
+  p.vsq_part[(int64_t)kvh * p.n_vis + t] = sq;
+}
+
+__global__ void finalize_kernel(FinalizeParams p) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= p.n_vis) return;
+  float cs = 0.f, sq = 0.f;
+  for (int h = 0; h < p.n_kv_heads; ++h) {
+    cs += p.colsum_part[(int64_t)h * p.n_vis + t];
+    sq += p.vsq_part[(int64_t)h * p.n_vis + t];
+  }
+  const float a = cs / p.n_rows_f;
+  const float v = sqrtf(sq);
+  const float s = a * v;
+  if (p.accumulate) {
+    p.s_acc[t] += s;
+    p.a_acc[t] += a;
+  } else {
+    p.s_acc[t] = s;
+    p.a_acc[t] = a;
+  }
+  if (p.a_out) p.a_out[t] = a;
+  if (p.vnorm_out) p.vnorm_out[t] = v;
+}
+
+}  // namespace
+
+hipError_t launch_build_maps(const ImageTable &tbl, int32_t n_ctx, int32_t *vis_pos, uint8_t *key_ok,
+                             hipStream_t s) {
+  build_maps_kernel<<<(n_ctx + 255) / 256, 256, 0, s>>>(tbl, n_ctx, vis_pos, key_ok);
+  return hipGetLastError();
+}
+
+hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, hipStream_t s) {
+  if (bf16) {
+    dim3 grid((p.n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock, p.n_kv_heads);
+    if (head_dim == 128) colsum_bf16_kernel<128><<<grid, kColsumThreads, 0, s>>>(p);
+    else colsum_bf16_kernel<64><<<grid, kColsumThreads, 0, s>>>(p);
+  } else {
+    dim3 grid((p.n_vis + 63) / 64, p.n_kv_heads);
+    if (head_dim == 128) colsum_f32_kernel<128><<<grid, 64, 0, s>>>(p);
+    else colsum_f32_kernel<64><<<grid, 64, 0, s>>>(p);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize(const FinalizeParams &p, hipStream_t s) {
+  finalize_kernel<<<(p.n_vis + 255) / 256, 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace conduit

@@ -1,0 +1,195 @@
+// Image reweighting and global top-k, gfx950 (Sec. 3.4 Eq. 8-9, Sec. 3.5
+// Eq. 10-11, the tail of Algorithm 1).
+//
+// One workgroup of 1024 threads:
+//  1. g_j = sum_{t in V_j} A_t / (|L| n_j): one wave per image, lane-strided
+//     partial sums and a butterfly reduction (fixed order);
+//  2. g_bar and c_j = (1 - lambda) + lambda g_j / g_bar  (c_j = 1 if g_bar = 0);
+//  3. s_hat_t = (s_t / |L|) c_pi(t), written once;
+//  4. the k-th largest s_hat by radix select on the fp32 bit patterns
+//     (s_hat >= 0, so unsigned bit order is value order): 11 + 11 + 10 bit
+//     passes with LDS histograms (integer atomics: exact);
+//  5. ordered compaction: everything above the threshold plus the first
+//     `need` entries equal to it in index order (ties to the lower index),
+//     with two block scans, so idx/pos come out ascending.
+#include "common.h"
+
+namespace conduit {
+namespace {
+
+constexpr int kSelThreads = 1024;
+constexpr int kWaves = kSelThreads / 64;
+
+__device__ __forceinline__ uint32_t order_key(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  return u == 0x80000000u ? 0u : u;  // -0 ranks as +0
+}
+
+// Exclusive scan of one int per thread over the block; also returns the total.
+__device__ int block_exclusive_scan(int x, int *s_wave, int &total) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) s_wave[w] = inc;
+  __syncthreads();
+  if (w == 0) {
+    int v = lane < kWaves ? s_wave[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < kWaves; o <<= 1) {
+      const int y = __shfl_up(v, o, 64);
+      if (lane >= o) v += y;
+    }
+    if (lane < kWaves) s_wave[lane] = v;
+  }
+  __syncthreads();
+  const int excl = inc - x + (w > 0 ? s_wave[w - 1] : 0);
+  total = s_wave[kWaves - 1];
+  __syncthreads();
+  return excl;
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, ImageTable tbl) {
+  __shared__ float s_g[kMaxImages];
+  __shared__ float s_c[kMaxImages];
+  __shared__ int hist[2048];
+  __shared__ int s_wave[kWaves];
+  __shared__ int s_bin, s_above;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = tbl.n_vis, K = tbl.n_images;
+  const float n_layers = (float)p.n_layers;
+
+  // 1. per-image mean attention
+  for (int j = wave; j < K; j += kWaves) {
+    const int lo = tbl.off[j], hi = tbl.off[j + 1];
+    float acc = 0.f;
+    for (int t = lo + lane; t < hi; t += 64) acc += p.a_acc[t];
+    acc = wave_sum(acc);
+    if (lane == 0) s_g[j] = acc / (n_layers * (float)(hi - lo));
+  }
+  __syncthreads();
+  // 2. coefficients
+  if (wave == 0) {
+    float acc = 0.f;
+    for (int j = lane; j < K; j += 64) acc += s_g[j];
+    const float g_bar = wave_sum(acc) / (float)K;
+    for (int j = lane; j < K; j += 64) {
+      // (1 - lambda) + lambda * x adds two non-negative terms, so it keeps full
+      // relative precision even for c << 1; x == 1 (one image, or an image at
+      // the mean) gives exactly 1.
+      const float x = s_g[j] / g_bar;
+      const float c = (g_bar == 0.f || x == 1.f) ? 1.f : (1.f - p.lambda) + p.lambda * x;
+      s_c[j] = c;
+      if (p.c_out) p.c_out[j] = c;
+    }
+  }
+  __syncthreads();
+  // 3. composite scores
+  for (int j = wave; j < K; j += kWaves) {
+    const int lo = tbl.off[j], hi = tbl.off[j + 1];
+    const float c = s_c[j];
+    for (int t = lo + lane; t < hi; t += 64) p.shat[t] = (p.s_acc[t] / n_layers) * c;
+  }
+  __syncthreads();
+
+  // 4. radix select of the k-th largest key
+  uint32_t prefix = 0, pmask = 0;
+  int kk = p.k;
+  const int shifts[3] = {21, 10, 0};
+  const int nbins[3] = {2048, 2048, 1024};
+#pragma unroll
+  for (int pass = 0; pass < 3; ++pass) {
+    const int sh = shifts[pass], nb = nbins[pass];
+    for (int b = tid; b < nb; b += kSelThreads) hist[b] = 0;
+    __syncthreads();
+    for (int t = tid; t < n; t += kSelThreads) {
+      const uint32_t key = order_key(p.shat[t]);
+      if ((key & pmask) == prefix) atomicAdd(&hist[(key >> sh) & (nb - 1)], 1);
+    }
+    __syncthreads();
+    // thread tid owns bins in descending order: nb-1-per*tid .. nb-per*(tid+1)
+    const int per = nb / kSelThreads;
+    int local = 0;
+    for (int i = 0; i < per; ++i) local += hist[nb - 1 - per * tid - i];
+    int total;
+    int run = block_exclusive_scan(local, s_wave, total);
+    for (int i = 0; i < per; ++i) {
+      const int b = nb - 1 - per * tid - i;
+      const int h = hist[b];
+      if (run < kk && run + h >= kk) {
+        s_bin = b;
+        s_above = run;
+      }
+      run += h;
+    }
+    __syncthreads();
+    prefix |= (uint32_t)s_bin << sh;
+    pmask |= (uint32_t)(nb - 1) << sh;
+    kk -= s_above;
+    __syncthreads();
+  }
+  const uint32_t tau = prefix;
+  const int need_eq = kk;  // entries equal to tau to take, lowest indices first
+
+  // 5. ordered compaction over contiguous per-thread segments
+  const int seg = (n + kSelThreads - 1) / kSelThreads;
+  const int lo = min(n, tid * seg), hi = min(n, lo + seg);
+  int gt = 0, eq = 0;
+  for (int t = lo; t < hi; ++t) {
+    const uint32_t key = order_key(p.shat[t]);
+    gt += key > tau;
+    eq += key == tau;
+  }
+  int total;
+  const int eq_before = block_exclusive_scan(eq, s_wave, total);
+  const int take_eq = max(0, min(eq, need_eq - eq_before));
+  int out = block_exclusive_scan(gt + take_eq, s_wave, total);
+  int j = 0;  // image of the segment start
+  if (lo < hi) {
+    int a = 0, b = K - 1;
+    while (a < b) {
+      const int mid = (a + b + 1) >> 1;
+      if (tbl.off[mid] <= lo) a = mid; else b = mid - 1;
+    }
+    j = a;
+  }
+  int eq_seen = 0;
+  for (int t = lo; t < hi; ++t) {
+    while (t >= tbl.off[j + 1]) ++j;
+    const uint32_t key = order_key(p.shat[t]);
+    bool sel = key > tau;
+    if (key == tau) {
+      sel = eq_seen < take_eq;
+      ++eq_seen;
+    }
+    if (p.mask_out) p.mask_out[t] = sel ? 1 : 0;
+    if (sel && out < p.k) {
+      p.idx_out[out] = t;
+      p.pos_out[out] = tbl.pos[j] + (t - tbl.off[j]);
+      ++out;
+    }
+  }
+}
+
+__global__ void clear_u8_kernel(uint8_t *p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+}  // namespace
+
+hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream_t s) {
+  select_kernel<<<1, kSelThreads, 0, s>>>(p, tbl);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s) {
+  clear_u8_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p, n);
+  return hipGetLastError();
+}
+
+}  // namespace conduit

@@ -75,6 +75,7 @@ class Workload:
     seed: int = 0
     lognormal_sigma: float = 0.5
     kappa: float = 0.5
+    rel_cos: float = 0.3            # query-key cosine of relevant images
 
     @property
     def n_images(self) -> int:
@@ -140,11 +141,12 @@ class Workload:
         head_kv = np.arange(hq) // g
         if self.n_relevant:
             zq = q
-            q = np.sqrt(0.7) * zq + np.sqrt(0.3) * np.sqrt(d) * sh["w"][head_kv][None, :, :]
+            rc = self.rel_cos
+            q = np.sqrt(1 - rc) * zq + np.sqrt(rc) * np.sqrt(d) * sh["w"][head_kv][None, :, :]
             for j in sh["relevant"]:
                 lo = int(self.img_pos[j])
                 hi = lo + int(self.img_off[j + 1] - self.img_off[j])
-                k[lo:hi] = np.sqrt(0.7) * k[lo:hi] + np.sqrt(0.3) * np.sqrt(d) * sh["w"][None]
+                k[lo:hi] = np.sqrt(1 - rc) * k[lo:hi] + np.sqrt(rc) * np.sqrt(d) * sh["w"][None]
         if self.n_sinks:
             q = q + 2.0 * sh["b"][head_kv][None, :, :]
             sp = P_vis[sh["sinks"]]

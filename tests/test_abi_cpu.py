@@ -1,0 +1,172 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/conduit.h declares, and rejects bad arguments on the host before any
+HIP call (nothing is launched, so no device is needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_05821_amd import api
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "conduit.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(api.LIB_PATH),
+                                 reason="libconduit.so not built (run __graft_entry__.build())")
+
+FAKE = 0x100000  # a 256-byte aligned non-NULL address; never dereferenced here
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(conduit_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported():
+    L = api.lib()
+    declared = header_functions()
+    assert len(declared) >= 11
+    for name in declared:
+        assert hasattr(L, name), name
+    assert sorted(declared) == sorted(api.EXPORTS)
+
+
+def test_budget_closed_form():
+    assert api.conduit_budget(576, 1, 10) == 57
+    assert api.conduit_budget(65536, 1, 10) == 6553
+    assert api.conduit_budget(100, 29, 100) == 29
+    assert api.conduit_budget(16384, 1, 10) == 1638
+    assert api.conduit_budget(7, 0, 1) == 0
+    assert api.conduit_budget(7, 1, 1) == 7
+    assert api.conduit_budget(2 ** 40, 3, 7) == (3 * 2 ** 40) // 7
+    for bad in ((-1, 1, 2), (5, 1, 0), (5, -1, 2), (5, 3, 2)):
+        assert api.conduit_budget(*bad) == -1
+
+
+def test_status_strings_and_version():
+    L = api.lib()
+    names = [L.conduit_status_str(s).decode() for s in range(5)]
+    assert names == ["CONDUIT_OK", "CONDUIT_ERR_INVALID_ARG", "CONDUIT_ERR_UNSUPPORTED",
+                     "CONDUIT_ERR_WORKSPACE", "CONDUIT_ERR_HIP"]
+    assert b"gfx950" in L.conduit_version()
+
+
+def kv(**over):
+    d = dict(k=FAKE, v=FAKE, k_stride=512, v_stride=512, n_ctx=1344, n_q_heads=28, n_kv_heads=4,
+             head_dim=128, dtype=api.BF16)
+    d.update(over)
+    return api.KV(**d)
+
+
+IMG = api.ImageTable([256], [0, 1024])
+
+
+def score(kvd=None, q=FAKE, n_q=64, q_pos0=1280, img=IMG, norm=0, scale=0.088, s=FAKE, a=FAKE,
+          acc=0, ws=FAKE, ws_bytes=1 << 30):
+    kvd = kvd or kv()
+    return api.lib().conduit_score(ctypes.byref(kvd), q, n_q, q_pos0, ctypes.byref(img.desc), norm,
+                                   scale, None, None, s, a, acc, None, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(kvd=kv(k=0)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(v=FAKE + 8)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(n_q_heads=30)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(head_dim=96, k_stride=384, v_stride=384)), api.ERR_UNSUPPORTED),
+    (dict(kvd=kv(dtype=7)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(k_stride=100)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(k_stride=516)), api.ERR_INVALID_ARG),
+    (dict(q=0), api.ERR_INVALID_ARG),
+    (dict(q=FAKE + 2), api.ERR_INVALID_ARG),
+    (dict(n_q=0), api.ERR_INVALID_ARG),
+    (dict(q_pos0=1300), api.ERR_INVALID_ARG),
+    (dict(norm=5), api.ERR_INVALID_ARG),
+    (dict(scale=0.0), api.ERR_INVALID_ARG),
+    (dict(scale=float("nan")), api.ERR_INVALID_ARG),
+    (dict(s=0), api.ERR_INVALID_ARG),
+    (dict(acc=2), api.ERR_INVALID_ARG),
+    (dict(img=api.ImageTable([1200], [0, 1024])), api.ERR_INVALID_ARG),   # runs into the span
+    (dict(img=api.ImageTable([256, 300], [0, 100, 200])), api.ERR_INVALID_ARG),  # overlap
+    (dict(img=api.ImageTable([400, 256], [0, 10, 20])), api.ERR_INVALID_ARG),    # out of order
+    (dict(img=api.ImageTable([256, 400], [0, 10, 10])), api.ERR_INVALID_ARG),    # empty image
+    (dict(img=api.ImageTable([256], [1, 1024])), api.ERR_INVALID_ARG),
+    (dict(img=api.ImageTable(list(range(0, 1028, 4)), list(range(0, 1032, 4)))), api.ERR_UNSUPPORTED),
+    (dict(ws_bytes=16), api.ERR_WORKSPACE),
+    (dict(ws=FAKE + 64), api.ERR_INVALID_ARG),
+])
+def test_score_rejects(case, status):
+    assert score(**case) == status
+    assert api.lib().conduit_last_error().decode() != ""
+
+
+def test_image_table_n_vis_mismatch():
+    img = api.ImageTable([256], [0, 1024])
+    img.desc.n_vis = 1000
+    assert score(img=img) == api.ERR_INVALID_ARG
+
+
+def select(s=FAKE, a=FAKE, n_layers=1, img=IMG, lam=1.0, k=102, idx=FAKE, pos=FAKE, ws=FAKE,
+           ws_bytes=1 << 20):
+    return api.lib().conduit_select_topk(s, a, n_layers, ctypes.byref(img.desc), lam, k, idx, pos,
+                                         None, None, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("case", [dict(s=0), dict(n_layers=0), dict(lam=-0.1), dict(lam=1.5),
+                                  dict(lam=float("nan")), dict(k=-1), dict(k=1025), dict(idx=0),
+                                  dict(pos=0)])
+def test_select_rejects(case):
+    assert select(**case) == api.ERR_INVALID_ARG
+
+
+def test_select_workspace_too_small():
+    assert select(ws_bytes=100) == api.ERR_WORKSPACE
+
+
+def test_scatter_rejects():
+    L = api.lib()
+    kvd = kv()
+    assert L.conduit_scatter_kv(ctypes.byref(kvd), FAKE, -1, FAKE, FAKE, None, None, None) == api.ERR_INVALID_ARG
+    assert L.conduit_scatter_kv(ctypes.byref(kvd), None, 3, FAKE, FAKE, None, None, None) == api.ERR_INVALID_ARG
+    assert L.conduit_scatter_kv(ctypes.byref(kvd), FAKE, 3, FAKE + 4, FAKE, None, None, None) == api.ERR_INVALID_ARG
+    assert L.conduit_scatter_kv(ctypes.byref(kvd), FAKE, 3, FAKE, FAKE, FAKE + 4, None, None) == api.ERR_INVALID_ARG
+    assert L.conduit_scatter_kv(ctypes.byref(kvd), FAKE, 2000, FAKE, FAKE, None, None, None) == api.ERR_INVALID_ARG
+    # k = 0 enqueues nothing and succeeds even without a device
+    assert L.conduit_scatter_kv(ctypes.byref(kvd), None, 0, None, None, None, None, None) == api.OK
+
+
+def test_refresh_rejects_and_sizes():
+    L = api.lib()
+    kvd = kv()
+    need = L.conduit_refresh_workspace_bytes(ctypes.byref(kvd), 102)
+    assert need > 0
+    assert L.conduit_refresh_workspace_bytes(ctypes.byref(kv(dtype=api.F32)), 102) == 0
+    args = lambda **o: dict(dict(q=FAKE, pos=FAKE, k=102, scale=0.088, o=FAKE, ws=FAKE, wsb=need), **o)
+    def call(a):
+        return L.conduit_refresh_attn(ctypes.byref(kvd), a["q"], a["pos"], a["k"], a["scale"], a["o"],
+                                      None, a["ws"], a["wsb"], None)
+    assert call(args(pos=None)) == api.ERR_INVALID_ARG
+    assert call(args(q=FAKE + 2)) == api.ERR_INVALID_ARG
+    assert call(args(o=None)) == api.ERR_INVALID_ARG
+    assert call(args(scale=-1.0)) == api.ERR_INVALID_ARG
+    assert call(args(k=-1)) == api.ERR_INVALID_ARG
+    assert call(args(wsb=need - 1)) == api.ERR_WORKSPACE
+    assert call(args(k=0, q=None, pos=None, o=None)) == api.OK
+
+
+def test_workspace_queries_are_consistent():
+    L = api.lib()
+    kvd = kv()
+    a = L.conduit_score_workspace_bytes(ctypes.byref(kvd), 64, ctypes.byref(IMG.desc))
+    assert a > 1024 * 4 * 4 * 2   # at least the two per-head partial arrays
+    assert L.conduit_select_workspace_bytes(1024, 1) >= 4096
+    assert L.conduit_score_workspace_bytes(ctypes.byref(kvd), 0, ctypes.byref(IMG.desc)) == 0
+
+
+@pytest.mark.skipif(__import__("torch").cuda.device_count() > 0,
+                    reason="needs a host without a GPU (the call would launch on fake pointers)")
+def test_valid_call_without_device_reports_hip_error():
+    assert score() == api.ERR_HIP
+    assert "build_maps" in api.lib().conduit_last_error().decode()
