@@ -7,9 +7,11 @@
 //  * the selective recompute needs, for every selected visual row, causal
 //    attention over the merged fresh/stale cache (values included).
 //
-// bf16 path: workgroups of 4 waves own 256 (row, head) pairs of one KV head
-// (grouped heads share the K/V tiles) and one key split.  Per 64-key tile,
-// K is staged in LDS row-major and V transposed; each wave computes
+// bf16 path: workgroups of 8 waves (two per SIMD, so one wave's MFMAs overlap
+// the other's softmax) own 256 (row, head) pairs of one KV head (grouped heads
+// share the K/V tiles) and one key split.  Per 64-key tile, double-buffered in
+// LDS with the next tile's global loads in flight, K is staged row-major and
+// V transposed; each wave computes
 // S^T = K Q^T with v_mfma_f32_32x32x16_bf16 so that every lane holds 16 keys
 // of one pair column and the online softmax runs in-lane; the probabilities
 // feed O^T = V^T P^T straight from the accumulator registers.  Splits write
@@ -20,16 +22,18 @@
 namespace conduit {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kWaves = 8;                  // two waves per SIMD
+constexpr int kThreads = kWaves * 64;
 constexpr int KT = kAttnKeyTile;
 constexpr float kNegInf = -__builtin_inff();
+static_assert(kWaves * 32 == kAttnPairsPerBlock, "one 32-column pair tile per wave");
 
 template <int D>
 struct AttnSmem {
-  u16 k[KT][D + 8];   // K tile, one row per key (+16 B pad against bank conflicts)
-  u16 vt[D][KT + 8];  // V^T tile, keys in MFMA-operand order
-  uint8_t ok[KT];     // key-domain filter for the tile
-  int maxpos;
+  alignas(16) u16 k[2][KT][D + 8];   // K tiles, one row per key (+16 B pad against bank conflicts)
+  alignas(16) u16 vt[2][D][KT + 8];  // V^T tiles, keys in MFMA-operand order
+  uint64_t okmask[2];                // key-domain filter per tile, bit = key
+  int maxpos, minpos;
 };
 
 __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, int r) {
@@ -46,194 +50,227 @@ __device__ __forceinline__ int vt_slot(int kl) {
   return sub * 32 + ks * 16 + h * 8 + e;
 }
 
+// Global -> register staging of one key tile (issued a tile ahead).
+template <int D, bool PV>
+struct TileRegs {
+  static constexpr int KCH = KT * D / 8 / kThreads;    // 16-byte K chunks per thread
+  static constexpr int VIT = (KT / 2) * (D / 8);       // 2-key x 8-dim V items
+  u32x4 k[KCH];
+  u32x4 v[PV ? 2 : 1];
+  uint8_t ok;
+};
+
+// The running maximum only moves when a sub-tile's maximum exceeds it by more
+// than this many log2 units; probabilities stay below 2^8 and O, l are
+// rescaled rarely.  Exact: O, l and the final normaliser share the reference.
+constexpr float kRescaleSlack = 8.f;
+
 template <int D, bool PV>
 __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int KS = D / 16;   // MFMA k-steps over the head dimension
   constexpr int DT = D / 32;   // 32-row tiles of O^T
+  using Regs = TileRegs<D, PV>;
   __shared__ AttnSmem<D> sm;
 
-  const int split = blockIdx.x, pb = blockIdx.y, kvh = blockIdx.z;
+  // Blocks of later rows see more keys: launch them first.
+  const int split = blockIdx.x, pb = gridDim.y - 1 - blockIdx.y, kvh = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
   const int G = p.group;
   const int n_pairs = p.n_rows * G;
   const int pair0 = pb * kAttnPairsPerBlock;
 
-  // Largest position among this block's rows bounds its key range.
-  if (tid == 0) sm.maxpos = -1;
+  // Position range of this block's rows bounds its keys and its masking.
+  if (tid == 0) {
+    sm.maxpos = -1;
+    sm.minpos = 0x7fffffff;
+  }
   __syncthreads();
   {
     const int r_first = pair0 / G;
     const int r_last = (min(pair0 + kAttnPairsPerBlock, n_pairs) - 1) / G;
-    for (int r = r_first + tid; r <= r_last; r += kThreads)
-      atomicMax(&sm.maxpos, row_position(p.row_pos, p.q_pos0, r));
+    for (int r = r_first + tid; r <= r_last; r += kThreads) {
+      const int rp = row_position(p.row_pos, p.q_pos0, r);
+      atomicMax(&sm.maxpos, rp);
+      atomicMin(&sm.minpos, rp);
+    }
   }
   __syncthreads();
   const int kbeg = split * p.chunk;
   const int kend = min(kbeg + p.chunk, sm.maxpos + 1);
+  const int minpos = sm.minpos;
   if (kbeg >= kend) return;
 
   const u16 *Kg = static_cast<const u16 *>(p.k);
   const u16 *Vg = static_cast<const u16 *>(p.v);
   const u16 *Qg = static_cast<const u16 *>(p.q);
+  const float c = p.scale_log2;
 
-  // Pair columns owned by this lane: two 32-wide tiles per wave.
-  int rp[2], gpair[2];
-  bool valid[2];
-  bf16x8 qreg[2][KS];
+  // The pair column owned by this lane.
+  const int pair = pair0 + wave * 32 + col;
+  const bool valid = pair < n_pairs;
+  const int r = valid ? pair / G : 0;
+  const int gpair = r * p.n_q_heads + kvh * G + (valid ? pair % G : 0);
+  const int rp = valid ? row_position(p.row_pos, p.q_pos0, r) : -1;
+  bf16x8 qreg[KS];
+  {
+    const u16 *qrow = Qg + (int64_t)gpair * D + 8 * half;
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    const int pair = pair0 + wave * 64 + nt * 32 + col;
-    valid[nt] = pair < n_pairs;
-    const int r = valid[nt] ? pair / G : 0;
-    const int hq = kvh * G + (valid[nt] ? pair % G : 0);
-    gpair[nt] = r * p.n_q_heads + hq;
-    rp[nt] = valid[nt] ? row_position(p.row_pos, p.q_pos0, r) : -1;
-    const u16 *qrow = Qg + (int64_t)gpair[nt] * D + 8 * half;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      uint4 v = valid[nt] ? *reinterpret_cast<const uint4 *>(qrow + ks * 16) : make_uint4(0, 0, 0, 0);
-      qreg[nt][ks] = as_bf16x8(v);
-    }
+    for (int ks = 0; ks < KS; ++ks)
+      qreg[ks] = as_bf16x8(valid ? ld16(qrow + ks * 16) : u32x4{0, 0, 0, 0});
   }
 
-  float m[2] = {kNegInf, kNegInf}, l[2] = {0.f, 0.f};
-  f32x16 o[2][DT];
+  u32x4 rk[Regs::KCH];
+  u32x4 rv[PV ? 2 : 1];
+  bool rok = false;
+  auto load_tile = [&](int t0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < Regs::KCH; ++i) {
+      const int cidx = tid + kThreads * i;
+      const int key = cidx / (D / 8), dc = cidx % (D / 8);
+      const int kp = min(t0 + key, kend - 1);  // rows past kend are masked
+      rk[i] = ld16(Kg + (int64_t)kp * p.k_stride + kvh * D + dc * 8);
+    }
+    if constexpr (PV) {
+      if (Regs::VIT >= kThreads || tid < Regs::VIT) {
+        const int dc = tid % (D / 8), kpair = tid / (D / 8);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const int kp = min(t0 + kpair * 2 + i, kend - 1);
+          rv[i] = ld16(Vg + (int64_t)kp * p.v_stride + kvh * D + dc * 8);
+        }
+      }
+    }
+    if (!PV && p.key_ok && tid < KT) {
+      const int kp = t0 + tid;
+      rok = kp < kend && p.key_ok[kp] != 0;
+    }
+  };
+  auto store_tile = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < Regs::KCH; ++i) {
+      const int cidx = tid + kThreads * i;
+      st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
+    }
+    if constexpr (PV) {
+      if (Regs::VIT >= kThreads || tid < Regs::VIT) {
+        const int dc = tid % (D / 8), kpair = tid / (D / 8);
+        const int slot = vt_slot(kpair * 2);
+        const u32x4 w0 = rv[0], w1 = rv[1];
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
+          *reinterpret_cast<uint32_t *>(&sm.vt[buf][dc * 8 + 2 * e2][slot]) =
+              (w0[e2] & 0xffffu) | (w1[e2] << 16);
+          *reinterpret_cast<uint32_t *>(&sm.vt[buf][dc * 8 + 2 * e2 + 1][slot]) =
+              (w0[e2] >> 16) | (w1[e2] & 0xffff0000u);
+        }
+      }
+    }
+    if (!PV && p.key_ok && tid < KT) {  // wave 0: one bit per key of the tile
+      const uint64_t bits = __ballot(rok != 0);
+      if (tid == 0) sm.okmask[buf] = bits;
+    }
+  };
+
+  float m = kNegInf, l = 0.f;
+  f32x16 o[DT];
   if constexpr (PV) {
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[nt][dt] = f32x16{};
+    for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
   }
 
+  // One 32-key sub-tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
+  auto subtile = [&](int buf, int sub, int t0, bool masked) __attribute__((always_inline)) {
+    bf16x8 ka[KS];
+    const u16 *krow = &sm.k[buf][sub * 32 + col][8 * half];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) ka[ks] = as_bf16x8(ld16(krow + ks * 16));
+    f32x16 s = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qreg[ks], s, 0, 0, 0);
+    // V^T operands of this sub-tile load while the softmax runs.
+    bf16x8 va[2][DT];
+    if constexpr (PV) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          va[ks][dt] = as_bf16x8(
+              ld16(&sm.vt[buf][dt * 32 + col][sub * 32 + ks * 16 + 8 * half]));
+    }
+    if (masked) {  // branch-free: causal / split end and the key domain
+      const int lim = min(kend - 1, rp) - t0;  // last visible key of the tile
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int kl = sub * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+        bool ok = kl <= lim;
+        if constexpr (!PV) {  // key-domain filter: statistics of visual-only scoring
+          const uint64_t dom = p.key_ok ? sm.okmask[buf] : ~0ull;
+          ok = ok & (((dom >> kl) & 1ull) != 0);
+        }
+        s[v] = ok ? s[v] : kNegInf;
+      }
+    }
+    float mx = kNegInf;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+    const bool grow = mx > m + kRescaleSlack;
+    const float m_new = grow ? mx : m;
+    const float alpha = grow ? fast_exp2(m - m_new) : 1.f;
+    m = m_new;
+    const float neg_m = (m_new == kNegInf) ? 0.f : -m_new;
+    float psum = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float e = fast_exp2(fmaf(s[v], c, neg_m));
+      s[v] = e;
+      psum += e;
+    }
+    l = l * alpha + psum;
+    if constexpr (PV) {
+      bf16x8 pk[2];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pk[ks][e] = static_cast<__bf16>(s[8 * ks + e]);
+      if (__ballot(grow)) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+      }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][dt], pk[ks], o[dt], 0, 0, 0);
+    }
+  };
+
+  // Double-buffered main loop: the next tile's global loads are in flight
+  // while the current tile computes; one barrier per tile.
+  load_tile(kbeg);
+  store_tile(0);
+  __syncthreads();
+  int buf = 0;
   for (int t0 = kbeg; t0 < kend; t0 += KT) {
-    __syncthreads();  // previous tile fully consumed
-    // ---- stage K (row-major) ----
-    constexpr int KCH = KT * D / 8;  // 16-byte chunks in a K tile
-#pragma unroll
-    for (int c = tid; c < KCH; c += kThreads) {
-      const int key = c / (D / 8), dc = c % (D / 8);
-      const int kp = t0 + key;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (kp < kend) v = *reinterpret_cast<const uint4 *>(Kg + (int64_t)kp * p.k_stride + kvh * D + dc * 8);
-      *reinterpret_cast<uint4 *>(&sm.k[key][dc * 8]) = v;
-    }
-    // ---- stage V transposed: a thread takes 4 consecutive keys x 8 dims ----
-    if constexpr (PV) {
-      constexpr int VIT = (KT / 4) * (D / 8);
-      for (int c = tid; c < VIT; c += kThreads) {
-        const int dc = c % (D / 8), quad = c / (D / 8);
-        u16 vals[4][8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int kp = t0 + quad * 4 + i;
-          uint4 v = make_uint4(0, 0, 0, 0);
-          if (kp < kend) v = *reinterpret_cast<const uint4 *>(Vg + (int64_t)kp * p.v_stride + kvh * D + dc * 8);
-          *reinterpret_cast<uint4 *>(vals[i]) = v;
-        }
-        const int slot = vt_slot(quad * 4);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          uint2 w;
-          w.x = (uint32_t)vals[0][e] | ((uint32_t)vals[1][e] << 16);
-          w.y = (uint32_t)vals[2][e] | ((uint32_t)vals[3][e] << 16);
-          *reinterpret_cast<uint2 *>(&sm.vt[dc * 8 + e][slot]) = w;
-        }
-      }
-    }
-    if (tid < KT) {
-      const int kp = t0 + tid;
-      sm.ok[tid] = (kp < kend) && (p.key_ok == nullptr || p.key_ok[kp]);
-    }
+    const bool more = t0 + KT < kend;
+    if (more) load_tile(t0 + KT);
+    const bool masked = (!PV && p.key_ok != nullptr) || t0 + KT > kend || t0 + KT - 1 > minpos;
+    subtile(buf, 0, t0, masked);
+    subtile(buf, 1, t0, masked);
+    if (more) store_tile(buf ^ 1);
     __syncthreads();
-
-    // ---- S^T = K Q^T for two 32-key sub-tiles x two pair tiles ----
-    f32x16 s[2][2];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      s[sub][0] = f32x16{};
-      s[sub][1] = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4 *>(&sm.k[sub * 32 + col][ks * 16 + 8 * half]));
-        s[sub][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[0][ks], s[sub][0], 0, 0, 0);
-        s[sub][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[1][ks], s[sub][1], 0, 0, 0);
-      }
-    }
-
-    // ---- online softmax, in-lane over 32 keys per pair column ----
-    bf16x8 pk[2][2][2];  // [sub][nt][ks] probabilities as PV operands
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      float mx = kNegInf;
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int kl = sub * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-          const bool ok = sm.ok[kl] && (t0 + kl <= rp[nt]);
-          const float z = ok ? s[sub][nt][v] * p.scale_log2 : kNegInf;
-          s[sub][nt][v] = z;
-          mx = fmaxf(mx, z);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m[nt], mx);
-      const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-      const float alpha = fast_exp2(m[nt] - m_use);
-      float psum = 0.f;
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float e = fast_exp2(s[sub][nt][v] - m_use);
-          s[sub][nt][v] = e;
-          psum += e;
-        }
-        if constexpr (PV) {
-#pragma unroll
-          for (int ks = 0; ks < 2; ++ks) {
-            bf16x8 b;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) b[e] = static_cast<__bf16>(s[sub][nt][8 * ks + e]);
-            pk[sub][nt][ks] = b;
-          }
-        }
-      }
-      l[nt] = l[nt] * alpha + psum;
-      m[nt] = m_new;
-      if constexpr (PV) {
-        if (alpha != 1.f) {
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[nt][dt] *= alpha;
-        }
-      }
-    }
-
-    // ---- O^T += V^T P^T ----
-    if constexpr (PV) {
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-            const bf16x8 a = as_bf16x8(
-                *reinterpret_cast<const uint4 *>(&sm.vt[dt * 32 + col][sub * 32 + ks * 16 + 8 * half]));
-            o[0][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pk[sub][0][ks], o[0][dt], 0, 0, 0);
-            o[1][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pk[sub][1][ks], o[1][dt], 0, 0, 0);
-          }
-    }
+    buf ^= 1;
   }
 
   // ---- write this split's partials ----
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
-#pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    const float l_tot = l[nt] + __shfl_xor(l[nt], 32, 64);
-    if (!valid[nt]) continue;
-    const int64_t idx = (int64_t)split * n_gp + gpair[nt];
+  const float l_tot = l + __shfl_xor(l, 32, 64);
+  if (valid) {
+    const int64_t idx = (int64_t)split * n_gp + gpair;
     if (half == 0) {
-      p.part_m[idx] = m[nt];
+      p.part_m[idx] = m;
       p.part_l[idx] = l_tot;
     }
     if constexpr (PV) {
@@ -242,7 +279,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          f32x4 w = {o[nt][dt][4 * g], o[nt][dt][4 * g + 1], o[nt][dt][4 * g + 2], o[nt][dt][4 * g + 3]};
+          f32x4 w = {o[dt][4 * g], o[dt][4 * g + 1], o[dt][4 * g + 2], o[dt][4 * g + 3]};
           *reinterpret_cast<f32x4 *>(dst + dt * 32 + 8 * g + 4 * half) = w;
         }
     }

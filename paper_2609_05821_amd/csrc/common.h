@@ -11,6 +11,7 @@ typedef uint16_t u16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // 16-byte register moves
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -27,7 +28,12 @@ struct ImageTable {
 // ---------------------------------------------------------------------------
 // Device helpers
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+template <typename T>
+__device__ __forceinline__ u32x4 ld16(const T *p) { return *reinterpret_cast<const u32x4 *>(p); }
+template <typename T>
+__device__ __forceinline__ void st16(T *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
 
 __device__ __forceinline__ float bf16_to_f32(u16 b) {
   return __builtin_bit_cast(float, static_cast<uint32_t>(b) << 16);
@@ -72,7 +78,7 @@ struct AttnParams {
   int32_t n_rows;
   const int32_t *row_pos;   // nullable: row r sits at q_pos0 + r
   int32_t q_pos0;
-  const uint8_t *key_ok;    // nullable: key-domain filter (visual-only scoring)
+  const uint8_t *key_ok;    // nullable: key-domain filter (statistics variant only)
   float scale_log2;         // logit scale * log2(e)
   int32_t chunk;            // keys per split (multiple of the key tile)
   int32_t n_split;

@@ -18,18 +18,12 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterParams p) {
   const char *ksrc = static_cast<const char *>(p.k_new) + (int64_t)row * p.row_bytes;
   const char *vsrc = static_cast<const char *>(p.v_new) + (int64_t)row * p.row_bytes;
   for (int c = lane; c < nch; c += 64) {
-    const uint4 kn = reinterpret_cast<const uint4 *>(ksrc)[c];
-    const uint4 vn = reinterpret_cast<const uint4 *>(vsrc)[c];
-    if (p.k_old) {
-      reinterpret_cast<uint4 *>(static_cast<char *>(p.k_old) + (int64_t)row * p.row_bytes)[c] =
-          reinterpret_cast<const uint4 *>(kdst)[c];
-    }
-    if (p.v_old) {
-      reinterpret_cast<uint4 *>(static_cast<char *>(p.v_old) + (int64_t)row * p.row_bytes)[c] =
-          reinterpret_cast<const uint4 *>(vdst)[c];
-    }
-    reinterpret_cast<uint4 *>(kdst)[c] = kn;
-    reinterpret_cast<uint4 *>(vdst)[c] = vn;
+    const u32x4 kn = ld16(ksrc + 16 * c);
+    const u32x4 vn = ld16(vsrc + 16 * c);
+    if (p.k_old) st16(static_cast<char *>(p.k_old) + (int64_t)row * p.row_bytes + 16 * c, ld16(kdst + 16 * c));
+    if (p.v_old) st16(static_cast<char *>(p.v_old) + (int64_t)row * p.row_bytes + 16 * c, ld16(vdst + 16 * c));
+    st16(kdst + 16 * c, kn);
+    st16(vdst + 16 * c, vn);
   }
 }
 

@@ -40,8 +40,8 @@ template <int D>
 __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParams p) {
   constexpr int KS = D / 16;
   constexpr int QCH = 32 * D / 8;       // 16-byte chunks in a 32-row Q block
-  __shared__ u16 qs[2][32][D + 8];
-  __shared__ float bs[2][32];
+  __shared__ alignas(16) u16 qs[2][32][D + 8];
+  __shared__ alignas(16) float bs[2][32];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
@@ -61,18 +61,18 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     const u16 *krow = Kg + (int64_t)(tvalid ? p.vis_pos[t] : 0) * p.k_stride + kvh * D + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      kreg[ks] = as_bf16x8(tvalid ? *reinterpret_cast<const uint4 *>(krow + ks * 16) : make_uint4(0, 0, 0, 0));
+      kreg[ks] = as_bf16x8(tvalid ? ld16(krow + ks * 16) : u32x4{0, 0, 0, 0});
   }
 
   // Cooperative load of row block `blk` (32 (span token, head) rows).
-  auto load_q = [&](int blk, uint4 &qv, float &bv) {
+  auto load_q = [&](int blk, u32x4 &qv, float &bv) {
     if (tid < QCH) {
       const int row = tid / (D / 8), dc = tid % (D / 8);
       const int pr = blk * 32 + row;
-      qv = make_uint4(0, 0, 0, 0);
+      qv = u32x4{0, 0, 0, 0};
       if (pr < n_pair) {
         const int i = pr / G, hq = kvh * G + pr % G;
-        qv = *reinterpret_cast<const uint4 *>(Qg + ((int64_t)i * p.n_q_heads + hq) * D + dc * 8);
+        qv = ld16(Qg + ((int64_t)i * p.n_q_heads + hq) * D + dc * 8);
       }
     }
     if (tid < 32) {
@@ -81,12 +81,12 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
       if (pr < n_pair) bv = p.row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
     }
   };
-  auto store_q = [&](int buf, const uint4 &qv, float bv) {
-    if (tid < QCH) *reinterpret_cast<uint4 *>(&qs[buf][tid / (D / 8)][(tid % (D / 8)) * 8]) = qv;
+  auto store_q = [&](int buf, const u32x4 &qv, float bv) {
+    if (tid < QCH) st16(&qs[buf][tid / (D / 8)][(tid % (D / 8)) * 8], qv);
     if (tid < 32) bs[buf][tid] = bv;
   };
 
-  uint4 qv = make_uint4(0, 0, 0, 0);
+  u32x4 qv = u32x4{0, 0, 0, 0};
   float bv = kInf;
   load_q(0, qv, bv);
   store_q(0, qv, bv);
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     f32x16 acc = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4 *>(&qs[buf][col][ks * 16 + 8 * half]));
+      const bf16x8 a = as_bf16x8(ld16(&qs[buf][col][ks * 16 + 8 * half]));
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kreg[ks], acc, 0, 0, 0);
     }
     // lane (col, half), register v holds row 8*(v/4) + 4*half + v%4
@@ -124,8 +124,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
       const u16 *vrow = Vg + (int64_t)p.vis_pos[tv] * p.v_stride + kvh * D + part * (D / 2);
 #pragma unroll
       for (int c = 0; c < D / 16; ++c) {
-        const uint4 w = *reinterpret_cast<const uint4 *>(vrow + c * 8);
-        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+        const u32x4 ws = ld16(vrow + c * 8);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float lo = __builtin_bit_cast(float, ws[e] << 16);
