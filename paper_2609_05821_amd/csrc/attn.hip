@@ -132,8 +132,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
       rk[i] = ld16(Kg + (int64_t)kp * p.k_stride + kvh * D + dc * 8);
     }
     if constexpr (PV) {
+      // kpair fastest: each half-wave later writes 32 different keys of one
+      // V^T row, i.e. 32 different LDS banks
       if (Regs::VIT >= kThreads || tid < Regs::VIT) {
-        const int dc = tid % (D / 8), kpair = tid / (D / 8);
+        const int kpair = tid % (KT / 2), dc = tid / (KT / 2);
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
           const int kp = min(t0 + kpair * 2 + i, kend - 1);
@@ -154,7 +156,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
     }
     if constexpr (PV) {
       if (Regs::VIT >= kThreads || tid < Regs::VIT) {
-        const int dc = tid % (D / 8), kpair = tid / (D / 8);
+        const int kpair = tid % (KT / 2), dc = tid / (KT / 2);
         const int slot = vt_slot(kpair * 2);
         const u32x4 w0 = rv[0], w1 = rv[1];
 #pragma unroll
