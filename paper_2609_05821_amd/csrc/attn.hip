@@ -26,6 +26,7 @@ constexpr int kWaves = 8;                  // two waves per SIMD
 constexpr int kThreads = kWaves * 64;
 constexpr int KT = kAttnKeyTile;
 constexpr float kNegInf = -__builtin_inff();
+constexpr float kMInit = -1e30f;  // initial running maximum (log2 units)
 static_assert(kWaves * 32 == kAttnPairsPerBlock, "one 32-column pair tile per wave");
 
 template <int D>
@@ -120,26 +121,50 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
       qreg[ks] = as_bf16x8(valid ? ld16(qrow + ks * 16) : u32x4{0, 0, 0, 0});
   }
 
+  // Per-thread offsets of its staging chunks inside a key tile; a tile's
+  // base moves by KT rows, and only a partial last tile clamps its rows.
+  int64_t koff[Regs::KCH], voff[2];
+#pragma unroll
+  for (int i = 0; i < Regs::KCH; ++i) {
+    const int cidx = tid + kThreads * i;
+    koff[i] = (int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8;
+  }
+  const int v_kpair = tid % (KT / 2), v_dc = tid / (KT / 2);
+  const bool v_active = Regs::VIT >= kThreads || tid < Regs::VIT;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) voff[i] = (int64_t)(v_kpair * 2 + i) * p.v_stride + kvh * D + v_dc * 8;
+
   u32x4 rk[Regs::KCH];
   u32x4 rv[PV ? 2 : 1];
   bool rok = false;
   auto load_tile = [&](int t0) __attribute__((always_inline)) {
+    const u16 *kb = Kg + (int64_t)t0 * p.k_stride;
+    const u16 *vb = Vg + (int64_t)t0 * p.v_stride;
+    if (t0 + KT <= kend) {
 #pragma unroll
-    for (int i = 0; i < Regs::KCH; ++i) {
-      const int cidx = tid + kThreads * i;
-      const int key = cidx / (D / 8), dc = cidx % (D / 8);
-      const int kp = min(t0 + key, kend - 1);  // rows past kend are masked
-      rk[i] = ld16(Kg + (int64_t)kp * p.k_stride + kvh * D + dc * 8);
-    }
-    if constexpr (PV) {
-      // kpair fastest: each half-wave later writes 32 different keys of one
-      // V^T row, i.e. 32 different LDS banks
-      if (Regs::VIT >= kThreads || tid < Regs::VIT) {
-        const int kpair = tid % (KT / 2), dc = tid / (KT / 2);
+      for (int i = 0; i < Regs::KCH; ++i) rk[i] = ld16(kb + koff[i]);
+      if constexpr (PV) {
+        // kpair fastest: each half-wave later writes 32 different keys of
+        // one V^T row, i.e. 32 different LDS banks
+        if (v_active) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const int kp = min(t0 + kpair * 2 + i, kend - 1);
-          rv[i] = ld16(Vg + (int64_t)kp * p.v_stride + kvh * D + dc * 8);
+          for (int i = 0; i < 2; ++i) rv[i] = ld16(vb + voff[i]);
+        }
+      }
+    } else {  // partial tile: rows past kend repeat the last row (masked later)
+#pragma unroll
+      for (int i = 0; i < Regs::KCH; ++i) {
+        const int cidx = tid + kThreads * i;
+        const int kp = min(t0 + cidx / (D / 8), kend - 1);
+        rk[i] = ld16(Kg + (int64_t)kp * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
+      }
+      if constexpr (PV) {
+        if (v_active) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            const int kp = min(t0 + v_kpair * 2 + i, kend - 1);
+            rv[i] = ld16(Vg + (int64_t)kp * p.v_stride + kvh * D + v_dc * 8);
+          }
         }
       }
     }
@@ -155,16 +180,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
       st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
     }
     if constexpr (PV) {
-      if (Regs::VIT >= kThreads || tid < Regs::VIT) {
-        const int kpair = tid % (KT / 2), dc = tid / (KT / 2);
-        const int slot = vt_slot(kpair * 2);
+      if (v_active) {
+        const int slot = vt_slot(v_kpair * 2);
         const u32x4 w0 = rv[0], w1 = rv[1];
 #pragma unroll
         for (int e2 = 0; e2 < 4; ++e2) {
           // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
-          *reinterpret_cast<uint32_t *>(&sm.vt[buf][dc * 8 + 2 * e2][slot]) =
+          *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc * 8 + 2 * e2][slot]) =
               (w0[e2] & 0xffffu) | (w1[e2] << 16);
-          *reinterpret_cast<uint32_t *>(&sm.vt[buf][dc * 8 + 2 * e2 + 1][slot]) =
+          *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc * 8 + 2 * e2 + 1][slot]) =
               (w0[e2] >> 16) | (w1[e2] & 0xffff0000u);
         }
       }
@@ -175,32 +199,30 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
     }
   };
 
-  float m = kNegInf, l = 0.f;
+  // Running maximum (log2 units) starts finite, so exp2(c*s - m) needs no
+  // special case: masked logits are -inf and give 0; the first valid
+  // sub-tile always moves m.
+  float m = kMInit, l = 0.f;
   f32x16 o[DT];
   if constexpr (PV) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
   }
 
-  // One 32-key sub-tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
-  auto subtile = [&](int buf, int sub, int t0, bool masked) __attribute__((always_inline)) {
+  // S^T of one 32-key sub-tile: K operands from LDS, 8 chained MFMAs.
+  auto scores = [&](int buf, int sub) __attribute__((always_inline)) {
     bf16x8 ka[KS];
     const u16 *krow = &sm.k[buf][sub * 32 + col][8 * half];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) ka[ks] = as_bf16x8(ld16(krow + ks * 16));
-    f32x16 s = f32x16{};
+    f32x16 sc = f32x16{};
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qreg[ks], s, 0, 0, 0);
-    // V^T operands of this sub-tile load while the softmax runs.
-    bf16x8 va[2][DT];
-    if constexpr (PV) {
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          va[ks][dt] = as_bf16x8(
-              ld16(&sm.vt[buf][dt * 32 + col][sub * 32 + ks * 16 + 8 * half]));
-    }
+    for (int ks = 0; ks < KS; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qreg[ks], sc, 0, 0, 0);
+    return sc;
+  };
+
+  // Online softmax of one sub-tile, then O^T += V^T P^T.
+  auto softmax_pv = [&](f32x16 sc, int buf, int sub, int t0, bool masked) __attribute__((always_inline)) {
     if (masked) {  // branch-free: causal / split end and the key domain
       const int lim = min(kend - 1, rp) - t0;  // last visible key of the tile
 #pragma unroll
@@ -211,46 +233,58 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
           const uint64_t dom = p.key_ok ? sm.okmask[buf] : ~0ull;
           ok = ok & (((dom >> kl) & 1ull) != 0);
         }
-        s[v] = ok ? s[v] : kNegInf;
+        sc[v] = ok ? sc[v] : kNegInf;
       }
     }
     float mx = kNegInf;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[v]);
+    mx = half_max(mx) * c;
     const bool grow = mx > m + kRescaleSlack;
-    const float m_new = grow ? mx : m;
-    const float alpha = grow ? fast_exp2(m - m_new) : 1.f;
-    m = m_new;
-    const float neg_m = (m_new == kNegInf) ? 0.f : -m_new;
-    float psum = 0.f;
+    const float alpha = grow ? fast_exp2(m - mx) : 1.f;
+    m = grow ? mx : m;
+    const float neg_m = -m;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const float e = fast_exp2(fmaf(s[v], c, neg_m));
-      s[v] = e;
-      psum += e;
-    }
-    l = l * alpha + psum;
+    for (int v = 0; v < 16; ++v) sc[v] = fast_exp2(fmaf(sc[v], c, neg_m));
     if constexpr (PV) {
       bf16x8 pk[2];
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pk[ks][e] = static_cast<__bf16>(s[8 * ks + e]);
+        for (int e = 0; e < 8; ++e) pk[ks][e] = static_cast<__bf16>(sc[8 * ks + e]);
+      // fp32 row sum (the log-sum-exp output needs it to 1e-4; summing the
+      // bf16-rounded probabilities is off by up to 2^-9 when few terms dominate)
+      float psum = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) psum += sc[v];
+      l = l * alpha + psum;
       if (__ballot(grow)) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
       }
+      bf16x8 va[2][DT];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          va[ks][dt] = as_bf16x8(ld16(&sm.vt[buf][dt * 32 + col][sub * 32 + ks * 16 + 8 * half]));
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][dt], pk[ks], o[dt], 0, 0, 0);
+    } else {
+      float psum = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) psum += sc[v];
+      l = l * alpha + psum;
     }
   };
 
   // Double-buffered main loop: the next tile's global loads are in flight
-  // while the current tile computes; one barrier per tile.
+  // while the current tile computes; one barrier per tile.  Both sub-tiles'
+  // S^T MFMAs are issued before the first softmax, so the VALU work of one
+  // sub-tile runs while the matrix core still works on the other.
   load_tile(kbeg);
   store_tile(0);
   __syncthreads();
@@ -259,8 +293,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
     const bool more = t0 + KT < kend;
     if (more) load_tile(t0 + KT);
     const bool masked = (!PV && p.key_ok != nullptr) || t0 + KT > kend || t0 + KT - 1 > minpos;
-    subtile(buf, 0, t0, masked);
-    subtile(buf, 1, t0, masked);
+    const f32x16 s0 = scores(buf, 0);
+    const f32x16 s1 = scores(buf, 1);
+    softmax_pv(s0, buf, 0, t0, masked);
+    softmax_pv(s1, buf, 1, t0, masked);
     if (more) store_tile(buf ^ 1);
     __syncthreads();
     buf ^= 1;
@@ -308,7 +344,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < ns; ++s) {
     const float ms = p.part_m[s * n_gp + gp];
-    const float w = (ms == kNegInf) ? 0.f : fast_exp2(ms - M);
+    const float w = fast_exp2(ms - M);  // m >= kMInit is finite
     L += w * p.part_l[s * n_gp + gp];
     if (values) acc += w * *reinterpret_cast<const f32x4 *>(p.part_o + (s * n_gp + gp) * D + 4 * c);
   }
