@@ -52,6 +52,32 @@ __device__ int block_exclusive_scan(int x, int *s_wave, int &total) {
   return excl;
 }
 
+// Bitwise AND / OR of one value per thread over the block (every thread
+// gets the result).
+__device__ uint32_t block_and(uint32_t x, int *s_wave) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x &= __shfl_xor(x, o, 64);
+  if (lane == 0) s_wave[w] = (int)x;
+  __syncthreads();
+  uint32_t r = 0xffffffffu;
+  for (int i = 0; i < kWaves; ++i) r &= (uint32_t)s_wave[i];
+  __syncthreads();
+  return r;
+}
+
+__device__ uint32_t block_or(uint32_t x, int *s_wave) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x |= __shfl_xor(x, o, 64);
+  if (lane == 0) s_wave[w] = (int)x;
+  __syncthreads();
+  uint32_t r = 0;
+  for (int i = 0; i < kWaves; ++i) r |= (uint32_t)s_wave[i];
+  __syncthreads();
+  return r;
+}
+
 __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, ImageTable tbl) {
   __shared__ float s_g[kMaxImages];
   __shared__ float s_c[kMaxImages];
@@ -175,6 +201,227 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Ima
   }
 }
 
+// Register-resident variant for n_vis <= 1024 * PER: thread t owns visual
+// tokens [t*PER, t*PER + PER), so scores are read once and the compaction is
+// in index order without re-reading.  The radix select first fixes the bits
+// every key shares (block AND/OR), then resolves the rest 11 bits per pass
+// with one shared 2,048-bin LDS histogram: below the shared prefix the
+// digits spread over the varying exponent and high mantissa bits, so LDS
+// atomics rarely collide.
+template <int PER>
+__global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p, ImageTable tbl) {
+  constexpr int kBits = 11, kBins = 1 << kBits;
+  __shared__ float s_g[kMaxImages];
+  __shared__ float s_c[kMaxImages];
+  __shared__ int s_off[kMaxImages + 1];
+  __shared__ int s_delta[kMaxImages];  // position - visual index, per image
+  __shared__ int hist[kBins];
+  __shared__ int s_wave[kWaves];
+  __shared__ int s_bin, s_above;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = tbl.n_vis, K = tbl.n_images;
+  const float n_layers = (float)p.n_layers;
+  const float inv_layers = 1.f / n_layers;
+
+  // The image table moves to LDS (per-lane lookups would otherwise be
+  // dependent loads from the kernel-argument segment).
+  for (int j = tid; j <= K; j += kSelThreads) {
+    s_off[j] = tbl.off[j];
+    if (j < K) s_delta[j] = tbl.pos[j] - tbl.off[j];
+  }
+  // This thread's tokens [lo, lo + cnt): their scores load while the
+  // per-image means are computed.
+  const int lo = min(n, tid * PER), cnt = min(n, lo + PER) - lo;
+  const bool whole = cnt == PER;
+  float sv[PER];
+  if (whole) {  // 16-byte loads, all in flight at once
+#pragma unroll
+    for (int e = 0; e < PER; e += 4) {
+      const f32x4 v4 = *reinterpret_cast<const f32x4 *>(p.s_acc + lo + e);
+      sv[e] = v4[0];
+      sv[e + 1] = v4[1];
+      sv[e + 2] = v4[2];
+      sv[e + 3] = v4[3];
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < PER; ++e) sv[e] = e < cnt ? p.s_acc[lo + e] : 0.f;
+  }
+  __syncthreads();
+
+  // 1. per-image mean attention (one wave per image, fixed-order sums)
+  for (int j = wave; j < K; j += kWaves) {
+    const int a = s_off[j], b = s_off[j + 1];
+    float tot = 0.f;
+    for (int t0 = a; t0 < b; t0 += 16 * 64) {  // 16 independent loads per round
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int t = t0 + 64 * u + lane;
+        v[u] = t < b ? p.a_acc[t] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) tot += v[u];
+    }
+    tot = wave_sum(tot);
+    if (lane == 0) s_g[j] = tot / (n_layers * (float)(b - a));
+  }
+  __syncthreads();
+  // 2. coefficients: (1 - lambda) + lambda * g_j / g_bar, exactly 1 at g_j = g_bar
+  if (wave == 0) {
+    float acc = 0.f;
+    for (int j = lane; j < K; j += 64) acc += s_g[j];
+    const float g_bar = wave_sum(acc) / (float)K;
+    for (int j = lane; j < K; j += 64) {
+      const float x = s_g[j] / g_bar;
+      const float c = (g_bar == 0.f || x == 1.f) ? 1.f : (1.f - p.lambda) + p.lambda * x;
+      s_c[j] = c;
+      if (p.c_out) p.c_out[j] = c;
+    }
+  }
+  __syncthreads();
+
+  // 3. composite scores (s / |L|) * c_pi(t) of this thread's tokens
+  int j0 = 0;  // image of the first token
+  if (cnt > 0) {
+    int a = 0, b = K - 1;
+    while (a < b) {
+      const int mid = (a + b + 1) >> 1;
+      if (s_off[mid] <= lo) a = mid; else b = mid - 1;
+    }
+    j0 = a;
+  }
+  uint32_t key[PER];
+  {
+    int j = j0, next = s_off[j0 + 1];
+    float c = s_c[j0];
+    float sh[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      if (e < cnt) {
+        while (lo + e >= next) {
+          ++j;
+          next = s_off[j + 1];
+          c = s_c[j];
+        }
+      }
+      sh[e] = (sv[e] * inv_layers) * c;
+      key[e] = order_key(sh[e]);
+    }
+    if (p.shat) {
+      if (whole) {
+#pragma unroll
+        for (int e = 0; e < PER; e += 4)
+          *reinterpret_cast<f32x4 *>(p.shat + lo + e) = f32x4{sh[e], sh[e + 1], sh[e + 2], sh[e + 3]};
+      } else {
+#pragma unroll
+        for (int e = 0; e < PER; ++e)
+          if (e < cnt) p.shat[lo + e] = sh[e];
+      }
+    }
+  }
+
+  // 4. radix select of the k-th largest key
+  uint32_t k_and = 0xffffffffu, k_or = 0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e)
+    if (e < cnt) {
+      k_and &= key[e];
+      k_or |= key[e];
+    }
+  k_and = block_and(k_and, s_wave);
+  k_or = block_or(k_or, s_wave);
+  const uint32_t varying = k_and ^ k_or;  // bits that differ between keys
+  uint32_t prefix = k_and, pmask = 0xffffffffu;
+  int kk = p.k;
+  if (varying) {
+    const int top = 31 - __builtin_clz(varying);
+    pmask = top == 31 ? 0u : ~((2u << top) - 1u);  // shared high bits
+    prefix = k_and & pmask;
+    for (int hi = top; hi >= 0; hi -= kBits) {  // digit = bits hi .. hi-10 (fewer at the end)
+      const int sh = hi - (kBits - 1);
+      for (int b = tid; b < kBins; b += kSelThreads) hist[b] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < PER; ++e)
+        if (e < cnt && (key[e] & pmask) == prefix)
+          atomicAdd(&hist[(sh >= 0 ? key[e] >> sh : key[e] << (-sh)) & (kBins - 1)], 1);
+      __syncthreads();
+      // thread tid owns bins kBins-1-2*tid, kBins-2-2*tid (descending)
+      const int b0 = kBins - 1 - 2 * tid;
+      const int h0 = hist[b0], h1 = hist[b0 - 1];
+      int total;
+      const int run = block_exclusive_scan(h0 + h1, s_wave, total);
+      if (run < kk && run + h0 >= kk) {
+        s_bin = b0;
+        s_above = run;
+      } else if (run + h0 < kk && run + h0 + h1 >= kk) {
+        s_bin = b0 - 1;
+        s_above = run + h0;
+      }
+      __syncthreads();
+      if (sh >= 0) {
+        prefix |= (uint32_t)s_bin << sh;
+        pmask |= (uint32_t)(kBins - 1) << sh;
+      } else {  // last, partial digit
+        prefix |= (uint32_t)s_bin >> (-sh);
+        pmask |= (uint32_t)(kBins - 1) >> (-sh);
+      }
+      kk -= s_above;
+    }
+  }
+  const uint32_t tau = prefix;
+  const int need_eq = kk;  // entries equal to tau to take, lowest indices first
+
+  // 5. ordered compaction
+  int gt = 0, eq = 0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    gt += (e < cnt) && key[e] > tau;
+    eq += (e < cnt) && key[e] == tau;
+  }
+  int total;
+  const int eq_before = block_exclusive_scan(eq, s_wave, total);
+  const int take_eq = max(0, min(eq, need_eq - eq_before));
+  int out = block_exclusive_scan(gt + take_eq, s_wave, total);
+  int j = j0, next = cnt > 0 ? s_off[j0 + 1] : 0, delta = cnt > 0 ? s_delta[j0] : 0, eq_seen = 0;
+  uint32_t mword[(PER + 3) / 4] = {};
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    if (e < cnt) {
+      const int t = lo + e;
+      while (t >= next) {
+        ++j;
+        next = s_off[j + 1];
+        delta = s_delta[j];
+      }
+      bool sel = key[e] > tau;
+      if (key[e] == tau) {
+        sel = eq_seen < take_eq;
+        ++eq_seen;
+      }
+      mword[e >> 2] |= (sel ? 1u : 0u) << (8 * (e & 3));
+      if (sel && out < p.k) {
+        p.idx_out[out] = t;
+        p.pos_out[out] = t + delta;
+        ++out;
+      }
+    }
+  }
+  if (p.mask_out) {
+    if (whole && (reinterpret_cast<uintptr_t>(p.mask_out) & 15) == 0 && PER % 16 == 0) {
+#pragma unroll
+      for (int w = 0; w < PER / 4; w += 4)
+        *reinterpret_cast<u32x4 *>(p.mask_out + lo + 4 * w) = u32x4{mword[w], mword[w + 1], mword[w + 2], mword[w + 3]};
+    } else {
+#pragma unroll
+      for (int e = 0; e < PER; ++e)
+        if (e < cnt) p.mask_out[lo + e] = (mword[e >> 2] >> (8 * (e & 3))) & 1u;
+    }
+  }
+}
+
 __global__ void clear_u8_kernel(uint8_t *p, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0;
@@ -183,7 +430,9 @@ __global__ void clear_u8_kernel(uint8_t *p, int64_t n) {
 }  // namespace
 
 hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream_t s) {
-  select_kernel<<<1, kSelThreads, 0, s>>>(p, tbl);
+  if (tbl.n_vis <= kSelThreads * 16) select_regs_kernel<16><<<1, kSelThreads, 0, s>>>(p, tbl);
+  else if (tbl.n_vis <= kSelThreads * 32) select_regs_kernel<32><<<1, kSelThreads, 0, s>>>(p, tbl);
+  else select_kernel<<<1, kSelThreads, 0, s>>>(p, tbl);
   return hipGetLastError();
 }
 
