@@ -102,8 +102,9 @@ conduit_status check_images(const conduit_images *img, int64_t limit, ImageTable
 // Key-split size for the attention kernel: enough workgroups to fill the
 // chip, each split a whole number of 64-key tiles.
 int32_t attn_chunk(int64_t n_rows, int32_t group, int32_t n_kv_heads, int64_t key_span,
-                   int64_t target_blocks, int64_t min_chunk) {
-  const int64_t pair_blocks = (n_rows * group + kAttnPairsPerBlock - 1) / kAttnPairsPerBlock;
+                   int64_t target_blocks, int64_t min_chunk, bool with_values) {
+  const int64_t ppb = attn_pairs_per_block(with_values);
+  const int64_t pair_blocks = (n_rows * group + ppb - 1) / ppb;
   const int64_t base = pair_blocks * n_kv_heads;
   int64_t splits = (target_blocks + base - 1) / base;
   if (splits < 1) splits = 1;
@@ -121,7 +122,7 @@ ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis, int32
   ScoreLayout L{};
   const int64_t rows = (int64_t)n_q * kv->n_q_heads;
   const bool bf16 = kv->dtype == CONDUIT_BF16;
-  L.chunk = attn_chunk(n_q, kv->n_q_heads / kv->n_kv_heads, kv->n_kv_heads, key_span, 512, 64);
+  L.chunk = attn_chunk(n_q, kv->n_q_heads / kv->n_kv_heads, kv->n_kv_heads, key_span, 512, 64, false);
   L.n_split = (key_span + L.chunk - 1) / L.chunk;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
@@ -145,7 +146,7 @@ RefreshLayout refresh_layout(const conduit_kv *kv, int32_t k) {
   RefreshLayout L{};
   if (kv->dtype != CONDUIT_BF16 || k <= 0) return L;
   const int64_t rows = (int64_t)k * kv->n_q_heads;
-  L.chunk = attn_chunk(k, kv->n_q_heads / kv->n_kv_heads, kv->n_kv_heads, kv->n_ctx, 1024, 256);
+  L.chunk = attn_chunk(k, kv->n_q_heads / kv->n_kv_heads, kv->n_kv_heads, kv->n_ctx, 1024, 256, true);
   L.n_split = (kv->n_ctx + L.chunk - 1) / L.chunk;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };

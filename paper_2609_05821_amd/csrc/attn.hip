@@ -22,12 +22,9 @@
 namespace conduit {
 namespace {
 
-constexpr int kWaves = 8;                  // two waves per SIMD
-constexpr int kThreads = kWaves * 64;
 constexpr int KT = kAttnKeyTile;
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kMInit = -1e30f;  // initial running maximum (log2 units)
-static_assert(kWaves * 32 == kAttnPairsPerBlock, "one 32-column pair tile per wave");
 
 template <int D>
 struct AttnSmem {
@@ -52,10 +49,12 @@ __device__ __forceinline__ int vt_slot(int kl) {
 }
 
 // Global -> register staging of one key tile (issued a tile ahead).
-template <int D, bool PV>
+template <int D, bool PV, int W>
 struct TileRegs {
+  static constexpr int kThreads = W * 64;
   static constexpr int KCH = KT * D / 8 / kThreads;    // 16-byte K chunks per thread
   static constexpr int VIT = (KT / 2) * (D / 8);       // 2-key x 8-dim V items
+  static constexpr int VPT = VIT >= kThreads ? VIT / kThreads : 1;  // items per thread
   u32x4 k[KCH];
   u32x4 v[PV ? 2 : 1];
   uint8_t ok;
@@ -66,20 +65,25 @@ struct TileRegs {
 // rescaled rarely.  Exact: O, l and the final normaliser share the reference.
 constexpr float kRescaleSlack = 8.f;
 
-template <int D, bool PV>
-__global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
+// W waves per workgroup, each owning 32 (row, head) pair columns.  With
+// values (refresh) W = 8: two waves per SIMD and 256 pairs sharing each K/V
+// tile; statistics only W = 4 with two workgroups per CU.
+template <int D, bool PV, int W>
+__global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) {
+  constexpr int kThreads = W * 64;
   constexpr int KS = D / 16;   // MFMA k-steps over the head dimension
   constexpr int DT = D / 32;   // 32-row tiles of O^T
-  using Regs = TileRegs<D, PV>;
+  using Regs = TileRegs<D, PV, W>;
   __shared__ AttnSmem<D> sm;
 
   // Blocks of later rows see more keys: launch them first.
+  constexpr int kPairs = W * 32;  // (row, head) pairs per workgroup
   const int split = blockIdx.x, pb = gridDim.y - 1 - blockIdx.y, kvh = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int col = lane & 31, half = lane >> 5;
   const int G = p.group;
   const int n_pairs = p.n_rows * G;
-  const int pair0 = pb * kAttnPairsPerBlock;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 31, half = lane >> 5;
+  const int pair0 = pb * kPairs;
 
   // Position range of this block's rows bounds its keys and its masking.
   if (tid == 0) {
@@ -89,7 +93,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
   __syncthreads();
   {
     const int r_first = pair0 / G;
-    const int r_last = (min(pair0 + kAttnPairsPerBlock, n_pairs) - 1) / G;
+    const int r_last = (min(pair0 + kPairs, n_pairs) - 1) / G;
     for (int r = r_first + tid; r <= r_last; r += kThreads) {
       const int rp = row_position(p.row_pos, p.q_pos0, r);
       atomicMax(&sm.maxpos, rp);
@@ -123,19 +127,30 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
 
   // Per-thread offsets of its staging chunks inside a key tile; a tile's
   // base moves by KT rows, and only a partial last tile clamps its rows.
-  int64_t koff[Regs::KCH], voff[2];
+  int64_t koff[Regs::KCH];
 #pragma unroll
   for (int i = 0; i < Regs::KCH; ++i) {
     const int cidx = tid + kThreads * i;
     koff[i] = (int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8;
   }
-  const int v_kpair = tid % (KT / 2), v_dc = tid / (KT / 2);
+  // V items: item = tid + kThreads * i; key pair fastest, so each half-wave
+  // later writes 32 different keys of one V^T row (32 different LDS banks).
+  constexpr int VPT = Regs::VPT;
   const bool v_active = Regs::VIT >= kThreads || tid < Regs::VIT;
+  int v_kpair[VPT], v_dc[VPT];
+  int64_t voff[VPT][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) voff[i] = (int64_t)(v_kpair * 2 + i) * p.v_stride + kvh * D + v_dc * 8;
+  for (int it = 0; it < VPT; ++it) {
+    const int item = tid + kThreads * it;
+    v_kpair[it] = item % (KT / 2);
+    v_dc[it] = item / (KT / 2);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      voff[it][i] = (int64_t)(v_kpair[it] * 2 + i) * p.v_stride + kvh * D + v_dc[it] * 8;
+  }
 
   u32x4 rk[Regs::KCH];
-  u32x4 rv[PV ? 2 : 1];
+  u32x4 rv[PV ? VPT : 1][2];
   bool rok = false;
   auto load_tile = [&](int t0) __attribute__((always_inline)) {
     const u16 *kb = Kg + (int64_t)t0 * p.k_stride;
@@ -144,11 +159,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
       for (int i = 0; i < Regs::KCH; ++i) rk[i] = ld16(kb + koff[i]);
       if constexpr (PV) {
-        // kpair fastest: each half-wave later writes 32 different keys of
-        // one V^T row, i.e. 32 different LDS banks
         if (v_active) {
 #pragma unroll
-          for (int i = 0; i < 2; ++i) rv[i] = ld16(vb + voff[i]);
+          for (int it = 0; it < VPT; ++it)
+#pragma unroll
+            for (int i = 0; i < 2; ++i) rv[it][i] = ld16(vb + voff[it][i]);
         }
       }
     } else {  // partial tile: rows past kend repeat the last row (masked later)
@@ -161,10 +176,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
       if constexpr (PV) {
         if (v_active) {
 #pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            const int kp = min(t0 + v_kpair * 2 + i, kend - 1);
-            rv[i] = ld16(Vg + (int64_t)kp * p.v_stride + kvh * D + v_dc * 8);
-          }
+          for (int it = 0; it < VPT; ++it)
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+              const int kp = min(t0 + v_kpair[it] * 2 + i, kend - 1);
+              rv[it][i] = ld16(Vg + (int64_t)kp * p.v_stride + kvh * D + v_dc[it] * 8);
+            }
         }
       }
     }
@@ -181,15 +198,18 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bf16_kernel(AttnParams p) {
     }
     if constexpr (PV) {
       if (v_active) {
-        const int slot = vt_slot(v_kpair * 2);
-        const u32x4 w0 = rv[0], w1 = rv[1];
 #pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
-          *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc * 8 + 2 * e2][slot]) =
-              (w0[e2] & 0xffffu) | (w1[e2] << 16);
-          *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc * 8 + 2 * e2 + 1][slot]) =
-              (w0[e2] >> 16) | (w1[e2] & 0xffff0000u);
+        for (int it = 0; it < VPT; ++it) {
+          const int slot = vt_slot(v_kpair[it] * 2);
+          const u32x4 w0 = rv[it][0], w1 = rv[it][1];
+#pragma unroll
+          for (int e2 = 0; e2 < 4; ++e2) {
+            // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
+            *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc[it] * 8 + 2 * e2][slot]) =
+                (w0[e2] & 0xffffu) | (w1[e2] << 16);
+            *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc[it] * 8 + 2 * e2 + 1][slot]) =
+                (w0[e2] >> 16) | (w1[e2] & 0xffff0000u);
+          }
         }
       }
     }
@@ -436,14 +456,19 @@ __global__ void lse_to_b_kernel(const float *lse, float *b, int n) {
 
 hipError_t launch_attn(const AttnParams &p, int head_dim, bool bf16, bool with_values, hipStream_t s) {
   const int n_pairs = p.n_rows * p.group;
-  dim3 grid(p.n_split, (n_pairs + kAttnPairsPerBlock - 1) / kAttnPairsPerBlock, p.n_kv_heads);
   if (!bf16) return hipErrorInvalidValue;
+  // refresh: 8 waves (256 pairs share each K/V tile); statistics: 4 waves,
+  // two workgroups per CU (many short splits)
+  const dim3 grid_v(p.n_split, (n_pairs + attn_pairs_per_block(true) - 1) / attn_pairs_per_block(true),
+                    p.n_kv_heads);
+  const dim3 grid_s(p.n_split, (n_pairs + attn_pairs_per_block(false) - 1) / attn_pairs_per_block(false),
+                    p.n_kv_heads);
   if (head_dim == 128) {
-    if (with_values) attn_bf16_kernel<128, true><<<grid, kThreads, 0, s>>>(p);
-    else attn_bf16_kernel<128, false><<<grid, kThreads, 0, s>>>(p);
+    if (with_values) attn_bf16_kernel<128, true, 8><<<grid_v, 8 * 64, 0, s>>>(p);
+    else attn_bf16_kernel<128, false, 4><<<grid_s, 4 * 64, 0, s>>>(p);
   } else {
-    if (with_values) attn_bf16_kernel<64, true><<<grid, kThreads, 0, s>>>(p);
-    else attn_bf16_kernel<64, false><<<grid, kThreads, 0, s>>>(p);
+    if (with_values) attn_bf16_kernel<64, true, 8><<<grid_v, 8 * 64, 0, s>>>(p);
+    else attn_bf16_kernel<64, false, 4><<<grid_s, 4 * 64, 0, s>>>(p);
   }
   return hipGetLastError();
 }

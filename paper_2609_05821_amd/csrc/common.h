@@ -195,7 +195,9 @@ hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
 
 // Tiling shared by the host layer (workspace sizing) and the kernels.
-constexpr int kAttnPairsPerBlock = 256;  // (row, head) pairs per workgroup
+// (row, head) pairs per attention workgroup: 256 with values (refresh),
+// 128 for the statistics-only variant.
+constexpr int attn_pairs_per_block(bool with_values) { return with_values ? 256 : 128; }
 constexpr int kAttnKeyTile = 64;         // keys per LDS tile
 constexpr int kColsumKeysPerBlock = 256; // visual keys per workgroup
 
