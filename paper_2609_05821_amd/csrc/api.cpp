@@ -99,38 +99,53 @@ conduit_status check_images(const conduit_images *img, int64_t limit, ImageTable
   return CONDUIT_OK;
 }
 
-// Key-split size for the attention kernel: enough workgroups to fill the
-// chip, each split a whole number of 64-key tiles.
-int32_t attn_chunk(int64_t n_rows, int32_t group, int32_t n_kv_heads, int64_t key_span,
-                   int64_t target_blocks, int64_t min_chunk, bool with_values) {
-  const int64_t ppb = attn_pairs_per_block(with_values);
-  const int64_t pair_blocks = (n_rows * group + ppb - 1) / ppb;
-  const int64_t base = pair_blocks * n_kv_heads;
-  int64_t splits = (target_blocks + base - 1) / base;
-  if (splits < 1) splits = 1;
-  int64_t chunk = (key_span + splits - 1) / splits;
-  chunk = align_up(chunk < min_chunk ? min_chunk : chunk, kAttnKeyTile);
-  return (int32_t)chunk;
-}
-
-struct ScoreLayout {
-  size_t vis_pos, key_ok, row_b, part_m, part_l, colsum, vsq, total;
-  int32_t chunk, n_split;
+// Workspace of the bf16 attention plan (see AttnPlan) and its partials.
+struct PlanLayout {
+  size_t pb_info, pb_base, items, hdr, part_m, part_l, part_o;
+  int32_t n_pb, max_items;
 };
 
-ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis, int32_t key_span) {
+int64_t attn_blocks(int64_t n_rows, int32_t group, bool with_values) {
+  const int64_t ppb = attn_pairs_per_block(with_values);
+  return (n_rows * group + ppb - 1) / ppb;
+}
+
+template <typename Take>
+PlanLayout plan_layout(const conduit_kv *kv, int64_t n_rows, bool with_values, Take &&take) {
+  PlanLayout P{};
+  const int32_t group = kv->n_q_heads / kv->n_kv_heads;
+  const int64_t n_pb = attn_blocks(n_rows, group, with_values);
+  const int64_t max_items = attn_max_items(n_pb, kv->n_kv_heads, with_values);
+  const int64_t slots = max_items * attn_pairs_per_block(with_values);
+  P.n_pb = (int32_t)n_pb;
+  P.max_items = (int32_t)max_items;
+  P.pb_info = take((size_t)n_pb * 16);
+  P.pb_base = take((size_t)n_pb * 4);
+  P.items = take((size_t)max_items * 16);
+  P.hdr = take(16);
+  P.part_m = take((size_t)slots * 4);
+  P.part_l = take((size_t)slots * 4);
+  P.part_o = take(with_values ? (size_t)slots * kv->head_dim * 4 : 0);
+  return P;
+}
+
+AttnPlan plan_at(void *ws, const PlanLayout &P);
+
+struct ScoreLayout {
+  size_t vis_pos, key_ok, row_b, colsum, vsq, total;
+  PlanLayout plan;
+};
+
+ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis) {
   ScoreLayout L{};
   const int64_t rows = (int64_t)n_q * kv->n_q_heads;
   const bool bf16 = kv->dtype == CONDUIT_BF16;
-  L.chunk = attn_chunk(n_q, kv->n_q_heads / kv->n_kv_heads, kv->n_kv_heads, key_span, 512, 64, false);
-  L.n_split = (key_span + L.chunk - 1) / L.chunk;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
   L.vis_pos = take((size_t)n_vis * 4);
   L.key_ok = take((size_t)kv->n_ctx);
   L.row_b = take((size_t)rows * 4);
-  L.part_m = take(bf16 ? (size_t)L.n_split * rows * 4 : 0);
-  L.part_l = take(bf16 ? (size_t)L.n_split * rows * 4 : 0);
+  if (bf16) L.plan = plan_layout(kv, n_q, false, take);
   L.colsum = take((size_t)kv->n_kv_heads * n_vis * 4);
   L.vsq = take((size_t)kv->n_kv_heads * n_vis * 4);
   L.total = off;
@@ -138,21 +153,16 @@ ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis, int32
 }
 
 struct RefreshLayout {
-  size_t part_m, part_l, part_o, total;
-  int32_t chunk, n_split;
+  size_t total;
+  PlanLayout plan;
 };
 
 RefreshLayout refresh_layout(const conduit_kv *kv, int32_t k) {
   RefreshLayout L{};
   if (kv->dtype != CONDUIT_BF16 || k <= 0) return L;
-  const int64_t rows = (int64_t)k * kv->n_q_heads;
-  L.chunk = attn_chunk(k, kv->n_q_heads / kv->n_kv_heads, kv->n_kv_heads, kv->n_ctx, 1024, 256, true);
-  L.n_split = (kv->n_ctx + L.chunk - 1) / L.chunk;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
-  L.part_m = take((size_t)L.n_split * rows * 4);
-  L.part_l = take((size_t)L.n_split * rows * 4);
-  L.part_o = take((size_t)L.n_split * rows * kv->head_dim * 4);
+  L.plan = plan_layout(kv, k, true, take);
   L.total = off;
   return L;
 }
@@ -167,6 +177,17 @@ conduit_status check_ws(const void *ws, size_t ws_bytes, size_t need) {
 
 char *at(void *ws, size_t off) { return static_cast<char *>(ws) + off; }
 
+AttnPlan plan_at(void *ws, const PlanLayout &P) {
+  AttnPlan a{};
+  a.pb_info = reinterpret_cast<int4 *>(at(ws, P.pb_info));
+  a.pb_base = reinterpret_cast<int32_t *>(at(ws, P.pb_base));
+  a.items = reinterpret_cast<int4 *>(at(ws, P.items));
+  a.hdr = reinterpret_cast<int32_t *>(at(ws, P.hdr));
+  a.n_pb = P.n_pb;
+  a.max_items = P.max_items;
+  return a;
+}
+
 }  // namespace
 
 extern "C" {
@@ -179,7 +200,7 @@ int64_t conduit_budget(int64_t n_vis, int64_t r_num, int64_t r_den) {
 size_t conduit_score_workspace_bytes(const conduit_kv *kv, int32_t n_q, const conduit_images *img) {
   if (!kv || !img || n_q < 1 || kv->n_kv_heads < 1 || kv->n_q_heads < kv->n_kv_heads || img->n_vis < 1)
     return 0;
-  return score_layout(kv, n_q, img->n_vis, kv->n_ctx).total;
+  return score_layout(kv, n_q, img->n_vis).total;
 }
 
 conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
@@ -202,11 +223,15 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   ImageTable tbl;
   st = check_images(img, q_pos0, &tbl);
   if (st) return st;
-  const ScoreLayout L = score_layout(kv, n_q, img->n_vis, kv->n_ctx);
+  const bool bf16 = kv->dtype == CONDUIT_BF16;
+  if (bf16 && attn_blocks(n_q, kv->n_q_heads / kv->n_kv_heads, false) > kAttnPlanMaxBlocks)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "n_q * n_q_heads / n_kv_heads = %lld exceeds %lld",
+                (long long)n_q * (kv->n_q_heads / kv->n_kv_heads),
+                (long long)kAttnPlanMaxBlocks * attn_pairs_per_block(false));
+  const ScoreLayout L = score_layout(kv, n_q, img->n_vis);
   st = check_ws(ws, ws_bytes, L.total);
   if (st) return st;
 
-  const bool bf16 = kv->dtype == CONDUIT_BF16;
   const int D = kv->head_dim;
   const float scale_log2 = scale * kLog2e;
   int32_t *vis_pos = reinterpret_cast<int32_t *>(at(ws, L.vis_pos));
@@ -241,29 +266,17 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
     ap.q_pos0 = q_pos0;
     ap.key_ok = vis_only ? key_ok : nullptr;
     ap.scale_log2 = scale_log2;
-    ap.chunk = L.chunk;
-    ap.n_split = L.n_split;
-    ap.part_m = reinterpret_cast<float *>(at(ws, L.part_m));
-    ap.part_l = reinterpret_cast<float *>(at(ws, L.part_l));
-    ap.part_o = nullptr;
-    CombineParams cp{};
-    cp.n_rows = n_q;
-    cp.n_q_heads = kv->n_q_heads;
-    cp.row_pos = nullptr;
-    cp.q_pos0 = q_pos0;
-    cp.chunk = L.chunk;
-    cp.part_m = ap.part_m;
-    cp.part_l = ap.part_l;
-    cp.part_o = nullptr;
-    cp.row_b = row_b;
-    cp.lse_out = row_lse_out;
+    ap.row_b = row_b;
+    ap.lse_out = row_lse_out;
     if (bf16) {
-      e = launch_attn(ap, D, true, false, stream);
+      ap.plan = plan_at(ws, L.plan);
+      ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
+      ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
+      e = launch_attn(ap, D, false, stream);
       if (e != hipSuccess) return hip_fail(e, "row statistics");
-      e = launch_combine(cp, D, stream);
-      if (e != hipSuccess) return hip_fail(e, "row statistics merge");
     } else {
-      e = launch_attn_f32(ap, cp, D, false, stream);
+      DirectOut out{row_b, row_lse_out, nullptr};
+      e = launch_attn_f32(ap, out, D, false, stream);
       if (e != hipSuccess) return hip_fail(e, "row statistics");
     }
   }
@@ -396,6 +409,10 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
   if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
   if (!q_sel || !aligned16(q_sel) || !o_out || !aligned16(o_out))
     return fail(CONDUIT_ERR_INVALID_ARG, "q_sel and o_out must be non-NULL and 16-byte aligned");
+  if (kv->dtype == CONDUIT_BF16 && attn_blocks(k, kv->n_q_heads / kv->n_kv_heads, true) > kAttnPlanMaxBlocks)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "k * n_q_heads / n_kv_heads = %lld exceeds %lld",
+                (long long)k * (kv->n_q_heads / kv->n_kv_heads),
+                (long long)kAttnPlanMaxBlocks * attn_pairs_per_block(true));
   const RefreshLayout L = refresh_layout(kv, k);
   st = check_ws(ws, ws_bytes, L.total);
   if (st) return st;
@@ -415,30 +432,19 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
   ap.q_pos0 = 0;
   ap.key_ok = nullptr;
   ap.scale_log2 = scale * kLog2e;
-  ap.chunk = L.chunk;
-  ap.n_split = L.n_split;
-  CombineParams cp{};
-  cp.n_rows = k;
-  cp.n_q_heads = kv->n_q_heads;
-  cp.row_pos = pos;
-  cp.chunk = L.chunk;
-  cp.lse_out = lse_out;
-  cp.o_out = o_out;
-  cp.o_bf16 = kv->dtype == CONDUIT_BF16;
+  ap.lse_out = lse_out;
+  ap.o_out = o_out;
   hipError_t e;
   if (kv->dtype == CONDUIT_BF16) {
-    ap.part_m = reinterpret_cast<float *>(at(ws, L.part_m));
-    ap.part_l = reinterpret_cast<float *>(at(ws, L.part_l));
-    ap.part_o = reinterpret_cast<float *>(at(ws, L.part_o));
-    cp.part_m = ap.part_m;
-    cp.part_l = ap.part_l;
-    cp.part_o = ap.part_o;
-    e = launch_attn(ap, kv->head_dim, true, true, stream);
+    ap.plan = plan_at(ws, L.plan);
+    ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
+    ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
+    ap.part_o = reinterpret_cast<float *>(at(ws, L.plan.part_o));
+    e = launch_attn(ap, kv->head_dim, true, stream);
     if (e != hipSuccess) return hip_fail(e, "refresh attention");
-    e = launch_combine(cp, kv->head_dim, stream);
-    if (e != hipSuccess) return hip_fail(e, "refresh merge");
   } else {
-    e = launch_attn_f32(ap, cp, kv->head_dim, true, stream);
+    DirectOut out{nullptr, lse_out, static_cast<float *>(o_out)};
+    e = launch_attn_f32(ap, out, kv->head_dim, true, stream);
     if (e != hipSuccess) return hip_fail(e, "refresh attention");
   }
   return ok();

@@ -7,16 +7,25 @@
 //  * the selective recompute needs, for every selected visual row, causal
 //    attention over the merged fresh/stale cache (values included).
 //
-// bf16 path: workgroups of 8 waves (two per SIMD, so one wave's MFMAs overlap
-// the other's softmax) own 256 (row, head) pairs of one KV head (grouped heads
-// share the K/V tiles) and one key split.  Per 64-key tile, double-buffered in
-// LDS with the next tile's global loads in flight, K is staged row-major and
-// V transposed; each wave computes
-// S^T = K Q^T with v_mfma_f32_32x32x16_bf16 so that every lane holds 16 keys
-// of one pair column and the online softmax runs in-lane; the probabilities
-// feed O^T = V^T P^T straight from the accumulator registers.  Splits write
-// (m, l, O) partials in the log2 domain that a combine kernel merges in a
-// fixed order (deterministic, no atomics).
+// bf16 path, three launches:
+//  1. attn_plan_kernel (one workgroup) reads the row positions and cuts the
+//     work into items: a block of (row, head) pairs of one KV head times a
+//     split of the block's causal key range.  Splits are near-equal, with the
+//     smallest split size whose item count fits one or two items per resident
+//     workgroup; items are listed largest first.
+//  2. attn_bf16_kernel runs a persistent grid (one 8-wave workgroup per CU
+//     with values, two 4-wave ones without) that walks the item list in
+//     snake order, so every CU gets a similar share of tiles.  Per 64-key
+//     tile, double-buffered in LDS with the next tile's global loads in
+//     flight, K is staged row-major and V transposed; each wave computes
+//     S^T = K Q^T with v_mfma_f32_32x32x16_bf16 so that every lane holds 16
+//     keys of one pair column and the online softmax runs in-lane; the
+//     probabilities feed O^T = V^T P^T straight from the accumulator
+//     registers.  A block whose keys form a single split writes its final
+//     outputs; otherwise each split writes (m, l, O) partials in the log2
+//     domain.
+//  3. combine_kernel merges the partials of split blocks in a fixed order
+//     (deterministic, no atomics).
 #include "common.h"
 
 namespace conduit {
@@ -31,7 +40,6 @@ struct AttnSmem {
   alignas(16) u16 k[2][KT][D + 8];   // K tiles, one row per key (+16 B pad against bank conflicts)
   alignas(16) u16 vt[2][D][KT + 8];  // V^T tiles, keys in MFMA-operand order
   uint64_t okmask[2];                // key-domain filter per tile, bit = key
-  int maxpos, minpos;
 };
 
 __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, int r) {
@@ -65,287 +73,490 @@ struct TileRegs {
 // rescaled rarely.  Exact: O, l and the final normaliser share the reference.
 constexpr float kRescaleSlack = 8.f;
 
+// Builds the work plan from the row positions (see AttnPlan).  One
+// workgroup of 1024 threads; blocks and histogram bins live in LDS.
+struct PlanArgs {
+  const int32_t *row_pos;  // nullable: row r sits at q_pos0 + r
+  int32_t q_pos0;
+  int32_t n_rows;
+  int32_t group;
+  int32_t n_kv_heads;
+  int32_t n_ctx;
+  int32_t ppb;             // pairs per block
+  int32_t target_items;    // grid slots * rounds
+  AttnPlan plan;
+};
+
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanWaves = kPlanThreads / 64;
+constexpr int kPlanBins = 2048;  // item sizes in tiles (larger sizes share the top bin)
+
+__device__ int plan_exclusive_scan(int x, int *s_wave, int &total) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) s_wave[w] = inc;
+  __syncthreads();
+  if (w == 0) {
+    int v = lane < kPlanWaves ? s_wave[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < kPlanWaves; o <<= 1) {
+      const int y = __shfl_up(v, o, 64);
+      if (lane >= o) v += y;
+    }
+    if (lane < kPlanWaves) s_wave[lane] = v;
+  }
+  __syncthreads();
+  const int excl = inc - x + (w > 0 ? s_wave[w - 1] : 0);
+  total = s_wave[kPlanWaves - 1];
+  __syncthreads();
+  return excl;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
+  __shared__ int s_max[kAttnPlanMaxBlocks], s_min[kAttnPlanMaxBlocks];
+  __shared__ int s_base[kAttnPlanMaxBlocks + 1], s_ct[kAttnPlanMaxBlocks];
+  __shared__ int s_bin[kPlanBins];
+  __shared__ int s_wave[kPlanWaves];
+  __shared__ int s_count;
+  const int tid = threadIdx.x;
+  const int n_pb = a.plan.n_pb;
+  const int G = a.group;
+  for (int b = tid; b < n_pb; b += kPlanThreads) {
+    s_max[b] = 0;
+    s_min[b] = 0x7fffffff;
+  }
+  for (int i = tid; i < kPlanBins; i += kPlanThreads) s_bin[i] = 0;
+  if (tid == 0) s_count = 0;
+  __syncthreads();
+
+  // Position range of every block: each row updates the blocks its G pairs
+  // fall in.  Positions are clamped to the cache, so no key tile of the plan
+  // lies outside it.
+  for (int r0 = 0; r0 < a.n_rows; r0 += 4 * kPlanThreads) {
+    int rp[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = r0 + tid + u * kPlanThreads;
+      rp[u] = r < a.n_rows ? (a.row_pos ? a.row_pos[r] : a.q_pos0 + r) : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = r0 + tid + u * kPlanThreads;
+      if (r >= a.n_rows) continue;
+      const int pos = min(max(rp[u], 0), a.n_ctx - 1);
+      const int64_t p0 = (int64_t)r * G;
+      for (int64_t b = p0 / a.ppb; b <= (p0 + G - 1) / a.ppb; ++b) {
+        atomicMax(&s_max[b], pos);
+        atomicMin(&s_min[b], pos);
+      }
+    }
+  }
+  __syncthreads();
+
+  // Wave 0 alone sizes the splits (wave-level reductions, no barriers);
+  // lane l owns blocks [l * per, (l + 1) * per).
+  if (tid < 64) {
+    const int lane = tid;
+    const int per = (n_pb + 63) / 64;
+    const int b0 = min(lane * per, n_pb), b1 = min(b0 + per, n_pb);
+    int max_tiles = 0;
+    for (int b = b0; b < b1; ++b) max_tiles = max(max_tiles, s_max[b] / kAttnKeyTile + 1);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) max_tiles = max(max_tiles, __shfl_xor(max_tiles, o, 64));
+
+    // Split size T: the smallest T >= kAttnPlanMinTiles whose item count
+    // n_kv * sum_b ceil(tiles_b / T) fits the target (bisection; the count
+    // does not grow with T).  Past T = max_tiles no block splits any more.
+    auto count_items = [&](int T) {
+      int my = 0;
+      for (int b = b0; b < b1; ++b) my += (s_max[b] / kAttnKeyTile + T) / T;  // ceil(tiles / T)
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) my += __shfl_xor(my, o, 64);
+      return (long long)my * a.n_kv_heads;
+    };
+    int lo = kAttnPlanMinTiles, hi = max(kAttnPlanMinTiles, max_tiles);
+    while (lo < hi) {
+      const int mid = lo + (hi - lo) / 2;
+      if (count_items(mid) <= a.target_items) hi = mid;
+      else lo = mid + 1;
+    }
+    const int T = lo;
+
+    // Splits per block: n_s = ceil(tiles / T) near-equal splits of ct <= T
+    // tiles; all but the last hold ct tiles, the last at least one.  Sizes
+    // go into a histogram (one count per KV head).
+    int my_ns = 0;
+    for (int b = b0; b < b1; ++b) my_ns += (s_max[b] / kAttnKeyTile + T) / T;
+    int inc = my_ns;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(inc, o, 64);
+      if (lane >= o) inc += y;
+    }
+    int base = inc - my_ns;
+    for (int b = b0; b < b1; ++b) {
+      const int tiles = s_max[b] / kAttnKeyTile + 1;
+      const int ns = (tiles + T - 1) / T;
+      const int ct = (tiles + ns - 1) / ns;
+      const int last = tiles - (ns - 1) * ct;
+      s_base[b] = base;
+      s_ct[b] = ct;
+      a.plan.pb_info[b] = make_int4(s_max[b], min(max(s_min[b], 0), a.n_ctx - 1), ns, ct * kAttnKeyTile);
+      a.plan.pb_base[b] = base;
+      base += ns;
+      if (ns > 1) atomicAdd(&s_bin[min(ct, kPlanBins - 1)], (ns - 1) * a.n_kv_heads);
+      atomicAdd(&s_bin[min(last, kPlanBins - 1)], a.n_kv_heads);
+    }
+    if (lane == 63) {
+      s_base[n_pb] = inc;  // S
+      s_count = inc;
+    }
+  }
+  __syncthreads();
+  const int S = s_count;
+
+  // Largest first: the offset of a size bin counts the items of larger bins.
+  constexpr int kBinsPer = kPlanBins / kPlanThreads;
+  int cnt[kBinsPer], my_cnt = 0;
+#pragma unroll
+  for (int i = 0; i < kBinsPer; ++i) {
+    cnt[i] = s_bin[kPlanBins - 1 - (tid * kBinsPer + i)];
+    my_cnt += cnt[i];
+  }
+  int n_items;
+  int off = plan_exclusive_scan(my_cnt, s_wave, n_items);
+#pragma unroll
+  for (int i = 0; i < kBinsPer; ++i) {
+    s_bin[kPlanBins - 1 - (tid * kBinsPer + i)] = off;
+    off += cnt[i];
+  }
+  __syncthreads();
+
+  // One thread per item id = h * S + base_b + s (its partial slot); the
+  // block is found by bisection over the bases.
+  for (int id = tid; id < n_items; id += kPlanThreads) {
+    const int h = id / S, rem = id - h * S;
+    int l2 = 0, h2 = n_pb - 1;  // last block with base <= rem
+    while (l2 < h2) {
+      const int mid = (l2 + h2 + 1) >> 1;
+      if (s_base[mid] <= rem) l2 = mid;
+      else h2 = mid - 1;
+    }
+    const int b = l2, sp = rem - s_base[b];
+    const int nsb = s_base[b + 1] - s_base[b], ct = s_ct[b];
+    const int size = sp + 1 < nsb ? ct : (s_max[b] / kAttnKeyTile + 1) - (nsb - 1) * ct;
+    const int at = atomicAdd(&s_bin[min(size, kPlanBins - 1)], 1);
+    if (at < a.plan.max_items) a.plan.items[at] = make_int4(h, b, sp, id);
+  }
+  if (tid == 0) {
+    a.plan.hdr[0] = min(n_items, a.plan.max_items);
+    a.plan.hdr[1] = S;
+  }
+}
+
 // W waves per workgroup, each owning 32 (row, head) pair columns.  With
 // values (refresh) W = 8: two waves per SIMD and 256 pairs sharing each K/V
-// tile; statistics only W = 4 with two workgroups per CU.
+// tile; statistics only W = 4 with two workgroups per CU.  The grid is
+// persistent: workgroup g takes items g, 2G' - 1 - g, 2G' + g, ... of the
+// plan (G' = grid size), i.e. snake order over a largest-first list.
 template <int D, bool PV, int W>
 __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) {
   constexpr int kThreads = W * 64;
-  constexpr int KS = D / 16;   // MFMA k-steps over the head dimension
-  constexpr int DT = D / 32;   // 32-row tiles of O^T
+  constexpr int kPairs = W * 32;  // (row, head) pairs per block
+  constexpr int KS = D / 16;      // MFMA k-steps over the head dimension
+  constexpr int DT = D / 32;      // 32-row tiles of O^T
   using Regs = TileRegs<D, PV, W>;
   __shared__ AttnSmem<D> sm;
 
-  // Blocks of later rows see more keys: launch them first.
-  constexpr int kPairs = W * 32;  // (row, head) pairs per workgroup
-  const int split = blockIdx.x, pb = gridDim.y - 1 - blockIdx.y, kvh = blockIdx.z;
   const int G = p.group;
   const int n_pairs = p.n_rows * G;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
-  const int pair0 = pb * kPairs;
-
-  // Position range of this block's rows bounds its keys and its masking.
-  if (tid == 0) {
-    sm.maxpos = -1;
-    sm.minpos = 0x7fffffff;
-  }
-  __syncthreads();
-  {
-    const int r_first = pair0 / G;
-    const int r_last = (min(pair0 + kPairs, n_pairs) - 1) / G;
-    for (int r = r_first + tid; r <= r_last; r += kThreads) {
-      const int rp = row_position(p.row_pos, p.q_pos0, r);
-      atomicMax(&sm.maxpos, rp);
-      atomicMin(&sm.minpos, rp);
-    }
-  }
-  __syncthreads();
-  const int kbeg = split * p.chunk;
-  const int kend = min(kbeg + p.chunk, sm.maxpos + 1);
-  const int minpos = sm.minpos;
-  if (kbeg >= kend) return;
-
   const u16 *Kg = static_cast<const u16 *>(p.k);
   const u16 *Vg = static_cast<const u16 *>(p.v);
   const u16 *Qg = static_cast<const u16 *>(p.q);
   const float c = p.scale_log2;
+  const int n_items = min(p.plan.hdr[0], p.plan.max_items);
+  const int grid = gridDim.x, g = blockIdx.x;
 
-  // The pair column owned by this lane.
-  const int pair = pair0 + wave * 32 + col;
-  const bool valid = pair < n_pairs;
-  const int r = valid ? pair / G : 0;
-  const int gpair = r * p.n_q_heads + kvh * G + (valid ? pair % G : 0);
-  const int rp = valid ? row_position(p.row_pos, p.q_pos0, r) : -1;
-  bf16x8 qreg[KS];
-  {
-    const u16 *qrow = Qg + (int64_t)gpair * D + 8 * half;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qreg[ks] = as_bf16x8(valid ? ld16(qrow + ks * 16) : u32x4{0, 0, 0, 0});
-  }
+  for (int round = 0;; ++round) {
+    const int idx = round * grid + ((round & 1) ? grid - 1 - g : g);
+    if (idx >= n_items) break;
+    const int4 item = p.plan.items[idx];  // {kv head, block, split, slot}
+    const int kvh = item.x, pb = item.y;
+    if (kvh < 0 || kvh >= p.n_kv_heads || pb < 0 || pb >= p.plan.n_pb || item.w < 0 ||
+        item.w >= p.plan.max_items)
+      continue;
+    const int4 info = p.plan.pb_info[pb];  // {maxpos, minpos, n_s, chunk}
+    const int kbeg = item.z * info.w;
+    const int kend = min(kbeg + info.w, info.x + 1);
+    const int minpos = info.y;
+    const bool single = info.z == 1;
+    if (kbeg >= kend) continue;
+    const int pair0 = pb * kPairs;
 
-  // Per-thread offsets of its staging chunks inside a key tile; a tile's
-  // base moves by KT rows, and only a partial last tile clamps its rows.
-  int64_t koff[Regs::KCH];
+    // The pair column owned by this lane.
+    const int pair = pair0 + wave * 32 + col;
+    const bool valid = pair < n_pairs;
+    const int r = valid ? pair / G : 0;
+    const int gpair = r * p.n_q_heads + kvh * G + (valid ? pair % G : 0);
+    const int rp = valid ? row_position(p.row_pos, p.q_pos0, r) : -1;
+    bf16x8 qreg[KS];
+    {
+      const u16 *qrow = Qg + (int64_t)gpair * D + 8 * half;
 #pragma unroll
-  for (int i = 0; i < Regs::KCH; ++i) {
-    const int cidx = tid + kThreads * i;
-    koff[i] = (int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8;
-  }
-  // V items: item = tid + kThreads * i; key pair fastest, so each half-wave
-  // later writes 32 different keys of one V^T row (32 different LDS banks).
-  constexpr int VPT = Regs::VPT;
-  const bool v_active = Regs::VIT >= kThreads || tid < Regs::VIT;
-  int v_kpair[VPT], v_dc[VPT];
-  int64_t voff[VPT][2];
-#pragma unroll
-  for (int it = 0; it < VPT; ++it) {
-    const int item = tid + kThreads * it;
-    v_kpair[it] = item % (KT / 2);
-    v_dc[it] = item / (KT / 2);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      voff[it][i] = (int64_t)(v_kpair[it] * 2 + i) * p.v_stride + kvh * D + v_dc[it] * 8;
-  }
+      for (int ks = 0; ks < KS; ++ks)
+        qreg[ks] = as_bf16x8(valid ? ld16(qrow + ks * 16) : u32x4{0, 0, 0, 0});
+    }
 
-  u32x4 rk[Regs::KCH];
-  u32x4 rv[PV ? VPT : 1][2];
-  bool rok = false;
-  auto load_tile = [&](int t0) __attribute__((always_inline)) {
-    const u16 *kb = Kg + (int64_t)t0 * p.k_stride;
-    const u16 *vb = Vg + (int64_t)t0 * p.v_stride;
-    if (t0 + KT <= kend) {
+    // Per-thread offsets of its staging chunks inside a key tile; a tile's
+    // base moves by KT rows, and only a partial last tile clamps its rows.
+    int64_t koff[Regs::KCH];
 #pragma unroll
-      for (int i = 0; i < Regs::KCH; ++i) rk[i] = ld16(kb + koff[i]);
-      if constexpr (PV) {
-        if (v_active) {
+    for (int i = 0; i < Regs::KCH; ++i) {
+      const int cidx = tid + kThreads * i;
+      koff[i] = (int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8;
+    }
+    // V items: item = tid + kThreads * i; key pair fastest, so each half-wave
+    // later writes 32 different keys of one V^T row (32 different LDS banks).
+    constexpr int VPT = Regs::VPT;
+    const bool v_active = Regs::VIT >= kThreads || tid < Regs::VIT;
+    int v_kpair[VPT], v_dc[VPT];
+    int64_t voff[VPT][2];
 #pragma unroll
-          for (int it = 0; it < VPT; ++it)
+    for (int it = 0; it < VPT; ++it) {
+      const int vi = tid + kThreads * it;
+      v_kpair[it] = vi % (KT / 2);
+      v_dc[it] = vi / (KT / 2);
 #pragma unroll
-            for (int i = 0; i < 2; ++i) rv[it][i] = ld16(vb + voff[it][i]);
+      for (int i = 0; i < 2; ++i)
+        voff[it][i] = (int64_t)(v_kpair[it] * 2 + i) * p.v_stride + kvh * D + v_dc[it] * 8;
+    }
+    u32x4 rk[Regs::KCH];
+    u32x4 rv[PV ? VPT : 1][2];
+    bool rok = false;
+    auto load_tile = [&](int t0) __attribute__((always_inline)) {
+      const u16 *kb = Kg + (int64_t)t0 * p.k_stride;
+      const u16 *vb = Vg + (int64_t)t0 * p.v_stride;
+      if (t0 + KT <= kend) {
+#pragma unroll
+        for (int i = 0; i < Regs::KCH; ++i) rk[i] = ld16(kb + koff[i]);
+        if constexpr (PV) {
+          if (v_active) {
+#pragma unroll
+            for (int it = 0; it < VPT; ++it)
+#pragma unroll
+              for (int i = 0; i < 2; ++i) rv[it][i] = ld16(vb + voff[it][i]);
+          }
+        }
+      } else {  // partial tile: rows past kend repeat the last row (masked later)
+#pragma unroll
+        for (int i = 0; i < Regs::KCH; ++i) {
+          const int cidx = tid + kThreads * i;
+          const int kp = min(t0 + cidx / (D / 8), kend - 1);
+          rk[i] = ld16(Kg + (int64_t)kp * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
+        }
+        if constexpr (PV) {
+          if (v_active) {
+#pragma unroll
+            for (int it = 0; it < VPT; ++it)
+#pragma unroll
+              for (int i = 0; i < 2; ++i) {
+                const int kp = min(t0 + v_kpair[it] * 2 + i, kend - 1);
+                rv[it][i] = ld16(Vg + (int64_t)kp * p.v_stride + kvh * D + v_dc[it] * 8);
+              }
+          }
         }
       }
-    } else {  // partial tile: rows past kend repeat the last row (masked later)
+      if (!PV && p.key_ok && tid < KT) {
+        const int kp = t0 + tid;
+        rok = kp < kend && p.key_ok[kp] != 0;
+      }
+    };
+    auto store_tile = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
       for (int i = 0; i < Regs::KCH; ++i) {
         const int cidx = tid + kThreads * i;
-        const int kp = min(t0 + cidx / (D / 8), kend - 1);
-        rk[i] = ld16(Kg + (int64_t)kp * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
+        st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
       }
       if constexpr (PV) {
         if (v_active) {
 #pragma unroll
-          for (int it = 0; it < VPT; ++it)
+          for (int it = 0; it < VPT; ++it) {
+            const int slot = vt_slot(v_kpair[it] * 2);
+            const u32x4 w0 = rv[it][0], w1 = rv[it][1];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-              const int kp = min(t0 + v_kpair[it] * 2 + i, kend - 1);
-              rv[it][i] = ld16(Vg + (int64_t)kp * p.v_stride + kvh * D + v_dc[it] * 8);
+            for (int e2 = 0; e2 < 4; ++e2) {
+              // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
+              *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc[it] * 8 + 2 * e2][slot]) =
+                  (w0[e2] & 0xffffu) | (w1[e2] << 16);
+              *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc[it] * 8 + 2 * e2 + 1][slot]) =
+                  (w0[e2] >> 16) | (w1[e2] & 0xffff0000u);
+            }
+          }
+        }
+      }
+      if (!PV && p.key_ok && tid < KT) {  // wave 0: one bit per key of the tile
+        const uint64_t bits = __ballot(rok != 0);
+        if (tid == 0) sm.okmask[buf] = bits;
+      }
+    };
+
+    // Running maximum (log2 units) starts finite, so exp2(c*s - m) needs no
+    // special case: masked logits are -inf and give 0; the first valid
+    // sub-tile always moves m.
+    float m = kMInit, l = 0.f;
+    f32x16 o[DT];
+    if constexpr (PV) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
+    }
+
+    // S^T of one 32-key sub-tile: K operands from LDS, 8 chained MFMAs.
+    auto scores = [&](int buf, int sub) __attribute__((always_inline)) {
+      bf16x8 ka[KS];
+      const u16 *krow = &sm.k[buf][sub * 32 + col][8 * half];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) ka[ks] = as_bf16x8(ld16(krow + ks * 16));
+      f32x16 sc = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qreg[ks], sc, 0, 0, 0);
+      return sc;
+    };
+
+    // Online softmax of one sub-tile, then O^T += V^T P^T.
+    auto softmax_pv = [&](f32x16 sc, int buf, int sub, int t0, bool masked) __attribute__((always_inline)) {
+      if (masked) {  // branch-free: causal / split end and the key domain
+        const int lim = min(kend - 1, rp) - t0;  // last visible key of the tile
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int kl = sub * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+          bool ok = kl <= lim;
+          if constexpr (!PV) {  // key-domain filter: statistics of visual-only scoring
+            const uint64_t dom = p.key_ok ? sm.okmask[buf] : ~0ull;
+            ok = ok & (((dom >> kl) & 1ull) != 0);
+          }
+          sc[v] = ok ? sc[v] : kNegInf;
+        }
+      }
+      float mx = kNegInf;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[v]);
+      mx = half_max(mx) * c;
+      const bool grow = mx > m + kRescaleSlack;
+      const float alpha = grow ? fast_exp2(m - mx) : 1.f;
+      m = grow ? mx : m;
+      const float neg_m = -m;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sc[v] = fast_exp2(fmaf(sc[v], c, neg_m));
+      if constexpr (PV) {
+        bf16x8 pk[2];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pk[ks][e] = static_cast<__bf16>(sc[8 * ks + e]);
+        // fp32 row sum (the log-sum-exp output needs it to 1e-4; summing the
+        // bf16-rounded probabilities is off by up to 2^-9 when few terms dominate)
+        float psum = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) psum += sc[v];
+        l = l * alpha + psum;
+        if (__ballot(grow)) {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        }
+        bf16x8 va[2][DT];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            va[ks][dt] = as_bf16x8(ld16(&sm.vt[buf][dt * 32 + col][sub * 32 + ks * 16 + 8 * half]));
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][dt], pk[ks], o[dt], 0, 0, 0);
+      } else {
+        float psum = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) psum += sc[v];
+        l = l * alpha + psum;
+      }
+    };
+
+    // Double-buffered main loop: the next tile's global loads are in flight
+    // while the current tile computes; one barrier per tile.  Both sub-tiles'
+    // S^T MFMAs are issued before the first softmax, so the VALU work of one
+    // sub-tile runs while the matrix core still works on the other.
+    load_tile(kbeg);
+    store_tile(0);
+    __syncthreads();
+    int buf = 0;
+    for (int t0 = kbeg; t0 < kend; t0 += KT) {
+      const bool more = t0 + KT < kend;
+      if (more) load_tile(t0 + KT);
+      const bool masked = (!PV && p.key_ok != nullptr) || t0 + KT > kend || t0 + KT - 1 > minpos;
+      const f32x16 s0 = scores(buf, 0);
+      const f32x16 s1 = scores(buf, 1);
+      softmax_pv(s0, buf, 0, t0, masked);
+      softmax_pv(s1, buf, 1, t0, masked);
+      if (more) store_tile(buf ^ 1);
+      __syncthreads();
+      buf ^= 1;
+    }
+
+    // ---- outputs: final values for a single-split block, else partials ----
+    const float l_tot = l + __shfl_xor(l, 32, 64);
+    if (valid) {
+      if (single) {
+        const float b = m + __log2f(l_tot);
+        if (half == 0) {
+          if (p.row_b) p.row_b[gpair] = b;
+          if (p.lse_out) p.lse_out[gpair] = b * kLn2;
+        }
+        if constexpr (PV) {
+          const float inv = 1.f / l_tot;
+          u16 *dst = static_cast<u16 *>(p.o_out) + (int64_t)gpair * D;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+              uint2 w;
+              w.x = (uint32_t)f32_to_bf16(o[dt][4 * g4] * inv) |
+                    ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 1] * inv) << 16);
+              w.y = (uint32_t)f32_to_bf16(o[dt][4 * g4 + 2] * inv) |
+                    ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 3] * inv) << 16);
+              *reinterpret_cast<uint2 *>(dst + dt * 32 + 8 * g4 + 4 * half) = w;
+            }
+        }
+      } else {
+        const int64_t idx2 = (int64_t)item.w * kPairs + wave * 32 + col;
+        if (half == 0) {
+          p.part_m[idx2] = m;
+          p.part_l[idx2] = l_tot;
+        }
+        if constexpr (PV) {
+          float *dst = p.part_o + idx2 * D;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+              f32x4 w = {o[dt][4 * g4], o[dt][4 * g4 + 1], o[dt][4 * g4 + 2], o[dt][4 * g4 + 3]};
+              *reinterpret_cast<f32x4 *>(dst + dt * 32 + 8 * g4 + 4 * half) = w;
             }
         }
       }
     }
-    if (!PV && p.key_ok && tid < KT) {
-      const int kp = t0 + tid;
-      rok = kp < kend && p.key_ok[kp] != 0;
-    }
-  };
-  auto store_tile = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < Regs::KCH; ++i) {
-      const int cidx = tid + kThreads * i;
-      st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
-    }
-    if constexpr (PV) {
-      if (v_active) {
-#pragma unroll
-        for (int it = 0; it < VPT; ++it) {
-          const int slot = vt_slot(v_kpair[it] * 2);
-          const u32x4 w0 = rv[it][0], w1 = rv[it][1];
-#pragma unroll
-          for (int e2 = 0; e2 < 4; ++e2) {
-            // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
-            *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc[it] * 8 + 2 * e2][slot]) =
-                (w0[e2] & 0xffffu) | (w1[e2] << 16);
-            *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc[it] * 8 + 2 * e2 + 1][slot]) =
-                (w0[e2] >> 16) | (w1[e2] & 0xffff0000u);
-          }
-        }
-      }
-    }
-    if (!PV && p.key_ok && tid < KT) {  // wave 0: one bit per key of the tile
-      const uint64_t bits = __ballot(rok != 0);
-      if (tid == 0) sm.okmask[buf] = bits;
-    }
-  };
-
-  // Running maximum (log2 units) starts finite, so exp2(c*s - m) needs no
-  // special case: masked logits are -inf and give 0; the first valid
-  // sub-tile always moves m.
-  float m = kMInit, l = 0.f;
-  f32x16 o[DT];
-  if constexpr (PV) {
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
-  }
-
-  // S^T of one 32-key sub-tile: K operands from LDS, 8 chained MFMAs.
-  auto scores = [&](int buf, int sub) __attribute__((always_inline)) {
-    bf16x8 ka[KS];
-    const u16 *krow = &sm.k[buf][sub * 32 + col][8 * half];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) ka[ks] = as_bf16x8(ld16(krow + ks * 16));
-    f32x16 sc = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qreg[ks], sc, 0, 0, 0);
-    return sc;
-  };
-
-  // Online softmax of one sub-tile, then O^T += V^T P^T.
-  auto softmax_pv = [&](f32x16 sc, int buf, int sub, int t0, bool masked) __attribute__((always_inline)) {
-    if (masked) {  // branch-free: causal / split end and the key domain
-      const int lim = min(kend - 1, rp) - t0;  // last visible key of the tile
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int kl = sub * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-        bool ok = kl <= lim;
-        if constexpr (!PV) {  // key-domain filter: statistics of visual-only scoring
-          const uint64_t dom = p.key_ok ? sm.okmask[buf] : ~0ull;
-          ok = ok & (((dom >> kl) & 1ull) != 0);
-        }
-        sc[v] = ok ? sc[v] : kNegInf;
-      }
-    }
-    float mx = kNegInf;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[v]);
-    mx = half_max(mx) * c;
-    const bool grow = mx > m + kRescaleSlack;
-    const float alpha = grow ? fast_exp2(m - mx) : 1.f;
-    m = grow ? mx : m;
-    const float neg_m = -m;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) sc[v] = fast_exp2(fmaf(sc[v], c, neg_m));
-    if constexpr (PV) {
-      bf16x8 pk[2];
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pk[ks][e] = static_cast<__bf16>(sc[8 * ks + e]);
-      // fp32 row sum (the log-sum-exp output needs it to 1e-4; summing the
-      // bf16-rounded probabilities is off by up to 2^-9 when few terms dominate)
-      float psum = 0.f;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) psum += sc[v];
-      l = l * alpha + psum;
-      if (__ballot(grow)) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
-      }
-      bf16x8 va[2][DT];
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          va[ks][dt] = as_bf16x8(ld16(&sm.vt[buf][dt * 32 + col][sub * 32 + ks * 16 + 8 * half]));
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][dt], pk[ks], o[dt], 0, 0, 0);
-    } else {
-      float psum = 0.f;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) psum += sc[v];
-      l = l * alpha + psum;
-    }
-  };
-
-  // Double-buffered main loop: the next tile's global loads are in flight
-  // while the current tile computes; one barrier per tile.  Both sub-tiles'
-  // S^T MFMAs are issued before the first softmax, so the VALU work of one
-  // sub-tile runs while the matrix core still works on the other.
-  load_tile(kbeg);
-  store_tile(0);
-  __syncthreads();
-  int buf = 0;
-  for (int t0 = kbeg; t0 < kend; t0 += KT) {
-    const bool more = t0 + KT < kend;
-    if (more) load_tile(t0 + KT);
-    const bool masked = (!PV && p.key_ok != nullptr) || t0 + KT > kend || t0 + KT - 1 > minpos;
-    const f32x16 s0 = scores(buf, 0);
-    const f32x16 s1 = scores(buf, 1);
-    softmax_pv(s0, buf, 0, t0, masked);
-    softmax_pv(s1, buf, 1, t0, masked);
-    if (more) store_tile(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
-  }
-
-  // ---- write this split's partials ----
-  const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
-  const float l_tot = l + __shfl_xor(l, 32, 64);
-  if (valid) {
-    const int64_t idx = (int64_t)split * n_gp + gpair;
-    if (half == 0) {
-      p.part_m[idx] = m;
-      p.part_l[idx] = l_tot;
-    }
-    if constexpr (PV) {
-      float *dst = p.part_o + idx * D;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          f32x4 w = {o[dt][4 * g], o[dt][4 * g + 1], o[dt][4 * g + 2], o[dt][4 * g + 3]};
-          *reinterpret_cast<f32x4 *>(dst + dt * 32 + 8 * g + 4 * half) = w;
-        }
-    }
   }
 }
 
-// Merge split partials: M = max m_s, L = sum l_s 2^(m_s - M),
-// O = sum O_s 2^(m_s - M) / L.  Splits 0..pos/chunk hold the row's keys.
+// Merge split partials of blocks with n_s > 1: M = max m_s,
+// L = sum l_s 2^(m_s - M), O = sum O_s 2^(m_s - M) / L, splits in order.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   constexpr int NC = D / 4;
@@ -355,18 +566,23 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   const int64_t gp = values ? gid / NC : gid;
   const int c = values ? (int)(gid % NC) : 0;
   if (gp >= n_gp) return;
-  const int r = (int)(gp / p.n_q_heads);
-  const int pos = p.row_pos ? p.row_pos[r] : p.q_pos0 + r;
-  const int ns = pos / p.chunk + 1;
+  const int r = (int)(gp / p.n_q_heads), hq = (int)(gp % p.n_q_heads);
+  const int h = hq / p.group;
+  const int64_t pair = (int64_t)r * p.group + hq % p.group;
+  const int pb = (int)(pair / p.ppb), j = (int)(pair % p.ppb);
+  const int ns = p.plan.pb_info[pb].z;
+  if (ns <= 1) return;  // written by the attention kernel
+  const int64_t slot0 = (int64_t)h * p.plan.hdr[1] + p.plan.pb_base[pb];
+  if (slot0 + ns > p.plan.max_items) return;  // never for a plan within its bound
   float M = kNegInf;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_m[s * n_gp + gp]);
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_m[(slot0 + s) * p.ppb + j]);
   float L = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < ns; ++s) {
-    const float ms = p.part_m[s * n_gp + gp];
-    const float w = fast_exp2(ms - M);  // m >= kMInit is finite
-    L += w * p.part_l[s * n_gp + gp];
-    if (values) acc += w * *reinterpret_cast<const f32x4 *>(p.part_o + (s * n_gp + gp) * D + 4 * c);
+    const int64_t idx = (slot0 + s) * p.ppb + j;
+    const float w = fast_exp2(p.part_m[idx] - M);  // m >= kMInit is finite
+    L += w * p.part_l[idx];
+    if (values) acc += w * *reinterpret_cast<const f32x4 *>(p.part_o + idx * D + 4 * c);
   }
   const float b = M + __log2f(L);
   if (c == 0) {
@@ -375,22 +591,18 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   }
   if (values) {
     const float inv = 1.f / L;
-    if (p.o_bf16) {
-      u16 *out = static_cast<u16 *>(p.o_out) + gp * D + 4 * c;
-      uint2 w;
-      w.x = (uint32_t)f32_to_bf16(acc[0] * inv) | ((uint32_t)f32_to_bf16(acc[1] * inv) << 16);
-      w.y = (uint32_t)f32_to_bf16(acc[2] * inv) | ((uint32_t)f32_to_bf16(acc[3] * inv) << 16);
-      *reinterpret_cast<uint2 *>(out) = w;
-    } else {
-      *reinterpret_cast<f32x4 *>(static_cast<float *>(p.o_out) + gp * D + 4 * c) = acc * inv;
-    }
+    u16 *out = static_cast<u16 *>(p.o_out) + gp * D + 4 * c;
+    uint2 w;
+    w.x = (uint32_t)f32_to_bf16(acc[0] * inv) | ((uint32_t)f32_to_bf16(acc[1] * inv) << 16);
+    w.y = (uint32_t)f32_to_bf16(acc[2] * inv) | ((uint32_t)f32_to_bf16(acc[3] * inv) << 16);
+    *reinterpret_cast<uint2 *>(out) = w;
   }
 }
 
 // fp32 path: one wave per (row, head) pair over the whole causal key range,
 // 64 keys per step (one per lane), written straight to the final outputs.
 template <int D, bool PV>
-__global__ __launch_bounds__(64) void attn_f32_kernel(AttnParams p, CombineParams out) {
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnParams p, DirectOut out) {
   constexpr int PER = D / 64;
   __shared__ float qs[D];
   const int64_t gp = blockIdx.x;
@@ -441,7 +653,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParams p, CombineParam
   }
   if constexpr (PV) {
     const float inv = 1.f / l;
-    float *dst = static_cast<float *>(out.o_out) + gp * D;
+    float *dst = out.o_out + gp * D;
 #pragma unroll
     for (int i = 0; i < PER; ++i) dst[lane + 64 * i] = o[i] * inv;
   }
@@ -454,35 +666,54 @@ __global__ void lse_to_b_kernel(const float *lse, float *b, int n) {
 
 }  // namespace
 
-hipError_t launch_attn(const AttnParams &p, int head_dim, bool bf16, bool with_values, hipStream_t s) {
-  const int n_pairs = p.n_rows * p.group;
-  if (!bf16) return hipErrorInvalidValue;
-  // refresh: 8 waves (256 pairs share each K/V tile); statistics: 4 waves,
-  // two workgroups per CU (many short splits)
-  const dim3 grid_v(p.n_split, (n_pairs + attn_pairs_per_block(true) - 1) / attn_pairs_per_block(true),
-                    p.n_kv_heads);
-  const dim3 grid_s(p.n_split, (n_pairs + attn_pairs_per_block(false) - 1) / attn_pairs_per_block(false),
-                    p.n_kv_heads);
+hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipStream_t s) {
+  const int ppb = attn_pairs_per_block(with_values);
+  PlanArgs pa{};
+  pa.row_pos = p.row_pos;
+  pa.q_pos0 = p.q_pos0;
+  pa.n_rows = p.n_rows;
+  pa.group = p.group;
+  pa.n_kv_heads = p.n_kv_heads;
+  pa.n_ctx = p.n_ctx;
+  pa.ppb = ppb;
+  pa.target_items = attn_grid(with_values) * attn_plan_rounds(with_values);
+  pa.plan = p.plan;
+  attn_plan_kernel<<<1, kPlanThreads, 0, s>>>(pa);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  const int grid = attn_grid(with_values);
   if (head_dim == 128) {
-    if (with_values) attn_bf16_kernel<128, true, 8><<<grid_v, 8 * 64, 0, s>>>(p);
-    else attn_bf16_kernel<128, false, 4><<<grid_s, 4 * 64, 0, s>>>(p);
+    if (with_values) attn_bf16_kernel<128, true, 8><<<grid, 8 * 64, 0, s>>>(p);
+    else attn_bf16_kernel<128, false, 4><<<grid, 4 * 64, 0, s>>>(p);
   } else {
-    if (with_values) attn_bf16_kernel<64, true, 8><<<grid_v, 8 * 64, 0, s>>>(p);
-    else attn_bf16_kernel<64, false, 4><<<grid_s, 4 * 64, 0, s>>>(p);
+    if (with_values) attn_bf16_kernel<64, true, 8><<<grid, 8 * 64, 0, s>>>(p);
+    else attn_bf16_kernel<64, false, 4><<<grid, 4 * 64, 0, s>>>(p);
   }
-  return hipGetLastError();
-}
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
 
-hipError_t launch_combine(const CombineParams &p, int head_dim, hipStream_t s) {
+  CombineParams cp{};
+  cp.n_rows = p.n_rows;
+  cp.n_q_heads = p.n_q_heads;
+  cp.group = p.group;
+  cp.ppb = ppb;
+  cp.plan = p.plan;
+  cp.part_m = p.part_m;
+  cp.part_l = p.part_l;
+  cp.part_o = with_values ? p.part_o : nullptr;
+  cp.row_b = p.row_b;
+  cp.lse_out = p.lse_out;
+  cp.o_out = with_values ? p.o_out : nullptr;
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
-  const int64_t n = p.part_o ? n_gp * (head_dim / 4) : n_gp;
+  const int64_t n = with_values ? n_gp * (head_dim / 4) : n_gp;
   const int blocks = (int)((n + 255) / 256);
-  if (head_dim == 128) combine_kernel<128><<<blocks, 256, 0, s>>>(p);
-  else combine_kernel<64><<<blocks, 256, 0, s>>>(p);
+  if (head_dim == 128) combine_kernel<128><<<blocks, 256, 0, s>>>(cp);
+  else combine_kernel<64><<<blocks, 256, 0, s>>>(cp);
   return hipGetLastError();
 }
 
-hipError_t launch_attn_f32(const AttnParams &p, const CombineParams &out, int head_dim,
+hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s) {
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   if (head_dim == 128) {

@@ -80,6 +80,23 @@ __device__ __forceinline__ float wave_sum(float x) {
 // Causal attention of a set of query rows against one layer's cache.  Used for
 // the row statistics of the scoring pass (no values) and for the refresh
 // attention of the selected rows (with values).
+// Work plan of the bf16 attention, built on the device from the row
+// positions (attn_plan_kernel).  A block is `ppb` consecutive (row, head)
+// pairs of one KV head; its causal key range [0, maxpos] is cut into n_s
+// near-equal splits of `chunk` keys.  An item is one (KV head, block, split);
+// items are listed largest first and each has a partial slot.
+struct AttnPlan {
+  int4 *pb_info;            // [n_pb] {maxpos, minpos, n_s, chunk}
+  int32_t *pb_base;         // [n_pb] slot of split 0 for KV head 0
+  int4 *items;              // [max_items] {kv head, block, split, slot}
+  int32_t *hdr;             // {n_items, slots per KV head}
+  int32_t n_pb;
+  int32_t max_items;
+};
+
+// Causal attention of a set of query rows against one layer's cache.  Used for
+// the row statistics of the scoring pass (no values) and for the refresh
+// attention of the selected rows (with values).
 struct AttnParams {
   const void *k;
   const void *v;
@@ -95,27 +112,36 @@ struct AttnParams {
   int32_t q_pos0;
   const uint8_t *key_ok;    // nullable: key-domain filter (statistics variant only)
   float scale_log2;         // logit scale * log2(e)
-  int32_t chunk;            // keys per split (multiple of the key tile)
-  int32_t n_split;
-  float *part_m;            // [n_split][n_rows * n_q_heads]
-  float *part_l;
-  float *part_o;            // [n_split][n_rows * n_q_heads][D] (values only)
+  AttnPlan plan;            // bf16 path
+  float *part_m;            // [max_items][ppb] running max (log2 units)
+  float *part_l;            // [max_items][ppb] softmax denominator
+  float *part_o;            // [max_items][ppb][D] unnormalised output (values only)
+  // Final outputs, written directly by blocks whose keys form one split.
+  float *row_b;             // nullable [n_rows * H_q]: log2-domain log-sum-exp
+  float *lse_out;           // nullable [n_rows * H_q]: natural-log log-sum-exp
+  void *o_out;              // [n_rows][H_q][D] bf16 (values only)
 };
 
-// Merge of split partials into final outputs.
+// Merge of split partials into final outputs (blocks with n_s > 1).
 struct CombineParams {
   int32_t n_rows;
   int32_t n_q_heads;
-  const int32_t *row_pos;   // nullable: q_pos0 + r
-  int32_t q_pos0;
-  int32_t chunk;
+  int32_t group;
+  int32_t ppb;
+  AttnPlan plan;
   const float *part_m;
   const float *part_l;
   const float *part_o;      // nullable (statistics only)
   float *row_b;             // nullable [n_rows * H_q]: log2-domain log-sum-exp
   float *lse_out;           // nullable [n_rows * H_q]: natural-log log-sum-exp
-  void *o_out;              // nullable [n_rows][H_q][D]
-  int32_t o_bf16;           // output element type
+  void *o_out;              // nullable [n_rows][H_q][D] bf16
+};
+
+// Inputs of the fp32 path, which writes its final outputs directly.
+struct DirectOut {
+  float *row_b;
+  float *lse_out;
+  float *o_out;
 };
 
 struct ColsumParams {
@@ -182,10 +208,9 @@ struct ScatterParams {
 // ---------------------------------------------------------------------------
 hipError_t launch_build_maps(const ImageTable &tbl, int32_t n_ctx, int32_t *vis_pos,
                              uint8_t *key_ok, hipStream_t s);
-hipError_t launch_attn(const AttnParams &p, int head_dim, bool bf16, bool with_values,
-                       hipStream_t s);
-hipError_t launch_combine(const CombineParams &p, int head_dim, hipStream_t s);
-hipError_t launch_attn_f32(const AttnParams &p, const CombineParams &out, int head_dim,
+// bf16 attention: plan, persistent attention over the plan's items, merge.
+hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipStream_t s);
+hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s);
 hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, hipStream_t s);
 hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, hipStream_t s);
@@ -195,9 +220,25 @@ hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
 
 // Tiling shared by the host layer (workspace sizing) and the kernels.
-// (row, head) pairs per attention workgroup: 256 with values (refresh),
-// 128 for the statistics-only variant.
+// (row, head) pairs per attention workgroup: 256 with values (refresh,
+// 8 waves, one workgroup per CU), 128 for the statistics-only variant
+// (4 waves, two workgroups per CU).
 constexpr int attn_pairs_per_block(bool with_values) { return with_values ? 256 : 128; }
+// Persistent attention grid: one resident workgroup slot per grid entry on
+// the 256 CUs of an MI355X.
+constexpr int attn_grid(bool with_values) { return with_values ? 256 : 512; }
+// The plan aims at this many items per grid slot: finer items balance the
+// CUs better, coarser ones write fewer partials and pay the per-item start
+// (query load, first tile) less often.  Statistics tiles are cheap (no PV),
+// so that variant keeps coarser items.
+constexpr int attn_plan_rounds(bool with_values) { return with_values ? 2 : 1; }
+constexpr int kAttnPlanMinTiles = 8;     // smallest split, in key tiles
+constexpr int kAttnPlanMaxBlocks = 4096; // pair blocks per KV head the planner holds
+// Upper bound on the items of one plan: sum_b ceil(tiles_b / T) over blocks
+// and KV heads, with T >= total tiles / (grid * rounds).
+constexpr int64_t attn_max_items(int64_t n_pb, int64_t n_kv_heads, bool with_values) {
+  return (int64_t)attn_grid(with_values) * attn_plan_rounds(with_values) + n_pb * n_kv_heads;
+}
 constexpr int kAttnKeyTile = 64;         // keys per LDS tile
 constexpr int kColsumKeysPerBlock = 256; // visual keys per workgroup
 
