@@ -38,8 +38,11 @@
  *     Device pointers must be 16-byte aligned and strides a multiple of
  *     16 bytes.
  *   - Query head h reads KV head h / (n_q_heads / n_kv_heads).
- *   - Supported: head_dim 64 or 128; CONDUIT_BF16 (MFMA kernels, fp32
- *     accumulation) or CONDUIT_F32 (fp32 throughout).
+ *   - Supported: head_dim 64 or 128; n_kv_heads <= 256; CONDUIT_BF16 (MFMA
+ *     kernels, fp32 accumulation) or CONDUIT_F32 (fp32 throughout).  The bf16
+ *     attention plans at most 4,096 blocks of (row, query head) pairs per KV
+ *     head: rows * n_q_heads / n_kv_heads <= 524,288 for conduit_score and
+ *     <= 1,048,576 for conduit_refresh_attn (CONDUIT_ERR_UNSUPPORTED past it).
  *   - Results are bitwise reproducible run to run (no floating-point atomics).
  */
 #ifndef CONDUIT_H

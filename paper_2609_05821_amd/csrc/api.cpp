@@ -52,6 +52,8 @@ conduit_status check_kv(const conduit_kv *kv) {
   if (kv->n_ctx < 1) return fail(CONDUIT_ERR_INVALID_ARG, "kv->n_ctx = %d < 1", kv->n_ctx);
   if (kv->n_kv_heads < 1 || kv->n_q_heads < 1)
     return fail(CONDUIT_ERR_INVALID_ARG, "head counts must be >= 1");
+  if (kv->n_kv_heads > 256)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "n_kv_heads %d (supported: up to 256)", kv->n_kv_heads);
   if (kv->n_q_heads % kv->n_kv_heads != 0)
     return fail(CONDUIT_ERR_INVALID_ARG, "n_q_heads %d is not a multiple of n_kv_heads %d",
                 kv->n_q_heads, kv->n_kv_heads);

@@ -89,7 +89,7 @@ struct PlanArgs {
 
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / 64;
-constexpr int kPlanBins = 2048;  // item sizes in tiles (larger sizes share the top bin)
+constexpr int kPlanBins = 2048;  // (size class, KV head) bins; larger sizes share the top class
 
 __device__ int plan_exclusive_scan(int x, int *s_wave, int &total) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -158,6 +158,9 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
   }
   __syncthreads();
 
+  // Items are ordered by size class (larger first), then by KV head, so the
+  // workgroups running at one time share few heads' K/V in L2.
+  const int max_class = kPlanBins / a.n_kv_heads - 1;
   // Wave 0 alone sizes the splits (wave-level reductions, no barriers);
   // lane l owns blocks [l * per, (l + 1) * per).
   if (tid < 64) {
@@ -209,8 +212,10 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
       a.plan.pb_info[b] = make_int4(s_max[b], min(max(s_min[b], 0), a.n_ctx - 1), ns, ct * kAttnKeyTile);
       a.plan.pb_base[b] = base;
       base += ns;
-      if (ns > 1) atomicAdd(&s_bin[min(ct, kPlanBins - 1)], (ns - 1) * a.n_kv_heads);
-      atomicAdd(&s_bin[min(last, kPlanBins - 1)], a.n_kv_heads);
+      for (int h = 0; h < a.n_kv_heads; ++h) {
+        if (ns > 1) atomicAdd(&s_bin[min(ct, max_class) * a.n_kv_heads + h], ns - 1);
+        atomicAdd(&s_bin[min(last, max_class) * a.n_kv_heads + h], 1);
+      }
     }
     if (lane == 63) {
       s_base[n_pb] = inc;  // S
@@ -250,7 +255,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
     const int b = l2, sp = rem - s_base[b];
     const int nsb = s_base[b + 1] - s_base[b], ct = s_ct[b];
     const int size = sp + 1 < nsb ? ct : (s_max[b] / kAttnKeyTile + 1) - (nsb - 1) * ct;
-    const int at = atomicAdd(&s_bin[min(size, kPlanBins - 1)], 1);
+    const int at = atomicAdd(&s_bin[min(size, max_class) * a.n_kv_heads + h], 1);
     if (at < a.plan.max_items) a.plan.items[at] = make_int4(h, b, sp, id);
   }
   if (tid == 0) {
