@@ -120,7 +120,8 @@ __device__ int plan_exclusive_scan(int x, int *s_wave, int &total) {
 __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
   __shared__ int s_max[kAttnPlanMaxBlocks], s_min[kAttnPlanMaxBlocks];
   __shared__ int s_base[kAttnPlanMaxBlocks + 1], s_ct[kAttnPlanMaxBlocks];
-  __shared__ int s_bin[kPlanBins];
+  __shared__ int s_bin[kPlanBins];   // per size class: count, then base
+  __shared__ int s_rank[kPlanBins];  // per (size class, KV head): items placed
   __shared__ int s_wave[kPlanWaves];
   __shared__ int s_count;
   const int tid = threadIdx.x;
@@ -158,8 +159,9 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
   }
   __syncthreads();
 
-  // Items are ordered by size class (larger first), then by KV head, so the
-  // workgroups running at one time share few heads' K/V in L2.
+  // Items are ordered by size class, larger first; within a class the KV
+  // heads alternate (item r of head h at class base + r * n_kv + h), so with
+  // workgroup g on XCD g mod 8 each XCD's L2 serves few heads at a time.
   const int max_class = kPlanBins / a.n_kv_heads - 1;
   // Wave 0 alone sizes the splits (wave-level reductions, no barriers);
   // lane l owns blocks [l * per, (l + 1) * per).
@@ -212,10 +214,9 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
       a.plan.pb_info[b] = make_int4(s_max[b], min(max(s_min[b], 0), a.n_ctx - 1), ns, ct * kAttnKeyTile);
       a.plan.pb_base[b] = base;
       base += ns;
-      for (int h = 0; h < a.n_kv_heads; ++h) {
-        if (ns > 1) atomicAdd(&s_bin[min(ct, max_class) * a.n_kv_heads + h], ns - 1);
-        atomicAdd(&s_bin[min(last, max_class) * a.n_kv_heads + h], 1);
-      }
+      // every KV head has the same splits: one count per size class
+      if (ns > 1) atomicAdd(&s_bin[min(ct, max_class)], ns - 1);
+      atomicAdd(&s_bin[min(last, max_class)], 1);
     }
     if (lane == 63) {
       s_base[n_pb] = inc;  // S
@@ -225,12 +226,13 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
   __syncthreads();
   const int S = s_count;
 
-  // Largest first: the offset of a size bin counts the items of larger bins.
+  // Largest first: the base of a size class counts the items of larger
+  // classes (all heads).
   constexpr int kBinsPer = kPlanBins / kPlanThreads;
   int cnt[kBinsPer], my_cnt = 0;
 #pragma unroll
   for (int i = 0; i < kBinsPer; ++i) {
-    cnt[i] = s_bin[kPlanBins - 1 - (tid * kBinsPer + i)];
+    cnt[i] = s_bin[kPlanBins - 1 - (tid * kBinsPer + i)] * a.n_kv_heads;
     my_cnt += cnt[i];
   }
   int n_items;
@@ -238,6 +240,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
 #pragma unroll
   for (int i = 0; i < kBinsPer; ++i) {
     s_bin[kPlanBins - 1 - (tid * kBinsPer + i)] = off;
+    s_rank[kPlanBins - 1 - (tid * kBinsPer + i)] = 0;
     off += cnt[i];
   }
   __syncthreads();
@@ -255,7 +258,8 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
     const int b = l2, sp = rem - s_base[b];
     const int nsb = s_base[b + 1] - s_base[b], ct = s_ct[b];
     const int size = sp + 1 < nsb ? ct : (s_max[b] / kAttnKeyTile + 1) - (nsb - 1) * ct;
-    const int at = atomicAdd(&s_bin[min(size, max_class) * a.n_kv_heads + h], 1);
+    const int cls = min(size, max_class);
+    const int at = s_bin[cls] + atomicAdd(&s_rank[cls * a.n_kv_heads + h], 1) * a.n_kv_heads + h;
     if (at < a.plan.max_items) a.plan.items[at] = make_int4(h, b, sp, id);
   }
   if (tid == 0) {
