@@ -135,6 +135,22 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
 
+    # Second timed pass of the same steps with per-launch kernel timing (HIP
+    # events recorded by the library around each launch, on this stream).
+    api.profile_enable(True)
+    for i in range(args.steps):
+        if not args.no_scrub:
+            scrub.fill_(i & 0xFF)
+        one_step()
+        restore()
+    torch.cuda.synchronize()
+    api.profile_enable(False)
+    kern = {}
+    for name, t in api.profile_records():
+        kern.setdefault(name, []).append(t)
+    kernels_ms = {name: {"calls_per_step": len(v) / args.steps, "mean": statistics.mean(v),
+                         "p10": pct(v, 10), "p90": pct(v, 90)} for name, v in kern.items()}
+
     per = {"score": [], "select": [], "scatter": [], "refresh": [], "step": []}
     for ev in events:
         per["score"].append(ev[0].elapsed_time(ev[1]))
@@ -145,6 +161,38 @@ def main():
     ms_step = statistics.mean(per["step"])
     ms = {key: statistics.mean(v) for key, v in per.items()}
     med = {key: statistics.median(v) for key, v in per.items()}
+    p10 = {key: pct(v, 10) for key, v in per.items()}
+    p90 = {key: pct(v, 90) for key, v in per.items()}
+
+    # Scoring with the row log-sum-exp supplied (the row-statistics pass is
+    # skipped), and the same pass at n_q = 8 (bandwidth probe: far below the
+    # MFMA ridge, so HBM-bound).
+    lse_rows = torch.empty(w.n_q * w.n_q_heads, dtype=torch.float32, device=dev)
+    api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, row_lse_out=lse_rows,
+                      ws=step.ws_score)
+    q8 = q[:8].contiguous()
+    ws8 = torch.empty(api.score_workspace_bytes(kv, 8, img), dtype=torch.uint8, device=dev)
+
+    def timed(fn):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
+        for _ in range(args.warmup):
+            fn()
+        out_ms = []
+        for i in range(args.steps):
+            if not args.no_scrub:
+                scrub.fill_(i & 0xFF)
+            ev[2 * i].record(stream)
+            fn()
+            ev[2 * i + 1].record(stream)
+        torch.cuda.synchronize()
+        out_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)]
+        return {"mean": statistics.mean(out_ms), "p10": pct(out_ms, 10), "p90": pct(out_ms, 90)}
+
+    score_lse_in = timed(lambda: api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc,
+                                                   row_lse_in=lse_rows, ws=step.ws_score))
+    probe = timed(lambda: api.conduit_score(kv, q8, w.q_pos0, img, step.s_acc, step.a_acc, ws=ws8))
+    tiny = torch.empty(1, dtype=torch.float32, device=dev)
+    launch_floor = timed(lambda: tiny.fill_(0.0))
 
     # Selection must be the same every step (deterministic).
     assert torch.equal(step.idx[:k], idx0), "selection changed between steps"
@@ -160,6 +208,9 @@ def main():
         2.0 * d * H * w.n_q * w.n_vis
     scatter_bytes = 2 * 2 * k * hkv * d * e
     refresh_tflops = refresh_flops / (ms["refresh"] * 1e-3) / 1e12
+    attn_ms = kernels_ms["attn_values"]["mean"]
+    attn_tflops = refresh_flops / (attn_ms * 1e-3) / 1e12
+    probe_bytes = (8 * H * d * e + w.n_ctx * hkv * d * e + w.n_vis * hkv * d * e + w.n_vis * 4 * 4)
 
     result = {
         "metric": METRIC,
@@ -181,18 +232,35 @@ def main():
             "lambda": 1.0, "norm": "causal_row", "cold_cache_scrub": not args.no_scrub,
         },
         "roofline": {
-            "kernel": "refresh attention (conduit_refresh_attn: MFMA attention + split merge)",
+            "kernel": "attn_bf16_kernel<128, true, 8> (refresh attention of conduit_refresh_attn)",
             "bound": "mfma",
-            "achieved": refresh_tflops,
+            "achieved": attn_tflops,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
-            "frac": refresh_tflops / PEAK_BF16_TFLOPS,
-            "traffic": None,
-            "algorithmic_flops": refresh_flops,
-            "avg_ms": ms["refresh"],
+            "frac": attn_tflops / PEAK_BF16_TFLOPS,
+            "traffic": traffic_from_profile(),
+            "algorithmic_flops_per_launch": refresh_flops,
+            "avg_launch_ms": attn_ms,
+            "timing": "HIP events around the kernel launch on its stream (library per-launch "
+                      "timing), same steps as the timed region, second pass",
+            "whole_call": {"ms": ms["refresh"], "tflops": refresh_tflops,
+                           "note": "conduit_refresh_attn = plan + attention + split merge"},
         },
         "per_call_ms_mean": ms,
         "per_call_ms_median": med,
+        "per_call_ms_p10": p10,
+        "per_call_ms_p90": p90,
+        "kernels_ms": kernels_ms,
+        "score_row_lse_in_ms": score_lse_in,
+        "bandwidth_probe": {
+            "what": "conduit_score at n_q = 8 on the same cache (supplementary; not a benchmark "
+                    "config): HBM-bound",
+            "ms": probe, "algorithmic_bytes": probe_bytes,
+            "gbs": probe_bytes / (probe["mean"] * 1e-3) / 1e9,
+            "hbm_frac": probe_bytes / (probe["mean"] * 1e-3) / 1e9 / PEAK_HBM_GBS,
+        },
+        "launch_floor_ms": launch_floor,
+        "provenance": provenance(),
         "score": {
             "algorithmic_bytes": score_bytes, "algorithmic_flops": score_flops,
             "gbs": score_bytes / (ms["score"] * 1e-3) / 1e9,
@@ -209,6 +277,63 @@ def main():
         result["cpu_baseline"] = cpu_baseline(w, L, q_sel_np, idx_np, pos_np, k,
                                               args.cpu_row_stride)
     print(json.dumps(result))
+
+
+def pct(v, q):
+    """q-th percentile (nearest rank) of a list."""
+    xs = sorted(v)
+    return xs[min(len(xs) - 1, max(0, int(round(q / 100.0 * (len(xs) - 1)))))]
+
+
+def source_digest(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_from_profile():
+    """HBM bytes per launch of the refresh attention kernel from the committed
+    FETCH_SIZE / WRITE_SIZE counter summary, scaled by the plain-copy factor
+    recorded there; None when the summary is missing or was taken on another
+    version of the kernel source."""
+    path = os.path.join(ROOT, "profiles", "attn_values_16k_traffic.md")
+    src = os.path.join(ROOT, "paper_2609_05821_amd", "csrc", "attn.hip")
+    try:
+        text = open(path).read()
+    except OSError:
+        return None
+    import re
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("attn_hip_sha256_16") != source_digest(src):
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
+def provenance():
+    import torch
+
+    from paper_2609_05821_amd import build as B
+    rocm = ""
+    try:
+        rocm = open("/opt/rocm/.info/version").read().strip()
+    except OSError:
+        pass
+    flags, skip = [], False
+    for f in B.FLAGS:  # drop include paths (machine-specific)
+        if skip or f.startswith("/"):
+            skip = False
+            continue
+        if f == "-I":
+            skip = True
+            continue
+        flags.append(f)
+    return {"rocm": rocm, "torch": torch.__version__,
+            "device": torch.cuda.get_device_name(0),
+            "arch": getattr(torch.cuda.get_device_properties(0), "gcnArchName", ""),
+            "hipcc_flags": " ".join(flags)}
 
 
 def cpu_baseline(w, L, q_sel, idx, pos, k, stride):

@@ -198,6 +198,23 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
                                     int32_t k, float scale, void *o_out, float *lse_out,
                                     void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Kernel timing, a tracing aid.  While enabled on the calling thread, every
+ * kernel launch made by the entry points above is bracketed by two HIP
+ * events recorded on the caller's stream; the first CONDUIT_PROFILE_MAX
+ * launches are kept.  conduit_profile_read(i, ...) waits for launch i to
+ * finish and returns its kernel's name (a static string) and duration in
+ * milliseconds.  Enabling clears the record; disabling keeps it for reading.
+ * The events add a small gap between launches, so leave timing off outside
+ * measurement.  Errors: CONDUIT_ERR_INVALID_ARG for i out of range or NULL
+ * outputs, CONDUIT_ERR_HIP if an event call fails.
+ * ------------------------------------------------------------------------ */
+#define CONDUIT_PROFILE_MAX 4096
+
+conduit_status conduit_profile_enable(int32_t enabled);
+int32_t conduit_profile_count(void);
+conduit_status conduit_profile_read(int32_t i, const char **name, float *ms);
+
 /* Status name, e.g. "CONDUIT_ERR_INVALID_ARG". */
 const char *conduit_status_str(conduit_status status);
 

@@ -27,7 +27,8 @@ EXPORTS = [
     "conduit_budget", "conduit_score_workspace_bytes", "conduit_score",
     "conduit_select_workspace_bytes", "conduit_select_topk", "conduit_scatter_kv",
     "conduit_refresh_workspace_bytes", "conduit_refresh_attn", "conduit_status_str",
-    "conduit_last_error", "conduit_version",
+    "conduit_last_error", "conduit_version", "conduit_profile_enable", "conduit_profile_count",
+    "conduit_profile_read",
 ]
 
 
@@ -86,6 +87,12 @@ def lib() -> ctypes.CDLL:
         L.conduit_last_error.restype = ctypes.c_char_p
         L.conduit_version.argtypes = []
         L.conduit_version.restype = ctypes.c_char_p
+        L.conduit_profile_enable.argtypes = [i32]
+        L.conduit_profile_enable.restype = ctypes.c_int
+        L.conduit_profile_count.argtypes = []
+        L.conduit_profile_count.restype = i32
+        L.conduit_profile_read.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(f32)]
+        L.conduit_profile_read.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -232,6 +239,24 @@ def conduit_refresh_attn(kv: KV, q_sel: torch.Tensor, pos: torch.Tensor, o_out: 
     _check(lib().conduit_refresh_attn(ctypes.byref(kv), q_sel.data_ptr(), pos.data_ptr(), k,
                                       scale, o_out.data_ptr(), _ptr(lse_out), _ptr(ws), _nbytes(ws),
                                       _stream(stream)))
+
+
+def profile_enable(enabled: bool) -> None:
+    """Turn per-launch kernel timing on (clearing the record) or off, for the
+    calling thread (conduit_profile_enable)."""
+    _check(lib().conduit_profile_enable(1 if enabled else 0))
+
+
+def profile_records() -> list:
+    """[(kernel name, ms)] of the launches recorded since timing was enabled;
+    waits for each to finish (conduit_profile_read)."""
+    L = lib()
+    out = []
+    name, ms = ctypes.c_char_p(), ctypes.c_float()
+    for i in range(L.conduit_profile_count()):
+        _check(L.conduit_profile_read(i, ctypes.byref(name), ctypes.byref(ms)))
+        out.append((name.value.decode(), ms.value))
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -190,9 +190,72 @@ AttnPlan plan_at(void *ws, const PlanLayout &P) {
   return a;
 }
 
+// Kernel timing state of one thread.  Events are created on first use and
+// kept for the life of the thread (never destroyed: the HIP runtime may be
+// gone when thread-local destructors run at exit).
+struct ProfRecord {
+  const char *name;
+  hipEvent_t start, stop;
+};
+struct ProfState {
+  bool enabled = false;
+  int count = 0;       // launches recorded
+  int created = 0;     // event pairs created
+  ProfRecord rec[CONDUIT_PROFILE_MAX];
+};
+thread_local ProfState *g_prof = nullptr;
+
 }  // namespace
 
+ProfScope::ProfScope(const char *name, hipStream_t s) : slot_(-1), stream_(s) {
+  ProfState *st = g_prof;
+  if (!st || !st->enabled || st->count >= CONDUIT_PROFILE_MAX) return;
+  const int i = st->count;
+  if (i >= st->created) {
+    if (hipEventCreate(&st->rec[i].start) != hipSuccess) return;
+    if (hipEventCreate(&st->rec[i].stop) != hipSuccess) {
+      (void)hipEventDestroy(st->rec[i].start);
+      return;
+    }
+    st->created = i + 1;
+  }
+  if (hipEventRecord(st->rec[i].start, s) != hipSuccess) return;
+  st->rec[i].name = name;
+  slot_ = i;
+  st->count = i + 1;
+}
+
+ProfScope::~ProfScope() {
+  if (slot_ >= 0) (void)hipEventRecord(g_prof->rec[slot_].stop, stream_);
+}
+
 extern "C" {
+
+conduit_status conduit_profile_enable(int32_t enabled) {
+  if (!g_prof) {
+    if (!enabled) return ok();
+    g_prof = new ProfState();
+  }
+  if (enabled) g_prof->count = 0;
+  g_prof->enabled = enabled != 0;
+  return ok();
+}
+
+int32_t conduit_profile_count(void) { return g_prof ? g_prof->count : 0; }
+
+conduit_status conduit_profile_read(int32_t i, const char **name, float *ms) {
+  if (!name || !ms) return fail(CONDUIT_ERR_INVALID_ARG, "name and ms are required");
+  if (!g_prof || i < 0 || i >= g_prof->count)
+    return fail(CONDUIT_ERR_INVALID_ARG, "launch %d not recorded (%d recorded)", i, conduit_profile_count());
+  const ProfRecord &r = g_prof->rec[i];
+  hipError_t e = hipEventSynchronize(r.stop);
+  if (e != hipSuccess) return hip_fail(e, "profile event");
+  e = hipEventElapsedTime(ms, r.start, r.stop);
+  if (e != hipSuccess) return hip_fail(e, "profile elapsed time");
+  *name = r.name;
+  return ok();
+}
+
 
 int64_t conduit_budget(int64_t n_vis, int64_t r_num, int64_t r_den) {
   if (n_vis < 0 || r_den <= 0 || r_num < 0 || r_num > r_den) return -1;

@@ -687,17 +687,23 @@ hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipS
   pa.ppb = ppb;
   pa.target_items = attn_grid(with_values) * attn_plan_rounds(with_values);
   pa.plan = p.plan;
-  attn_plan_kernel<<<1, kPlanThreads, 0, s>>>(pa);
+  {
+    ProfScope ps("attn_plan", s);
+    attn_plan_kernel<<<1, kPlanThreads, 0, s>>>(pa);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
 
   const int grid = attn_grid(with_values);
-  if (head_dim == 128) {
-    if (with_values) attn_bf16_kernel<128, true, 8><<<grid, 8 * 64, 0, s>>>(p);
-    else attn_bf16_kernel<128, false, 4><<<grid, 4 * 64, 0, s>>>(p);
-  } else {
-    if (with_values) attn_bf16_kernel<64, true, 8><<<grid, 8 * 64, 0, s>>>(p);
-    else attn_bf16_kernel<64, false, 4><<<grid, 4 * 64, 0, s>>>(p);
+  {
+    ProfScope ps(with_values ? "attn_values" : "attn_stats", s);
+    if (head_dim == 128) {
+      if (with_values) attn_bf16_kernel<128, true, 8><<<grid, 8 * 64, 0, s>>>(p);
+      else attn_bf16_kernel<128, false, 4><<<grid, 4 * 64, 0, s>>>(p);
+    } else {
+      if (with_values) attn_bf16_kernel<64, true, 8><<<grid, 8 * 64, 0, s>>>(p);
+      else attn_bf16_kernel<64, false, 4><<<grid, 4 * 64, 0, s>>>(p);
+    }
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -717,6 +723,7 @@ hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipS
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   const int64_t n = with_values ? n_gp * (head_dim / 4) : n_gp;
   const int blocks = (int)((n + 255) / 256);
+  ProfScope ps("attn_merge", s);
   if (head_dim == 128) combine_kernel<128><<<blocks, 256, 0, s>>>(cp);
   else combine_kernel<64><<<blocks, 256, 0, s>>>(cp);
   return hipGetLastError();
@@ -725,6 +732,7 @@ hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipS
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s) {
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
+  ProfScope ps("attn_f32", s);
   if (head_dim == 128) {
     if (with_values) attn_f32_kernel<128, true><<<n_gp, 64, 0, s>>>(p, out);
     else attn_f32_kernel<128, false><<<n_gp, 64, 0, s>>>(p, out);
@@ -736,6 +744,7 @@ hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_d
 }
 
 hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, hipStream_t s) {
+  ProfScope ps("lse_to_b", s);
   lse_to_b_kernel<<<(n + 255) / 256, 256, 0, s>>>(lse_in, row_b, n);
   return hipGetLastError();
 }

@@ -202,6 +202,20 @@ struct ScatterParams {
   void *v_old;              // nullable
 };
 
+// Brackets one kernel launch with HIP events when kernel timing is enabled
+// on the calling thread (conduit_profile_enable); otherwise does nothing.
+class ProfScope {
+ public:
+  ProfScope(const char *name, hipStream_t s);
+  ~ProfScope();
+  ProfScope(const ProfScope &) = delete;
+  ProfScope &operator=(const ProfScope &) = delete;
+
+ private:
+  int slot_;
+  hipStream_t stream_;
+};
+
 // ---------------------------------------------------------------------------
 // Launchers (host side, defined next to their kernels).  Each returns the
 // status of the launch.

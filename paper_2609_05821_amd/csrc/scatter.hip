@@ -30,6 +30,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterParams p) {
 }  // namespace
 
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s) {
+  ProfScope ps("scatter", s);
   scatter_kernel<<<(p.n_rows + 3) / 4, 256, 0, s>>>(p);
   return hipGetLastError();
 }

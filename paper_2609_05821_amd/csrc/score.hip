@@ -196,6 +196,7 @@ __global__ void finalize_kernel(FinalizeParams p) {
 
 hipError_t launch_build_maps(const ImageTable &tbl, int32_t n_ctx, int32_t *vis_pos, uint8_t *key_ok,
                              hipStream_t s) {
+  ProfScope ps("build_maps", s);
   build_maps_kernel<<<(n_ctx + 255) / 256, 256, 0, s>>>(tbl, n_ctx, vis_pos, key_ok);
   return hipGetLastError();
 }
@@ -203,10 +204,12 @@ hipError_t launch_build_maps(const ImageTable &tbl, int32_t n_ctx, int32_t *vis_
 hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, hipStream_t s) {
   if (bf16) {
     dim3 grid((p.n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock, p.n_kv_heads);
+    ProfScope ps("colsum", s);
     if (head_dim == 128) colsum_bf16_kernel<128><<<grid, kColsumThreads, 0, s>>>(p);
     else colsum_bf16_kernel<64><<<grid, kColsumThreads, 0, s>>>(p);
   } else {
     dim3 grid((p.n_vis + 63) / 64, p.n_kv_heads);
+    ProfScope ps("colsum_f32", s);
     if (head_dim == 128) colsum_f32_kernel<128><<<grid, 64, 0, s>>>(p);
     else colsum_f32_kernel<64><<<grid, 64, 0, s>>>(p);
   }
@@ -214,6 +217,7 @@ hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, hipStre
 }
 
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t s) {
+  ProfScope ps("finalize", s);
   finalize_kernel<<<(p.n_vis + 255) / 256, 256, 0, s>>>(p);
   return hipGetLastError();
 }

@@ -430,6 +430,7 @@ __global__ void clear_u8_kernel(uint8_t *p, int64_t n) {
 }  // namespace
 
 hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream_t s) {
+  ProfScope ps("select", s);
   if (tbl.n_vis <= kSelThreads * 16) select_regs_kernel<16><<<1, kSelThreads, 0, s>>>(p, tbl);
   else if (tbl.n_vis <= kSelThreads * 32) select_regs_kernel<32><<<1, kSelThreads, 0, s>>>(p, tbl);
   else select_kernel<<<1, kSelThreads, 0, s>>>(p, tbl);
@@ -437,6 +438,7 @@ hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream
 }
 
 hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s) {
+  ProfScope ps("clear_mask", s);
   clear_u8_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p, n);
   return hipGetLastError();
 }

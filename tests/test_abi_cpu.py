@@ -170,3 +170,16 @@ def test_workspace_queries_are_consistent():
 def test_valid_call_without_device_reports_hip_error():
     assert score() == api.ERR_HIP
     assert "build_maps" in api.lib().conduit_last_error().decode()
+
+
+def test_kernel_timing_without_records():
+    """conduit_profile_*: nothing recorded before any launch; reading an
+    unrecorded launch or passing NULL outputs is rejected."""
+    L = api.lib()
+    assert L.conduit_profile_enable(1) == api.OK
+    assert L.conduit_profile_count() == 0
+    name, ms = ctypes.c_char_p(), ctypes.c_float()
+    assert L.conduit_profile_read(0, ctypes.byref(name), ctypes.byref(ms)) == api.ERR_INVALID_ARG
+    assert L.conduit_profile_read(-1, ctypes.byref(name), ctypes.byref(ms)) == api.ERR_INVALID_ARG
+    assert L.conduit_profile_read(0, None, None) == api.ERR_INVALID_ARG
+    assert L.conduit_profile_enable(0) == api.OK

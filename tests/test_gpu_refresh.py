@@ -123,3 +123,25 @@ def test_zero_budget_refresh_enqueues_nothing():
     api.conduit_refresh_attn(kv, kc[:0].view(0, 1, 1), empty, out)
     torch.cuda.synchronize()
     assert (to_f64(out) == 3.0).all()
+
+
+def test_kernel_timing_records_each_launch():
+    """conduit_profile_*: while enabled, the refresh call's three bf16 launches
+    (plan, attention, split merge) are recorded with positive durations, and
+    the result equals the untimed call's bit for bit."""
+    w = CASES["ragged_bf16_gqa7"]()
+    L = w.layer(0)
+    sel = np.arange(0, w.n_vis, 3)
+    out_plain, _, _, _ = run_refresh(w, L, sel)
+    api.profile_enable(True)
+    out_timed, _, _, _ = run_refresh(w, L, sel)
+    api.profile_enable(False)
+    recs = api.profile_records()
+    names = [n for n, _ in recs]
+    assert names[-3:] == ["attn_plan", "attn_values", "attn_merge"], names
+    assert "scatter" in names
+    assert all(ms > 0 for _, ms in recs)
+    assert np.array_equal(bits(out_plain), bits(out_timed))
+    api.profile_enable(True)  # enabling clears the record
+    assert api.lib().conduit_profile_count() == 0
+    api.profile_enable(False)
