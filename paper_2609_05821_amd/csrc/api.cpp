@@ -134,7 +134,7 @@ PlanLayout plan_layout(const conduit_kv *kv, int64_t n_rows, bool with_values, T
 AttnPlan plan_at(void *ws, const PlanLayout &P);
 
 struct ScoreLayout {
-  size_t vis_pos, key_ok, row_b, colsum, vsq, total;
+  size_t row_b, colsum, vsq, total;
   PlanLayout plan;
 };
 
@@ -144,8 +144,6 @@ ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis) {
   const bool bf16 = kv->dtype == CONDUIT_BF16;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
-  L.vis_pos = take((size_t)n_vis * 4);
-  L.key_ok = take((size_t)kv->n_ctx);
   L.row_b = take((size_t)rows * 4);
   if (bf16) L.plan = plan_layout(kv, n_q, false, take);
   L.colsum = take((size_t)kv->n_kv_heads * n_vis * 4);
@@ -299,14 +297,10 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
 
   const int D = kv->head_dim;
   const float scale_log2 = scale * kLog2e;
-  int32_t *vis_pos = reinterpret_cast<int32_t *>(at(ws, L.vis_pos));
-  uint8_t *key_ok = reinterpret_cast<uint8_t *>(at(ws, L.key_ok));
   float *row_b = reinterpret_cast<float *>(at(ws, L.row_b));
   const bool vis_only = norm == CONDUIT_NORM_VISUAL_ONLY;
 
-  hipError_t e = launch_build_maps(tbl, kv->n_ctx, vis_pos, vis_only ? key_ok : nullptr, stream);
-  if (e != hipSuccess) return hip_fail(e, "build_maps");
-
+  hipError_t e;
   if (row_lse_in) {
     e = launch_lse_to_b(row_lse_in, row_b, n_q * kv->n_q_heads, stream);
     if (e != hipSuccess) return hip_fail(e, "lse_to_b");
@@ -329,7 +323,8 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
     ap.n_rows = n_q;
     ap.row_pos = nullptr;
     ap.q_pos0 = q_pos0;
-    ap.key_ok = vis_only ? key_ok : nullptr;
+    ap.vis_only = vis_only ? 1 : 0;
+    ap.tbl = tbl;
     ap.scale_log2 = scale_log2;
     ap.row_b = row_b;
     ap.lse_out = row_lse_out;
@@ -357,7 +352,7 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   cs.q = q;
   cs.n_q = n_q;
   cs.row_b = row_b;
-  cs.vis_pos = vis_pos;
+  cs.tbl = tbl;
   cs.n_vis = img->n_vis;
   cs.scale_log2 = scale_log2;
   cs.colsum_part = reinterpret_cast<float *>(at(ws, L.colsum));
@@ -495,7 +490,7 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
   ap.n_rows = k;
   ap.row_pos = pos;
   ap.q_pos0 = 0;
-  ap.key_ok = nullptr;
+  ap.vis_only = 0;
   ap.scale_log2 = scale * kLog2e;
   ap.lse_out = lse_out;
   ap.o_out = o_out;

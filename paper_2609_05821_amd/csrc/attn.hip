@@ -40,6 +40,7 @@ struct AttnSmem {
   alignas(16) u16 k[2][KT][D + 8];   // K tiles, one row per key (+16 B pad against bank conflicts)
   alignas(16) u16 vt[2][D][KT + 8];  // V^T tiles, keys in MFMA-operand order
   uint64_t okmask[2];                // key-domain filter per tile, bit = key
+  ImageLds img;                      // visual-only statistics: the image table
 };
 
 __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, int r) {
@@ -292,6 +293,10 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const float c = p.scale_log2;
   const int n_items = min(p.plan.hdr[0], p.plan.max_items);
   const int grid = gridDim.x, g = blockIdx.x;
+  if (!PV && p.vis_only) {
+    image_table_to_lds(p.tbl, sm.img, tid, kThreads);
+    __syncthreads();
+  }
 
   for (int round = 0;; ++round) {
     const int idx = round * grid + ((round & 1) ? grid - 1 - g : g);
@@ -382,9 +387,9 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
           }
         }
       }
-      if (!PV && p.key_ok && tid < KT) {
+      if (!PV && p.vis_only && tid < KT) {
         const int kp = t0 + tid;
-        rok = kp < kend && p.key_ok[kp] != 0;
+        rok = kp < kend && is_visual(sm.img, kp);
       }
     };
     auto store_tile = [&](int buf) __attribute__((always_inline)) {
@@ -410,7 +415,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
           }
         }
       }
-      if (!PV && p.key_ok && tid < KT) {  // wave 0: one bit per key of the tile
+      if (!PV && p.vis_only && tid < KT) {  // wave 0: one bit per key of the tile
         const uint64_t bits = __ballot(rok != 0);
         if (tid == 0) sm.okmask[buf] = bits;
       }
@@ -447,7 +452,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
           const int kl = sub * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
           bool ok = kl <= lim;
           if constexpr (!PV) {  // key-domain filter: statistics of visual-only scoring
-            const uint64_t dom = p.key_ok ? sm.okmask[buf] : ~0ull;
+            const uint64_t dom = p.vis_only ? sm.okmask[buf] : ~0ull;
             ok = ok & (((dom >> kl) & 1ull) != 0);
           }
           sc[v] = ok ? sc[v] : kNegInf;
@@ -509,7 +514,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     for (int t0 = kbeg; t0 < kend; t0 += KT) {
       const bool more = t0 + KT < kend;
       if (more) load_tile(t0 + KT);
-      const bool masked = (!PV && p.key_ok != nullptr) || t0 + KT > kend || t0 + KT - 1 > minpos;
+      const bool masked = (!PV && p.vis_only) || t0 + KT > kend || t0 + KT - 1 > minpos;
       const f32x16 s0 = scores(buf, 0);
       const f32x16 s1 = scores(buf, 1);
       softmax_pv(s0, buf, 0, t0, masked);
@@ -628,7 +633,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParams p, DirectOut ou
   for (int i = 0; i < PER; ++i) o[i] = 0.f;
   for (int base = 0; base <= rpos; base += 64) {
     const int kp = base + lane;
-    const bool ok = kp <= rpos && (p.key_ok == nullptr || p.key_ok[kp]);
+    const bool ok = kp <= rpos && (!p.vis_only || is_visual(p.tbl, kp));
     float z = kNegInf;
     if (ok) {
       const float *kr = Kg + (int64_t)kp * p.k_stride + kvh * D;

@@ -26,6 +26,48 @@ struct ImageTable {
   int32_t off[kMaxImages + 1];  // visual-index offsets
 };
 
+// The image table staged in LDS by a workgroup, for per-key lookups.
+struct ImageLds {
+  int32_t n_images;
+  int32_t pos[kMaxImages];
+  int32_t off[kMaxImages + 1];
+};
+
+// Cooperative copy of the table into LDS; the caller synchronises after it.
+__device__ __forceinline__ void image_table_to_lds(const ImageTable &t, ImageLds &s, int tid, int nthreads) {
+  const int n = t.n_images;
+  for (int j = tid; j <= n; j += nthreads) {
+    s.off[j] = t.off[j];
+    if (j < n) s.pos[j] = t.pos[j];
+  }
+  if (tid == 0) s.n_images = n;
+}
+
+// Sequence position of visual index t (0 <= t < n_vis): image j is the last
+// one with off[j] <= t.  T is ImageLds or ImageTable.
+template <typename T>
+__device__ __forceinline__ int vis_position(const T &s, int t) {
+  int lo = 0, hi = s.n_images - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (s.off[mid] <= t) lo = mid;
+    else hi = mid - 1;
+  }
+  return s.pos[lo] + (t - s.off[lo]);
+}
+
+// Whether sequence position q holds a visual token.
+template <typename T>
+__device__ __forceinline__ bool is_visual(const T &s, int q) {
+  int lo = 0, hi = s.n_images - 1;  // last image with pos[j] <= q
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (s.pos[mid] <= q) lo = mid;
+    else hi = mid - 1;
+  }
+  return q >= s.pos[lo] && q < s.pos[lo] + (s.off[lo + 1] - s.off[lo]);
+}
+
 // ---------------------------------------------------------------------------
 // Device helpers
 // ---------------------------------------------------------------------------
@@ -110,7 +152,7 @@ struct AttnParams {
   int32_t n_rows;
   const int32_t *row_pos;   // nullable: row r sits at q_pos0 + r
   int32_t q_pos0;
-  const uint8_t *key_ok;    // nullable: key-domain filter (statistics variant only)
+  int32_t vis_only;         // statistics only: keys restricted to visual tokens (tbl)
   float scale_log2;         // logit scale * log2(e)
   AttnPlan plan;            // bf16 path
   float *part_m;            // [max_items][ppb] running max (log2 units)
@@ -120,6 +162,7 @@ struct AttnParams {
   float *row_b;             // nullable [n_rows * H_q]: log2-domain log-sum-exp
   float *lse_out;           // nullable [n_rows * H_q]: natural-log log-sum-exp
   void *o_out;              // [n_rows][H_q][D] bf16 (values only)
+  ImageTable tbl;           // read when vis_only
 };
 
 // Merge of split partials into final outputs (blocks with n_s > 1).
@@ -155,7 +198,7 @@ struct ColsumParams {
   const void *q;            // [n_q][n_q_heads][D]
   int32_t n_q;
   const float *row_b;       // [n_q * n_q_heads] log2-domain log-sum-exp
-  const int32_t *vis_pos;   // [n_vis] sequence position of each visual token
+  ImageTable tbl;           // visual index -> sequence position
   int32_t n_vis;
   float scale_log2;
   float *colsum_part;       // [n_kv_heads][n_vis]
@@ -220,8 +263,6 @@ class ProfScope {
 // Launchers (host side, defined next to their kernels).  Each returns the
 // status of the launch.
 // ---------------------------------------------------------------------------
-hipError_t launch_build_maps(const ImageTable &tbl, int32_t n_ctx, int32_t *vis_pos,
-                             uint8_t *key_ok, hipStream_t s);
 // bf16 attention: plan, persistent attention over the plan's items, merge.
 hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipStream_t s);
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,

@@ -1,4 +1,6 @@
 // Scoring pass kernels, gfx950 (Sec. 3.3 Eq. 6-7; Algorithm 1 scoring loop).
+// Visual keys are located through the image table (copied into LDS), so no
+// index map is built beforehand.
 //
 // Once every span row's log-sum-exp b_r (log2 domain) is known, the visual
 // column sums of Eq. 6 are  sum_r 2^(c * <q_r, k_t> - b_r)  with
@@ -11,6 +13,8 @@
 // Per-KV-head partials are reduced in a fixed order by the finalize kernel,
 // which also applies the 1/(n_q H_q) mean and accumulates the layer into
 // s = sum_l a v and A = sum_l a (Eq. 7).
+#include <type_traits>
+
 #include "common.h"
 
 namespace conduit {
@@ -18,23 +22,13 @@ namespace {
 
 constexpr float kInf = __builtin_inff();
 
-// Visual index <-> sequence position maps from the image table.
-__global__ void build_maps_kernel(ImageTable tbl, int n_ctx, int32_t *vis_pos, uint8_t *key_ok) {
-  const int p = blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= n_ctx) return;
-  int lo = 0, hi = tbl.n_images - 1;  // last image with pos[j] <= p
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (tbl.pos[mid] <= p) lo = mid; else hi = mid - 1;
-  }
-  const int j = lo;
-  const int n_j = tbl.off[j + 1] - tbl.off[j];
-  const bool vis = p >= tbl.pos[j] && p < tbl.pos[j] + n_j;
-  if (vis) vis_pos[tbl.off[j] + (p - tbl.pos[j])] = p;
-  if (key_ok) key_ok[p] = vis ? 1 : 0;
-}
-
 constexpr int kColsumThreads = 512;   // 8 waves x 32 keys
+
+// Q row blocks stream through two LDS slots; block x is fetched into
+// register set x mod 3, three blocks ahead of its use, so the global load
+// latency hides behind the MFMA and exponential work of the blocks in
+// between (one barrier per block).
+constexpr int kQAhead = 3;
 
 template <int D>
 __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParams p) {
@@ -42,6 +36,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   constexpr int QCH = 32 * D / 8;       // 16-byte chunks in a 32-row Q block
   __shared__ alignas(16) u16 qs[2][32][D + 8];
   __shared__ alignas(16) float bs[2][32];
+  __shared__ ImageLds img;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
@@ -53,19 +48,9 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   const u16 *Vg = static_cast<const u16 *>(p.v);
   const u16 *Qg = static_cast<const u16 *>(p.q);
 
-  // This lane's key column, held as the B operand for every row block.
-  const int t = blockIdx.x * kColsumKeysPerBlock + wave * 32 + col;
-  const bool tvalid = t < p.n_vis;
-  bf16x8 kreg[KS];
-  {
-    const u16 *krow = Kg + (int64_t)(tvalid ? p.vis_pos[t] : 0) * p.k_stride + kvh * D + 8 * half;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      kreg[ks] = as_bf16x8(tvalid ? ld16(krow + ks * 16) : u32x4{0, 0, 0, 0});
-  }
-
   // Cooperative load of row block `blk` (32 (span token, head) rows).
-  auto load_q = [&](int blk, u32x4 &qv, float &bv) {
+  auto load_q = [&](int blk, u32x4 &qv, float &bv) __attribute__((always_inline)) {
+    if (blk >= nblk) return;
     if (tid < QCH) {
       const int row = tid / (D / 8), dc = tid % (D / 8);
       const int pr = blk * 32 + row;
@@ -81,36 +66,66 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
       if (pr < n_pair) bv = p.row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
     }
   };
-  auto store_q = [&](int buf, const u32x4 &qv, float bv) {
-    if (tid < QCH) st16(&qs[buf][tid / (D / 8)][(tid % (D / 8)) * 8], qv);
-    if (tid < 32) bs[buf][tid] = bv;
+  auto store_q = [&](int slot, const u32x4 &qv, float bv) __attribute__((always_inline)) {
+    if (tid < QCH) st16(&qs[slot][tid / (D / 8)][(tid % (D / 8)) * 8], qv);
+    if (tid < 32) bs[slot][tid] = bv;
   };
 
-  u32x4 qv = u32x4{0, 0, 0, 0};
-  float bv = kInf;
-  load_q(0, qv, bv);
-  store_q(0, qv, bv);
+  u32x4 qv[kQAhead];
+  float bv[kQAhead];
+#pragma unroll
+  for (int i = 0; i < kQAhead; ++i) {
+    qv[i] = u32x4{0, 0, 0, 0};
+    bv[i] = kInf;
+    load_q(i, qv[i], bv[i]);
+  }
+
+  // This lane's key column, held as the B operand for every row block.
+  image_table_to_lds(p.tbl, img, tid, kColsumThreads);
+  __syncthreads();
+  const int t = blockIdx.x * kColsumKeysPerBlock + wave * 32 + col;
+  const bool tvalid = t < p.n_vis;
+  bf16x8 kreg[KS];
+  {
+    const u16 *krow = Kg + (int64_t)(tvalid ? vis_position(img, t) : 0) * p.k_stride + kvh * D + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      kreg[ks] = as_bf16x8(tvalid ? ld16(krow + ks * 16) : u32x4{0, 0, 0, 0});
+  }
+  store_q(0, qv[0], bv[0]);
+  load_q(kQAhead, qv[0], bv[0]);
   __syncthreads();
 
   float colsum = 0.f;
-  for (int blk = 0; blk < nblk; ++blk) {
-    const int buf = blk & 1;
-    if (blk + 1 < nblk) load_q(blk + 1, qv, bv);
+  // Block b: compute from slot b & 1, then store block b + 1 (register set
+  // (b + 1) % 3) into the other slot and fetch block b + 4 into that set.
+  auto step = [&](int b, auto j_tag) __attribute__((always_inline)) {
+    constexpr int J = decltype(j_tag)::value;  // == (b + 1) % 3
+    if (b >= nblk) return;
+    const int slot = b & 1;
     f32x16 acc = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 a = as_bf16x8(ld16(&qs[buf][col][ks * 16 + 8 * half]));
+      const bf16x8 a = as_bf16x8(ld16(&qs[slot][col][ks * 16 + 8 * half]));
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kreg[ks], acc, 0, 0, 0);
     }
     // lane (col, half), register v holds row 8*(v/4) + 4*half + v%4
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 b = *reinterpret_cast<const f32x4 *>(&bs[buf][8 * g + 4 * half]);
+      const f32x4 bb = *reinterpret_cast<const f32x4 *>(&bs[slot][8 * g + 4 * half]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) colsum += fast_exp2(fmaf(acc[4 * g + i], p.scale_log2, -b[i]));
+      for (int i = 0; i < 4; ++i) colsum += fast_exp2(fmaf(acc[4 * g + i], p.scale_log2, -bb[i]));
     }
-    if (blk + 1 < nblk) store_q(buf ^ 1, qv, bv);
+    if (b + 1 < nblk) {
+      store_q(slot ^ 1, qv[J], bv[J]);
+      load_q(b + 1 + kQAhead, qv[J], bv[J]);
+    }
     __syncthreads();
+  };
+  for (int b = 0; b < nblk; b += 3) {
+    step(b, std::integral_constant<int, 1>{});
+    step(b + 1, std::integral_constant<int, 2>{});
+    step(b + 2, std::integral_constant<int, 0>{});
   }
   colsum += __shfl_xor(colsum, 32, 64);
   if (half == 0 && tvalid) p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
@@ -121,7 +136,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     const int tv = blockIdx.x * kColsumKeysPerBlock + kk;
     float sq = 0.f;
     if (tv < p.n_vis) {
-      const u16 *vrow = Vg + (int64_t)p.vis_pos[tv] * p.v_stride + kvh * D + part * (D / 2);
+      const u16 *vrow = Vg + (int64_t)vis_position(img, tv) * p.v_stride + kvh * D + part * (D / 2);
 #pragma unroll
       for (int c = 0; c < D / 16; ++c) {
         const u32x4 ws = ld16(vrow + c * 8);
@@ -148,7 +163,7 @@ __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p) {
   const float *Kg = static_cast<const float *>(p.k);
   const float *Vg = static_cast<const float *>(p.v);
   const float *Qg = static_cast<const float *>(p.q);
-  const int64_t pos = p.vis_pos[t];
+  const int64_t pos = vis_position(p.tbl, t);
   float kr[D];
 #pragma unroll
   for (int e = 0; e < D; ++e) kr[e] = Kg[pos * p.k_stride + kvh * D + e];
@@ -193,13 +208,6 @@ __global__ void finalize_kernel(FinalizeParams p) {
 }
 
 }  // namespace
-
-hipError_t launch_build_maps(const ImageTable &tbl, int32_t n_ctx, int32_t *vis_pos, uint8_t *key_ok,
-                             hipStream_t s) {
-  ProfScope ps("build_maps", s);
-  build_maps_kernel<<<(n_ctx + 255) / 256, 256, 0, s>>>(tbl, n_ctx, vis_pos, key_ok);
-  return hipGetLastError();
-}
 
 hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, hipStream_t s) {
   if (bf16) {

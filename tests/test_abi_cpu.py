@@ -169,7 +169,7 @@ def test_workspace_queries_are_consistent():
                     reason="needs a host without a GPU (the call would launch on fake pointers)")
 def test_valid_call_without_device_reports_hip_error():
     assert score() == api.ERR_HIP
-    assert "build_maps" in api.lib().conduit_last_error().decode()
+    assert "row statistics" in api.lib().conduit_last_error().decode()
 
 
 def test_kernel_timing_without_records():
