@@ -24,18 +24,22 @@ constexpr float kInf = __builtin_inff();
 
 constexpr int kColsumThreads = 512;   // 8 waves x 32 keys
 
-// Q row blocks stream through two LDS slots; block x is fetched into
-// register set x mod 3, three blocks ahead of its use, so the global load
-// latency hides behind the MFMA and exponential work of the blocks in
-// between (one barrier per block).
-constexpr int kQAhead = 3;
+// Q rows stream through LDS in chunks of kQChunk (span token, head) rows,
+// double-buffered: the next chunk's global loads (unconditional, clamped
+// addresses) are in flight while the current chunk's kQChunk / 32 MFMA row
+// tiles and exponentials run, one barrier per chunk.  The V rows for the
+// value norms are fetched at the start and consumed at the end.
+constexpr int kQChunk = 256;
 
 template <int D>
 __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParams p) {
   constexpr int KS = D / 16;
-  constexpr int QCH = 32 * D / 8;       // 16-byte chunks in a 32-row Q block
-  __shared__ alignas(16) u16 qs[2][32][D + 8];
-  __shared__ alignas(16) float bs[2][32];
+  constexpr int QCH = kQChunk * D / 8;       // 16-byte chunks in a Q chunk
+  constexpr int CPT = QCH / kColsumThreads;  // per thread
+  constexpr int VPT = kColsumKeysPerBlock * D / 8 / kColsumThreads;  // V chunks per thread
+  static_assert(QCH % kColsumThreads == 0, "Q chunk split");
+  __shared__ alignas(16) u16 qs[2][kQChunk][D + 8];
+  __shared__ alignas(16) float bs[2][kQChunk];
   __shared__ ImageLds img;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -43,114 +47,115 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   const int kvh = blockIdx.y;
   const int G = p.group;
   const int n_pair = p.n_q * G;
-  const int nblk = (n_pair + 31) / 32;
+  const int nch = (n_pair + kQChunk - 1) / kQChunk;
   const u16 *Kg = static_cast<const u16 *>(p.k);
   const u16 *Vg = static_cast<const u16 *>(p.v);
   const u16 *Qg = static_cast<const u16 *>(p.q);
 
-  // Cooperative load of row block `blk` (32 (span token, head) rows).
-  auto load_q = [&](int blk, u32x4 &qv, float &bv) __attribute__((always_inline)) {
-    if (blk >= nblk) return;
-    if (tid < QCH) {
-      const int row = tid / (D / 8), dc = tid % (D / 8);
-      const int pr = blk * 32 + row;
-      qv = u32x4{0, 0, 0, 0};
-      if (pr < n_pair) {
-        const int i = pr / G, hq = kvh * G + pr % G;
-        qv = ld16(Qg + ((int64_t)i * p.n_q_heads + hq) * D + dc * 8);
-      }
-    }
-    if (tid < 32) {
-      const int pr = blk * 32 + tid;
-      bv = kInf;  // padding rows contribute 2^-inf = 0
-      if (pr < n_pair) bv = p.row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
-    }
-  };
-  auto store_q = [&](int slot, const u32x4 &qv, float bv) __attribute__((always_inline)) {
-    if (tid < QCH) st16(&qs[slot][tid / (D / 8)][(tid % (D / 8)) * 8], qv);
-    if (tid < 32) bs[slot][tid] = bv;
-  };
-
-  u32x4 qv[kQAhead];
-  float bv[kQAhead];
+  // Chunk c into registers: rows past n_pair load row n_pair - 1 and are
+  // zeroed (b = +inf) when stored.
+  auto load_chunk = [&](int c, u32x4 (&qv)[CPT], float &bv) __attribute__((always_inline)) {
 #pragma unroll
-  for (int i = 0; i < kQAhead; ++i) {
-    qv[i] = u32x4{0, 0, 0, 0};
-    bv[i] = kInf;
-    load_q(i, qv[i], bv[i]);
-  }
+    for (int i = 0; i < CPT; ++i) {
+      const int cidx = tid + kColsumThreads * i;
+      const int pr = min(c * kQChunk + cidx / (D / 8), n_pair - 1);
+      qv[i] = ld16(Qg + ((int64_t)(pr / G) * p.n_q_heads + kvh * G + pr % G) * D + (cidx % (D / 8)) * 8);
+    }
+    if (tid < kQChunk) {
+      const int pr = min(c * kQChunk + tid, n_pair - 1);
+      bv = p.row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
+    }
+  };
+  auto store_chunk = [&](int c, int buf, const u32x4 (&qv)[CPT], float bv) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int cidx = tid + kColsumThreads * i;
+      const bool live = c * kQChunk + cidx / (D / 8) < n_pair;
+      st16(&qs[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], live ? qv[i] : u32x4{0, 0, 0, 0});
+    }
+    if (tid < kQChunk) bs[buf][tid] = c * kQChunk + tid < n_pair ? bv : kInf;  // 2^-inf = 0
+  };
 
-  // This lane's key column, held as the B operand for every row block.
+  u32x4 qv[CPT];
+  float bv = kInf;
+  load_chunk(0, qv, bv);
+
   image_table_to_lds(p.tbl, img, tid, kColsumThreads);
   __syncthreads();
+  // This lane's key column, held as the B operand for every row tile.
   const int t = blockIdx.x * kColsumKeysPerBlock + wave * 32 + col;
   const bool tvalid = t < p.n_vis;
   bf16x8 kreg[KS];
   {
-    const u16 *krow = Kg + (int64_t)(tvalid ? vis_position(img, t) : 0) * p.k_stride + kvh * D + 8 * half;
+    const u16 *krow = Kg + (int64_t)vis_position(img, tvalid ? t : p.n_vis - 1) * p.k_stride + kvh * D + 8 * half;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      kreg[ks] = as_bf16x8(tvalid ? ld16(krow + ks * 16) : u32x4{0, 0, 0, 0});
+    for (int ks = 0; ks < KS; ++ks) kreg[ks] = as_bf16x8(ld16(krow + ks * 16));
   }
-  store_q(0, qv[0], bv[0]);
-  load_q(kQAhead, qv[0], bv[0]);
+  // V rows of the block's keys for the value norms, 16 bytes per item.
+  u32x4 vv[VPT];
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int vi = tid + kColsumThreads * i;
+    const int tv = min(blockIdx.x * kColsumKeysPerBlock + vi / (D / 8), p.n_vis - 1);
+    vv[i] = ld16(Vg + (int64_t)vis_position(img, tv) * p.v_stride + kvh * D + (vi % (D / 8)) * 8);
+  }
+  store_chunk(0, 0, qv, bv);
   __syncthreads();
 
   float colsum = 0.f;
-  // Block b: compute from slot b & 1, then store block b + 1 (register set
-  // (b + 1) % 3) into the other slot and fetch block b + 4 into that set.
-  auto step = [&](int b, auto j_tag) __attribute__((always_inline)) {
-    constexpr int J = decltype(j_tag)::value;  // == (b + 1) % 3
-    if (b >= nblk) return;
-    const int slot = b & 1;
-    f32x16 acc = f32x16{};
+  for (int c = 0; c < nch; ++c) {
+    const int buf = c & 1;
+    const bool more = c + 1 < nch;
+    if (more) load_chunk(c + 1, qv, bv);
+    const int rows = min(kQChunk, n_pair - c * kQChunk);
+    for (int r0 = 0; r0 < rows; r0 += 64) {
+      f32x16 acc0 = f32x16{}, acc1 = f32x16{};
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 a = as_bf16x8(ld16(&qs[slot][col][ks * 16 + 8 * half]));
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kreg[ks], acc, 0, 0, 0);
-    }
-    // lane (col, half), register v holds row 8*(v/4) + 4*half + v%4
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 a0 = as_bf16x8(ld16(&qs[buf][r0 + col][ks * 16 + 8 * half]));
+        const bf16x8 a1 = as_bf16x8(ld16(&qs[buf][r0 + 32 + col][ks * 16 + 8 * half]));
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, kreg[ks], acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, kreg[ks], acc1, 0, 0, 0);
+      }
+      // lane (col, half), register v holds row 8*(v/4) + 4*half + v%4 of its tile
+      float part0 = 0.f, part1 = 0.f;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 bb = *reinterpret_cast<const f32x4 *>(&bs[slot][8 * g + 4 * half]);
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 b0 = *reinterpret_cast<const f32x4 *>(&bs[buf][r0 + 8 * g + 4 * half]);
+        const f32x4 b1 = *reinterpret_cast<const f32x4 *>(&bs[buf][r0 + 32 + 8 * g + 4 * half]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) colsum += fast_exp2(fmaf(acc[4 * g + i], p.scale_log2, -bb[i]));
+        for (int i = 0; i < 4; ++i) {
+          part0 += fast_exp2(fmaf(acc0[4 * g + i], p.scale_log2, -b0[i]));
+          part1 += fast_exp2(fmaf(acc1[4 * g + i], p.scale_log2, -b1[i]));
+        }
+      }
+      colsum += part0 + part1;
     }
-    if (b + 1 < nblk) {
-      store_q(slot ^ 1, qv[J], bv[J]);
-      load_q(b + 1 + kQAhead, qv[J], bv[J]);
-    }
+    if (more) store_chunk(c + 1, buf ^ 1, qv, bv);
     __syncthreads();
-  };
-  for (int b = 0; b < nblk; b += 3) {
-    step(b, std::integral_constant<int, 1>{});
-    step(b + 1, std::integral_constant<int, 2>{});
-    step(b + 2, std::integral_constant<int, 0>{});
   }
   colsum += __shfl_xor(colsum, 32, 64);
   if (half == 0 && tvalid) p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
 
-  // Value-norm proxy: this head's share of ||V_t||^2, two threads per key.
-  {
-    const int kk = tid >> 1, part = tid & 1;
-    const int tv = blockIdx.x * kColsumKeysPerBlock + kk;
+  // Value-norm proxy: this head's share of ||V_t||^2.  Item vi covers
+  // dims (vi % (D/8))*8 .. +7 of key vi / (D/8); the D/8 items of a key sit
+  // in consecutive lanes and are summed with lane shuffles.
+  static_assert((D / 8) <= 64 && 64 % (D / 8) == 0, "key items within a wave");
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
     float sq = 0.f;
-    if (tv < p.n_vis) {
-      const u16 *vrow = Vg + (int64_t)vis_position(img, tv) * p.v_stride + kvh * D + part * (D / 2);
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const u32x4 ws = ld16(vrow + c * 8);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float lo = __builtin_bit_cast(float, ws[e] << 16);
-          const float hi = __builtin_bit_cast(float, ws[e] & 0xffff0000u);
-          sq = fmaf(lo, lo, sq);
-          sq = fmaf(hi, hi, sq);
-        }
-      }
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __builtin_bit_cast(float, vv[i][e] << 16);
+      const float hi = __builtin_bit_cast(float, vv[i][e] & 0xffff0000u);
+      sq = fmaf(lo, lo, sq);
+      sq = fmaf(hi, hi, sq);
     }
-    sq += __shfl_xor(sq, 1, 64);
-    if (part == 0 && tv < p.n_vis) p.vsq_part[(int64_t)kvh * p.n_vis + tv] = sq;
+#pragma unroll
+    for (int o = 1; o < D / 8; o <<= 1) sq += __shfl_xor(sq, o, 64);
+    const int vi = tid + kColsumThreads * i;
+    const int tv = blockIdx.x * kColsumKeysPerBlock + vi / (D / 8);
+    if (vi % (D / 8) == 0 && tv < p.n_vis) p.vsq_part[(int64_t)kvh * p.n_vis + tv] = sq;
   }
 }
 
