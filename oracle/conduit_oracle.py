@@ -30,7 +30,16 @@ Readings of points the paper leaves open (labels used below):
   R6  top-k ties go to the lower visual index;
   R8  if the cross-image mean is 0 every c_j is 1;
   R11 refresh attention of a selected row at position p covers keys 0..p of
-      the merged cache, itself included.
+      the merged cache, itself included;
+  R25 the RMS aggregation (Eq. 4's bar-alpha, the squared-error surrogate)
+      runs over the same (span token, query head) set as Eq. 6's mean;
+  R26 explicit quotas k_j proportional to c_j n_j (App. D cross-image
+      diagnostic): largest-remainder apportionment of k, capped at n_j with
+      the surplus re-apportioned, ties to the lower image index; if the
+      remaining weights are all zero they fall back to n_j; the arithmetic is
+      float32 in image order (floating point decides integers there, so the
+      decision is taken in the kernel's precision).  Within an image the k_j
+      largest s_t are kept (R6 ties).
 
 Inputs are numpy arrays; bf16 data arrives as raw uint16 bit patterns and is
 decoded here (the oracle never sees a value the GPU path produced).
@@ -41,6 +50,15 @@ import numpy as np
 
 NORM_CAUSAL_ROW = 0
 NORM_VISUAL_ONLY = 1
+
+# Aggregation of the cached-key attention over span tokens and heads.
+AGG_MEAN = 0   # Eq. 6: mean
+AGG_RMS = 1    # Eq. 4: root-mean-square (R25)
+
+# Selection rules.
+RANK_COMPOSITE = 0   # Eq. 10-11: global top-k of s_t * c_pi(t)
+RANK_ATTENTION = 1   # value norm dropped: global top-k of (A_t / |L|) * c_pi(t)
+RANK_EXPLICIT = 2    # quotas k_j ~ c_j n_j, then top-k_j of s_t inside image j (R26)
 
 
 # --------------------------------------------------------------------------
@@ -99,19 +117,30 @@ def attention_row(q_vec, keys, scale):
     return e / total, m + np.log(total)
 
 
+def value_norms(v_cache, img_pos, img_off):
+    """Eq. 7's value-norm proxy ||V_t|| over the concatenated cached heads
+    (R4), for every visual token.  It depends on the cache only, so it can be
+    tabulated once when the cache is built (Sec. 4.3) and is exactly the
+    norm the scoring pass would read."""
+    v_cache = to_f64(v_cache)
+    P_vis, _ = visual_layout(img_pos, img_off)
+    v_rows = v_cache[P_vis].reshape(len(P_vis), -1)
+    return np.sqrt(np.sum(v_rows * v_rows, axis=1))
+
+
 def score_layer(q, k_cache, v_cache, q_pos0, img_pos, img_off, norm=NORM_CAUSAL_ROW,
-                scale=None):
+                scale=None, agg=AGG_MEAN):
     """One scored layer of the query-conditioned scoring pass.
 
     q        [n_q, H_q, d]     span queries; span token i sits at q_pos0 + i
     k_cache  [N_ctx, H_kv, d]  the layer's cached keys (stale visual rows)
     v_cache  [N_ctx, H_kv, d]  the layer's cached values
-    Returns a [N_vis] (Eq. 6), v [N_vis] (value-norm proxy of Eq. 7) and the
-    row log-sum-exp lse [n_q, H_q] of each softmax (natural log).
+    Returns a [N_vis] (Eq. 6 mean, or Eq. 4's root-mean-square with
+    agg=AGG_RMS), v [N_vis] (value-norm proxy of Eq. 7) and the row
+    log-sum-exp lse [n_q, H_q] of each softmax (natural log).
     """
     q = to_f64(q)
     k_cache = to_f64(k_cache)
-    v_cache = to_f64(v_cache)
     n_q, n_q_heads, d = q.shape
     n_kv_heads = k_cache.shape[1]
     group = n_q_heads // n_kv_heads
@@ -129,15 +158,14 @@ def score_layer(q, k_cache, v_cache, q_pos0, img_pos, img_off, norm=NORM_CAUSAL_
             if norm == NORM_CAUSAL_ROW:
                 # keys 0..p; visual positions all lie before the span
                 alpha, lse[i, h] = attention_row(q[i, h], k_cache[: p + 1, kv, :], scale)
-                col_sum += alpha[P_vis]
+                alpha = alpha[P_vis]
             else:
                 alpha, lse[i, h] = attention_row(q[i, h], k_cache[P_vis, kv, :], scale)
-                col_sum += alpha
+            col_sum += alpha if agg == AGG_MEAN else alpha * alpha
     a = col_sum / (n_q * n_q_heads)
-
-    v_rows = v_cache[P_vis].reshape(n_vis, -1)
-    v = np.sqrt(np.sum(v_rows * v_rows, axis=1))
-    return a, v, lse
+    if agg == AGG_RMS:
+        a = np.sqrt(a)
+    return a, value_norms(v_cache, img_pos, img_off), lse
 
 
 # --------------------------------------------------------------------------
@@ -255,30 +283,109 @@ def refresh_attention(q_sel, k_merged, v_merged, pos, scale=None, rows=None):
 # Algorithm 1 end to end, then the per-layer refresh
 # --------------------------------------------------------------------------
 
-def select(layers, q_pos0, img_pos, img_off, k, lam=1.0, norm=NORM_CAUSAL_ROW, scale=None):
+def explicit_quotas(c, n, k):
+    """R26: quotas k_j proportional to c_j n_j that sum to k, each <= n_j.
+
+    Largest remainder with caps: images whose proportional share reaches n_j
+    take n_j and leave the apportionment; the rest share what remains.  All
+    arithmetic is float32 in image order.  Returns an int64 array.
+    """
+    c = np.asarray(c, dtype=np.float32)
+    n = np.asarray(n, dtype=np.int64)
+    K = len(n)
+    quota = np.zeros(K, dtype=np.int64)
+    live = np.ones(K, dtype=bool)
+    left = int(k)
+    while True:
+        w = np.array([np.float32(c[j]) * np.float32(n[j]) for j in range(K)], dtype=np.float32)
+        total = np.float32(0.0)
+        for j in range(K):
+            if live[j]:
+                total = np.float32(total + w[j])
+        if total == np.float32(0.0):  # no weight left: share by size
+            w = n.astype(np.float32)
+            total = np.float32(0.0)
+            for j in range(K):
+                if live[j]:
+                    total = np.float32(total + w[j])
+        share = np.zeros(K, dtype=np.float32)
+        for j in range(K):
+            if live[j]:
+                share[j] = np.float32(np.float32(left) * w[j]) / total
+        capped = [j for j in range(K) if live[j] and share[j] >= np.float32(n[j])]
+        if not capped:
+            break
+        for j in capped:
+            quota[j] = n[j]
+            live[j] = False
+            left -= int(n[j])
+    base = np.zeros(K, dtype=np.int64)
+    frac = np.full(K, -1.0, dtype=np.float32)
+    for j in range(K):
+        if live[j]:
+            base[j] = min(int(np.floor(share[j])), int(n[j]))
+            frac[j] = np.float32(share[j] - np.float32(base[j]))
+    quota[live] = base[live]
+    rest = left - int(base[live].sum())
+    # remaining seats to the largest fractional parts, ties to the lower image
+    order = sorted((j for j in range(K) if live[j] and quota[j] < n[j]), key=lambda j: (-frac[j], j))
+    for j in order[:rest]:
+        quota[j] += 1
+    return quota
+
+
+def select_explicit(s, c, img_off, k):
+    """R26: quotas from explicit_quotas, then the k_j largest s_t of each
+    image (R6 ties).  Returns (quota, ascending visual indices)."""
+    n = np.diff(np.asarray(img_off, dtype=np.int64))
+    quota = explicit_quotas(c, n, k)
+    chosen = []
+    for j in range(len(n)):
+        lo = int(img_off[j])
+        chosen.extend((lo + topk_select(s[lo:lo + int(n[j])], int(quota[j]))).tolist())
+    return quota, np.sort(np.asarray(chosen, dtype=np.int64))
+
+
+def select(layers, q_pos0, img_pos, img_off, k, lam=1.0, norm=NORM_CAUSAL_ROW, scale=None,
+           agg=AGG_MEAN, rule=RANK_COMPOSITE, v_tables=None):
     """Algorithm 1: scoring over every scored layer, reweighting, top-k.
 
-    layers: sequence of dicts with 'q', 'k', 'v' (one per scored layer).
+    layers: sequence of dicts with 'q', 'k', 'v' (one per scored layer); any
+    subset of a model's layers may be passed (|L| = len(layers)).
+    v_tables: optional per-layer value-norm tables used instead of the norms
+    of the cached V (they are equal by construction, Sec. 4.3).
     Returns a dict with per-layer a, v, lse and the shared s, A, g, c, s_hat,
-    idx, pos, mask.  With k == 0 nothing is scored (Algorithm 1 early exit).
+    idx, pos, mask (and quota for RANK_EXPLICIT).  With k == 0 nothing is
+    scored (Algorithm 1 early exit).
     """
     P_vis, pi = visual_layout(img_pos, img_off)
     if k == 0:
         idx, pos, mask = refresh_mask(np.zeros(len(P_vis)), 0, img_pos, img_off)
         return {"idx": idx, "pos": pos, "mask": mask}
     a_l, v_l, lse_l = [], [], []
-    for layer in layers:
+    for li, layer in enumerate(layers):
         a, v, lse = score_layer(layer["q"], layer["k"], layer["v"], q_pos0, img_pos, img_off,
-                                norm=norm, scale=scale)
+                                norm=norm, scale=scale, agg=agg)
+        if v_tables is not None:
+            v = np.asarray(v_tables[li], dtype=np.float64)
         a_l.append(a)
         v_l.append(v)
         lse_l.append(lse)
     s, A = aggregate_layers(a_l, v_l)
     g, g_bar, c = image_coefficients(A, len(layers), img_off, lam)
-    s_hat = composite_score(s, c, pi)
+    out = {"a": a_l, "v": v_l, "lse": lse_l, "s": s, "A": A, "g": g, "g_bar": g_bar, "c": c}
+    if rule == RANK_EXPLICIT:
+        quota, idx = select_explicit(s, c, img_off, k)
+        mask = np.zeros(len(P_vis), dtype=np.uint8)
+        mask[idx] = 1
+        out.update({"s_hat": composite_score(s, c, pi), "quota": quota, "idx": idx,
+                    "pos": P_vis[idx], "mask": mask})
+        return out
+    base = s if rule == RANK_COMPOSITE else A / len(layers)
+    s_hat = composite_score(base, c, pi)
     idx, pos, mask = refresh_mask(s_hat, k, img_pos, img_off)
-    return {"a": a_l, "v": v_l, "lse": lse_l, "s": s, "A": A, "g": g, "g_bar": g_bar,
-            "c": c, "s_hat": s_hat, "idx": idx, "pos": pos, "mask": mask}
+    out.update({"s_hat": s_hat, "idx": idx, "pos": pos, "mask": mask})
+    return out
 
 
 def refresh_layer(k_cache, v_cache, pos, k_new, v_new, q_sel, scale=None, rows=None):

@@ -19,7 +19,17 @@ What pins what:
                           over all subsets of Lemma 1's objective;
   * refresh              torch SDPA over the merged cache, the 100% budget
                           (full prefill) and 0% budget (cache reuse) anchors,
-                          and closed forms for equal keys / equal values.
+                          and closed forms for equal keys / equal values;
+  * RMS aggregation (Eq. 4)  SDPA weights squared and averaged per column, and
+                          the closed form of equal keys over rows of growing
+                          length;
+  * value-norm table     numpy.linalg.norm, and the identity of scoring with
+                          the table and scoring from the cache (Sec. 4.3);
+  * attention-only rule  s_hat rebuilt from SDPA weights and c_j, brute-force
+                          ranking;
+  * explicit quotas      hand-worked apportionments (proportional, capped,
+                          tied), an exact rational implementation on random
+                          cases away from ties, and brute-force in-image top-k.
 """
 from __future__ import annotations
 
@@ -413,6 +423,151 @@ def pin_end_to_end_sdpa(o):
     res = o.select(layers, cur, img_pos, img_off, 4, lam=1.0)
     np.testing.assert_allclose(res["s_hat"], s_hat, rtol=1e-10)
     np.testing.assert_allclose(res["c"], c, rtol=1e-10)
+
+
+def pin_scoring_rms(o):
+    """Eq. 4's root-mean-square aggregation: SDPA weights squared, averaged over
+    (span token, query head) and rooted; equal keys give a closed form."""
+    rng = np.random.default_rng(11)
+    for trial, (hq, hkv, d, n_q, n_img) in enumerate([(4, 2, 8, 3, 2), (3, 1, 4, 2, 3)]):
+        img_pos, img_off, cur = _rand_layout(rng, n_img, prefix=2, sep=trial)
+        n_ctx = cur + n_q
+        q = rng.standard_normal((n_q, hq, d))
+        k = rng.standard_normal((n_ctx, hkv, d))
+        v = rng.standard_normal((n_ctx, hkv, d))
+        P = _p_vis(img_pos, img_off)
+        causal = np.arange(n_ctx)[None, :] <= (cur + np.arange(n_q))[:, None]
+        w = _sdpa_weights(q, k, causal)[:, :, P]
+        a, _, _ = o.score_layer(q, k, v, cur, img_pos, img_off, agg=o.AGG_RMS)
+        np.testing.assert_allclose(a, np.sqrt((w ** 2).sum(axis=(0, 1)) / (n_q * hq)), rtol=1e-10)
+    # equal keys: row i (position q_pos0 + i) is uniform over q_pos0 + i + 1 keys
+    q_pos0, n_q = 5, 3
+    img_pos, img_off = np.array([1]), np.array([0, 3])
+    k = np.ones((q_pos0 + n_q, 1, 2))
+    a, _, _ = o.score_layer(np.ones((n_q, 2, 2)), k, np.zeros_like(k), q_pos0, img_pos, img_off,
+                            agg=o.AGG_RMS)
+    expect = math.sqrt(sum((1.0 / (q_pos0 + i + 1)) ** 2 for i in range(n_q)) / n_q)
+    np.testing.assert_allclose(a, [expect] * 3, rtol=1e-12)
+
+
+def pin_value_norm_table(o):
+    """The precomputed table equals the norms of the cached rows, and scoring
+    with it leaves every score unchanged (Sec. 4.3: exact)."""
+    rng = np.random.default_rng(12)
+    img_pos, img_off, cur = _rand_layout(rng, 3, prefix=2, sep=1)
+    n_q = 2
+    layers = [{"q": rng.standard_normal((n_q, 4, 4)), "k": rng.standard_normal((cur + n_q, 2, 4)),
+               "v": rng.standard_normal((cur + n_q, 2, 4))} for _ in range(2)]
+    P = _p_vis(img_pos, img_off)
+    tables = [o.value_norms(L["v"], img_pos, img_off) for L in layers]
+    for L, t in zip(layers, tables):
+        np.testing.assert_allclose(t, np.linalg.norm(L["v"][P].reshape(len(P), -1), axis=1),
+                                   rtol=1e-13)
+    k = max(1, len(P) // 3)
+    r1 = o.select(layers, cur, img_pos, img_off, k)
+    r2 = o.select(layers, cur, img_pos, img_off, k, v_tables=tables)
+    np.testing.assert_array_equal(r1["s"], r2["s"])
+    np.testing.assert_array_equal(r1["idx"], r2["idx"])
+
+
+def _bruteforce_topk(x, k):
+    order = sorted(range(len(x)), key=lambda t: (-x[t], t))
+    return sorted(order[:k])
+
+
+def pin_attention_rule(o):
+    """Value norm dropped: s_hat = (A / |L|) c_pi(t), rebuilt from SDPA weights;
+    the selection is the brute-force top-k of it."""
+    rng = np.random.default_rng(13)
+    img_pos, img_off, cur = _rand_layout(rng, 3, prefix=3, sep=1)
+    n_q, hq, hkv, d = 2, 4, 2, 4
+    n_ctx = cur + n_q
+    layers = [{"q": rng.standard_normal((n_q, hq, d)), "k": rng.standard_normal((n_ctx, hkv, d)),
+               "v": rng.standard_normal((n_ctx, hkv, d))} for _ in range(2)]
+    P = _p_vis(img_pos, img_off)
+    causal = np.arange(n_ctx)[None, :] <= (cur + np.arange(n_q))[:, None]
+    A = sum(_sdpa_weights(L["q"], L["k"], causal)[:, :, P].sum(axis=(0, 1)) / (n_q * hq)
+            for L in layers)
+    n = np.diff(img_off)
+    g = np.array([A[img_off[j]:img_off[j + 1]].sum() / (2 * n[j]) for j in range(len(n))])
+    lam = 0.7
+    c = (1 - lam) + lam * g / g.mean()
+    pi = np.repeat(np.arange(len(n)), n)
+    s_hat = (A / 2) * c[pi]
+    for k in (1, len(P) // 2, len(P)):
+        r = o.select(layers, cur, img_pos, img_off, k, lam=lam, rule=o.RANK_ATTENTION)
+        np.testing.assert_allclose(r["s_hat"], s_hat, rtol=1e-10)
+        assert list(r["idx"]) == _bruteforce_topk(s_hat, k)
+
+
+def _exact_quotas(c, n, k):
+    """Largest remainder with caps, in exact rational arithmetic."""
+    c = [Fraction(float(np.float32(x))) for x in c]
+    K = len(n)
+    quota, live, left = [0] * K, [True] * K, k
+    while True:
+        w = [c[j] * n[j] for j in range(K)]
+        total = sum(w[j] for j in range(K) if live[j])
+        if total == 0:
+            w = [Fraction(n[j]) for j in range(K)]
+            total = sum(w[j] for j in range(K) if live[j])
+        share = [left * w[j] / total if live[j] else Fraction(0) for j in range(K)]
+        capped = [j for j in range(K) if live[j] and share[j] >= n[j]]
+        if not capped:
+            break
+        for j in capped:
+            quota[j], live[j] = n[j], False
+            left -= n[j]
+    for j in range(K):
+        if live[j]:
+            quota[j] = min(math.floor(share[j]), n[j])
+    rest = left - sum(quota[j] for j in range(K) if live[j])
+    cand = sorted((j for j in range(K) if live[j] and quota[j] < n[j]),
+                  key=lambda j: (-(share[j] - math.floor(share[j])), j))
+    for j in cand[:rest]:
+        quota[j] += 1
+    return quota, share
+
+
+def pin_explicit_quotas(o):
+    """R26: hand-worked apportionments, an exact rational reference on random
+    cases away from ties, and brute-force top-k inside each image."""
+    eq = lambda c, n, k: list(o.explicit_quotas(np.array(c), np.array(n), k))
+    assert eq([1, 2], [3, 3], 4) == [1, 3]            # shares 4/3, 8/3
+    assert eq([1, 1, 1], [4, 4, 4], 5) == [2, 2, 1]   # equal fractions: lower images first
+    assert eq([10, 1, 1], [2, 10, 10], 9) == [2, 4, 3]  # image 0 capped, 7 left
+    assert eq([0, 0], [2, 3], 4) == [2, 2]            # no weight: by size (shares 8/5, 12/5)
+    assert eq([3.0], [7], 5) == [5]                   # one image
+    rng = np.random.default_rng(14)
+    checked = 0
+    for _ in range(300):
+        K = int(rng.integers(1, 7))
+        n = [int(x) for x in rng.integers(1, 12, size=K)]
+        c = [float(x) for x in rng.uniform(0.0, 2.0, size=K)]
+        k = int(rng.integers(0, sum(n) + 1))
+        ref, share = _exact_quotas(c, n, k)
+        fr = sorted(float(x - math.floor(x)) for x in share if x > 0)
+        live = [float(x) for x in share if x > 0]
+        near = any(abs(x - round(x)) < 1e-4 for x in live) or \
+            any(b - a < 1e-4 for a, b in zip(fr, fr[1:]))
+        got = eq(c, n, k)
+        assert sum(got) == k and all(0 <= g_ <= m for g_, m in zip(got, n)), (c, n, k, got)
+        if not near:
+            assert got == ref, (c, n, k, got, ref)
+            checked += 1
+    assert checked > 150
+    # in-image top-k of s with those quotas
+    img_off = np.array([0, 4, 9, 11])
+    s = rng.random(11)
+    s[5] = s[6]  # a tie inside image 1
+    for k in (0, 3, 7, 11):
+        quota, idx = o.select_explicit(s, np.array([1.3, 0.6, 1.1]), img_off, k)
+        expect = []
+        for j in range(3):
+            lo, hi = img_off[j], img_off[j + 1]
+            expect += [lo + t for t in _bruteforce_topk(list(s[lo:hi]), int(quota[j]))]
+        assert list(idx) == sorted(expect)
+        assert sum(quota) == k
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

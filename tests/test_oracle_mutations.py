@@ -16,15 +16,26 @@ from tests import oracle_pins
 MUTATIONS = {
     "scale_1_over_d": ("scale = 1.0 / np.sqrt(d)", "scale = 1.0 / d", 2),
     "gqa_modulo_mapping": ("kv = h // group", "kv = h % n_kv_heads", 2),
-    "causal_excludes_self": ("k_cache[: p + 1, kv, :], scale)\n                col_sum",
-                             "k_cache[: p, kv, :], scale)\n                col_sum"),
-    "visual_column_off_by_one": ("col_sum += alpha[P_vis]", "col_sum += alpha[P_vis - 1]"),
+    "causal_excludes_self": ("k_cache[: p + 1, kv, :], scale)\n                alpha = alpha[P_vis]",
+                             "k_cache[: p, kv, :], scale)\n                alpha = alpha[P_vis]"),
+    "visual_column_off_by_one": ("alpha = alpha[P_vis]", "alpha = alpha[P_vis - 1]"),
     "head_mean_over_kv_heads": ("a = col_sum / (n_q * n_q_heads)", "a = col_sum / (n_q * n_kv_heads)"),
     "no_query_mean": ("a = col_sum / (n_q * n_q_heads)", "a = col_sum / n_q_heads"),
-    "squared_norm": ("v = np.sqrt(np.sum(v_rows * v_rows, axis=1))",
-                     "v = np.sum(v_rows * v_rows, axis=1)"),
-    "per_head_norm": ("v_rows = v_cache[P_vis].reshape(n_vis, -1)",
+    "squared_norm": ("return np.sqrt(np.sum(v_rows * v_rows, axis=1))",
+                     "return np.sum(v_rows * v_rows, axis=1)"),
+    "per_head_norm": ("v_rows = v_cache[P_vis].reshape(len(P_vis), -1)",
                       "v_rows = v_cache[P_vis][:, 0, :]"),
+    "rms_without_root": ("        a = np.sqrt(a)\n", "        a = a\n"),
+    "rms_not_squared": ("col_sum += alpha if agg == AGG_MEAN else alpha * alpha", "col_sum += alpha"),
+    "attention_rule_uses_s": ("base = s if rule == RANK_COMPOSITE else A / len(layers)", "base = s"),
+    "attention_rule_no_layer_mean": ("base = s if rule == RANK_COMPOSITE else A / len(layers)",
+                                     "base = s if rule == RANK_COMPOSITE else A"),
+    "quota_ignores_c": ("w = np.array([np.float32(c[j]) * np.float32(n[j])", "w = np.array([np.float32(n[j])"),
+    "quota_no_cap": ("capped = [j for j in range(K) if live[j] and share[j] >= np.float32(n[j])]",
+                     "capped = []"),
+    "quota_ties_to_upper_image": ("key=lambda j: (-frac[j], j)", "key=lambda j: (-frac[j], -j)"),
+    "explicit_bottom_k": ("lo + topk_select(s[lo:lo + int(n[j])], int(quota[j]))",
+                          "lo + topk_select(-s[lo:lo + int(n[j])], int(quota[j]))"),
     "lse_log2": ("return e / total, m + np.log(total)", "return e / total, m + np.log2(total)"),
     "lse_drops_max": ("return e / total, m + np.log(total)", "return e / total, np.log(total)"),
     "layer_sum_not_mean": ("return s / n_layers, A", "return s, A"),
@@ -43,7 +54,8 @@ MUTATIONS = {
                       "return int(round(r_num * n_vis / r_den))"),
     "budget_float_floor": ("return (int(r_num) * int(n_vis)) // int(r_den)",
                            "return int(math.floor(r_num / r_den * n_vis))"),
-    "mask_missing": ("    mask[idx] = 1\n", "    pass\n"),
+    "mask_missing": ("    mask[idx] = 1\n    return idx, P_vis[idx], mask",
+                     "    pass\n    return idx, P_vis[idx], mask"),
     "refresh_excludes_self": ("k_merged[: p + 1, kv, :], scale)", "k_merged[: p, kv, :], scale)"),
     "refresh_gqa_modulo": ("            kv = h // group\n            alpha, lse[i, h] = attention_row(q_sel",
                            "            kv = h % n_kv_heads\n            alpha, lse[i, h] = attention_row(q_sel"),
