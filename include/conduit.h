@@ -73,6 +73,19 @@ typedef enum { CONDUIT_F32 = 0, CONDUIT_BF16 = 1 } conduit_dtype;
  * over the visual keys alone. */
 typedef enum { CONDUIT_NORM_CAUSAL_ROW = 0, CONDUIT_NORM_VISUAL_ONLY = 1 } conduit_norm;
 
+/* Aggregation of the cached-key attention over span tokens and query heads. */
+typedef enum {
+  CONDUIT_AGG_MEAN = 0,   /* Eq. 6: mean (the deployed policy)                   */
+  CONDUIT_AGG_RMS = 1     /* Eq. 4: root-mean-square, the squared-error surrogate */
+} conduit_agg;
+
+/* Selection rule of conduit_select_topk. */
+typedef enum {
+  CONDUIT_RANK_COMPOSITE = 0,  /* Eq. 10-11: global top-k of (s/|L|) * c_pi(t)        */
+  CONDUIT_RANK_ATTENTION = 1,  /* value norm dropped: global top-k of (A/|L|) * c_pi(t) */
+  CONDUIT_RANK_EXPLICIT = 2    /* quotas k_j ~ c_j n_j, then the k_j largest s of image j */
+} conduit_rule;
+
 #define CONDUIT_MAX_IMAGES 256
 
 /* One layer's KV cache. */
@@ -118,10 +131,18 @@ int64_t conduit_budget(int64_t n_vis, int64_t r_num, int64_t r_den);
  *          attention of the span.  When given, the row-statistics pass is
  *          skipped.
  * row_lse_out  nullable device [n_q][n_q_heads] fp32: the row log-sum-exp.
+ * agg      CONDUIT_AGG_MEAN: a_t is the mean of the attention probabilities over
+ *          (span token, query head) (Eq. 6); CONDUIT_AGG_RMS: their root mean
+ *          square (Eq. 4's surrogate).
+ * vnorm_in nullable device [n_vis] fp32: the layer's value norms ||V_t|| as made
+ *          by conduit_value_norms when the cache was built (Sec. 4.3).  When
+ *          given, the cached V is not read.
  * s_acc, a_acc device [n_vis] fp32, in/out.  With accumulate = 0 they are
  *          overwritten with a_t * ||V_t|| and a_t; with accumulate = 1 these are
  *          added to the current contents.  Calling once per scored layer in
- *          layer order gives sum_l a_t^(l) ||V_t^(l)|| and sum_l a_t^(l).
+ *          layer order gives sum_l a_t^(l) ||V_t^(l)|| and sum_l a_t^(l).  Any
+ *          subset of a model's layers may be scored this way (|L| is then the
+ *          count passed to conduit_select_topk).
  * a_out, vnorm_out  nullable device [n_vis] fp32: this layer's a_t and ||V_t||
  *          (the norm of the n_kv_heads * head_dim concatenated cached value).
  * ws       device workspace of at least conduit_score_workspace_bytes(...).
@@ -129,11 +150,23 @@ int64_t conduit_budget(int64_t n_vis, int64_t r_num, int64_t r_den);
 size_t conduit_score_workspace_bytes(const conduit_kv *kv, int32_t n_q, const conduit_images *img);
 
 conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
-                             const conduit_images *img, conduit_norm norm, float scale,
-                             const float *row_lse_in, float *row_lse_out,
-                             float *s_acc, float *a_acc, int32_t accumulate,
+                             const conduit_images *img, conduit_norm norm, conduit_agg agg,
+                             float scale, const float *row_lse_in, float *row_lse_out,
+                             const float *vnorm_in, float *s_acc, float *a_acc, int32_t accumulate,
                              float *a_out, float *vnorm_out,
                              void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * Value-norm table of one layer (Eq. 7's proxy; Sec. 4.3: the norms depend on
+ * the cache only, so storing one scalar per visual token and layer when the
+ * cache is built preserves the scores exactly and removes the V reads from
+ * every later scoring pass).
+ *
+ * vnorm_out  device [img->n_vis] fp32: ||V_t|| over the n_kv_heads * head_dim
+ *            concatenated cached value of each visual token, in visual order.
+ * ------------------------------------------------------------------------ */
+conduit_status conduit_value_norms(const conduit_kv *kv, const conduit_images *img, float *vnorm_out,
+                                   hipStream_t stream);
 
 /* ------------------------------------------------------------------------ *
  * Image reweighting and global top-k (Sec. 3.4 Eq. 8-9, Sec. 3.5 Eq. 10-11,
@@ -141,24 +174,37 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
  *
  * s_acc, a_acc  device [n_vis] fp32: the layer sums produced by conduit_score.
  * n_layers      |L| >= 1, the number of layers accumulated.
- * lambda        reweighting strength in [0, 1] (1 in the paper's main setting).
+ * lambda        reweighting strength in [0, 1] (1 in the paper's main setting;
+ *               0 ranks by s alone, the "global top-k" of App. D).
  *               c_j = (1 - lambda) + lambda * g_j / g_bar, exactly 1 when
  *               g_j = g_bar (so always with one image) or when g_bar = 0.
- * k             budget, 0 <= k <= n_vis.  Ties in the composite score go to
- *               the lower visual index.  k = 0 only clears mask_out.
+ * rule          CONDUIT_RANK_COMPOSITE: the global top-k of
+ *               s_hat_t = (s_acc_t / n_layers) * c_pi(t) (Eq. 10-11).
+ *               CONDUIT_RANK_ATTENTION: the same with a_acc in place of s_acc
+ *               (the value-norm factor dropped, Table 9's ablation).
+ *               CONDUIT_RANK_EXPLICIT: quotas k_j proportional to c_j * n_j
+ *               (largest remainder, float32 in image order, capped at n_j
+ *               with the surplus re-apportioned, ties to the lower image; all
+ *               weights zero falls back to n_j), then the k_j largest s_acc of
+ *               each image (App. D's explicit reweighting).
+ * k             budget, 0 <= k <= n_vis.  Ties in the ranked score go to the
+ *               lower visual index.  k = 0 only clears mask_out.
  * idx_out       device [k] int32: selected visual indices, ascending.
  * pos_out       device [k] int32: their sequence positions, ascending.
  * mask_out      nullable device [n_vis] uint8: the refresh mask M.
- * shat_out      nullable device [n_vis] fp32: composite scores
- *               s_hat_t = (s_acc_t / n_layers) * c_pi(t).
+ * shat_out      nullable device [n_vis] fp32: the ranked score (composite and
+ *               explicit rules: (s_acc_t / n_layers) * c_pi(t); attention
+ *               rule: (a_acc_t / n_layers) * c_pi(t)).
  * c_out         nullable device [n_images] fp32: the coefficients c_j.
+ * quota_out     nullable device [n_images] int32: the quotas k_j
+ *               (CONDUIT_RANK_EXPLICIT only; ignored otherwise).
  * ------------------------------------------------------------------------ */
 size_t conduit_select_workspace_bytes(int32_t n_vis, int32_t n_images);
 
 conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32_t n_layers,
-                                   const conduit_images *img, float lambda, int32_t k,
-                                   int32_t *idx_out, int32_t *pos_out, uint8_t *mask_out,
-                                   float *shat_out, float *c_out,
+                                   const conduit_images *img, float lambda, conduit_rule rule,
+                                   int32_t k, int32_t *idx_out, int32_t *pos_out, uint8_t *mask_out,
+                                   float *shat_out, float *c_out, int32_t *quota_out,
                                    void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ *

@@ -21,6 +21,8 @@ LIB_PATH = os.path.join(_PKG, "libconduit.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 F32, BF16 = 0, 1
 NORM_CAUSAL_ROW, NORM_VISUAL_ONLY = 0, 1
+AGG_MEAN, AGG_RMS = 0, 1
+RANK_COMPOSITE, RANK_ATTENTION, RANK_EXPLICIT = 0, 1, 2
 MAX_IMAGES = 256
 
 EXPORTS = [
@@ -28,7 +30,7 @@ EXPORTS = [
     "conduit_select_workspace_bytes", "conduit_select_topk", "conduit_scatter_kv",
     "conduit_refresh_workspace_bytes", "conduit_refresh_attn", "conduit_status_str",
     "conduit_last_error", "conduit_version", "conduit_profile_enable", "conduit_profile_count",
-    "conduit_profile_read",
+    "conduit_profile_read", "conduit_value_norms",
 ]
 
 
@@ -68,12 +70,15 @@ def lib() -> ctypes.CDLL:
         L.conduit_budget.restype = i64
         L.conduit_score_workspace_bytes.argtypes = [pkv, i32, pimg]
         L.conduit_score_workspace_bytes.restype = sz
-        L.conduit_score.argtypes = [pkv, vp, i32, i32, pimg, ctypes.c_int, f32, vp, vp, vp, vp, i32,
-                                    vp, vp, vp, sz, vp]
+        L.conduit_score.argtypes = [pkv, vp, i32, i32, pimg, ctypes.c_int, ctypes.c_int, f32, vp, vp,
+                                    vp, vp, vp, i32, vp, vp, vp, sz, vp]
         L.conduit_score.restype = ctypes.c_int
         L.conduit_select_workspace_bytes.argtypes = [i32, i32]
         L.conduit_select_workspace_bytes.restype = sz
-        L.conduit_select_topk.argtypes = [vp, vp, i32, pimg, f32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.conduit_select_topk.argtypes = [vp, vp, i32, pimg, f32, ctypes.c_int, i32, vp, vp, vp, vp,
+                                          vp, vp, vp, sz, vp]
+        L.conduit_value_norms.argtypes = [pkv, pimg, vp, vp]
+        L.conduit_value_norms.restype = ctypes.c_int
         L.conduit_select_topk.restype = ctypes.c_int
         L.conduit_scatter_kv.argtypes = [pkv, vp, i32, vp, vp, vp, vp, vp]
         L.conduit_scatter_kv.restype = ctypes.c_int
@@ -187,16 +192,23 @@ def conduit_score(kv: KV, q: torch.Tensor, q_pos0: int, img: ImageTable, s_acc: 
                   scale: Optional[float] = None, row_lse_in: Optional[torch.Tensor] = None,
                   row_lse_out: Optional[torch.Tensor] = None, a_out: Optional[torch.Tensor] = None,
                   vnorm_out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                  stream=None) -> None:
-    """Scoring pass of one layer (Eq. 6-7); see conduit_score in conduit.h."""
+                  stream=None, agg: int = AGG_MEAN,
+                  vnorm_in: Optional[torch.Tensor] = None) -> None:
+    """Scoring pass of one layer (Eq. 4/6-7); see conduit_score in conduit.h."""
     n_q = q.shape[0]
     if scale is None:
         scale = 1.0 / math.sqrt(kv.head_dim)
     ws = _workspace(score_workspace_bytes(kv, n_q, img), q.device, ws)
     _check(lib().conduit_score(ctypes.byref(kv), q.data_ptr(), n_q, q_pos0, ctypes.byref(img.desc),
-                               norm, scale, _ptr(row_lse_in), _ptr(row_lse_out), s_acc.data_ptr(),
-                               a_acc.data_ptr(), int(accumulate), _ptr(a_out), _ptr(vnorm_out),
-                               _ptr(ws), _nbytes(ws), _stream(stream)))
+                               norm, agg, scale, _ptr(row_lse_in), _ptr(row_lse_out), _ptr(vnorm_in),
+                               s_acc.data_ptr(), a_acc.data_ptr(), int(accumulate), _ptr(a_out),
+                               _ptr(vnorm_out), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def conduit_value_norms(kv: KV, img: ImageTable, vnorm_out: torch.Tensor, stream=None) -> None:
+    """Value-norm table of one layer (Eq. 7 proxy, Sec. 4.3); see conduit_value_norms."""
+    _check(lib().conduit_value_norms(ctypes.byref(kv), ctypes.byref(img.desc), vnorm_out.data_ptr(),
+                                     _stream(stream)))
 
 
 def conduit_select_topk(s_acc: torch.Tensor, a_acc: torch.Tensor, n_layers: int, img: ImageTable,
@@ -204,15 +216,16 @@ def conduit_select_topk(s_acc: torch.Tensor, a_acc: torch.Tensor, n_layers: int,
                         mask_out: Optional[torch.Tensor] = None,
                         shat_out: Optional[torch.Tensor] = None,
                         c_out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                        stream=None) -> None:
-    """Reweighting and global top-k (Eq. 8-11); see conduit_select_topk."""
+                        stream=None, rule: int = RANK_COMPOSITE,
+                        quota_out: Optional[torch.Tensor] = None) -> None:
+    """Reweighting and top-k (Eq. 8-11, or a variant rule); see conduit_select_topk."""
     need = 0 if shat_out is not None else int(
         lib().conduit_select_workspace_bytes(img.n_vis, img.n_images))
     ws = _workspace(need, s_acc.device, ws)
     _check(lib().conduit_select_topk(s_acc.data_ptr(), a_acc.data_ptr(), n_layers,
-                                     ctypes.byref(img.desc), lam, k, _ptr(idx_out), _ptr(pos_out),
-                                     _ptr(mask_out), _ptr(shat_out), _ptr(c_out), _ptr(ws),
-                                     _nbytes(ws), _stream(stream)))
+                                     ctypes.byref(img.desc), lam, rule, k, _ptr(idx_out),
+                                     _ptr(pos_out), _ptr(mask_out), _ptr(shat_out), _ptr(c_out),
+                                     _ptr(quota_out), _ptr(ws), _nbytes(ws), _stream(stream)))
 
 
 def conduit_scatter_kv(kv: KV, pos: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
@@ -274,10 +287,13 @@ class RefreshStep:
     """
 
     def __init__(self, layers, n_q_heads: int, q_pos0: int, img: ImageTable, k: int,
-                 lam: float = 1.0, norm: int = NORM_CAUSAL_ROW, device="cuda"):
+                 lam: float = 1.0, norm: int = NORM_CAUSAL_ROW, device="cuda",
+                 agg: int = AGG_MEAN, rule: int = RANK_COMPOSITE, vnorm_tables=None):
+        """vnorm_tables: optional per-layer value-norm tables (conduit_value_norms)."""
         self.layers = layers
         self.kvs = [kv_desc(L["k"], L["v"], n_q_heads) for L in layers]
         self.q_pos0, self.img, self.k, self.lam, self.norm = q_pos0, img, k, lam, norm
+        self.agg, self.rule, self.vnorm_tables = agg, rule, vnorm_tables
         self.n_q = layers[0]["q"].shape[0]
         nv = img.n_vis
         f32 = dict(dtype=torch.float32, device=device)
@@ -285,6 +301,7 @@ class RefreshStep:
         self.a_acc = torch.zeros(nv, **f32)
         self.shat = torch.zeros(nv, **f32)
         self.c = torch.zeros(img.n_images, **f32)
+        self.quota = torch.zeros(img.n_images, dtype=torch.int32, device=device)
         self.idx = torch.zeros(max(k, 1), dtype=torch.int32, device=device)
         self.pos = torch.zeros(max(k, 1), dtype=torch.int32, device=device)
         self.mask = torch.zeros(nv, dtype=torch.uint8, device=device)
@@ -300,14 +317,17 @@ class RefreshStep:
     def score_and_select(self, stream=None):
         if self.k == 0:
             conduit_select_topk(self.s_acc, self.a_acc, len(self.layers), self.img, self.lam, 0,
-                                self.idx, self.pos, mask_out=self.mask, stream=stream)
+                                self.idx, self.pos, mask_out=self.mask, stream=stream,
+                                rule=self.rule)
             return
         for li, (L, kv) in enumerate(zip(self.layers, self.kvs)):
             conduit_score(kv, L["q"], self.q_pos0, self.img, self.s_acc, self.a_acc,
-                          accumulate=li > 0, norm=self.norm, ws=self.ws_score, stream=stream)
+                          accumulate=li > 0, norm=self.norm, ws=self.ws_score, stream=stream,
+                          agg=self.agg,
+                          vnorm_in=None if self.vnorm_tables is None else self.vnorm_tables[li])
         conduit_select_topk(self.s_acc, self.a_acc, len(self.layers), self.img, self.lam, self.k,
                             self.idx, self.pos, mask_out=self.mask, shat_out=self.shat,
-                            c_out=self.c, stream=stream)
+                            c_out=self.c, stream=stream, rule=self.rule, quota_out=self.quota)
 
     def refresh(self, fresh, stream=None, k_old=None, v_old=None):
         if self.k == 0:

@@ -267,10 +267,10 @@ size_t conduit_score_workspace_bytes(const conduit_kv *kv, int32_t n_q, const co
 }
 
 conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
-                             const conduit_images *img, conduit_norm norm, float scale,
-                             const float *row_lse_in, float *row_lse_out, float *s_acc, float *a_acc,
-                             int32_t accumulate, float *a_out, float *vnorm_out, void *ws, size_t ws_bytes,
-                             hipStream_t stream) {
+                             const conduit_images *img, conduit_norm norm, conduit_agg agg, float scale,
+                             const float *row_lse_in, float *row_lse_out, const float *vnorm_in,
+                             float *s_acc, float *a_acc, int32_t accumulate, float *a_out, float *vnorm_out,
+                             void *ws, size_t ws_bytes, hipStream_t stream) {
   conduit_status st = check_kv(kv);
   if (st) return st;
   if (!q || !aligned16(q)) return fail(CONDUIT_ERR_INVALID_ARG, "q must be non-NULL and 16-byte aligned");
@@ -280,6 +280,8 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
                 (long long)q_pos0 + n_q, kv->n_ctx);
   if (norm != CONDUIT_NORM_CAUSAL_ROW && norm != CONDUIT_NORM_VISUAL_ONLY)
     return fail(CONDUIT_ERR_INVALID_ARG, "norm %d is not a conduit_norm", (int)norm);
+  if (agg != CONDUIT_AGG_MEAN && agg != CONDUIT_AGG_RMS)
+    return fail(CONDUIT_ERR_INVALID_ARG, "agg %d is not a conduit_agg", (int)agg);
   if (!(scale > 0.f) || scale == __builtin_inff()) return fail(CONDUIT_ERR_INVALID_ARG, "scale must be finite and > 0");
   if (!s_acc || !a_acc) return fail(CONDUIT_ERR_INVALID_ARG, "s_acc and a_acc are required");
   if (accumulate != 0 && accumulate != 1) return fail(CONDUIT_ERR_INVALID_ARG, "accumulate must be 0 or 1");
@@ -357,12 +359,15 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   cs.scale_log2 = scale_log2;
   cs.colsum_part = reinterpret_cast<float *>(at(ws, L.colsum));
   cs.vsq_part = reinterpret_cast<float *>(at(ws, L.vsq));
-  e = launch_colsum(cs, D, bf16, stream);
+  cs.vnorm_in = vnorm_in;
+  e = launch_colsum(cs, D, bf16, agg == CONDUIT_AGG_RMS, stream);
   if (e != hipSuccess) return hip_fail(e, "column sums");
 
   FinalizeParams fp{};
   fp.colsum_part = cs.colsum_part;
   fp.vsq_part = cs.vsq_part;
+  fp.vnorm_in = vnorm_in;
+  fp.rms = agg == CONDUIT_AGG_RMS;
   fp.n_kv_heads = kv->n_kv_heads;
   fp.n_vis = img->n_vis;
   fp.n_rows_f = (float)((int64_t)n_q * kv->n_q_heads);
@@ -376,6 +381,20 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   return ok();
 }
 
+conduit_status conduit_value_norms(const conduit_kv *kv, const conduit_images *img, float *vnorm_out,
+                                   hipStream_t stream) {
+  conduit_status st = check_kv(kv);
+  if (st) return st;
+  if (!vnorm_out) return fail(CONDUIT_ERR_INVALID_ARG, "vnorm_out is NULL");
+  ImageTable tbl;
+  st = check_images(img, kv->n_ctx, &tbl);
+  if (st) return st;
+  hipError_t e = launch_value_norms(kv->v, kv->v_stride, kv->n_kv_heads * kv->head_dim,
+                                    kv->dtype == CONDUIT_BF16, tbl, vnorm_out, stream);
+  if (e != hipSuccess) return hip_fail(e, "value norms");
+  return ok();
+}
+
 size_t conduit_select_workspace_bytes(int32_t n_vis, int32_t n_images) {
   (void)n_images;
   if (n_vis < 1) return 0;
@@ -383,12 +402,15 @@ size_t conduit_select_workspace_bytes(int32_t n_vis, int32_t n_images) {
 }
 
 conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32_t n_layers,
-                                   const conduit_images *img, float lambda, int32_t k, int32_t *idx_out,
-                                   int32_t *pos_out, uint8_t *mask_out, float *shat_out, float *c_out, void *ws,
-                                   size_t ws_bytes, hipStream_t stream) {
+                                   const conduit_images *img, float lambda, conduit_rule rule, int32_t k,
+                                   int32_t *idx_out, int32_t *pos_out, uint8_t *mask_out, float *shat_out,
+                                   float *c_out, int32_t *quota_out, void *ws, size_t ws_bytes,
+                                   hipStream_t stream) {
   if (!s_acc || !a_acc) return fail(CONDUIT_ERR_INVALID_ARG, "s_acc and a_acc are required");
   if (n_layers < 1) return fail(CONDUIT_ERR_INVALID_ARG, "n_layers = %d < 1", n_layers);
   if (!(lambda >= 0.f && lambda <= 1.f)) return fail(CONDUIT_ERR_INVALID_ARG, "lambda must lie in [0, 1]");
+  if (rule != CONDUIT_RANK_COMPOSITE && rule != CONDUIT_RANK_ATTENTION && rule != CONDUIT_RANK_EXPLICIT)
+    return fail(CONDUIT_ERR_INVALID_ARG, "rule %d is not a conduit_rule", (int)rule);
   conduit_status st = check_images(img, INT32_MAX, nullptr);
   if (st) return st;
   ImageTable tbl;
@@ -406,10 +428,15 @@ conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32
       e = launch_clear_u8(mask_out, img->n_vis, stream);
       if (e != hipSuccess) return hip_fail(e, "clear mask");
     }
+    if (rule == CONDUIT_RANK_EXPLICIT && quota_out) {
+      e = launch_clear_u8(reinterpret_cast<uint8_t *>(quota_out), (int64_t)img->n_images * 4, stream);
+      if (e != hipSuccess) return hip_fail(e, "clear quotas");
+    }
     return ok();
   }
   SelectParams sp{};
-  sp.s_acc = s_acc;
+  // The attention-only rule ranks A where the composite ranks s (Table 9).
+  sp.s_acc = rule == CONDUIT_RANK_ATTENTION ? a_acc : s_acc;
   sp.a_acc = a_acc;
   sp.n_layers = n_layers;
   sp.lambda = lambda;
@@ -419,7 +446,8 @@ conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32
   sp.mask_out = mask_out;
   sp.shat = shat_out ? shat_out : static_cast<float *>(ws);
   sp.c_out = c_out;
-  e = launch_select(sp, tbl, stream);
+  sp.quota_out = quota_out;
+  e = rule == CONDUIT_RANK_EXPLICIT ? launch_select_explicit(sp, tbl, stream) : launch_select(sp, tbl, stream);
   if (e != hipSuccess) return hip_fail(e, "select");
   return ok();
 }

@@ -201,16 +201,19 @@ struct ColsumParams {
   ImageTable tbl;           // visual index -> sequence position
   int32_t n_vis;
   float scale_log2;
-  float *colsum_part;       // [n_kv_heads][n_vis]
+  float *colsum_part;       // [n_kv_heads][n_vis]: sum of alpha (or alpha^2 for RMS)
   float *vsq_part;          // [n_kv_heads][n_vis]
+  const float *vnorm_in;    // nullable: value norms given, V not read
 };
 
 struct FinalizeParams {
   const float *colsum_part;
   const float *vsq_part;
+  const float *vnorm_in;    // nullable: value norms given
   int32_t n_kv_heads;
   int32_t n_vis;
   float n_rows_f;           // n_q * n_q_heads, as float
+  int32_t rms;              // a = sqrt(colsum / n_rows) (Eq. 4) instead of the mean
   int32_t accumulate;
   float *s_acc;
   float *a_acc;
@@ -229,6 +232,7 @@ struct SelectParams {
   uint8_t *mask_out;        // nullable
   float *shat;              // [n_vis]: caller's shat_out or workspace
   float *c_out;             // nullable
+  int32_t *quota_out;       // nullable (explicit rule)
 };
 
 struct ScatterParams {
@@ -268,9 +272,12 @@ hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipS
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s);
 hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, hipStream_t s);
-hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, hipStream_t s);
+hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s);
+hipError_t launch_value_norms(const void *v, int64_t v_stride, int32_t row_elems, bool bf16,
+                              const ImageTable &tbl, float *out, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t s);
 hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream_t s);
+hipError_t launch_select_explicit(const SelectParams &p, const ImageTable &tbl, hipStream_t s);
 hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
 

@@ -31,7 +31,8 @@ constexpr int kColsumThreads = 512;   // 8 waves x 32 keys
 // value norms are fetched at the start and consumed at the end.
 constexpr int kQChunk = 256;
 
-template <int D>
+// RMS: accumulate alpha^2 (Eq. 4's surrogate) instead of alpha.
+template <int D, bool RMS>
 __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParams p) {
   constexpr int KS = D / 16;
   constexpr int QCH = kQChunk * D / 8;       // 16-byte chunks in a Q chunk
@@ -91,13 +92,16 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) kreg[ks] = as_bf16x8(ld16(krow + ks * 16));
   }
-  // V rows of the block's keys for the value norms, 16 bytes per item.
+  // V rows of the block's keys for the value norms, 16 bytes per item (not
+  // read when the norms are given).
+  const bool read_v = p.vnorm_in == nullptr;
   u32x4 vv[VPT];
 #pragma unroll
   for (int i = 0; i < VPT; ++i) {
     const int vi = tid + kColsumThreads * i;
     const int tv = min(blockIdx.x * kColsumKeysPerBlock + vi / (D / 8), p.n_vis - 1);
-    vv[i] = ld16(Vg + (int64_t)vis_position(img, tv) * p.v_stride + kvh * D + (vi % (D / 8)) * 8);
+    vv[i] = read_v ? ld16(Vg + (int64_t)vis_position(img, tv) * p.v_stride + kvh * D + (vi % (D / 8)) * 8)
+                   : u32x4{0, 0, 0, 0};
   }
   store_chunk(0, 0, qv, bv);
   __syncthreads();
@@ -125,8 +129,11 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
         const f32x4 b1 = *reinterpret_cast<const f32x4 *>(&bs[buf][r0 + 32 + 8 * g + 4 * half]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          part0 += fast_exp2(fmaf(acc0[4 * g + i], p.scale_log2, -b0[i]));
-          part1 += fast_exp2(fmaf(acc1[4 * g + i], p.scale_log2, -b1[i]));
+          // alpha = 2^(c z - b); RMS sums alpha^2 = 2^(2 (c z - b))
+          const float z0 = fmaf(acc0[4 * g + i], p.scale_log2, -b0[i]);
+          const float z1 = fmaf(acc1[4 * g + i], p.scale_log2, -b1[i]);
+          part0 += fast_exp2(RMS ? 2.f * z0 : z0);
+          part1 += fast_exp2(RMS ? 2.f * z1 : z1);
         }
       }
       colsum += part0 + part1;
@@ -141,6 +148,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   // dims (vi % (D/8))*8 .. +7 of key vi / (D/8); the D/8 items of a key sit
   // in consecutive lanes and are summed with lane shuffles.
   static_assert((D / 8) <= 64 && 64 % (D / 8) == 0, "key items within a wave");
+  if (!read_v) return;
 #pragma unroll
   for (int i = 0; i < VPT; ++i) {
     float sq = 0.f;
@@ -161,7 +169,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
 
 // fp32 path: one thread per (visual key, KV head).
 template <int D>
-__global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p) {
+__global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p, bool rms) {
   const int t = blockIdx.x * 64 + threadIdx.x;
   const int kvh = blockIdx.y;
   if (t >= p.n_vis) return;
@@ -180,13 +188,15 @@ __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p) {
     float dot = 0.f;
 #pragma unroll
     for (int e = 0; e < D; ++e) dot = fmaf(q[e], kr[e], dot);
-    colsum += fast_exp2(fmaf(dot, p.scale_log2, -p.row_b[(int64_t)i * p.n_q_heads + hq]));
+    const float z = fmaf(dot, p.scale_log2, -p.row_b[(int64_t)i * p.n_q_heads + hq]);
+    colsum += fast_exp2(rms ? 2.f * z : z);
   }
+  p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
+  if (p.vnorm_in) return;
   float sq = 0.f;
   const float *vr = Vg + pos * p.v_stride + kvh * D;
 #pragma unroll 8
   for (int e = 0; e < D; ++e) sq = fmaf(vr[e], vr[e], sq);
-  p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
   p.vsq_part[(int64_t)kvh * p.n_vis + t] = sq;
 }
 
@@ -196,10 +206,10 @@ __global__ void finalize_kernel(FinalizeParams p) {
   float cs = 0.f, sq = 0.f;
   for (int h = 0; h < p.n_kv_heads; ++h) {
     cs += p.colsum_part[(int64_t)h * p.n_vis + t];
-    sq += p.vsq_part[(int64_t)h * p.n_vis + t];
+    if (!p.vnorm_in) sq += p.vsq_part[(int64_t)h * p.n_vis + t];
   }
-  const float a = cs / p.n_rows_f;
-  const float v = sqrtf(sq);
+  const float a = p.rms ? sqrtf(cs / p.n_rows_f) : cs / p.n_rows_f;
+  const float v = p.vnorm_in ? p.vnorm_in[t] : sqrtf(sq);
   const float s = a * v;
   if (p.accumulate) {
     p.s_acc[t] += s;
@@ -212,19 +222,66 @@ __global__ void finalize_kernel(FinalizeParams p) {
   if (p.vnorm_out) p.vnorm_out[t] = v;
 }
 
+// Value-norm table (Eq. 7's proxy, tabulated when the cache is built): one
+// wave per visual token sums the squares of its row_elems cached values
+// (all KV heads concatenated), 16 bytes per lane and step.
+template <bool BF16>
+__global__ __launch_bounds__(256) void value_norms_kernel(const void *v, int64_t v_stride, int row_elems,
+                                                          ImageTable tbl, float *out) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (t >= tbl.n_vis) return;
+  constexpr int EPC = BF16 ? 8 : 4;  // elements per 16-byte chunk
+  const char *row = static_cast<const char *>(v) + (int64_t)vis_position(tbl, t) * v_stride * (BF16 ? 2 : 4);
+  float sq = 0.f;
+  for (int c = lane; c < row_elems / EPC; c += 64) {
+    const u32x4 w = ld16(row + 16 * c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (BF16) {
+        const float lo = __builtin_bit_cast(float, w[e] << 16);
+        const float hi = __builtin_bit_cast(float, w[e] & 0xffff0000u);
+        sq = fmaf(lo, lo, sq);
+        sq = fmaf(hi, hi, sq);
+      } else {
+        // The element goes through a scalar first: hipcc compiled a bit_cast
+        // of the vector-element lvalue itself into a read of element 0.
+        const uint32_t u = w[e];
+        const float x = __builtin_bit_cast(float, u);
+        sq = fmaf(x, x, sq);
+      }
+    }
+  }
+  sq = wave_sum(sq);
+  if (lane == 0) out[t] = sqrtf(sq);
+}
+
 }  // namespace
 
-hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, hipStream_t s) {
+hipError_t launch_value_norms(const void *v, int64_t v_stride, int32_t row_elems, bool bf16,
+                              const ImageTable &tbl, float *out, hipStream_t s) {
+  ProfScope ps("value_norms", s);
+  const int blocks = (tbl.n_vis + 3) / 4;
+  if (bf16) value_norms_kernel<true><<<blocks, 256, 0, s>>>(v, v_stride, row_elems, tbl, out);
+  else value_norms_kernel<false><<<blocks, 256, 0, s>>>(v, v_stride, row_elems, tbl, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s) {
   if (bf16) {
     dim3 grid((p.n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock, p.n_kv_heads);
     ProfScope ps("colsum", s);
-    if (head_dim == 128) colsum_bf16_kernel<128><<<grid, kColsumThreads, 0, s>>>(p);
-    else colsum_bf16_kernel<64><<<grid, kColsumThreads, 0, s>>>(p);
+    if (head_dim == 128) {
+      if (rms) colsum_bf16_kernel<128, true><<<grid, kColsumThreads, 0, s>>>(p);
+      else colsum_bf16_kernel<128, false><<<grid, kColsumThreads, 0, s>>>(p);
+    } else {
+      if (rms) colsum_bf16_kernel<64, true><<<grid, kColsumThreads, 0, s>>>(p);
+      else colsum_bf16_kernel<64, false><<<grid, kColsumThreads, 0, s>>>(p);
+    }
   } else {
     dim3 grid((p.n_vis + 63) / 64, p.n_kv_heads);
     ProfScope ps("colsum_f32", s);
-    if (head_dim == 128) colsum_f32_kernel<128><<<grid, 64, 0, s>>>(p);
-    else colsum_f32_kernel<64><<<grid, 64, 0, s>>>(p);
+    if (head_dim == 128) colsum_f32_kernel<128><<<grid, 64, 0, s>>>(p, rms);
+    else colsum_f32_kernel<64><<<grid, 64, 0, s>>>(p, rms);
   }
   return hipGetLastError();
 }

@@ -12,6 +12,7 @@
 //  5. ordered compaction: everything above the threshold plus the first
 //     `need` entries equal to it in index order (ties to the lower index),
 //     with two block scans, so idx/pos come out ascending.
+// The explicit-quota rule (select_explicit_kernel) shares steps 1-2.
 #include "common.h"
 
 namespace conduit {
@@ -201,6 +202,45 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Ima
   }
 }
 
+// Steps 1-2 with the image table (s_off) in LDS: g_j into s_g (one wave per
+// image, lane-strided partial sums, butterfly reduction: a fixed order), then
+// g_bar and c_j = (1 - lambda) + lambda g_j / g_bar into s_c, exactly 1 where
+// g_j = g_bar or g_bar = 0.  All 1024 threads take part; ends synchronised.
+__device__ void image_coefficients(const SelectParams &p, int K, const int *s_off, float *s_g,
+                                   float *s_c, bool write_c) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float n_layers = (float)p.n_layers;
+  for (int j = wave; j < K; j += kWaves) {
+    const int a = s_off[j], b = s_off[j + 1];
+    float tot = 0.f;
+    for (int t0 = a; t0 < b; t0 += 16 * 64) {  // 16 independent loads per round
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int t = t0 + 64 * u + lane;
+        v[u] = t < b ? p.a_acc[t] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) tot += v[u];
+    }
+    tot = wave_sum(tot);
+    if (lane == 0) s_g[j] = tot / (n_layers * (float)(b - a));
+  }
+  __syncthreads();
+  if (wave == 0) {
+    float acc = 0.f;
+    for (int j = lane; j < K; j += 64) acc += s_g[j];
+    const float g_bar = wave_sum(acc) / (float)K;
+    for (int j = lane; j < K; j += 64) {
+      const float x = s_g[j] / g_bar;
+      const float c = (g_bar == 0.f || x == 1.f) ? 1.f : (1.f - p.lambda) + p.lambda * x;
+      s_c[j] = c;
+      if (write_c && p.c_out) p.c_out[j] = c;
+    }
+  }
+  __syncthreads();
+}
+
 // Register-resident variant for n_vis <= 1024 * PER: thread t owns visual
 // tokens [t*PER, t*PER + PER), so scores are read once and the compaction is
 // in index order without re-reading.  The radix select first fixes the bits
@@ -250,37 +290,8 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
   }
   __syncthreads();
 
-  // 1. per-image mean attention (one wave per image, fixed-order sums)
-  for (int j = wave; j < K; j += kWaves) {
-    const int a = s_off[j], b = s_off[j + 1];
-    float tot = 0.f;
-    for (int t0 = a; t0 < b; t0 += 16 * 64) {  // 16 independent loads per round
-      float v[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int t = t0 + 64 * u + lane;
-        v[u] = t < b ? p.a_acc[t] : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 16; ++u) tot += v[u];
-    }
-    tot = wave_sum(tot);
-    if (lane == 0) s_g[j] = tot / (n_layers * (float)(b - a));
-  }
-  __syncthreads();
-  // 2. coefficients: (1 - lambda) + lambda * g_j / g_bar, exactly 1 at g_j = g_bar
-  if (wave == 0) {
-    float acc = 0.f;
-    for (int j = lane; j < K; j += 64) acc += s_g[j];
-    const float g_bar = wave_sum(acc) / (float)K;
-    for (int j = lane; j < K; j += 64) {
-      const float x = s_g[j] / g_bar;
-      const float c = (g_bar == 0.f || x == 1.f) ? 1.f : (1.f - p.lambda) + p.lambda * x;
-      s_c[j] = c;
-      if (p.c_out) p.c_out[j] = c;
-    }
-  }
-  __syncthreads();
+  // 1-2. per-image mean attention and coefficients
+  image_coefficients(p, K, s_off, s_g, s_c, true);
 
   // 3. composite scores (s / |L|) * c_pi(t) of this thread's tokens
   int j0 = 0;  // image of the first token
@@ -422,6 +433,163 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
   }
 }
 
+// Explicit per-image quotas: one workgroup per image.  Every workgroup
+// derives the same c_j (steps 1-2) and the same quotas k_j ~ c_j n_j:
+// largest remainder in float32, image order, shares capped at n_j with the
+// surplus re-apportioned, all-zero weights falling back to n_j, remaining
+// seats to the largest fractional parts (ties to the lower image).
+// Workgroup j then keeps the k_j largest s_t of image j: the k_j-th largest
+// key by bisection on the fp32 bit patterns (s >= 0), then everything above
+// it plus the lowest-index entries equal to it, compacted in index order
+// behind the quotas of the images before j.
+__global__ __launch_bounds__(kSelThreads) void select_explicit_kernel(SelectParams p, ImageTable tbl) {
+  __shared__ float s_g[kMaxImages];
+  __shared__ float s_c[kMaxImages];
+  __shared__ float s_share[kMaxImages];
+  __shared__ float s_frac[kMaxImages];
+  __shared__ int s_off[kMaxImages + 1];
+  __shared__ int s_delta[kMaxImages];
+  __shared__ int s_quota[kMaxImages];
+  __shared__ int s_live[kMaxImages];
+  __shared__ int s_wave[kWaves];
+  __shared__ float s_total;
+  __shared__ int s_left, s_capped, s_bysize, s_rest;
+
+  const int tid = threadIdx.x;
+  const int K = tbl.n_images, jimg = blockIdx.x;
+  for (int j = tid; j <= K; j += kSelThreads) {
+    s_off[j] = tbl.off[j];
+    if (j < K) {
+      s_delta[j] = tbl.pos[j] - tbl.off[j];
+      s_quota[j] = 0;
+      s_live[j] = 1;
+    }
+  }
+  if (tid == 0) s_left = p.k;
+  __syncthreads();
+  image_coefficients(p, K, s_off, s_g, s_c, jimg == 0);
+
+  // quotas
+  for (;;) {
+    if (tid == 0) {
+      float total = 0.f;
+      for (int j = 0; j < K; ++j)
+        if (s_live[j]) total = __fadd_rn(total, __fmul_rn(s_c[j], (float)(s_off[j + 1] - s_off[j])));
+      int by_size = total == 0.f;
+      if (by_size) {
+        total = 0.f;
+        for (int j = 0; j < K; ++j)
+          if (s_live[j]) total = __fadd_rn(total, (float)(s_off[j + 1] - s_off[j]));
+      }
+      s_total = total;
+      s_bysize = by_size;
+      s_capped = 0;
+    }
+    __syncthreads();
+    const float total = s_total;
+    const float left = (float)s_left;
+    for (int j = tid; j < K; j += kSelThreads) {
+      if (!s_live[j]) continue;
+      const float nj = (float)(s_off[j + 1] - s_off[j]);
+      const float w = s_bysize ? nj : __fmul_rn(s_c[j], nj);
+      const float share = __fdiv_rn(__fmul_rn(left, w), total);
+      s_share[j] = share;
+      if (share >= nj) atomicAdd(&s_capped, 1);
+    }
+    __syncthreads();
+    if (s_capped == 0) break;
+    for (int j = tid; j < K; j += kSelThreads) {
+      const int nj = s_off[j + 1] - s_off[j];
+      if (s_live[j] && s_share[j] >= (float)nj) {
+        s_quota[j] = nj;
+        s_live[j] = 0;
+        atomicSub(&s_left, nj);
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0) s_rest = s_left;
+  __syncthreads();
+  for (int j = tid; j < K; j += kSelThreads) {
+    s_frac[j] = -1.f;
+    if (!s_live[j]) continue;
+    const int nj = s_off[j + 1] - s_off[j];
+    const int base = min((int)floorf(s_share[j]), nj);
+    s_quota[j] = base;
+    s_frac[j] = __fsub_rn(s_share[j], (float)base);
+    atomicSub(&s_rest, base);
+  }
+  __syncthreads();
+  {
+    int plus[(kMaxImages + kSelThreads - 1) / kSelThreads] = {};
+    for (int j = tid, i = 0; j < K; j += kSelThreads, ++i) {
+      const int nj = s_off[j + 1] - s_off[j];
+      if (!s_live[j] || s_quota[j] >= nj) continue;
+      int rank = 0;  // candidates ahead of j: larger fraction, or equal and lower index
+      for (int u = 0; u < K; ++u) {
+        const int nu = s_off[u + 1] - s_off[u];
+        if (!s_live[u] || s_quota[u] >= nu) continue;
+        rank += s_frac[u] > s_frac[j] || (s_frac[u] == s_frac[j] && u < j);
+      }
+      plus[i] = rank < s_rest;
+    }
+    __syncthreads();
+    for (int j = tid, i = 0; j < K; j += kSelThreads, ++i) s_quota[j] += plus[i];
+  }
+  __syncthreads();
+  if (jimg == 0 && p.quota_out)
+    for (int j = tid; j < K; j += kSelThreads) p.quota_out[j] = s_quota[j];
+
+  // selection inside image jimg
+  const int a = s_off[jimg], b = s_off[jimg + 1];
+  const int kq = s_quota[jimg];
+  int out0 = 0;
+  for (int j = 0; j < jimg; ++j) out0 += s_quota[j];
+  const float inv_layers = 1.f / (float)p.n_layers;
+  const float cj = s_c[jimg];
+  auto block_count = [&](uint32_t thr, bool strict) {
+    int c = 0;
+    for (int t = a + tid; t < b; t += kSelThreads) {
+      const uint32_t key = order_key(p.s_acc[t]);
+      c += strict ? key > thr : key >= thr;
+    }
+    int total;
+    (void)block_exclusive_scan(c, s_wave, total);
+    return total;
+  };
+  uint32_t thr = 0;
+  if (kq > 0) {
+    for (int bit = 31; bit >= 0; --bit) {
+      const uint32_t cand = thr | (1u << bit);
+      if (block_count(cand, false) >= kq) thr = cand;
+    }
+  }
+  const int need_eq = kq > 0 ? kq - block_count(thr, true) : 0;
+  int eq_base = 0, sel_base = 0;
+  for (int t0 = a; t0 < b; t0 += kSelThreads) {
+    const int t = t0 + tid;
+    const bool live = t < b;
+    const float sv = live ? p.s_acc[t] : 0.f;
+    const uint32_t key = order_key(sv);
+    const bool gt = live && kq > 0 && key > thr;
+    const bool eq = live && kq > 0 && key == thr;
+    int n_eq, n_sel;
+    const int eq_before = eq_base + block_exclusive_scan(eq ? 1 : 0, s_wave, n_eq);
+    const bool sel = gt || (eq && eq_before < need_eq);
+    const int rank = sel_base + block_exclusive_scan(sel ? 1 : 0, s_wave, n_sel);
+    if (live) {
+      if (sel && rank < kq && out0 + rank < p.k) {
+        p.idx_out[out0 + rank] = t;
+        p.pos_out[out0 + rank] = t + s_delta[jimg];
+      }
+      if (p.mask_out) p.mask_out[t] = sel ? 1 : 0;
+      if (p.shat) p.shat[t] = (sv * inv_layers) * cj;
+    }
+    eq_base += n_eq;
+    sel_base += n_sel;
+  }
+}
+
 __global__ void clear_u8_kernel(uint8_t *p, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0;
@@ -434,6 +602,12 @@ hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream
   if (tbl.n_vis <= kSelThreads * 16) select_regs_kernel<16><<<1, kSelThreads, 0, s>>>(p, tbl);
   else if (tbl.n_vis <= kSelThreads * 32) select_regs_kernel<32><<<1, kSelThreads, 0, s>>>(p, tbl);
   else select_kernel<<<1, kSelThreads, 0, s>>>(p, tbl);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_explicit(const SelectParams &p, const ImageTable &tbl, hipStream_t s) {
+  ProfScope ps("select_explicit", s);
+  select_explicit_kernel<<<tbl.n_images, kSelThreads, 0, s>>>(p, tbl);
   return hipGetLastError();
 }
 

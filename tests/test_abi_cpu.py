@@ -64,11 +64,12 @@ def kv(**over):
 IMG = api.ImageTable([256], [0, 1024])
 
 
-def score(kvd=None, q=FAKE, n_q=64, q_pos0=1280, img=IMG, norm=0, scale=0.088, s=FAKE, a=FAKE,
+def score(kvd=None, q=FAKE, n_q=64, q_pos0=1280, img=IMG, norm=0, agg=0, scale=0.088, s=FAKE, a=FAKE,
           acc=0, ws=FAKE, ws_bytes=1 << 30):
     kvd = kvd or kv()
     return api.lib().conduit_score(ctypes.byref(kvd), q, n_q, q_pos0, ctypes.byref(img.desc), norm,
-                                   scale, None, None, s, a, acc, None, None, ws, ws_bytes, None)
+                                   agg, scale, None, None, None, s, a, acc, None, None, ws, ws_bytes,
+                                   None)
 
 
 @pytest.mark.parametrize("case,status", [
@@ -84,6 +85,8 @@ def score(kvd=None, q=FAKE, n_q=64, q_pos0=1280, img=IMG, norm=0, scale=0.088, s
     (dict(n_q=0), api.ERR_INVALID_ARG),
     (dict(q_pos0=1300), api.ERR_INVALID_ARG),
     (dict(norm=5), api.ERR_INVALID_ARG),
+    (dict(agg=2), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(n_kv_heads=512, n_q_heads=512, k_stride=65536, v_stride=65536)), api.ERR_UNSUPPORTED),
     (dict(scale=0.0), api.ERR_INVALID_ARG),
     (dict(scale=float("nan")), api.ERR_INVALID_ARG),
     (dict(s=0), api.ERR_INVALID_ARG),
@@ -108,15 +111,15 @@ def test_image_table_n_vis_mismatch():
     assert score(img=img) == api.ERR_INVALID_ARG
 
 
-def select(s=FAKE, a=FAKE, n_layers=1, img=IMG, lam=1.0, k=102, idx=FAKE, pos=FAKE, ws=FAKE,
+def select(s=FAKE, a=FAKE, n_layers=1, img=IMG, lam=1.0, rule=0, k=102, idx=FAKE, pos=FAKE, ws=FAKE,
            ws_bytes=1 << 20):
-    return api.lib().conduit_select_topk(s, a, n_layers, ctypes.byref(img.desc), lam, k, idx, pos,
-                                         None, None, None, ws, ws_bytes, None)
+    return api.lib().conduit_select_topk(s, a, n_layers, ctypes.byref(img.desc), lam, rule, k, idx,
+                                         pos, None, None, None, None, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("case", [dict(s=0), dict(n_layers=0), dict(lam=-0.1), dict(lam=1.5),
                                   dict(lam=float("nan")), dict(k=-1), dict(k=1025), dict(idx=0),
-                                  dict(pos=0)])
+                                  dict(pos=0), dict(rule=3), dict(rule=-1)])
 def test_select_rejects(case):
     assert select(**case) == api.ERR_INVALID_ARG
 
@@ -183,3 +186,12 @@ def test_kernel_timing_without_records():
     assert L.conduit_profile_read(-1, ctypes.byref(name), ctypes.byref(ms)) == api.ERR_INVALID_ARG
     assert L.conduit_profile_read(0, None, None) == api.ERR_INVALID_ARG
     assert L.conduit_profile_enable(0) == api.OK
+
+
+def test_value_norms_rejects():
+    L = api.lib()
+    out = ctypes.c_void_p(FAKE)
+    assert L.conduit_value_norms(ctypes.byref(kv()), ctypes.byref(IMG.desc), None, None) == api.ERR_INVALID_ARG
+    assert L.conduit_value_norms(ctypes.byref(kv(v=0)), ctypes.byref(IMG.desc), out, None) == api.ERR_INVALID_ARG
+    bad = api.ImageTable([1500], [0, 1024])  # runs past the cache
+    assert L.conduit_value_norms(ctypes.byref(kv()), ctypes.byref(bad.desc), out, None) == api.ERR_INVALID_ARG

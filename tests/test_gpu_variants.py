@@ -1,0 +1,240 @@
+"""The scoring and selection variants on the GPU against the CPU oracle:
+RMS aggregation (Eq. 4), the value-norm table (Sec. 4.3), the attention-only
+and explicit-quota rules (Table 9, App. D), and scored-layer subsets."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import conduit_oracle as O
+from paper_2609_05821_amd import api, workloads as W
+from tests.gpu_helpers import DEV, assert_attention, assert_scores, assert_selection, bits, to_dev, to_f64
+from tests.oracle_pins import _exact_quotas
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "cfg1_fp32_mha": lambda: W.config(1),
+    "cfg2_bf16_gqa": lambda: W.config(2),
+    "ragged_bf16_gqa7": lambda: W.custom(1, 28, 4, 128, 19, 13, [37, 250, 301], 5, "bf16", n_sinks=6,
+                                         n_relevant=1, seed=3),
+    "ragged_bf16_d64_gqa4": lambda: W.custom(1, 8, 2, 64, 40, 7, [100, 33], 3, "bf16", seed=4),
+    "ragged_fp32_d128_gqa2": lambda: W.custom(1, 4, 2, 128, 5, 3, [20, 45, 11], 2, "f32", seed=6),
+}
+
+
+def score(w, L, kv, q, agg=O.AGG_MEAN, norm=O.NORM_CAUSAL_ROW, vnorm_in=None):
+    nv = w.n_vis
+    f32 = dict(dtype=torch.float32, device=DEV)
+    out = {x: torch.zeros(nv, **f32) for x in ("a", "v", "s", "A")}
+    out["lse"] = torch.zeros((w.n_q, w.n_q_heads), **f32)
+    api.conduit_score(kv, q, w.q_pos0, api.ImageTable(w.img_pos, w.img_off), out["s"], out["A"],
+                      norm=norm, agg=agg, row_lse_out=out["lse"], a_out=out["a"], vnorm_out=out["v"],
+                      vnorm_in=vnorm_in)
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("norm", [O.NORM_CAUSAL_ROW, O.NORM_VISUAL_ONLY], ids=["causal", "visual"])
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_rms_aggregation_matches_oracle(case, norm):
+    w = CASES[case]()
+    L = w.layer(0, fresh=False)
+    k, v, q = (to_dev(L[x]) for x in ("k", "v", "q"))
+    got = score(w, L, api.kv_desc(k, v, w.n_q_heads), q, agg=O.AGG_RMS, norm=norm)
+    a, vn, lse = O.score_layer(L["q"], L["k"], L["v"], w.q_pos0, w.img_pos, w.img_off, norm=norm,
+                               agg=O.AGG_RMS)
+    assert_scores(to_f64(got["a"]), a, what="RMS a_t")
+    assert_scores(to_f64(got["s"]), a * vn, what="s")
+    assert_scores(to_f64(got["A"]), a, what="A")
+    assert_scores(to_f64(got["lse"]), lse, what="row lse")
+
+
+@pytest.mark.parametrize("case", sorted(CASES) + ["cfg4_16k"])
+def test_value_norm_table(case):
+    """conduit_value_norms equals the oracle's norms; scoring with the table
+    gives the oracle's scores and does not read V (V is overwritten with NaN
+    before that call)."""
+    w = W.config(4) if case == "cfg4_16k" else CASES[case]()
+    L = w.layer(0, fresh=False)
+    k, v, q = (to_dev(L[x]) for x in ("k", "v", "q"))
+    kv = api.kv_desc(k, v, w.n_q_heads)
+    img = api.ImageTable(w.img_pos, w.img_off)
+    table = torch.empty(w.n_vis, dtype=torch.float32, device=DEV)
+    api.conduit_value_norms(kv, img, table)
+    torch.cuda.synchronize()
+    vn = O.value_norms(L["v"], w.img_pos, w.img_off)
+    assert_scores(to_f64(table), vn, what="||V_t|| table")
+    v.fill_(float("nan"))
+    got = score(w, L, kv, q, vnorm_in=table)
+    a, _, lse = O.score_layer(L["q"], L["k"], L["v"], w.q_pos0, w.img_pos, w.img_off)
+    assert np.array_equal(bits(got["v"]), bits(table)), "vnorm_out must be the table"
+    assert_scores(to_f64(got["a"]), a, what="a_t")
+    assert_scores(to_f64(got["s"]), a * vn, what="s")
+    assert_scores(to_f64(got["lse"]), lse, what="row lse")
+
+
+def layout(sizes, gap=3, start=5):
+    pos, off, cur = [], [0], start
+    for n in sizes:
+        pos.append(cur)
+        cur += n + gap
+        off.append(off[-1] + n)
+    return np.array(pos), np.array(off)
+
+
+def run_select(s_acc, a_acc, n_layers, img_pos, img_off, lam, k, rule):
+    img = api.ImageTable(img_pos, img_off)
+    nv, K = img.n_vis, len(img_pos)
+    s = torch.from_numpy(s_acc.astype(np.float32)).to(DEV)
+    a = torch.from_numpy(a_acc.astype(np.float32)).to(DEV)
+    out = {"idx": torch.full((max(k, 1),), -1, dtype=torch.int32, device=DEV),
+           "pos": torch.full((max(k, 1),), -1, dtype=torch.int32, device=DEV),
+           "mask": torch.full((nv,), 7, dtype=torch.uint8, device=DEV),
+           "shat": torch.zeros(nv, device=DEV), "c": torch.zeros(K, device=DEV),
+           "quota": torch.full((K,), -1, dtype=torch.int32, device=DEV)}
+    api.conduit_select_topk(s, a, n_layers, img, lam, k, out["idx"], out["pos"], mask_out=out["mask"],
+                            shat_out=out["shat"], c_out=out["c"], rule=rule, quota_out=out["quota"])
+    torch.cuda.synchronize()
+    return {key: val.cpu().numpy() for key, val in out.items()}
+
+
+SIZES = {
+    "one_token": [1],
+    "single_image_ragged": [1000],
+    "three_images": [37, 250, 301],
+    "sixteen_images": [1024] * 16,
+    "many_small": [7] * 256,
+    "long_document": [1024] * 64,
+}
+
+
+def inputs(name, lam):
+    rng = np.random.default_rng(zlib.crc32(f"{name}/{lam}".encode()))
+    img_pos, img_off = layout(SIZES[name])
+    nv = int(img_off[-1])
+    a = rng.random(nv) * 1e-3 * np.repeat(rng.random(len(img_pos)) * 4, np.diff(img_off))
+    s = a * rng.lognormal(0, 0.5, nv) * 3
+    return img_pos, img_off, s, a
+
+
+@pytest.mark.parametrize("lam", [0.0, 1.0])
+@pytest.mark.parametrize("name", sorted(SIZES))
+def test_attention_rule(name, lam):
+    img_pos, img_off, s, a = inputs(name, lam)
+    nv = int(img_off[-1])
+    for k in sorted({1, max(1, nv // 10), nv}):
+        got = run_select(s, a, 3, img_pos, img_off, lam, k, O.RANK_ATTENTION)
+        A = a.astype(np.float32).astype(np.float64)
+        _, pi = O.visual_layout(img_pos, img_off)
+        _, _, c = O.image_coefficients(A, 3, img_off, lam)
+        assert_scores(got["shat"], O.composite_score(A / 3, c, pi), rtol=1e-5, what="s_hat (A)")
+        ref_idx = O.topk_select(got["shat"].astype(np.float64), k)  # bit-exact on the GPU's scores
+        np.testing.assert_array_equal(got["idx"][:k], ref_idx)
+
+
+@pytest.mark.parametrize("lam", [0.0, 0.5, 1.0])
+@pytest.mark.parametrize("name", sorted(SIZES))
+def test_explicit_rule(name, lam):
+    """Quotas equal the oracle's away from float near-ties (and are valid
+    within one seat of its exact shares everywhere); inside each image the
+    selection is the brute-force top-k_j of s with lower-index ties."""
+    img_pos, img_off, s, a = inputs(name, lam)
+    nv, K = int(img_off[-1]), len(img_pos)
+    n = np.diff(img_off)
+    s32 = s.astype(np.float32).astype(np.float64)
+    A = a.astype(np.float32).astype(np.float64)
+    _, _, c = O.image_coefficients(A, 3, img_off, lam)
+    P, pi = O.visual_layout(img_pos, img_off)
+    for k in sorted({0, 1, max(1, nv // 10), nv // 2, nv}):
+        got = run_select(s, a, 3, img_pos, img_off, lam, k, O.RANK_EXPLICIT)
+        q = got["quota"]
+        assert q.sum() == k and (q >= 0).all() and (q <= n).all(), q
+        if k == 0:
+            assert not got["mask"].any()
+            continue
+        ref_q = O.explicit_quotas(c, n, k)
+        _, share = _exact_quotas(c, n.tolist(), k)
+        fr = sorted(float(x - int(x)) for x in share if x > 0)
+        near = any(abs(float(x) - round(float(x))) < 1e-4 for x in share if x > 0) or \
+            any(bb - aa < 1e-4 for aa, bb in zip(fr, fr[1:]))
+        if not near:
+            np.testing.assert_array_equal(q, ref_q)
+        assert np.abs(q - ref_q).max() <= 1
+        expect = []
+        for j in range(K):
+            lo = int(img_off[j])
+            expect += (lo + O.topk_select(s32[lo:lo + n[j]], int(q[j]))).tolist()
+        expect = np.sort(np.array(expect, dtype=np.int64))
+        np.testing.assert_array_equal(got["idx"][:k], expect)
+        np.testing.assert_array_equal(got["pos"][:k], P[expect])
+        m = np.zeros(nv, np.uint8)
+        m[expect] = 1
+        np.testing.assert_array_equal(got["mask"], m)
+        assert_scores(got["c"], c, rtol=1e-5, what="c_j")
+        assert_scores(got["shat"], O.composite_score(s32 / 3, c, pi), rtol=1e-5, what="s_hat")
+
+
+def test_scored_layer_subset_end_to_end():
+    """Scoring layers {0, 2} of a three-layer workload and selecting with
+    |L| = 2 equals the oracle over those layers; merge and refresh follow."""
+    w = W.config(3, n_layers=3)
+    k = w.budgets["10%"]
+    layers_np = [w.layer(li) for li in range(3)]
+    sub = [layers_np[0], layers_np[2]]
+    layers = [{"k": to_dev(L["k"]), "v": to_dev(L["v"]), "q": to_dev(L["q"])} for L in sub]
+    img = api.ImageTable(w.img_pos, w.img_off)
+    step = api.RefreshStep(layers, w.n_q_heads, w.q_pos0, img, k, device=DEV)
+    step.score_and_select()
+    torch.cuda.synchronize()
+    ref = O.select([{"q": L["q"], "k": L["k"], "v": L["v"]} for L in sub], w.q_pos0, w.img_pos,
+                   w.img_off, k)
+    assert_scores(to_f64(step.shat), ref["s_hat"], what="s_hat")
+    assert_selection(step.idx[:k].cpu().numpy(), ref["s_hat"], k)
+
+
+@pytest.mark.parametrize("agg,rule", [(O.AGG_RMS, O.RANK_COMPOSITE), (O.AGG_MEAN, O.RANK_ATTENTION),
+                                      (O.AGG_MEAN, O.RANK_EXPLICIT)])
+def test_variant_step_end_to_end(agg, rule):
+    """A whole step with a variant (and the value-norm tables): scores and
+    selection against the oracle, then the refresh of the selected rows."""
+    w = W.config(3, n_layers=2)
+    k = w.budgets["20%"]
+    layers_np = [w.layer(li) for li in range(2)]
+    layers = [{"k": to_dev(L["k"]), "v": to_dev(L["v"]), "q": to_dev(L["q"])} for L in layers_np]
+    img = api.ImageTable(w.img_pos, w.img_off)
+    tables = []
+    for L in layers:
+        t = torch.empty(w.n_vis, dtype=torch.float32, device=DEV)
+        api.conduit_value_norms(api.kv_desc(L["k"], L["v"], w.n_q_heads), img, t)
+        tables.append(t)
+    step = api.RefreshStep(layers, w.n_q_heads, w.q_pos0, img, k, device=DEV, agg=agg, rule=rule,
+                           vnorm_tables=tables)
+    step.score_and_select()
+    torch.cuda.synchronize()
+    ref = O.select([{"q": L["q"], "k": L["k"], "v": L["v"]} for L in layers_np], w.q_pos0,
+                   w.img_pos, w.img_off, k, agg=agg, rule=rule)
+    idx = step.idx[:k].cpu().numpy()
+    assert_scores(to_f64(step.shat), ref["s_hat"], what="s_hat")
+    if rule == O.RANK_EXPLICIT:
+        q = step.quota.cpu().numpy()
+        assert q.sum() == k and np.abs(q - ref["quota"]).max() <= 1
+        n = np.diff(w.img_off)
+        for j in range(len(n)):  # per image: a valid top-q_j of the oracle's s
+            lo = int(w.img_off[j])
+            mine = idx[(idx >= lo) & (idx < lo + n[j])] - lo
+            assert len(mine) == q[j]
+            assert_selection(mine, ref["s"][lo:lo + n[j]], int(q[j]))
+    else:
+        assert_selection(idx, ref["s_hat"], k)
+    fresh = [{"k_new": to_dev(L["k_star"][idx]), "v_new": to_dev(L["v_star"][idx]),
+              "q_sel": to_dev(L["q_star"][idx])} for L in layers_np]
+    step.refresh(fresh)
+    torch.cuda.synchronize()
+    P = w.vis_positions()
+    rows = [0, k // 2, k - 1]
+    for li, L in enumerate(layers_np):
+        _, _, o_ref, _ = O.refresh_layer(L["k"], L["v"], P[idx], L["k_star"][idx], L["v_star"][idx],
+                                         L["q_star"][idx], rows=rows)
+        assert_attention(to_f64(step.out[li][:k])[rows], o_ref[rows], w.dtype, what=f"O layer {li}")
