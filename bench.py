@@ -197,6 +197,25 @@ def main():
     # Selection must be the same every step (deterministic).
     assert torch.equal(step.idx[:k], idx0), "selection changed between steps"
 
+    # Variants on the same workload: the value-norm table (built once per
+    # cache), scoring that reads the table instead of V, RMS aggregation, and
+    # the attention-only and explicit-quota selection rules.
+    table = torch.empty(w.n_vis, dtype=torch.float32, device=dev)
+    quota = torch.empty(w.n_images, dtype=torch.int32, device=dev)
+    variants_ms = {
+        "value_norms": timed(lambda: api.conduit_value_norms(kv, img, table)),
+        "score_vnorm_table": timed(lambda: api.conduit_score(kv, q, w.q_pos0, img, step.s_acc,
+                                                             step.a_acc, ws=step.ws_score,
+                                                             vnorm_in=table)),
+        "score_rms": timed(lambda: api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc,
+                                                     ws=step.ws_score, agg=api.AGG_RMS)),
+    }
+    api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score)
+    for name, rule in (("select_attention", api.RANK_ATTENTION), ("select_explicit", api.RANK_EXPLICIT)):
+        variants_ms[name] = timed(lambda rule=rule: api.conduit_select_topk(
+            step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos, mask_out=step.mask,
+            shat_out=step.shat, c_out=step.c, rule=rule, quota_out=quota))
+
     # Algorithmic work.
     H, d, hkv = w.n_q_heads, w.head_dim, w.n_kv_heads
     refresh_flops = 4.0 * H * d * float(np.sum(pos_np + 1))
@@ -207,6 +226,8 @@ def main():
     score_flops = 2.0 * d * H * sum(w.q_pos0 + i + 1 for i in range(w.n_q)) + \
         2.0 * d * H * w.n_q * w.n_vis
     scatter_bytes = 2 * 2 * k * hkv * d * e
+    vnorm_bytes = w.n_vis * hkv * d * e + w.n_vis * 4
+    score_table_bytes = score_bytes - w.n_vis * hkv * d * e + w.n_vis * 4
     refresh_tflops = refresh_flops / (ms["refresh"] * 1e-3) / 1e12
     attn_ms = kernels_ms["attn_values"]["mean"]
     attn_tflops = refresh_flops / (attn_ms * 1e-3) / 1e12
@@ -266,6 +287,14 @@ def main():
             "gbs": score_bytes / (ms["score"] * 1e-3) / 1e9,
             "hbm_frac": score_bytes / (ms["score"] * 1e-3) / 1e9 / PEAK_HBM_GBS,
             "mfma_frac": score_flops / (ms["score"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        },
+        "variants_ms": variants_ms,
+        "variants_bytes": {
+            "value_norms": vnorm_bytes,
+            "value_norms_gbs": vnorm_bytes / (variants_ms["value_norms"]["mean"] * 1e-3) / 1e9,
+            "score_vnorm_table": score_table_bytes,
+            "score_vnorm_table_gbs": score_table_bytes /
+            (variants_ms["score_vnorm_table"]["mean"] * 1e-3) / 1e9,
         },
         "scatter_gbs": scatter_bytes / (ms["scatter"] * 1e-3) / 1e9,
         "refresh_exps_per_s": refresh_exps / (ms["refresh"] * 1e-3),
