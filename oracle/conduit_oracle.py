@@ -40,6 +40,14 @@ Readings of points the paper leaves open (labels used below):
       float32 in image order (floating point decides integers there, so the
       decision is taken in the kernel's precision).  Within an image the k_j
       largest s_t are kept (R6 ties).
+  R27 the request's text (every position outside the images: changed prefix,
+      separators, span) is processed normally (Sec. 3.1): its rows get fresh
+      K/V and attend like the selected visual rows, outside the budget; a
+      step's recompute rows are the selected visual positions followed by the
+      text positions;
+  R28 a paged cache keeps token t in row t mod P of page table[t div P]
+      (block-table KV storage of a serving engine, Sec. 4.3); it holds the same
+      logical cache as the contiguous layout, so every result is the same.
 
 Inputs are numpy arrays; bf16 data arrives as raw uint16 bit patterns and is
 decoded here (the oracle never sees a value the GPU path produced).
@@ -385,6 +393,39 @@ def select(layers, q_pos0, img_pos, img_off, k, lam=1.0, norm=NORM_CAUSAL_ROW, s
     s_hat = composite_score(base, c, pi)
     idx, pos, mask = refresh_mask(s_hat, k, img_pos, img_off)
     out.update({"s_hat": s_hat, "idx": idx, "pos": pos, "mask": mask})
+    return out
+
+
+# --------------------------------------------------------------------------
+# Text rows and paged caches
+# --------------------------------------------------------------------------
+
+def text_positions(n_ctx, img_pos, img_off):
+    """Positions 0..n_ctx-1 that hold no visual token: the request's text,
+    processed normally (Sec. 3.1, R27)."""
+    P_vis, _ = visual_layout(img_pos, img_off)
+    is_visual = np.zeros(int(n_ctx), dtype=bool)
+    is_visual[P_vis] = True
+    return np.flatnonzero(~is_visual).astype(np.int64)
+
+
+def recompute_rows(sel_pos, text_pos):
+    """The rows one layer recomputes: selected visual rows, then text rows
+    (R27)."""
+    return np.concatenate([np.asarray(sel_pos, np.int64), np.asarray(text_pos, np.int64)])
+
+
+def paged_to_contiguous(pages, block_table, n_ctx):
+    """The logical cache a page pool holds (R28).
+
+    pages [n_pages, P, H_kv, d]; block_table[i] is the page of tokens
+    i*P .. i*P + P - 1.  Returns [n_ctx, H_kv, d].
+    """
+    pages = np.asarray(pages)
+    P = pages.shape[1]
+    out = np.empty((int(n_ctx),) + pages.shape[2:], dtype=pages.dtype)
+    for t in range(int(n_ctx)):
+        out[t] = pages[int(block_table[t // P]), t % P]
     return out
 
 

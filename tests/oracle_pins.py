@@ -29,7 +29,14 @@ What pins what:
                           ranking;
   * explicit quotas      hand-worked apportionments (proportional, capped,
                           tied), an exact rational implementation on random
-                          cases away from ties, and brute-force in-image top-k.
+                          cases away from ties, and brute-force in-image top-k;
+  * text rows            brute-force set complement of the image runs; with
+                          every visual row selected plus the text rows the
+                          recompute equals SDPA full prefill at every position;
+                          a partial selection plus text rows equals SDPA over
+                          the merged cache;
+  * paged caches         a hand-worked page table, and random page
+                          permutations that must give back the original cache.
 """
 from __future__ import annotations
 
@@ -568,6 +575,69 @@ def pin_explicit_quotas(o):
             expect += [lo + t for t in _bruteforce_topk(list(s[lo:hi]), int(quota[j]))]
         assert list(idx) == sorted(expect)
         assert sum(quota) == k
+
+
+def pin_text_positions(o):
+    rng = np.random.default_rng(15)
+    for _ in range(20):
+        img_pos, img_off, cur = _rand_layout(rng, int(rng.integers(1, 5)), prefix=int(rng.integers(0, 3)),
+                                             sep=int(rng.integers(0, 3)))
+        n_ctx = cur + int(rng.integers(0, 4))
+        P = set(_p_vis(img_pos, img_off).tolist())
+        expect = [t for t in range(n_ctx) if t not in P]
+        got = o.text_positions(n_ctx, img_pos, img_off)
+        assert list(got) == expect
+        assert len(got) == n_ctx - int(img_off[-1])
+    # hand-worked: images at 2..3 and 6..8 of 10 positions
+    assert list(o.text_positions(10, np.array([2, 6]), np.array([0, 2, 5]))) == [0, 1, 4, 5, 9]
+
+
+def pin_refresh_text_rows(o):
+    """Every visual row plus the text rows recomputed = full prefill at every
+    position; a partial selection plus the text rows = SDPA over the merged
+    cache whose text rows are fresh too."""
+    rng = np.random.default_rng(16)
+    hq, hkv, d = 4, 2, 8
+    img_pos, img_off, cur = _rand_layout(rng, 3, prefix=3, sep=2)
+    n_ctx = cur + 3
+    k = rng.standard_normal((n_ctx, hkv, d))
+    v = rng.standard_normal((n_ctx, hkv, d))
+    k_f = rng.standard_normal((n_ctx, hkv, d))   # fresh rows of every position
+    v_f = rng.standard_normal((n_ctx, hkv, d))
+    q_f = rng.standard_normal((n_ctx, hq, d))
+    P = _p_vis(img_pos, img_off)
+    T = o.text_positions(n_ctx, img_pos, img_off)
+    causal = np.arange(n_ctx)[None, :] <= np.arange(n_ctx)[:, None]
+    full = _sdpa_out(q_f, k_f, v_f, causal)
+    rows = o.recompute_rows(P, T)
+    assert sorted(rows.tolist()) == list(range(n_ctx))
+    km, vm, out, _ = o.refresh_layer(k, v, rows, k_f[rows], v_f[rows], q_f[rows])
+    np.testing.assert_allclose(out, full[rows], rtol=1e-10, atol=1e-12)
+    np.testing.assert_array_equal(km, k_f)
+    sel = P[np.sort(rng.choice(len(P), size=len(P) // 2, replace=False))]
+    rows = o.recompute_rows(sel, T)
+    km, vm, out, _ = o.refresh_layer(k, v, rows, k_f[rows], v_f[rows], q_f[rows])
+    mk, mv = k.copy(), v.copy()
+    mk[rows], mv[rows] = k_f[rows], v_f[rows]
+    mask = np.arange(n_ctx)[None, :] <= rows[:, None]
+    np.testing.assert_allclose(out, _sdpa_out(q_f[rows], mk, mv, mask), rtol=1e-10, atol=1e-12)
+
+
+def pin_paged_cache(o):
+    pages = np.arange(8, dtype=np.float64).reshape(4, 2, 1, 1)
+    got = o.paged_to_contiguous(pages, np.array([2, 0, 3]), 5)
+    assert got.ravel().tolist() == [4, 5, 0, 1, 6]
+    rng = np.random.default_rng(17)
+    for P, n_ctx in ((4, 13), (8, 16), (2, 1)):
+        cache = rng.standard_normal((n_ctx, 2, 3))
+        n_log = -(-n_ctx // P)
+        n_pages = n_log + 3
+        perm = rng.permutation(n_pages)[:n_log]
+        pool = rng.standard_normal((n_pages, P, 2, 3))
+        for i in range(n_log):
+            blk = cache[i * P:(i + 1) * P]
+            pool[perm[i], :len(blk)] = blk
+        np.testing.assert_array_equal(o.paged_to_contiguous(pool, perm, n_ctx), cache)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

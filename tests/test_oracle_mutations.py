@@ -36,6 +36,15 @@ MUTATIONS = {
     "quota_ties_to_upper_image": ("key=lambda j: (-frac[j], j)", "key=lambda j: (-frac[j], -j)"),
     "explicit_bottom_k": ("lo + topk_select(s[lo:lo + int(n[j])], int(quota[j]))",
                           "lo + topk_select(-s[lo:lo + int(n[j])], int(quota[j]))"),
+    "text_rows_are_visual": ("return np.flatnonzero(~is_visual).astype(np.int64)",
+                             "return np.flatnonzero(is_visual).astype(np.int64)"),
+    "text_rows_drop_last": ("is_visual = np.zeros(int(n_ctx), dtype=bool)",
+                            "is_visual = np.zeros(int(n_ctx), dtype=bool); is_visual[-1:] = True"),
+    "recompute_drops_text": ("np.asarray(sel_pos, np.int64), np.asarray(text_pos, np.int64)])",
+                             "np.asarray(sel_pos, np.int64), np.asarray(text_pos, np.int64)[:0]])"),
+    "paged_ignores_table": ("out[t] = pages[int(block_table[t // P]), t % P]", "out[t] = pages[t // P, t % P]"),
+    "paged_row_from_page_index": ("out[t] = pages[int(block_table[t // P]), t % P]",
+                                  "out[t] = pages[int(block_table[t // P]), (t // P) % P]"),
     "lse_log2": ("return e / total, m + np.log(total)", "return e / total, m + np.log2(total)"),
     "lse_drops_max": ("return e / total, m + np.log(total)", "return e / total, np.log(total)"),
     "layer_sum_not_mean": ("return s / n_layers, A", "return s, A"),
