@@ -33,7 +33,9 @@
  *     conduit_last_error() then describes the problem.  With no usable GPU a
  *     valid call returns CONDUIT_ERR_HIP.
  *   - Caches are token-major: element (token t, KV head h, dim e) sits at
- *     base[t * stride + h * head_dim + e].  Queries and outputs are dense
+ *     base[row(t) * stride + h * head_dim + e], with row(t) = t for a
+ *     contiguous cache and the block-table lookup of conduit_kv for a paged
+ *     one.  Queries and outputs are dense
  *     [rows][n_q_heads][head_dim].  bf16 is IEEE binary32's top 16 bits.
  *     Device pointers must be 16-byte aligned and strides a multiple of
  *     16 bytes.
@@ -88,11 +90,25 @@ typedef enum {
 
 #define CONDUIT_MAX_IMAGES 256
 
-/* One layer's KV cache. */
+/* One layer's KV cache, contiguous or paged.
+ *
+ * Contiguous (block_table NULL, page_size = n_pages = 0): token t is row t of
+ * k and v.
+ *
+ * Paged (the block-table KV storage of a serving engine, Sec. 4.3): k and v
+ * hold n_pages physical pages of page_size rows each; logical token t lives
+ * in row block_table[t / page_size] * page_size + t % page_size.  page_size
+ * is a power of two from 64 to 2^20 (a 64-key attention tile then never
+ * crosses a page; smaller powers of two return CONDUIT_ERR_UNSUPPORTED).
+ * block_table is device int32 [ceil(n_ctx / page_size)], caller-owned and
+ * read by the kernels; an entry outside [0, n_pages) is clamped into it (the
+ * results are then meaningless, but no access leaves the pages).  Pages may
+ * be shared between tables or unused. */
 typedef struct {
-  void *k;                /* device [n_ctx][n_kv_heads][head_dim], dtype         */
+  void *k;                /* device [rows][n_kv_heads][head_dim], dtype; rows =
+                             n_ctx (contiguous) or n_pages * page_size (paged) */
   void *v;                /* device, same layout                                 */
-  int64_t k_stride;       /* elements between consecutive tokens of k,
+  int64_t k_stride;       /* elements between consecutive rows of k,
                              >= n_kv_heads * head_dim                            */
   int64_t v_stride;       /* same for v                                          */
   int32_t n_ctx;          /* tokens in the cache (sequence positions 0..n_ctx-1) */
@@ -100,6 +116,9 @@ typedef struct {
   int32_t n_kv_heads;     /* H_kv                                                */
   int32_t head_dim;       /* 64 or 128                                           */
   int32_t dtype;          /* conduit_dtype                                       */
+  int32_t page_size;      /* paged: tokens per page; contiguous: 0               */
+  const int32_t *block_table; /* paged: device [ceil(n_ctx / page_size)]; else NULL */
+  int32_t n_pages;        /* paged: physical pages in k and v; contiguous: 0    */
 } conduit_kv;
 
 /* The visual-token sets of Eq. 1: K images, each one contiguous run of
@@ -209,11 +228,15 @@ conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32
 
 /* ------------------------------------------------------------------------ *
  * Cache merge for one layer (Sec. 3: selected rows are recomputed, all other
- * cached visual entries are reused).  For each i < k, row pos[i] of kv->k and
- * kv->v is replaced by row i of k_new / v_new, in place.
+ * cached visual entries are reused).  For each i < k, token pos[i] of kv->k and
+ * kv->v is replaced by row i of k_new / v_new, in place.  The rows may mix
+ * the selected visual tokens with the request's text tokens (changed prefix,
+ * separators, span), which are processed normally (Sec. 3.1).
  *
- * pos           device [k] int32, strictly ascending, each < kv->n_ctx
- *               (device-side precondition, not checked on the device).
+ * pos           device [k] int32, distinct, each in [0, kv->n_ctx), any order
+ *               (device-side precondition: a position outside the range is
+ *               clamped into it, so no access leaves the cache; repeated
+ *               positions race).
  * k_new, v_new  device [k][n_kv_heads][head_dim] dense, kv->dtype.
  * k_old_out, v_old_out  nullable device [k][n_kv_heads][head_dim]: receive the
  *               replaced (stale) rows, so the merge can be undone.
@@ -227,12 +250,18 @@ conduit_status conduit_scatter_kv(const conduit_kv *kv, const int32_t *pos, int3
  * Refresh attention for one layer: causal attention of the selected rows over
  * the merged cache (the selective recompute of Sec. 3 and Sec. 4.1).  Row i
  * sits at position pos[i] and attends to keys 0 .. pos[i] of kv (already
- * merged by conduit_scatter_kv on the same stream), itself included.
+ * merged by conduit_scatter_kv on the same stream), itself included.  The rows
+ * may include the request's text tokens, so one launch covers the whole
+ * per-layer recompute attention (selected visual rows and text rows).
  *
  * q_sel   device [k][n_q_heads][head_dim], kv->dtype: fresh queries, row i for
  *         pos[i].
- * pos     device [k] int32, ascending, each < kv->n_ctx (device-side
- *         precondition).
+ * pos     device [k] int32, each in [0, kv->n_ctx), any order (device-side
+ *         precondition: for a position outside the range no access leaves
+ *         the cache, but that row's output is meaningless).
+ *         Rows are blocked in the given order, so ascending runs (e.g. the
+ *         selected rows followed by the text rows) keep blocks' key ranges
+ *         tight.
  * o_out   device [k][n_q_heads][head_dim], kv->dtype (bf16 rounded to nearest
  *         even from fp32 accumulation).
  * lse_out nullable device [k][n_q_heads] fp32: natural-log log-sum-exp.

@@ -44,7 +44,9 @@ class KV(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("k_stride", ctypes.c_int64),
                 ("v_stride", ctypes.c_int64), ("n_ctx", ctypes.c_int32),
                 ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
-                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("block_table", ctypes.c_void_p),
+                ("n_pages", ctypes.c_int32)]
 
 
 class Images(ctypes.Structure):
@@ -141,7 +143,27 @@ def kv_desc(k: torch.Tensor, v: torch.Tensor, n_q_heads: int) -> KV:
         raise ConduitError(ERR_INVALID_ARG, "k and v must match in shape and dtype")
     n_ctx, hkv, d = k.shape
     return KV(k.data_ptr(), v.data_ptr(), k.stride(0), v.stride(0), n_ctx, n_q_heads, hkv, d,
-              _dtype_code(k))
+              _dtype_code(k), 0, None, 0)
+
+
+def kv_desc_paged(k_pages: torch.Tensor, v_pages: torch.Tensor, block_table: torch.Tensor,
+                  n_ctx: int, n_q_heads: int) -> KV:
+    """Descriptor of one layer's paged cache: k_pages, v_pages are
+    [n_pages, page_size, H_kv, d] device tensors (last two dims dense, pages
+    evenly strided); block_table is a device int32 tensor whose entry i is the
+    page holding tokens i*page_size .. (i+1)*page_size - 1."""
+    for t in (k_pages, v_pages):
+        if t.dim() != 4 or t.stride(3) != 1 or t.stride(2) != t.shape[3] or \
+                t.stride(0) != t.shape[1] * t.stride(1):
+            raise ConduitError(ERR_INVALID_ARG, "page tensors must be [n_pages, page, H_kv, d], rows dense")
+    if k_pages.shape != v_pages.shape or k_pages.dtype != v_pages.dtype:
+        raise ConduitError(ERR_INVALID_ARG, "k and v pages must match in shape and dtype")
+    n_pages, page, hkv, d = k_pages.shape
+    if block_table.dtype != torch.int32 or block_table.dim() != 1 or \
+            block_table.numel() < -(-n_ctx // page):
+        raise ConduitError(ERR_INVALID_ARG, "block_table must be int32 with ceil(n_ctx / page) entries")
+    return KV(k_pages.data_ptr(), v_pages.data_ptr(), k_pages.stride(1), v_pages.stride(1), n_ctx,
+              n_q_heads, hkv, d, _dtype_code(k_pages), page, block_table.data_ptr(), n_pages)
 
 
 class ImageTable:

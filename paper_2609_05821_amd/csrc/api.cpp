@@ -65,7 +65,31 @@ conduit_status check_kv(const conduit_kv *kv) {
                 (long long)kv->k_stride, (long long)kv->v_stride, (long long)row);
   if ((kv->k_stride * esize(kv->dtype)) % 16 || (kv->v_stride * esize(kv->dtype)) % 16)
     return fail(CONDUIT_ERR_INVALID_ARG, "token strides must be multiples of 16 bytes");
+  if (!kv->block_table) {
+    if (kv->page_size != 0 || kv->n_pages != 0)
+      return fail(CONDUIT_ERR_INVALID_ARG, "page_size and n_pages must be 0 without a block table");
+    return CONDUIT_OK;
+  }
+  const int32_t ps = kv->page_size;
+  if (ps < 1 || (ps & (ps - 1)) != 0)
+    return fail(CONDUIT_ERR_INVALID_ARG, "page_size %d is not a power of two", ps);
+  if (ps < 64 || ps > (1 << 20))
+    return fail(CONDUIT_ERR_UNSUPPORTED, "page_size %d (supported: powers of two from 64 to 2^20)", ps);
+  if (kv->n_pages < 1) return fail(CONDUIT_ERR_INVALID_ARG, "n_pages = %d < 1", kv->n_pages);
+  if (reinterpret_cast<uintptr_t>(kv->block_table) % 4)
+    return fail(CONDUIT_ERR_INVALID_ARG, "block_table must be 4-byte aligned");
   return CONDUIT_OK;
+}
+
+// Token -> cache row addressing of a checked descriptor.
+KvPages pages_of(const conduit_kv *kv) {
+  KvPages pg{};
+  if (kv->block_table) {
+    pg.table = kv->block_table;
+    pg.shift = __builtin_ctz((unsigned)kv->page_size);
+    pg.n_pages = kv->n_pages;
+  }
+  return pg;
 }
 
 // The image table; `limit` is the first position that may not hold visual tokens.
@@ -317,6 +341,7 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
     ap.v = kv->v;
     ap.k_stride = kv->k_stride;
     ap.v_stride = kv->v_stride;
+    ap.pages = pages_of(kv);
     ap.n_kv_heads = kv->n_kv_heads;
     ap.group = kv->n_q_heads / kv->n_kv_heads;
     ap.n_q_heads = kv->n_q_heads;
@@ -348,6 +373,7 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   cs.v = kv->v;
   cs.k_stride = kv->k_stride;
   cs.v_stride = kv->v_stride;
+  cs.pages = pages_of(kv);
   cs.n_kv_heads = kv->n_kv_heads;
   cs.group = kv->n_q_heads / kv->n_kv_heads;
   cs.n_q_heads = kv->n_q_heads;
@@ -389,7 +415,7 @@ conduit_status conduit_value_norms(const conduit_kv *kv, const conduit_images *i
   ImageTable tbl;
   st = check_images(img, kv->n_ctx, &tbl);
   if (st) return st;
-  hipError_t e = launch_value_norms(kv->v, kv->v_stride, kv->n_kv_heads * kv->head_dim,
+  hipError_t e = launch_value_norms(kv->v, kv->v_stride, pages_of(kv), kv->n_kv_heads * kv->head_dim,
                                     kv->dtype == CONDUIT_BF16, tbl, vnorm_out, stream);
   if (e != hipSuccess) return hip_fail(e, "value norms");
   return ok();
@@ -468,6 +494,8 @@ conduit_status conduit_scatter_kv(const conduit_kv *kv, const int32_t *pos, int3
   sp.v = kv->v;
   sp.k_stride_bytes = kv->k_stride * esize(kv->dtype);
   sp.v_stride_bytes = kv->v_stride * esize(kv->dtype);
+  sp.pages = pages_of(kv);
+  sp.n_ctx = kv->n_ctx;
   sp.row_bytes = kv->n_kv_heads * kv->head_dim * esize(kv->dtype);
   sp.pos = pos;
   sp.n_rows = k;
@@ -510,6 +538,7 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
   ap.v = kv->v;
   ap.k_stride = kv->k_stride;
   ap.v_stride = kv->v_stride;
+  ap.pages = pages_of(kv);
   ap.n_kv_heads = kv->n_kv_heads;
   ap.group = kv->n_q_heads / kv->n_kv_heads;
   ap.n_q_heads = kv->n_q_heads;

@@ -355,8 +355,11 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     u32x4 rv[PV ? VPT : 1][2];
     bool rok = false;
     auto load_tile = [&](int t0) __attribute__((always_inline)) {
-      const u16 *kb = Kg + (int64_t)t0 * p.k_stride;
-      const u16 *vb = Vg + (int64_t)t0 * p.v_stride;
+      // t0 is a multiple of the tile and a page holds a whole number of
+      // tiles, so the tile's rows are consecutive rows of the cache.
+      const int64_t row0 = kv_row(p.pages, t0);
+      const u16 *kb = Kg + row0 * p.k_stride;
+      const u16 *vb = Vg + row0 * p.v_stride;
       if (t0 + KT <= kend) {
 #pragma unroll
         for (int i = 0; i < Regs::KCH; ++i) rk[i] = ld16(kb + koff[i]);
@@ -373,7 +376,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         for (int i = 0; i < Regs::KCH; ++i) {
           const int cidx = tid + kThreads * i;
           const int kp = min(t0 + cidx / (D / 8), kend - 1);
-          rk[i] = ld16(Kg + (int64_t)kp * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
+          rk[i] = ld16(kb + (int64_t)(kp - t0) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
         }
         if constexpr (PV) {
           if (v_active) {
@@ -382,7 +385,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
 #pragma unroll
               for (int i = 0; i < 2; ++i) {
                 const int kp = min(t0 + v_kpair[it] * 2 + i, kend - 1);
-                rv[it][i] = ld16(Vg + (int64_t)kp * p.v_stride + kvh * D + v_dc[it] * 8);
+                rv[it][i] = ld16(vb + (int64_t)(kp - t0) * p.v_stride + kvh * D + v_dc[it] * 8);
               }
           }
         }
@@ -622,7 +625,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParams p, DirectOut ou
   const int64_t gp = blockIdx.x;
   const int lane = threadIdx.x;
   const int r = (int)(gp / p.n_q_heads), hq = (int)(gp % p.n_q_heads), kvh = hq / p.group;
-  const int rpos = row_position(p.row_pos, p.q_pos0, r);
+  const int rpos = min(row_position(p.row_pos, p.q_pos0, r), p.n_ctx - 1);
   const float *Kg = static_cast<const float *>(p.k);
   const float *Vg = static_cast<const float *>(p.v);
   const float *q = static_cast<const float *>(p.q) + gp * D;
@@ -636,7 +639,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParams p, DirectOut ou
     const bool ok = kp <= rpos && (!p.vis_only || is_visual(p.tbl, kp));
     float z = kNegInf;
     if (ok) {
-      const float *kr = Kg + (int64_t)kp * p.k_stride + kvh * D;
+      const float *kr = Kg + kv_row(p.pages, kp) * p.k_stride + kvh * D;
       float dot = 0.f;
 #pragma unroll 8
       for (int e = 0; e < D; ++e) dot = fmaf(qs[e], kr[e], dot);
@@ -654,7 +657,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnParams p, DirectOut ou
       const int nk = min(64, rpos - base + 1);
       for (int j = 0; j < nk; ++j) {
         const float pj = __shfl(e, j, 64);
-        const float *vr = Vg + (int64_t)(base + j) * p.v_stride + kvh * D;
+        const float *vr = Vg + kv_row(p.pages, base + j) * p.v_stride + kvh * D;
 #pragma unroll
         for (int i = 0; i < PER; ++i) o[i] = fmaf(pj, vr[lane + 64 * i], o[i]);
       }

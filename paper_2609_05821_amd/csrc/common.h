@@ -109,6 +109,22 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
+// Cache row of a token.  A paged cache keeps token t in row
+// table[t >> shift] * 2^shift + (t mod 2^shift) of its page pool; without a
+// table the row is t.  Table entries are clamped into the pool, so a bad
+// entry cannot send an access outside it.
+struct KvPages {
+  const int32_t *table;     // nullable: contiguous cache
+  int32_t shift;            // log2 of the page size
+  int32_t n_pages;          // pages in the pool
+};
+
+__device__ __forceinline__ int64_t kv_row(const KvPages &pg, int t) {
+  if (!pg.table) return t;
+  const int page = min(max(pg.table[t >> pg.shift], 0), pg.n_pages - 1);
+  return ((int64_t)page << pg.shift) | (t & ((1 << pg.shift) - 1));
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
@@ -142,8 +158,9 @@ struct AttnPlan {
 struct AttnParams {
   const void *k;
   const void *v;
-  int64_t k_stride;         // elements between tokens
+  int64_t k_stride;         // elements between cache rows
   int64_t v_stride;
+  KvPages pages;            // token -> cache row (pages hold >= 64 rows)
   int32_t n_kv_heads;
   int32_t group;            // n_q_heads / n_kv_heads
   int32_t n_q_heads;
@@ -192,6 +209,7 @@ struct ColsumParams {
   const void *v;
   int64_t k_stride;
   int64_t v_stride;
+  KvPages pages;
   int32_t n_kv_heads;
   int32_t group;
   int32_t n_q_heads;
@@ -240,6 +258,8 @@ struct ScatterParams {
   void *v;
   int64_t k_stride_bytes;
   int64_t v_stride_bytes;
+  KvPages pages;
+  int32_t n_ctx;            // positions are clamped to [0, n_ctx)
   int32_t row_bytes;        // n_kv_heads * head_dim * element size
   const int32_t *pos;
   int32_t n_rows;
@@ -273,8 +293,8 @@ hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_d
                            bool with_values, hipStream_t s);
 hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, hipStream_t s);
 hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s);
-hipError_t launch_value_norms(const void *v, int64_t v_stride, int32_t row_elems, bool bf16,
-                              const ImageTable &tbl, float *out, hipStream_t s);
+hipError_t launch_value_norms(const void *v, int64_t v_stride, const KvPages &pages, int32_t row_elems,
+                              bool bf16, const ImageTable &tbl, float *out, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t s);
 hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream_t s);
 hipError_t launch_select_explicit(const SelectParams &p, const ImageTable &tbl, hipStream_t s);

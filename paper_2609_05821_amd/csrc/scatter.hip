@@ -11,7 +11,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterParams p) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= p.n_rows) return;
-  const int64_t pos = p.pos[row];
+  const int64_t pos = kv_row(p.pages, min(max(p.pos[row], 0), p.n_ctx - 1));  // cache row
   const int nch = p.row_bytes / 16;
   char *kdst = static_cast<char *>(p.k) + pos * p.k_stride_bytes;
   char *vdst = static_cast<char *>(p.v) + pos * p.v_stride_bytes;

@@ -88,7 +88,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   const bool tvalid = t < p.n_vis;
   bf16x8 kreg[KS];
   {
-    const u16 *krow = Kg + (int64_t)vis_position(img, tvalid ? t : p.n_vis - 1) * p.k_stride + kvh * D + 8 * half;
+    const u16 *krow = Kg + kv_row(p.pages, vis_position(img, tvalid ? t : p.n_vis - 1)) * p.k_stride + kvh * D + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) kreg[ks] = as_bf16x8(ld16(krow + ks * 16));
   }
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   for (int i = 0; i < VPT; ++i) {
     const int vi = tid + kColsumThreads * i;
     const int tv = min(blockIdx.x * kColsumKeysPerBlock + vi / (D / 8), p.n_vis - 1);
-    vv[i] = read_v ? ld16(Vg + (int64_t)vis_position(img, tv) * p.v_stride + kvh * D + (vi % (D / 8)) * 8)
+    vv[i] = read_v ? ld16(Vg + kv_row(p.pages, vis_position(img, tv)) * p.v_stride + kvh * D + (vi % (D / 8)) * 8)
                    : u32x4{0, 0, 0, 0};
   }
   store_chunk(0, 0, qv, bv);
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p, bool rms
   const float *Kg = static_cast<const float *>(p.k);
   const float *Vg = static_cast<const float *>(p.v);
   const float *Qg = static_cast<const float *>(p.q);
-  const int64_t pos = vis_position(p.tbl, t);
+  const int64_t pos = kv_row(p.pages, vis_position(p.tbl, t));  // cache row
   float kr[D];
 #pragma unroll
   for (int e = 0; e < D; ++e) kr[e] = Kg[pos * p.k_stride + kvh * D + e];
@@ -226,12 +226,12 @@ __global__ void finalize_kernel(FinalizeParams p) {
 // wave per visual token sums the squares of its row_elems cached values
 // (all KV heads concatenated), 16 bytes per lane and step.
 template <bool BF16>
-__global__ __launch_bounds__(256) void value_norms_kernel(const void *v, int64_t v_stride, int row_elems,
-                                                          ImageTable tbl, float *out) {
+__global__ __launch_bounds__(256) void value_norms_kernel(const void *v, int64_t v_stride, KvPages pages,
+                                                          int row_elems, ImageTable tbl, float *out) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (t >= tbl.n_vis) return;
   constexpr int EPC = BF16 ? 8 : 4;  // elements per 16-byte chunk
-  const char *row = static_cast<const char *>(v) + (int64_t)vis_position(tbl, t) * v_stride * (BF16 ? 2 : 4);
+  const char *row = static_cast<const char *>(v) + kv_row(pages, vis_position(tbl, t)) * v_stride * (BF16 ? 2 : 4);
   float sq = 0.f;
   for (int c = lane; c < row_elems / EPC; c += 64) {
     const u32x4 w = ld16(row + 16 * c);
@@ -257,12 +257,12 @@ __global__ __launch_bounds__(256) void value_norms_kernel(const void *v, int64_t
 
 }  // namespace
 
-hipError_t launch_value_norms(const void *v, int64_t v_stride, int32_t row_elems, bool bf16,
-                              const ImageTable &tbl, float *out, hipStream_t s) {
+hipError_t launch_value_norms(const void *v, int64_t v_stride, const KvPages &pages, int32_t row_elems,
+                              bool bf16, const ImageTable &tbl, float *out, hipStream_t s) {
   ProfScope ps("value_norms", s);
   const int blocks = (tbl.n_vis + 3) / 4;
-  if (bf16) value_norms_kernel<true><<<blocks, 256, 0, s>>>(v, v_stride, row_elems, tbl, out);
-  else value_norms_kernel<false><<<blocks, 256, 0, s>>>(v, v_stride, row_elems, tbl, out);
+  if (bf16) value_norms_kernel<true><<<blocks, 256, 0, s>>>(v, v_stride, pages, row_elems, tbl, out);
+  else value_norms_kernel<false><<<blocks, 256, 0, s>>>(v, v_stride, pages, row_elems, tbl, out);
   return hipGetLastError();
 }
 

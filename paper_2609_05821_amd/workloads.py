@@ -22,7 +22,9 @@ multi-page documents.  The distributions are:
   * fresh rows for the refresh follow the isotropic staleness model of the
     Monte Carlo estimator (App. D.1) with kappa = 0.5:
     K*_t = K_t + xi, xi ~ N(0, kappa^2 ||K_t||^2 / (H_kv d) I), same for V*;
-    fresh queries Q*_t ~ N(0, 1) (drawn in float32).
+    fresh queries Q*_t ~ N(0, 1) (drawn in float32);
+  * the text rows a refresh also recomputes (every non-visual position) get
+    fresh K/V and queries drawn the same way, on streams of their own.
 
 Sequence layout: [changed prefix][for each image: separator, visual tokens]
 [span].  Caches are token-major [N_ctx, H_kv, d].  bf16 arrays are returned as
@@ -36,7 +38,7 @@ from typing import Dict, List, Optional
 import numpy as np
 
 # random stream ids
-_S_Q, _S_K, _S_VDIR, _S_VNORM, _S_SINK, _S_REL, _S_XI, _S_QSTAR = range(8)
+_S_Q, _S_K, _S_VDIR, _S_VNORM, _S_SINK, _S_REL, _S_XI, _S_QSTAR, _S_XI_TEXT, _S_QSTAR_TEXT = range(10)
 _GLOBAL_LAYER = 65535  # stream for draws shared by all layers
 
 
@@ -119,12 +121,19 @@ class Workload:
         w /= np.linalg.norm(w, axis=1, keepdims=True)
         return {"sinks": sinks, "relevant": rel, "b": b, "w": w}
 
-    def layer(self, layer: int, fresh: bool = True) -> dict:
+    def text_positions(self) -> np.ndarray:
+        """Positions outside the images (prefix, separators, span), ascending."""
+        keep = np.ones(self.n_ctx, dtype=bool)
+        keep[self.vis_positions()] = False
+        return np.flatnonzero(keep).astype(np.int64)
+
+    def layer(self, layer: int, fresh: bool = True, text: bool = False) -> dict:
         """All tensors of one layer, already cast to the cache dtype.
 
         q [n_q, H_q, d]; k, v [N_ctx, H_kv, d]; with fresh=True also
         q_star [N_vis, H_q, d], k_star, v_star [N_vis, H_kv, d] (fresh rows in
-        visual-index order).
+        visual-index order); with text=True also q_text_star, k_text_star,
+        v_text_star for the rows of text_positions(), in that order.
         """
         d, hq, hkv, nq, nctx = self.head_dim, self.n_q_heads, self.n_kv_heads, self.n_q, \
             self.n_ctx
@@ -169,6 +178,16 @@ class Workload:
             out["v_star"] = self._cast(v_star)
             out["q_star"] = self._cast(self._rng(layer, _S_QSTAR).standard_normal(
                 (len(P_vis), hq, d), dtype=np.float32))
+        if text:
+            T = self.text_positions()
+            rx = self._rng(layer, _S_XI_TEXT)
+            kt, vt = k[T], v[T]
+            sd_k = self.kappa * np.linalg.norm(kt.reshape(len(T), -1), axis=1) / np.sqrt(hkv * d)
+            sd_v = self.kappa * np.linalg.norm(vt.reshape(len(T), -1), axis=1) / np.sqrt(hkv * d)
+            out["k_text_star"] = self._cast(kt + sd_k[:, None, None] * rx.standard_normal(kt.shape))
+            out["v_text_star"] = self._cast(vt + sd_v[:, None, None] * rx.standard_normal(vt.shape))
+            out["q_text_star"] = self._cast(self._rng(layer, _S_QSTAR_TEXT).standard_normal(
+                (len(T), hq, d), dtype=np.float32))
         return out
 
 

@@ -97,6 +97,13 @@ def score(kvd=None, q=FAKE, n_q=64, q_pos0=1280, img=IMG, norm=0, agg=0, scale=0
     (dict(img=api.ImageTable([256, 400], [0, 10, 10])), api.ERR_INVALID_ARG),    # empty image
     (dict(img=api.ImageTable([256], [1, 1024])), api.ERR_INVALID_ARG),
     (dict(img=api.ImageTable(list(range(0, 1028, 4)), list(range(0, 1032, 4)))), api.ERR_UNSUPPORTED),
+    (dict(kvd=kv(page_size=64)), api.ERR_INVALID_ARG),                         # no table
+    (dict(kvd=kv(n_pages=4)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(block_table=FAKE, page_size=32, n_pages=64)), api.ERR_UNSUPPORTED),
+    (dict(kvd=kv(block_table=FAKE, page_size=96, n_pages=64)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(block_table=FAKE, page_size=1 << 21, n_pages=1)), api.ERR_UNSUPPORTED),
+    (dict(kvd=kv(block_table=FAKE, page_size=64, n_pages=0)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(block_table=FAKE + 2, page_size=64, n_pages=64)), api.ERR_INVALID_ARG),
     (dict(ws_bytes=16), api.ERR_WORKSPACE),
     (dict(ws=FAKE + 64), api.ERR_INVALID_ARG),
 ])
@@ -186,6 +193,16 @@ def test_kernel_timing_without_records():
     assert L.conduit_profile_read(-1, ctypes.byref(name), ctypes.byref(ms)) == api.ERR_INVALID_ARG
     assert L.conduit_profile_read(0, None, None) == api.ERR_INVALID_ARG
     assert L.conduit_profile_enable(0) == api.OK
+
+
+def test_paged_descriptor_is_accepted_on_the_host():
+    """A valid paged descriptor passes every host check (the call then fails
+    only at the first HIP call, or succeeds where a GPU is present)."""
+    kvd = kv(block_table=FAKE, page_size=256, n_pages=8)
+    L = api.lib()
+    assert L.conduit_scatter_kv(ctypes.byref(kvd), None, 0, None, None, None, None, None) == api.OK
+    need = L.conduit_refresh_workspace_bytes(ctypes.byref(kvd), 102)
+    assert need == L.conduit_refresh_workspace_bytes(ctypes.byref(kv()), 102)
 
 
 def test_value_norms_rejects():
