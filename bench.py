@@ -66,7 +66,7 @@ def main():
     w = W.config(args.cfg, n_layers=1)
     k = w.budgets[args.budget]
     t_gen = time.time()
-    L = w.layer(0)
+    L = w.layer(0, text=True)
     t_gen = time.time() - t_gen
 
     def up(x):
@@ -216,10 +216,44 @@ def main():
             step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos, mask_out=step.mask,
             shat_out=step.shat, c_out=step.c, rule=rule, quota_out=quota))
 
+    # Paged cache (256-token pages, shuffled pool) and the recompute with the
+    # request's text rows in the same merge and attention launch.
+    page = 256
+    n_log = -(-w.n_ctx // page)
+    table_np = np.random.default_rng(7).permutation(n_log + 8)[:n_log].astype(np.int32)
+    table = torch.from_numpy(table_np).to(dev)
+    tok = np.arange(w.n_ctx)
+    rows_idx = torch.from_numpy(table_np[tok // page].astype(np.int64) * page + tok % page).to(dev)
+    k_pool = torch.zeros(((n_log + 8) * page, w.n_kv_heads, w.head_dim), dtype=kc.dtype, device=dev)
+    v_pool = torch.zeros_like(k_pool)
+    k_pool[rows_idx] = k_pristine
+    v_pool[rows_idx] = v_pristine
+    kv_paged = api.kv_desc_paged(k_pool.view(n_log + 8, page, w.n_kv_heads, w.head_dim),
+                                 v_pool.view(n_log + 8, page, w.n_kv_heads, w.head_dim), table,
+                                 w.n_ctx, w.n_q_heads)
+    text_np = w.text_positions()
+    rows_all = torch.cat([pos, torch.from_numpy(text_np.astype(np.int32)).to(dev)])
+    k_all = torch.cat([fresh["k_new"], up(L["k_text_star"])])
+    v_all = torch.cat([fresh["v_new"], up(L["v_text_star"])])
+    q_all = torch.cat([fresh["q_sel"], up(L["q_text_star"])])
+    n_all = rows_all.numel()
+    out_all = torch.empty((n_all, w.n_q_heads, w.head_dim), dtype=q_all.dtype, device=dev)
+    ws_all = torch.empty(api.refresh_workspace_bytes(kv, n_all), dtype=torch.uint8, device=dev)
+    variants_ms["score_paged256"] = timed(lambda: api.conduit_score(
+        kv_paged, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score))
+    api.conduit_scatter_kv(kv_paged, pos, fresh["k_new"], fresh["v_new"])
+    variants_ms["refresh_paged256"] = timed(lambda: api.conduit_refresh_attn(
+        kv_paged, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh))
+    variants_ms["recompute_with_text_rows"] = timed(lambda: (
+        api.conduit_scatter_kv(kv, rows_all, k_all, v_all),
+        api.conduit_refresh_attn(kv, q_all, rows_all, out_all, ws=ws_all)))
+    restore()
+
     # Algorithmic work.
     H, d, hkv = w.n_q_heads, w.head_dim, w.n_kv_heads
     refresh_flops = 4.0 * H * d * float(np.sum(pos_np + 1))
     refresh_exps = H * float(np.sum(pos_np + 1))
+    text_flops = refresh_flops + 4.0 * H * d * float(np.sum(text_np + 1))
     e = 2  # bf16 bytes
     score_bytes = (w.n_q * H * d * e + w.n_ctx * hkv * d * e + w.n_vis * hkv * d * e
                    + w.n_vis * 4 * 4)
@@ -289,6 +323,14 @@ def main():
             "mfma_frac": score_flops / (ms["score"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         },
         "variants_ms": variants_ms,
+        "recompute_with_text_rows": {
+            "rows": n_all, "text_rows": int(len(text_np)),
+            "algorithmic_flops": text_flops,
+            "tflops_whole_call": text_flops / (variants_ms["recompute_with_text_rows"]["mean"] * 1e-3) / 1e12,
+            "note": "merge + refresh attention of the selected rows and every text row, one launch each",
+        },
+        "paged": {"page_size": page, "pages": n_log + 8,
+                  "note": "same workload with K/V in a shuffled pool of 256-token pages"},
         "variants_bytes": {
             "value_norms": vnorm_bytes,
             "value_norms_gbs": vnorm_bytes / (variants_ms["value_norms"]["mean"] * 1e-3) / 1e9,

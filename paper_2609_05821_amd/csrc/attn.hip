@@ -289,6 +289,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const int col = lane & 31, half = lane >> 5;
   const u16 *Kg = static_cast<const u16 *>(p.k);
   const u16 *Vg = static_cast<const u16 *>(p.v);
+  const KvPageReader pr = page_reader(p.pages, p.n_ctx);
   const u16 *Qg = static_cast<const u16 *>(p.q);
   const float c = p.scale_log2;
   const int n_items = min(p.plan.hdr[0], p.plan.max_items);
@@ -354,10 +355,9 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     u32x4 rk[Regs::KCH];
     u32x4 rv[PV ? VPT : 1][2];
     bool rok = false;
-    auto load_tile = [&](int t0) __attribute__((always_inline)) {
-      // t0 is a multiple of the tile and a page holds a whole number of
-      // tiles, so the tile's rows are consecutive rows of the cache.
-      const int64_t row0 = kv_row(p.pages, t0);
+    // t0 is a multiple of the tile and a page holds a whole number of tiles,
+    // so a tile's rows are consecutive rows of the cache starting at row0.
+    auto load_tile = [&](int t0, int64_t row0) __attribute__((always_inline)) {
       const u16 *kb = Kg + row0 * p.k_stride;
       const u16 *vb = Vg + row0 * p.v_stride;
       if (t0 + KT <= kend) {
@@ -510,13 +510,25 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     // while the current tile computes; one barrier per tile.  Both sub-tiles'
     // S^T MFMAs are issued before the first softmax, so the VALU work of one
     // sub-tile runs while the matrix core still works on the other.
-    load_tile(kbeg);
+    // Block-table entries of 64 consecutive tiles are read at once, one per
+    // lane, and each tile takes its entry with a lane read; only every 64th
+    // tile waits for the table.
+    int page_vec = 0, page_base = INT32_MIN;
+    auto tile_row = [&](int t0) __attribute__((always_inline)) {
+      const int ti = t0 / KT;
+      if (ti - page_base >= 64) {
+        page_base = ti;
+        page_vec = read_page(pr, (ti + (tid & 63)) * KT);
+      }
+      return page_row(pr, __builtin_amdgcn_readlane(page_vec, ti - page_base), t0);
+    };
+    load_tile(kbeg, tile_row(kbeg));
     store_tile(0);
     __syncthreads();
     int buf = 0;
     for (int t0 = kbeg; t0 < kend; t0 += KT) {
       const bool more = t0 + KT < kend;
-      if (more) load_tile(t0 + KT);
+      if (more) load_tile(t0 + KT, tile_row(t0 + KT));
       const bool masked = (!PV && p.vis_only) || t0 + KT > kend || t0 + KT - 1 > minpos;
       const f32x16 s0 = scores(buf, 0);
       const f32x16 s1 = scores(buf, 1);

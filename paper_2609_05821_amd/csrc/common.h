@@ -125,6 +125,45 @@ __device__ __forceinline__ int64_t kv_row(const KvPages &pg, int t) {
   return ((int64_t)page << pg.shift) | (t & ((1 << pg.shift) - 1));
 }
 
+// Block-table reads for pipelined loops: a buffer load returns 0 for a read
+// past the resource's record count instead of touching memory, so the read is
+// unconditional (no branch, hence no early wait on every load in flight).  A
+// contiguous cache gets 0 records and a 31-bit in-page mask, so the row is the
+// token itself.
+struct KvPageReader {
+  __amdgpu_buffer_rsrc_t rsrc;
+  int32_t shift;
+  int32_t last_page;
+};
+
+__device__ __forceinline__ KvPageReader page_reader(const KvPages &pg, int n_ctx) {
+  KvPageReader r;
+  constexpr int kRsrcWord3 = 0x00020000;  // gfx9 raw buffer: 32-bit data format
+  if (pg.table) {
+    const int entries = ((n_ctx - 1) >> pg.shift) + 1;
+    r.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(pg.table), (short)0, entries * 4,
+                                               kRsrcWord3);
+    r.shift = pg.shift;
+    r.last_page = pg.n_pages - 1;
+  } else {
+    r.rsrc = __builtin_amdgcn_make_buffer_rsrc(nullptr, (short)0, 0, kRsrcWord3);
+    r.shift = 31;
+    r.last_page = 0;
+  }
+  return r;
+}
+
+// Page entry of token t (raw; 0 past the table).
+__device__ __forceinline__ int read_page(const KvPageReader &r, int t) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r.rsrc, (t >> r.shift) * 4, 0, 0);
+}
+
+// Cache row of token t from its raw page entry.
+__device__ __forceinline__ int64_t page_row(const KvPageReader &r, int page, int t) {
+  const int pg = min(max(page, 0), r.last_page);
+  return ((int64_t)pg << r.shift) | (int64_t)((uint32_t)t & ((1u << r.shift) - 1u));
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
