@@ -14,6 +14,8 @@ step over reused visual KV caches:
   * Eq. 8-9 (Sec. 3.4)      image means g_j, cross-image mean, coefficients c_j;
   * Eq. 10-11 (Sec. 3.5)    composite score s_hat and one global top-k;
   * Algorithm 1 (App. A.1)  the order of these steps and the k = 0 exit;
+  * Eq. 3 and App. D.1/D.3 the residual value-write error left by a refresh set:
+    isotropic Monte Carlo displacements and the projected error;
   * selective recompute (Sec. 3, Sec. 4.1 cache-reuse protocol): the selected
     visual rows get their fresh K/V written into the cache, unselected rows are
     reused stale, and each selected row attends causally over that merged
@@ -45,6 +47,16 @@ Readings of points the paper leaves open (labels used below):
       K/V and attend like the selected visual rows, outside the budget; a
       step's recompute rows are the selected visual positions followed by the
       text positions;
+  R29 the isotropic displacement of App. D.1 spans the concatenated cached
+      value (R4), so its dimensionality is H_kv * d: xi_t = kappa ||V_t||
+      z_t / sqrt(H_kv d) with z_t ~ N(0, I) given as input, hence
+      E ||xi_t||^2 = kappa^2 ||V_t||^2;
+  R30 the residual of Eq. 3 is evaluated for every span row and query head
+      (query head h reads the KV-head-h/G slice of xi) with the cached-key
+      attention of R1, the output map taken as the identity (no weights);
+      the estimate is the mean over samples, rows and heads.  The projected
+      error (App. D.3: stale values set to zero) is the same residual with
+      xi_t = V_t;
   R28 a paged cache keeps token t in row t mod P of page table[t div P]
       (block-table KV storage of a serving engine, Sec. 4.3); it holds the same
       logical cache as the contiguous layout, so every result is the same.
@@ -394,6 +406,70 @@ def select(layers, q_pos0, img_pos, img_off, k, lam=1.0, norm=NORM_CAUSAL_ROW, s
     idx, pos, mask = refresh_mask(s_hat, k, img_pos, img_off)
     out.update({"s_hat": s_hat, "idx": idx, "pos": pos, "mask": mask})
     return out
+
+
+# --------------------------------------------------------------------------
+# Residual value-write error of a refresh set (Eq. 3, App. D.1, App. D.3)
+# --------------------------------------------------------------------------
+
+def iso_displacements(v_cache, img_pos, img_off, z, kappa):
+    """App. D.1 isotropic staleness samples (R29).
+
+    z [M, N_vis, H_kv, d]: standard normal draws.  Returns
+    xi [M, N_vis, H_kv, d] with xi_t = kappa ||V_t|| / sqrt(H_kv d) * z_t.
+    """
+    z = to_f64(z)
+    dim = z.shape[2] * z.shape[3]
+    sigma = kappa * value_norms(v_cache, img_pos, img_off) / np.sqrt(dim)
+    return sigma[None, :, None, None] * z
+
+
+def projected_displacements(v_cache, img_pos, img_off):
+    """App. D.3: with every stale visual value set to zero, the displacement
+    of a non-refreshed token is its value; returns [1, N_vis, H_kv, d]."""
+    P_vis, _ = visual_layout(img_pos, img_off)
+    return to_f64(v_cache)[P_vis][None]
+
+
+def residual_error(q, k_cache, q_pos0, img_pos, img_off, refreshed, xi, norm=NORM_CAUSAL_ROW,
+                   scale=None):
+    """Squared norm of Eq. 3's residual, sum over non-refreshed visual t of
+    alpha^c_{q,t} xi_t, for each displacement sample, span row and query head
+    (R30).
+
+    refreshed [N_vis]: nonzero for tokens in the refresh set T.
+    xi [M, N_vis, H_kv, d].  Returns err [M, n_q, H_q].
+    """
+    q = to_f64(q)
+    k_cache = to_f64(k_cache)
+    xi = np.asarray(xi, dtype=np.float64)
+    n_q, n_q_heads, d = q.shape
+    group = n_q_heads // k_cache.shape[1]
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    P_vis, _ = visual_layout(img_pos, img_off)
+    keep = np.asarray(refreshed) == 0
+    err = np.zeros((xi.shape[0], n_q, n_q_heads))
+    for i in range(n_q):
+        p = q_pos0 + i
+        for h in range(n_q_heads):
+            kv = h // group
+            if norm == NORM_CAUSAL_ROW:
+                alpha, _ = attention_row(q[i, h], k_cache[: p + 1, kv, :], scale)
+                alpha = alpha[P_vis]
+            else:
+                alpha, _ = attention_row(q[i, h], k_cache[P_vis, kv, :], scale)
+            alpha = np.where(keep, alpha, 0.0)
+            for m in range(xi.shape[0]):
+                y = alpha @ xi[m, :, kv, :]
+                err[m, i, h] = y @ y
+    return err
+
+
+def iso_estimate(err):
+    """App. D.1's estimate: the mean of the sampled squared residuals (over
+    samples, span rows and query heads, R30)."""
+    return float(np.mean(err))
 
 
 # --------------------------------------------------------------------------

@@ -36,7 +36,15 @@ What pins what:
                           a partial selection plus text rows equals SDPA over
                           the merged cache;
   * paged caches         a hand-worked page table, and random page
-                          permutations that must give back the original cache.
+                          permutations that must give back the original cache;
+  * residual error       (Eq. 3, App. D.1/D.3) torch SDPA whose values are the
+                          displacements, zeroed outside the non-refreshed
+                          visual keys; zero when every visual token is
+                          refreshed; the moments App. D.1 states for the
+                          isotropic samples (mean 0, E||xi||^2 =
+                          kappa^2 ||V||^2, checked with numpy.linalg.norm over
+                          many samples); unbiasedness of the estimate against
+                          the closed form built from SDPA weights.
 """
 from __future__ import annotations
 
@@ -638,6 +646,97 @@ def pin_paged_cache(o):
             blk = cache[i * P:(i + 1) * P]
             pool[perm[i], :len(blk)] = blk
         np.testing.assert_array_equal(o.paged_to_contiguous(pool, perm, n_ctx), cache)
+
+
+def _residual_case(rng, hq=4, hkv=2, d=8, n_q=3):
+    img_pos, img_off, cur = _rand_layout(rng, 3, prefix=2, sep=1)
+    n_ctx = cur + n_q
+    q = rng.standard_normal((n_q, hq, d))
+    k = rng.standard_normal((n_ctx, hkv, d))
+    v = rng.standard_normal((n_ctx, hkv, d))
+    return img_pos, img_off, cur, n_ctx, q, k, v
+
+
+def pin_residual_sdpa(o):
+    """The residual of every row and head is SDPA's output when the values are
+    the displacements on the non-refreshed visual keys and zero elsewhere."""
+    rng = np.random.default_rng(18)
+    for norm in (o.NORM_CAUSAL_ROW, o.NORM_VISUAL_ONLY):
+        img_pos, img_off, cur, n_ctx, q, k, v = _residual_case(rng)
+        P = _p_vis(img_pos, img_off)
+        refreshed = (rng.random(len(P)) < 0.4).astype(np.uint8)
+        xi = rng.standard_normal((2, len(P), 2, 8))
+        err = o.residual_error(q, k, cur, img_pos, img_off, refreshed, xi, norm=norm)
+        mask = np.arange(n_ctx)[None, :] <= (cur + np.arange(3))[:, None]
+        if norm == o.NORM_VISUAL_ONLY:
+            vis = np.zeros(n_ctx, dtype=bool)
+            vis[P] = True
+            mask = mask & vis[None, :]
+        for m in range(2):
+            vals = np.zeros((n_ctx, 2, 8))
+            vals[P] = xi[m] * (refreshed == 0)[:, None, None]
+            y = _sdpa_out(q, k, vals, mask)
+            np.testing.assert_allclose(err[m], (y * y).sum(axis=2), rtol=1e-10, atol=1e-14)
+        every = np.ones(len(P), dtype=np.uint8)
+        assert not o.residual_error(q, k, cur, img_pos, img_off, every, xi, norm=norm).any()
+
+
+def pin_projected_error(o):
+    """App. D.3: stale values zeroed, so the displacement is V itself; with an
+    empty refresh set the residual is SDPA over the visual values."""
+    rng = np.random.default_rng(19)
+    img_pos, img_off, cur, n_ctx, q, k, v = _residual_case(rng)
+    P = _p_vis(img_pos, img_off)
+    xi = o.projected_displacements(v, img_pos, img_off)
+    assert xi.shape == (1, len(P), 2, 8)
+    err = o.residual_error(q, k, cur, img_pos, img_off, np.zeros(len(P), np.uint8), xi)
+    vals = np.zeros_like(v)
+    vals[P] = v[P]
+    mask = np.arange(n_ctx)[None, :] <= (cur + np.arange(3))[:, None]
+    y = _sdpa_out(q, k, vals, mask)
+    np.testing.assert_allclose(err[0], (y * y).sum(axis=2), rtol=1e-10)
+
+
+def pin_iso_moments(o):
+    """App. D.1: the samples have mean 0 and E||xi_t||^2 = kappa^2 ||V_t||^2."""
+    rng = np.random.default_rng(20)
+    img_pos, img_off = np.array([1, 6]), np.array([0, 3, 5])
+    v = rng.standard_normal((9, 2, 4)) * rng.lognormal(0, 0.5, (9, 1, 1))
+    M, kappa = 20000, 0.7
+    z = rng.standard_normal((M, 5, 2, 4))
+    xi = o.iso_displacements(v, img_pos, img_off, z, kappa)
+    P = _p_vis(img_pos, img_off)
+    target = kappa ** 2 * np.linalg.norm(v[P].reshape(5, -1), axis=1) ** 2
+    sq = (xi.reshape(M, 5, -1) ** 2).sum(axis=2)        # ||xi_t||^2 per sample
+    se = sq.std(axis=0) / math.sqrt(M)
+    assert np.all(np.abs(sq.mean(axis=0) - target) < 5 * se), (sq.mean(axis=0), target)
+    mean = xi.mean(axis=0)
+    assert np.all(np.abs(mean) < 5 * xi.std(axis=0) / math.sqrt(M))
+    # scaling: doubling kappa quadruples every sampled residual term
+    xi2 = o.iso_displacements(v, img_pos, img_off, z[:3], 2 * kappa)
+    np.testing.assert_allclose(xi2, 2 * o.iso_displacements(v, img_pos, img_off, z[:3], kappa), rtol=1e-14)
+
+
+def pin_iso_unbiased(o):
+    """The estimate's expectation is the isotropic closed form
+    sum over non-refreshed t of alpha^2 kappa^2 ||V_t||^2 / H_kv (cross-token
+    terms vanish), averaged over rows and heads; alpha from SDPA weights."""
+    rng = np.random.default_rng(21)
+    img_pos, img_off, cur, n_ctx, q, k, v = _residual_case(rng, hq=4, hkv=2, d=4, n_q=2)
+    P = _p_vis(img_pos, img_off)
+    refreshed = np.zeros(len(P), np.uint8)
+    refreshed[::3] = 1
+    M, kappa = 6000, 0.5
+    z = rng.standard_normal((M, len(P), 2, 4))
+    err = o.residual_error(q, k, cur, img_pos, img_off, refreshed,
+                           o.iso_displacements(v, img_pos, img_off, z, kappa))
+    mask = np.arange(n_ctx)[None, :] <= (cur + np.arange(2))[:, None]
+    w = _sdpa_weights(q, k, mask)[:, :, P] * (refreshed == 0)        # [n_q, H_q, N_vis]
+    vn2 = np.linalg.norm(v[P].reshape(len(P), -1), axis=1) ** 2
+    expect = float(np.mean((w ** 2 * vn2).sum(axis=2))) * kappa ** 2 / 2   # H_kv = 2
+    per_sample = err.mean(axis=(1, 2))
+    se = per_sample.std() / math.sqrt(M)
+    assert abs(o.iso_estimate(err) - expect) < 5 * se, (o.iso_estimate(err), expect, se)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -14,11 +14,11 @@ from oracle import conduit_oracle
 from tests import oracle_pins
 
 MUTATIONS = {
-    "scale_1_over_d": ("scale = 1.0 / np.sqrt(d)", "scale = 1.0 / d", 2),
-    "gqa_modulo_mapping": ("kv = h // group", "kv = h % n_kv_heads", 2),
+    "scale_1_over_d": ("scale = 1.0 / np.sqrt(d)", "scale = 1.0 / d", 3),
+    "gqa_modulo_mapping": ("kv = h // group", "kv = h % n_kv_heads", 3),
     "causal_excludes_self": ("k_cache[: p + 1, kv, :], scale)\n                alpha = alpha[P_vis]",
-                             "k_cache[: p, kv, :], scale)\n                alpha = alpha[P_vis]"),
-    "visual_column_off_by_one": ("alpha = alpha[P_vis]", "alpha = alpha[P_vis - 1]"),
+                             "k_cache[: p, kv, :], scale)\n                alpha = alpha[P_vis]", 2),
+    "visual_column_off_by_one": ("alpha = alpha[P_vis]", "alpha = alpha[P_vis - 1]", 2),
     "head_mean_over_kv_heads": ("a = col_sum / (n_q * n_q_heads)", "a = col_sum / (n_q * n_kv_heads)"),
     "no_query_mean": ("a = col_sum / (n_q * n_q_heads)", "a = col_sum / n_q_heads"),
     "squared_norm": ("return np.sqrt(np.sum(v_rows * v_rows, axis=1))",
@@ -45,6 +45,15 @@ MUTATIONS = {
     "paged_ignores_table": ("out[t] = pages[int(block_table[t // P]), t % P]", "out[t] = pages[t // P, t % P]"),
     "paged_row_from_page_index": ("out[t] = pages[int(block_table[t // P]), t % P]",
                                   "out[t] = pages[int(block_table[t // P]), (t // P) % P]"),
+    "iso_per_head_dim": ("dim = z.shape[2] * z.shape[3]", "dim = z.shape[3]"),
+    "iso_variance_not_std": ("sigma = kappa * value_norms(v_cache, img_pos, img_off) / np.sqrt(dim)",
+                             "sigma = kappa ** 2 * value_norms(v_cache, img_pos, img_off) ** 2 / dim"),
+    "residual_keeps_refreshed": ("alpha = np.where(keep, alpha, 0.0)", "alpha = alpha"),
+    "residual_drops_kept": ("alpha = np.where(keep, alpha, 0.0)", "alpha = np.where(keep, 0.0, alpha)"),
+    "residual_wrong_kv_head": ("y = alpha @ xi[m, :, kv, :]", "y = alpha @ xi[m, :, 0, :]"),
+    "residual_not_squared": ("err[m, i, h] = y @ y", "err[m, i, h] = np.sqrt(y @ y)"),
+    "residual_visual_renormalised": ("                alpha, _ = attention_row(q[i, h], k_cache[: p + 1, kv, :], scale)\n                alpha = alpha[P_vis]\n            else:\n                alpha, _ = attention_row(q[i, h], k_cache[P_vis, kv, :], scale)\n            alpha = np.where",
+                                     "                alpha, _ = attention_row(q[i, h], k_cache[P_vis, kv, :], scale)\n            else:\n                alpha, _ = attention_row(q[i, h], k_cache[P_vis, kv, :], scale)\n            alpha = np.where"),
     "lse_log2": ("return e / total, m + np.log(total)", "return e / total, m + np.log2(total)"),
     "lse_drops_max": ("return e / total, m + np.log(total)", "return e / total, np.log(total)"),
     "layer_sum_not_mean": ("return s / n_layers, A", "return s, A"),
