@@ -273,6 +273,46 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
                                     int32_t k, float scale, void *o_out, float *lse_out,
                                     void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------ *
+ * Residual value-write error of a refresh set, a quality diagnostic of a
+ * selection (the local model of Eq. 3; App. D.1 isotropic Monte Carlo
+ * estimator; App. D.3 projected error).  For displacement sample m, span row i
+ * (position q_pos0 + i) and query head h it computes
+ *     err[m][i][h] = || sum over visual t with refreshed[t] == 0 of
+ *                       alpha_{i,h,t} xi^(m)_t[h / G] ||^2
+ * where alpha is the cached-key attention of the scoring pass, normalised by
+ * the row log-sum-exp row_lse_in (conduit_score's row_lse_out; its norm
+ * decides causal-row or visual-only normalisation), and xi_t[kv] is the
+ * KV-head-kv slice of the displacement:
+ *   z != NULL (isotropic):  xi^(m)_t = kappa * ||V_t|| / sqrt(n_kv_heads *
+ *       head_dim) * z[m][t], so E ||xi_t||^2 = kappa^2 ||V_t||^2 when z holds
+ *       standard normal draws; App. D.1 averages err over m (M = 5).
+ *   z == NULL (projected):  xi_t = V_t, the residual when every stale visual
+ *       value is set to zero (App. D.3); n_samples must be 1.
+ * The attention output map is the identity (the library holds no weights).
+ *
+ * q           device [n_q][n_q_heads][head_dim], kv->dtype: span queries.
+ * row_lse_in  device [n_q][n_q_heads] fp32, natural-log log-sum-exp.
+ * refreshed   device [n_vis] uint8: nonzero = in the refresh set T (e.g.
+ *             conduit_select_topk's mask_out).
+ * z           nullable device [n_samples][n_vis][n_kv_heads][head_dim],
+ *             kv->dtype, 16-byte aligned.
+ * err_out     device [n_samples][n_q][n_q_heads] fp32.
+ * ws          256-byte aligned, conduit_residual_workspace_bytes(kv, n_q,
+ *             img, n_samples, z != NULL) bytes.
+ * Errors: CONDUIT_ERR_INVALID_ARG (NULL row_lse_in / refreshed / err_out,
+ * kappa not finite and > 0 with z, n_samples != 1 without z, ...),
+ * CONDUIT_ERR_UNSUPPORTED if n_samples * n_kv_heads > 65535.
+ * ------------------------------------------------------------------------ */
+size_t conduit_residual_workspace_bytes(const conduit_kv *kv, int32_t n_q, const conduit_images *img,
+                                        int32_t n_samples, int32_t iso);
+
+conduit_status conduit_residual_error(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
+                                      const conduit_images *img, float scale, const float *row_lse_in,
+                                      const uint8_t *refreshed, const void *z, int32_t n_samples,
+                                      float kappa, float *err_out, void *ws, size_t ws_bytes,
+                                      hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * Kernel timing, a tracing aid.  While enabled on the calling thread, every
  * kernel launch made by the entry points above is bracketed by two HIP

@@ -30,7 +30,8 @@ EXPORTS = [
     "conduit_select_workspace_bytes", "conduit_select_topk", "conduit_scatter_kv",
     "conduit_refresh_workspace_bytes", "conduit_refresh_attn", "conduit_status_str",
     "conduit_last_error", "conduit_version", "conduit_profile_enable", "conduit_profile_count",
-    "conduit_profile_read", "conduit_value_norms",
+    "conduit_profile_read", "conduit_value_norms", "conduit_residual_workspace_bytes",
+    "conduit_residual_error",
 ]
 
 
@@ -80,6 +81,11 @@ def lib() -> ctypes.CDLL:
         L.conduit_select_topk.argtypes = [vp, vp, i32, pimg, f32, ctypes.c_int, i32, vp, vp, vp, vp,
                                           vp, vp, vp, sz, vp]
         L.conduit_value_norms.argtypes = [pkv, pimg, vp, vp]
+        L.conduit_residual_workspace_bytes.argtypes = [pkv, i32, pimg, i32, i32]
+        L.conduit_residual_workspace_bytes.restype = sz
+        L.conduit_residual_error.argtypes = [pkv, vp, i32, i32, pimg, f32, vp, vp, vp, i32, f32, vp, vp,
+                                             sz, vp]
+        L.conduit_residual_error.restype = ctypes.c_int
         L.conduit_value_norms.restype = ctypes.c_int
         L.conduit_select_topk.restype = ctypes.c_int
         L.conduit_scatter_kv.argtypes = [pkv, vp, i32, vp, vp, vp, vp, vp]
@@ -231,6 +237,32 @@ def conduit_value_norms(kv: KV, img: ImageTable, vnorm_out: torch.Tensor, stream
     """Value-norm table of one layer (Eq. 7 proxy, Sec. 4.3); see conduit_value_norms."""
     _check(lib().conduit_value_norms(ctypes.byref(kv), ctypes.byref(img.desc), vnorm_out.data_ptr(),
                                      _stream(stream)))
+
+
+def residual_workspace_bytes(kv: KV, n_q: int, img: ImageTable, n_samples: int, iso: bool) -> int:
+    return int(lib().conduit_residual_workspace_bytes(ctypes.byref(kv), n_q, ctypes.byref(img.desc),
+                                                      n_samples, int(iso)))
+
+
+def conduit_residual_error(kv: KV, q: torch.Tensor, q_pos0: int, img: ImageTable,
+                           row_lse: torch.Tensor, refreshed: torch.Tensor, err_out: torch.Tensor,
+                           z: Optional[torch.Tensor] = None, kappa: float = 0.5,
+                           scale: Optional[float] = None, ws: Optional[torch.Tensor] = None,
+                           stream=None) -> None:
+    """Residual value-write error of a refresh set (Eq. 3, App. D.1/D.3); see
+    conduit_residual_error.  z [M, N_vis, H_kv, d] gives the isotropic
+    estimator's draws; without z the projected error is computed."""
+    n_q = q.shape[0]
+    n_samples = 1 if z is None else z.shape[0]
+    if scale is None:
+        scale = 1.0 / math.sqrt(kv.head_dim)
+    need = residual_workspace_bytes(kv, n_q, img, n_samples, z is not None)
+    if ws is None:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _check(lib().conduit_residual_error(ctypes.byref(kv), q.data_ptr(), n_q, q_pos0, ctypes.byref(img.desc),
+                                        scale, row_lse.data_ptr(), refreshed.data_ptr(), _ptr(z), n_samples,
+                                        kappa, err_out.data_ptr(), ws.data_ptr(), ws.numel(),
+                                        _stream(stream)))
 
 
 def conduit_select_topk(s_acc: torch.Tensor, a_acc: torch.Tensor, n_layers: int, img: ImageTable,

@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <string>
 
 #include "common.h"
@@ -418,6 +419,119 @@ conduit_status conduit_value_norms(const conduit_kv *kv, const conduit_images *i
   hipError_t e = launch_value_norms(kv->v, kv->v_stride, pages_of(kv), kv->n_kv_heads * kv->head_dim,
                                     kv->dtype == CONDUIT_BF16, tbl, vnorm_out, stream);
   if (e != hipSuccess) return hip_fail(e, "value norms");
+  return ok();
+}
+
+namespace {
+
+struct ResidualLayout {
+  size_t row_b, vnorm, part, total;
+  int32_t n_splits, tiles_per_split, pairs_pad;
+};
+
+ResidualLayout residual_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis, int32_t n_samples, bool iso) {
+  ResidualLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
+  L.row_b = take((size_t)n_q * kv->n_q_heads * 4);
+  if (iso) L.vnorm = take((size_t)n_vis * 4);
+  if (kv->dtype == CONDUIT_BF16) {
+    const int64_t pairs = (int64_t)n_q * (kv->n_q_heads / kv->n_kv_heads);
+    const int64_t n_pb = (pairs + kResidualPairs - 1) / kResidualPairs;
+    const int tiles = (n_vis + kAttnKeyTile - 1) / kAttnKeyTile;
+    const int64_t base = n_pb * kv->n_kv_heads * n_samples;
+    int splits = (int)std::min<int64_t>((kResidualTargetBlocks + base - 1) / base,
+                                        std::max(1, tiles / kResidualMinTiles));
+    splits = std::max(1, splits);
+    L.tiles_per_split = (tiles + splits - 1) / splits;
+    L.n_splits = (tiles + L.tiles_per_split - 1) / L.tiles_per_split;
+    L.pairs_pad = (int32_t)(n_pb * kResidualPairs);
+    L.part = take((size_t)n_samples * L.n_splits * kv->n_kv_heads * L.pairs_pad * kv->head_dim * 4);
+  }
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+size_t conduit_residual_workspace_bytes(const conduit_kv *kv, int32_t n_q, const conduit_images *img,
+                                        int32_t n_samples, int32_t iso) {
+  if (!kv || !img || n_q < 1 || n_samples < 1 || kv->n_kv_heads < 1 || kv->n_q_heads < kv->n_kv_heads ||
+      img->n_vis < 1 || (kv->head_dim != 64 && kv->head_dim != 128))
+    return 0;
+  return residual_layout(kv, n_q, img->n_vis, n_samples, iso != 0).total;
+}
+
+conduit_status conduit_residual_error(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
+                                      const conduit_images *img, float scale, const float *row_lse_in,
+                                      const uint8_t *refreshed, const void *z, int32_t n_samples, float kappa,
+                                      float *err_out, void *ws, size_t ws_bytes, hipStream_t stream) {
+  conduit_status st = check_kv(kv);
+  if (st) return st;
+  if (!q || !aligned16(q)) return fail(CONDUIT_ERR_INVALID_ARG, "q must be non-NULL and 16-byte aligned");
+  if (n_q < 1) return fail(CONDUIT_ERR_INVALID_ARG, "n_q = %d < 1", n_q);
+  if (q_pos0 < 0 || (int64_t)q_pos0 + n_q > kv->n_ctx)
+    return fail(CONDUIT_ERR_INVALID_ARG, "span [%d, %lld) outside the cache of %d tokens", q_pos0,
+                (long long)q_pos0 + n_q, kv->n_ctx);
+  if (!(scale > 0.f) || scale == __builtin_inff()) return fail(CONDUIT_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (!row_lse_in) return fail(CONDUIT_ERR_INVALID_ARG, "row_lse_in is required (conduit_score's row_lse_out)");
+  if (!refreshed) return fail(CONDUIT_ERR_INVALID_ARG, "refreshed is required");
+  if (!err_out) return fail(CONDUIT_ERR_INVALID_ARG, "err_out is required");
+  const bool iso = z != nullptr;
+  if (iso) {
+    if (!aligned16(z)) return fail(CONDUIT_ERR_INVALID_ARG, "z must be 16-byte aligned");
+    if (n_samples < 1) return fail(CONDUIT_ERR_INVALID_ARG, "n_samples = %d < 1", n_samples);
+    if (!(kappa > 0.f) || kappa == __builtin_inff())
+      return fail(CONDUIT_ERR_INVALID_ARG, "kappa must be finite and > 0");
+  } else if (n_samples != 1) {
+    return fail(CONDUIT_ERR_INVALID_ARG, "the projected error (z = NULL) takes n_samples = 1");
+  }
+  if ((int64_t)n_samples * kv->n_kv_heads > 65535)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "n_samples * n_kv_heads = %lld > 65535",
+                (long long)n_samples * kv->n_kv_heads);
+  if ((int64_t)n_samples * n_q * kv->n_q_heads > INT32_MAX)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "n_samples * n_q * n_q_heads exceeds 2^31 - 1");
+  ImageTable tbl;
+  st = check_images(img, q_pos0, &tbl);
+  if (st) return st;
+  const ResidualLayout L = residual_layout(kv, n_q, img->n_vis, n_samples, iso);
+  st = check_ws(ws, ws_bytes, L.total);
+  if (st) return st;
+  char *w = static_cast<char *>(ws);
+  const bool bf16 = kv->dtype == CONDUIT_BF16;
+  ResidualParams rp{};
+  rp.k = kv->k;
+  rp.k_stride = kv->k_stride;
+  rp.pages = pages_of(kv);
+  rp.disp = iso ? z : kv->v;
+  rp.disp_stride = kv->v_stride;
+  rp.vnorm = iso ? reinterpret_cast<float *>(w + L.vnorm) : nullptr;
+  rp.sigma_scale = iso ? kappa / sqrtf((float)(kv->n_kv_heads * kv->head_dim)) : 1.f;
+  rp.refreshed = refreshed;
+  rp.q = q;
+  rp.n_q = n_q;
+  rp.n_q_heads = kv->n_q_heads;
+  rp.n_kv_heads = kv->n_kv_heads;
+  rp.group = kv->n_q_heads / kv->n_kv_heads;
+  rp.n_vis = img->n_vis;
+  rp.n_samples = n_samples;
+  rp.row_b = reinterpret_cast<float *>(w + L.row_b);
+  rp.scale_log2 = scale * kLog2e;
+  rp.tbl = tbl;
+  rp.n_splits = L.n_splits;
+  rp.tiles_per_split = L.tiles_per_split;
+  rp.pairs_pad = L.pairs_pad;
+  rp.part = bf16 ? reinterpret_cast<float *>(w + L.part) : nullptr;
+  rp.err_out = err_out;
+  hipError_t e = launch_lse_to_b(row_lse_in, reinterpret_cast<float *>(w + L.row_b), n_q * kv->n_q_heads, stream);
+  if (e != hipSuccess) return hip_fail(e, "row statistics");
+  if (iso) {
+    e = launch_value_norms(kv->v, kv->v_stride, pages_of(kv), kv->n_kv_heads * kv->head_dim, bf16, tbl,
+                           reinterpret_cast<float *>(w + L.vnorm), stream);
+    if (e != hipSuccess) return hip_fail(e, "value norms");
+  }
+  e = launch_residual(rp, kv->head_dim, bf16, stream);
+  if (e != hipSuccess) return hip_fail(e, "residual error");
   return ok();
 }
 

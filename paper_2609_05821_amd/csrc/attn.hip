@@ -47,16 +47,6 @@ __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, 
   return row_pos ? row_pos[r] : q_pos0 + r;
 }
 
-// Slot of key `kl` (0..63) of a tile inside a V^T row.  The S^T accumulator
-// gives lane half h, register v the key 8*(v/4) + 4*h + (v%4) of a 32-key
-// sub-tile; the PV product consumes registers 8*ks..8*ks+7 as one 16-deep
-// k-step, so those eight keys are stored contiguously per lane half.
-__device__ __forceinline__ int vt_slot(int kl) {
-  const int sub = kl >> 5, w = kl & 31, ks = w >> 4, r = w & 15;
-  const int h = (r & 7) >> 2, e = 4 * (r >> 3) + (r & 3);
-  return sub * 32 + ks * 16 + h * 8 + e;
-}
-
 // Global -> register staging of one key tile (issued a tile ahead).
 template <int D, bool PV, int W>
 struct TileRegs {

@@ -164,6 +164,16 @@ __device__ __forceinline__ int64_t page_row(const KvPageReader &r, int page, int
   return ((int64_t)pg << r.shift) | (int64_t)((uint32_t)t & ((1u << r.shift) - 1u));
 }
 
+// Slot of key `kl` (0..63) of a tile inside a V^T row.  The S^T accumulator
+// gives lane half h, register v the key 8*(v/4) + 4*h + (v%4) of a 32-key
+// sub-tile; the PV product consumes registers 8*ks..8*ks+7 as one 16-deep
+// k-step, so those eight keys are stored contiguously per lane half.
+__device__ __forceinline__ int vt_slot(int kl) {
+  const int sub = kl >> 5, w = kl & 31, ks = w >> 4, r = w & 15;
+  const int h = (r & 7) >> 2, e = 4 * (r >> 3) + (r & 3);
+  return sub * 32 + ks * 16 + h * 8 + e;
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
@@ -308,6 +318,37 @@ struct ScatterParams {
   void *v_old;              // nullable
 };
 
+// Residual value-write error of a refresh set: for each displacement sample
+// m and (span row, query head) pair, || sum over non-refreshed visual t of
+// alpha_t xi_t ||^2 with alpha from the row's known log-sum-exp.  The bf16
+// path writes per-split partial sums of the residual vector, which a second
+// kernel adds in split order and squares.
+struct ResidualParams {
+  const void *k;
+  int64_t k_stride;
+  KvPages pages;
+  const void *disp;         // iso: z [M][n_vis][H_kv][D]; projected: the V cache
+  int64_t disp_stride;      // projected: elements between V cache rows
+  const float *vnorm;       // iso: ||V_t|| [n_vis]; projected: nullptr
+  float sigma_scale;        // iso: kappa / sqrt(H_kv * D)
+  const uint8_t *refreshed; // [n_vis]: 1 = in the refresh set (left out)
+  const void *q;            // [n_q][n_q_heads][D]
+  int32_t n_q;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t group;
+  int32_t n_vis;
+  int32_t n_samples;
+  const float *row_b;       // [n_q * n_q_heads] log2-domain log-sum-exp
+  float scale_log2;
+  ImageTable tbl;
+  int32_t n_splits;         // bf16: key splits
+  int32_t tiles_per_split;  // bf16: 64-key tiles per split
+  int32_t pairs_pad;        // bf16: pair slots per KV head (blocks of 256)
+  float *part;              // bf16: [M][n_splits][n_kv_heads][pairs_pad][D]
+  float *err_out;           // [M][n_q][n_q_heads]
+};
+
 // Brackets one kernel launch with HIP events when kernel timing is enabled
 // on the calling thread (conduit_profile_enable); otherwise does nothing.
 class ProfScope {
@@ -339,6 +380,13 @@ hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream
 hipError_t launch_select_explicit(const SelectParams &p, const ImageTable &tbl, hipStream_t s);
 hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
+hipError_t launch_residual(const ResidualParams &p, int head_dim, bool bf16, hipStream_t s);
+
+// Residual-error tiling: 256 pairs of one KV head per workgroup (8 waves),
+// 64 visual keys per tile, at least this many tiles per key split.
+constexpr int kResidualPairs = 256;
+constexpr int kResidualMinTiles = 8;
+constexpr int kResidualTargetBlocks = 512;
 
 // Tiling shared by the host layer (workspace sizing) and the kernels.
 // (row, head) pairs per attention workgroup: 256 with values (refresh,

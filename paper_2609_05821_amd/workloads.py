@@ -24,7 +24,10 @@ multi-page documents.  The distributions are:
     K*_t = K_t + xi, xi ~ N(0, kappa^2 ||K_t||^2 / (H_kv d) I), same for V*;
     fresh queries Q*_t ~ N(0, 1) (drawn in float32);
   * the text rows a refresh also recomputes (every non-visual position) get
-    fresh K/V and queries drawn the same way, on streams of their own.
+    fresh K/V and queries drawn the same way, on streams of their own;
+  * the residual-error diagnostic draws M standard normal direction samples
+    per visual token over the concatenated H_kv*d value dims (M = 5 in App.
+    D.1), in the cache dtype.
 
 Sequence layout: [changed prefix][for each image: separator, visual tokens]
 [span].  Caches are token-major [N_ctx, H_kv, d].  bf16 arrays are returned as
@@ -38,7 +41,8 @@ from typing import Dict, List, Optional
 import numpy as np
 
 # random stream ids
-_S_Q, _S_K, _S_VDIR, _S_VNORM, _S_SINK, _S_REL, _S_XI, _S_QSTAR, _S_XI_TEXT, _S_QSTAR_TEXT = range(10)
+(_S_Q, _S_K, _S_VDIR, _S_VNORM, _S_SINK, _S_REL, _S_XI, _S_QSTAR, _S_XI_TEXT, _S_QSTAR_TEXT,
+ _S_ISO) = range(11)
 _GLOBAL_LAYER = 65535  # stream for draws shared by all layers
 
 
@@ -189,6 +193,13 @@ class Workload:
             out["q_text_star"] = self._cast(self._rng(layer, _S_QSTAR_TEXT).standard_normal(
                 (len(T), hq, d), dtype=np.float32))
         return out
+
+
+def iso_directions(w: "Workload", layer: int, n_samples: int) -> np.ndarray:
+    """Standard normal draws z [n_samples, N_vis, H_kv, d] in the cache dtype."""
+    z = w._rng(layer, _S_ISO).standard_normal((n_samples, w.n_vis, w.n_kv_heads, w.head_dim),
+                                                dtype=np.float32)
+    return w._cast(z)
 
 
 def _layout(prefix: int, n_img: int, per_img: int, sep: int, n_q: int):

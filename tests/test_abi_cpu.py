@@ -212,3 +212,39 @@ def test_value_norms_rejects():
     assert L.conduit_value_norms(ctypes.byref(kv(v=0)), ctypes.byref(IMG.desc), out, None) == api.ERR_INVALID_ARG
     bad = api.ImageTable([1500], [0, 1024])  # runs past the cache
     assert L.conduit_value_norms(ctypes.byref(kv()), ctypes.byref(bad.desc), out, None) == api.ERR_INVALID_ARG
+
+
+def residual(kvd=None, q=FAKE, n_q=64, q_pos0=1280, img=IMG, scale=0.088, lse=FAKE, refreshed=FAKE,
+             z=FAKE, n_samples=5, kappa=0.5, err=FAKE, ws=FAKE, ws_bytes=1 << 30):
+    kvd = kvd or kv()
+    return api.lib().conduit_residual_error(ctypes.byref(kvd), q, n_q, q_pos0, ctypes.byref(img.desc), scale,
+                                            lse, refreshed, z, n_samples, kappa, err, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(lse=None), api.ERR_INVALID_ARG),
+    (dict(refreshed=None), api.ERR_INVALID_ARG),
+    (dict(err=None), api.ERR_INVALID_ARG),
+    (dict(z=FAKE + 4), api.ERR_INVALID_ARG),
+    (dict(kappa=0.0), api.ERR_INVALID_ARG),
+    (dict(kappa=float("inf")), api.ERR_INVALID_ARG),
+    (dict(n_samples=0), api.ERR_INVALID_ARG),
+    (dict(z=None, n_samples=2), api.ERR_INVALID_ARG),
+    (dict(n_samples=20000), api.ERR_UNSUPPORTED),
+    (dict(q_pos0=1300), api.ERR_INVALID_ARG),
+    (dict(scale=-1.0), api.ERR_INVALID_ARG),
+    (dict(img=api.ImageTable([1200], [0, 1024])), api.ERR_INVALID_ARG),
+    (dict(ws_bytes=64), api.ERR_WORKSPACE),
+    (dict(kvd=kv(head_dim=96, k_stride=384, v_stride=384)), api.ERR_UNSUPPORTED),
+])
+def test_residual_rejects(case, status):
+    assert residual(**case) == status
+
+
+def test_residual_workspace_sizes():
+    L = api.lib()
+    kvd = kv()
+    iso = L.conduit_residual_workspace_bytes(ctypes.byref(kvd), 64, ctypes.byref(IMG.desc), 5, 1)
+    proj = L.conduit_residual_workspace_bytes(ctypes.byref(kvd), 64, ctypes.byref(IMG.desc), 1, 0)
+    assert iso > proj > 64 * 28 * 4
+    assert L.conduit_residual_workspace_bytes(ctypes.byref(kvd), 0, ctypes.byref(IMG.desc), 5, 1) == 0
