@@ -249,12 +249,27 @@ def main():
         api.conduit_refresh_attn(kv, q_all, rows_all, out_all, ws=ws_all)))
     restore()
 
+    # Residual-error diagnostic: the isotropic estimate (M = 5) of the step's
+    # own 10% refresh set, timed, and the rule comparison table.
+    from paper_2609_05821_amd import diagnostics as D
+    n_samples = 5
+    z_dev = up(W.iso_directions(w, 0, n_samples))
+    err_iso = torch.empty((n_samples, w.n_q, w.n_q_heads), dtype=torch.float32, device=dev)
+    ws_res = torch.empty(api.residual_workspace_bytes(kv, w.n_q, img, n_samples, True), dtype=torch.uint8,
+                         device=dev)
+    variants_ms["residual_iso_m5"] = timed(lambda: api.conduit_residual_error(
+        kv, q, w.q_pos0, img, lse_rows, step.mask, err_iso, z=z_dev, ws=ws_res))
+    diag = D.rule_errors(kv, q, w.q_pos0, img, z_dev, seed=0)
+    del z_dev
+
     # Algorithmic work.
     H, d, hkv = w.n_q_heads, w.head_dim, w.n_kv_heads
     refresh_flops = 4.0 * H * d * float(np.sum(pos_np + 1))
     refresh_exps = H * float(np.sum(pos_np + 1))
     text_flops = refresh_flops + 4.0 * H * d * float(np.sum(text_np + 1))
     e = 2  # bf16 bytes
+    res_flops = 2.0 * w.n_q * H * w.n_vis * d * (1 + n_samples)   # S once, then one product per sample
+    res_bytes = (n_samples + 2) * w.n_vis * hkv * d * e + w.n_q * H * d * e  # z, K and V rows, Q
     score_bytes = (w.n_q * H * d * e + w.n_ctx * hkv * d * e + w.n_vis * hkv * d * e
                    + w.n_vis * 4 * 4)
     score_flops = 2.0 * d * H * sum(w.q_pos0 + i + 1 for i in range(w.n_q)) + \
@@ -329,6 +344,13 @@ def main():
             "tflops_whole_call": text_flops / (variants_ms["recompute_with_text_rows"]["mean"] * 1e-3) / 1e12,
             "note": "merge + refresh attention of the selected rows and every text row, one launch each",
         },
+        "residual_iso_m5": {
+            "algorithmic_flops": res_flops, "algorithmic_bytes": res_bytes,
+            "tflops": res_flops / (variants_ms["residual_iso_m5"]["mean"] * 1e-3) / 1e12,
+            "gbs": res_bytes / (variants_ms["residual_iso_m5"]["mean"] * 1e-3) / 1e9,
+            "note": "conduit_residual_error, isotropic estimator, M = 5, the step's 10% set, all span rows",
+        },
+        "diagnostics": diag,
         "paged": {"page_size": page, "pages": n_log + 8,
                   "note": "same workload with K/V in a shuffled pool of 256-token pages"},
         "variants_bytes": {

@@ -442,6 +442,7 @@ ResidualLayout residual_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis,
     const int64_t base = n_pb * kv->n_kv_heads * n_samples;
     int splits = (int)std::min<int64_t>((kResidualTargetBlocks + base - 1) / base,
                                         std::max(1, tiles / kResidualMinTiles));
+    splits = std::max(splits, (tiles + kResidualMaxTiles - 1) / kResidualMaxTiles);
     splits = std::max(1, splits);
     L.tiles_per_split = (tiles + splits - 1) / splits;
     L.n_splits = (tiles + L.tiles_per_split - 1) / L.tiles_per_split;

@@ -387,6 +387,7 @@ hipError_t launch_residual(const ResidualParams &p, int head_dim, bool bf16, hip
 constexpr int kResidualPairs = 256;
 constexpr int kResidualMinTiles = 8;
 constexpr int kResidualTargetBlocks = 512;
+constexpr int kResidualMaxTiles = 32;   // key metadata of a split is held in LDS
 
 // Tiling shared by the host layer (workspace sizing) and the kernels.
 // (row, head) pairs per attention workgroup: 256 with values (refresh,

@@ -16,6 +16,8 @@
 // the last visual token get a zero displacement row at staging.  Partial y
 // per split go to the workspace; residual_sum_kernel adds them in split order
 // and squares.
+#include <type_traits>
+
 #include "common.h"
 
 namespace conduit {
@@ -28,6 +30,8 @@ template <int D>
 struct ResidualSmem {
   alignas(16) u16 k[2][KT][D + 8];   // K rows of the tile's visual keys
   alignas(16) u16 xt[2][D][KT + 8];  // displacement tile, transposed (MFMA operand order)
+  int64_t row[kResidualMaxTiles * KT];   // cache row of each key of the split
+  float scale[kResidualMaxTiles * KT];   // displacement scale: sigma_t, 1, or 0 (refreshed)
   ImageLds img;
 };
 
@@ -70,42 +74,55 @@ __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualPara
   const int tv_beg = split * p.tiles_per_split * KT;
   const int tv_end = min(tv_beg + p.tiles_per_split * KT, p.n_vis);
   __syncthreads();  // image table in LDS
+  // Per-key metadata of the split, resolved once: the tile loop then reads
+  // only LDS before its global loads (a dependent global read there would
+  // make every tile wait for the loads already in flight).
+  for (int j = tid; j < tv_end - tv_beg; j += kThreads) {
+    const int tv = tv_beg + j;
+    sm.row[j] = kv_row(p.pages, vis_position(sm.img, tv));
+    sm.scale[j] = p.refreshed[tv] ? 0.f : (iso ? p.vnorm[tv] * p.sigma_scale : 1.f);
+  }
+  __syncthreads();
+  const int last = max(tv_end - tv_beg - 1, 0);
 
-  u32x4 rk[KCH];
-  u32x4 rx[XPT][2];
-  float sx[XPT][2];
-  // Global -> registers for the tile of visual keys tv0 .. tv0 + 63.
-  auto load_tile = [&](int tv0) __attribute__((always_inline)) {
+  // Two register sets: tiles are loaded two ahead of the one computing, so
+  // each load has two tiles' compute to arrive.
+  u32x4 rk[2][KCH];
+  u32x4 rx[2][XPT][2];
+  float sx[2][XPT][2];
+  // Global -> register set R for the tile of visual keys tv0 .. tv0 + 63.
+  auto load_tile = [&](int tv0, auto set) __attribute__((always_inline)) {
+    constexpr int R = decltype(set)::value;
+    const int j0 = tv0 - tv_beg;
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int cidx = tid + kThreads * i;
-      const int tv = min(tv0 + cidx / (D / 8), p.n_vis - 1);
-      const int64_t row = kv_row(p.pages, vis_position(sm.img, tv));
-      rk[i] = ld16(Kg + row * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
+      const int j = min(j0 + cidx / (D / 8), last);
+      rk[R][i] = ld16(Kg + sm.row[j] * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
     }
 #pragma unroll
     for (int it = 0; it < XPT; ++it) {
-      const int xi = tid + kThreads * it;
+      const int xi = min(tid + kThreads * it, XIT - 1);
       const int kp = xi % (KT / 2), dc = xi / (KT / 2);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const int tv = tv0 + 2 * kp + e;
-        const int tc = min(tv, p.n_vis - 1);
-        const bool keep = xi < XIT && tv < p.n_vis && p.refreshed[tc] == 0;
-        const u16 *src = iso ? Xg + (((int64_t)m * p.n_vis + tc) * p.n_kv_heads + kvh) * D + dc * 8
-                             : Xg + kv_row(p.pages, vis_position(sm.img, tc)) * p.disp_stride + kvh * D + dc * 8;
-        rx[it][e] = xi < XIT ? ld16(src) : u32x4{0, 0, 0, 0};
-        sx[it][e] = keep ? (iso ? p.vnorm[tc] * p.sigma_scale : 1.f) : 0.f;
+        const int jr = j0 + 2 * kp + e;
+        const int j = min(jr, last);
+        const int64_t off = iso ? (((int64_t)m * p.n_vis + tv_beg + j) * p.n_kv_heads + kvh) * D
+                                : sm.row[j] * p.disp_stride + kvh * D;
+        rx[R][it][e] = ld16(Xg + off + dc * 8);
+        sx[R][it][e] = jr <= last && tid + kThreads * it < XIT ? sm.scale[j] : 0.f;
       }
     }
   };
   // Registers -> LDS: K rows as loaded; the displacement scaled, rounded to
   // bf16 and written transposed, two keys per 32-bit word.
-  auto store_tile = [&](int buf) __attribute__((always_inline)) {
+  auto store_tile = [&](int buf, auto set) __attribute__((always_inline)) {
+    constexpr int R = decltype(set)::value;
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int cidx = tid + kThreads * i;
-      st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
+      st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[R][i]);
     }
 #pragma unroll
     for (int it = 0; it < XPT; ++it) {
@@ -118,9 +135,9 @@ __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualPara
         uint32_t w[2];
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
-          const uint32_t u = rx[it][e][e2];
-          const float lo = __builtin_bit_cast(float, u << 16) * sx[it][e];
-          const float hi = __builtin_bit_cast(float, u & 0xffff0000u) * sx[it][e];
+          const uint32_t u = rx[R][it][e][e2];
+          const float lo = __builtin_bit_cast(float, u << 16) * sx[R][it][e];
+          const float hi = __builtin_bit_cast(float, u & 0xffff0000u) * sx[R][it][e];
           w[e] = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
         }
         // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
@@ -158,18 +175,29 @@ __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualPara
     }
   };
 
-  if (tv_beg < tv_end) {
-    load_tile(tv_beg);
-    store_tile(0);
+  constexpr std::integral_constant<int, 0> S0{};
+  constexpr std::integral_constant<int, 1> S1{};
+  const int n_t = (tv_end - tv_beg + KT - 1) / KT;
+  if (n_t > 0) {
+    // LDS buffer b holds the tile being computed; register set 1 - b holds
+    // the next tile and set b receives the one after it.
+    // Loads are unconditional (past the split's end they repeat its last
+    // tile and are never stored), so each wait covers only the older set.
+    auto tile_at = [&](int i) { return tv_beg + min(i, n_t - 1) * KT; };
+    load_tile(tile_at(0), S0);
+    load_tile(tile_at(1), S1);
+    store_tile(0, S0);
     __syncthreads();
-    int buf = 0;
-    for (int tv0 = tv_beg; tv0 < tv_end; tv0 += KT) {
-      const bool more = tv0 + KT < tv_end;
-      if (more) load_tile(tv0 + KT);
-      tile(buf);
-      if (more) store_tile(buf ^ 1);
+    for (int i = 0; i < n_t; i += 2) {
+      load_tile(tile_at(i + 2), S0);
+      tile(0);
+      if (i + 1 < n_t) store_tile(1, S1);
       __syncthreads();
-      buf ^= 1;
+      if (i + 1 >= n_t) break;
+      load_tile(tile_at(i + 3), S1);
+      tile(1);
+      if (i + 2 < n_t) store_tile(0, S0);
+      __syncthreads();
     }
   }
 
