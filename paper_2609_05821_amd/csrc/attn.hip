@@ -35,13 +35,40 @@ constexpr int KT = kAttnKeyTile;
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kMInit = -1e30f;  // initial running maximum (log2 units)
 
-template <int D>
+template <int D, bool PV>
 struct AttnSmem {
   alignas(16) u16 k[2][KT][D + 8];   // K tiles, one row per key (+16 B pad against bank conflicts)
-  alignas(16) u16 vt[2][D][KT + 8];  // V^T tiles, keys in MFMA-operand order
+  alignas(16) u16 v[2][PV ? KT : 1][D + 32];  // V tiles, one row per key; rows 16 words apart mod 64 banks
   uint64_t okmask[2];                // key-domain filter per tile, bit = key
   ImageLds img;                      // visual-only statistics: the image table
 };
+
+// The A operand of O^T += V^T P^T for one 16-key MFMA step, read from the
+// row-major V tile with two transposing LDS reads (ds_read_b64_tr_b16): in
+// each group of 16 lanes, lane 4j + q reads 4 head dims of key j and lane
+// 4q + r receives dim 4q + r of keys 0..3.  Lane (m, h) of the wave ends up
+// with keys 4h + 0..3 and 8 + 4h + 0..3 of the step for head dim m, the
+// order in which the S^T accumulator holds them (so P needs no shuffle).
+typedef short short4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) short4 lds_short4;
+
+typedef short short8 __attribute__((ext_vector_type(8)));
+
+// Element offset, inside a V tile with row stride VS, of the 4 dims this
+// lane reads for the first half of an MFMA step (keys 0..7); the second
+// half (keys 8..15) is 8 rows further.
+template <int VS>
+__device__ __forceinline__ int v_operand_lane_offset(int lane) {
+  const int s = lane & 15, h = lane >> 5, dgrp = (lane >> 4) & 1;
+  return (4 * h + (s >> 2)) * VS + 16 * dgrp + 4 * (s & 3);
+}
+
+template <int VS>
+__device__ __forceinline__ bf16x8 v_operand(const u16 *at) {
+  const short4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(at));
+  const short4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(at + 8 * VS));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
 
 __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, int r) {
   return row_pos ? row_pos[r] : q_pos0 + r;
@@ -51,11 +78,9 @@ __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, 
 template <int D, bool PV, int W>
 struct TileRegs {
   static constexpr int kThreads = W * 64;
-  static constexpr int KCH = KT * D / 8 / kThreads;    // 16-byte K chunks per thread
-  static constexpr int VIT = (KT / 2) * (D / 8);       // 2-key x 8-dim V items
-  static constexpr int VPT = VIT >= kThreads ? VIT / kThreads : 1;  // items per thread
+  static constexpr int KCH = KT * D / 8 / kThreads;    // 16-byte K (and V) chunks per thread
   u32x4 k[KCH];
-  u32x4 v[PV ? 2 : 1];
+  u32x4 v[PV ? KCH : 1];
   uint8_t ok;
 };
 
@@ -271,7 +296,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   constexpr int KS = D / 16;      // MFMA k-steps over the head dimension
   constexpr int DT = D / 32;      // 32-row tiles of O^T
   using Regs = TileRegs<D, PV, W>;
-  __shared__ AttnSmem<D> sm;
+  __shared__ AttnSmem<D, PV> sm;
 
   const int G = p.group;
   const int n_pairs = p.n_rows * G;
@@ -280,6 +305,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const u16 *Kg = static_cast<const u16 *>(p.k);
   const u16 *Vg = static_cast<const u16 *>(p.v);
   const KvPageReader pr = page_reader(p.pages, p.n_ctx);
+  const int v_lane = v_operand_lane_offset<D + 32>(lane);  // PV operand reads
   const u16 *Qg = static_cast<const u16 *>(p.q);
   const float c = p.scale_log2;
   const int n_items = min(p.plan.hdr[0], p.plan.max_items);
@@ -319,31 +345,18 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         qreg[ks] = as_bf16x8(valid ? ld16(qrow + ks * 16) : u32x4{0, 0, 0, 0});
     }
 
-    // Per-thread offsets of its staging chunks inside a key tile; a tile's
-    // base moves by KT rows, and only a partial last tile clamps its rows.
-    int64_t koff[Regs::KCH];
+    // Per-thread offsets of its staging chunks inside a key tile (16 lanes
+    // per key row, so K and V loads are coalesced); a tile's base moves by KT
+    // rows, and only a partial last tile clamps its rows.
+    int64_t koff[Regs::KCH], voff[Regs::KCH];
 #pragma unroll
     for (int i = 0; i < Regs::KCH; ++i) {
       const int cidx = tid + kThreads * i;
       koff[i] = (int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8;
-    }
-    // V items: item = tid + kThreads * i; key pair fastest, so each half-wave
-    // later writes 32 different keys of one V^T row (32 different LDS banks).
-    constexpr int VPT = Regs::VPT;
-    const bool v_active = Regs::VIT >= kThreads || tid < Regs::VIT;
-    int v_kpair[VPT], v_dc[VPT];
-    int64_t voff[VPT][2];
-#pragma unroll
-    for (int it = 0; it < VPT; ++it) {
-      const int vi = tid + kThreads * it;
-      v_kpair[it] = vi % (KT / 2);
-      v_dc[it] = vi / (KT / 2);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        voff[it][i] = (int64_t)(v_kpair[it] * 2 + i) * p.v_stride + kvh * D + v_dc[it] * 8;
+      voff[i] = (int64_t)(cidx / (D / 8)) * p.v_stride + kvh * D + (cidx % (D / 8)) * 8;
     }
     u32x4 rk[Regs::KCH];
-    u32x4 rv[PV ? VPT : 1][2];
+    u32x4 rv[PV ? Regs::KCH : 1];
     bool rok = false;
     // t0 is a multiple of the tile and a page holds a whole number of tiles,
     // so a tile's rows are consecutive rows of the cache starting at row0.
@@ -354,12 +367,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
 #pragma unroll
         for (int i = 0; i < Regs::KCH; ++i) rk[i] = ld16(kb + koff[i]);
         if constexpr (PV) {
-          if (v_active) {
 #pragma unroll
-            for (int it = 0; it < VPT; ++it)
-#pragma unroll
-              for (int i = 0; i < 2; ++i) rv[it][i] = ld16(vb + voff[it][i]);
-          }
+          for (int i = 0; i < Regs::KCH; ++i) rv[i] = ld16(vb + voff[i]);
         }
       } else {  // partial tile: rows past kend repeat the last row (masked later)
 #pragma unroll
@@ -369,14 +378,11 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
           rk[i] = ld16(kb + (int64_t)(kp - t0) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
         }
         if constexpr (PV) {
-          if (v_active) {
 #pragma unroll
-            for (int it = 0; it < VPT; ++it)
-#pragma unroll
-              for (int i = 0; i < 2; ++i) {
-                const int kp = min(t0 + v_kpair[it] * 2 + i, kend - 1);
-                rv[it][i] = ld16(vb + (int64_t)(kp - t0) * p.v_stride + kvh * D + v_dc[it] * 8);
-              }
+          for (int i = 0; i < Regs::KCH; ++i) {
+            const int cidx = tid + kThreads * i;
+            const int kp = min(t0 + cidx / (D / 8), kend - 1);
+            rv[i] = ld16(vb + (int64_t)(kp - t0) * p.v_stride + kvh * D + (cidx % (D / 8)) * 8);
           }
         }
       }
@@ -392,20 +398,10 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
       }
       if constexpr (PV) {
-        if (v_active) {
 #pragma unroll
-          for (int it = 0; it < VPT; ++it) {
-            const int slot = vt_slot(v_kpair[it] * 2);
-            const u32x4 w0 = rv[it][0], w1 = rv[it][1];
-#pragma unroll
-            for (int e2 = 0; e2 < 4; ++e2) {
-              // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
-              *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc[it] * 8 + 2 * e2][slot]) =
-                  (w0[e2] & 0xffffu) | (w1[e2] << 16);
-              *reinterpret_cast<uint32_t *>(&sm.vt[buf][v_dc[it] * 8 + 2 * e2 + 1][slot]) =
-                  (w0[e2] >> 16) | (w1[e2] & 0xffff0000u);
-            }
-          }
+        for (int i = 0; i < Regs::KCH; ++i) {
+          const int cidx = tid + kThreads * i;
+          st16(&sm.v[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rv[i]);
         }
       }
       if (!PV && p.vis_only && tid < KT) {  // wave 0: one bit per key of the tile
@@ -482,7 +478,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
-            va[ks][dt] = as_bf16x8(ld16(&sm.vt[buf][dt * 32 + col][sub * 32 + ks * 16 + 8 * half]));
+            va[ks][dt] = v_operand<D + 32>(&sm.v[buf][sub * 32 + ks * 16][dt * 32] + v_lane);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
