@@ -302,7 +302,7 @@ def main():
             "lambda": 1.0, "norm": "causal_row", "cold_cache_scrub": not args.no_scrub,
         },
         "roofline": {
-            "kernel": "attn_bf16_kernel<128, true, 8> (refresh attention of conduit_refresh_attn)",
+            "kernel": "attn_bf16_kernel<128, true, 8, false> (refresh attention of conduit_refresh_attn)",
             "bound": "mfma",
             "achieved": attn_tflops,
             "peak": PEAK_BF16_TFLOPS,

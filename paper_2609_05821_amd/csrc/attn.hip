@@ -26,6 +26,9 @@
 //     domain.
 //  3. combine_kernel merges the partials of split blocks in a fixed order
 //     (deterministic, no atomics).
+#include <algorithm>
+#include <climits>
+
 #include "common.h"
 
 namespace conduit {
@@ -72,6 +75,18 @@ __device__ __forceinline__ bf16x8 v_operand(const u16 *at) {
 
 __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, int r) {
   return row_pos ? row_pos[r] : q_pos0 + r;
+}
+
+// Closed-form plan of rows at q_pos0 + r: block pb's {maxpos, minpos, n_s,
+// chunk} (positions clamped to the cache, n_s near-equal splits).
+__device__ __forceinline__ int4 uniform_block_info(int pb, int ppb, int group, int n_rows, int q_pos0,
+                                                   int n_ctx, int ns) {
+  const int64_t p0 = (int64_t)pb * ppb;
+  const int64_t p1 = min(p0 + ppb, (int64_t)n_rows * group) - 1;
+  const int minpos = min(q_pos0 + (int)(p0 / group), n_ctx - 1);
+  const int maxpos = min(q_pos0 + (int)(p1 / group), n_ctx - 1);
+  const int tiles = maxpos / KT + 1;
+  return make_int4(maxpos, minpos, ns, ((tiles + ns - 1) / ns) * KT);
 }
 
 // Global -> register staging of one key tile (issued a tile ahead).
@@ -289,7 +304,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
 // tile; statistics only W = 4 with two workgroups per CU.  The grid is
 // persistent: workgroup g takes items g, 2G' - 1 - g, 2G' + g, ... of the
 // plan (G' = grid size), i.e. snake order over a largest-first list.
-template <int D, bool PV, int W>
+template <int D, bool PV, int W, bool UNI>
 __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) {
   constexpr int kThreads = W * 64;
   constexpr int kPairs = W * 32;  // (row, head) pairs per block
@@ -308,7 +323,9 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const int v_lane = v_operand_lane_offset<D + 32>(lane);  // PV operand reads
   const u16 *Qg = static_cast<const u16 *>(p.q);
   const float c = p.scale_log2;
-  const int n_items = min(p.plan.hdr[0], p.plan.max_items);
+  // UNI: the closed-form plan of contiguous rows (no plan loads at all).
+  constexpr bool uniform = UNI;
+  const int n_items = uniform ? p.plan.uniform_items : min(p.plan.hdr[0], p.plan.max_items);
   const int grid = gridDim.x, g = blockIdx.x;
   if (!PV && p.vis_only) {
     image_table_to_lds(p.tbl, sm.img, tid, kThreads);
@@ -318,12 +335,15 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   for (int round = 0;; ++round) {
     const int idx = round * grid + ((round & 1) ? grid - 1 - g : g);
     if (idx >= n_items) break;
-    const int4 item = p.plan.items[idx];  // {kv head, block, split, slot}
+    const int uns = p.plan.uniform_ns;
+    const int4 item = uniform ? make_int4((idx / uns) % p.n_kv_heads, idx / (uns * p.n_kv_heads), idx % uns, idx)
+                              : p.plan.items[idx];  // {kv head, block, split, slot}
     const int kvh = item.x, pb = item.y;
     if (kvh < 0 || kvh >= p.n_kv_heads || pb < 0 || pb >= p.plan.n_pb || item.w < 0 ||
         item.w >= p.plan.max_items)
       continue;
-    const int4 info = p.plan.pb_info[pb];  // {maxpos, minpos, n_s, chunk}
+    const int4 info = uniform ? uniform_block_info(pb, kPairs, G, p.n_rows, p.q_pos0, p.n_ctx, uns)
+                              : p.plan.pb_info[pb];  // {maxpos, minpos, n_s, chunk}
     const int kbeg = item.z * info.w;
     const int kend = min(kbeg + info.w, info.x + 1);
     const int minpos = info.y;
@@ -585,9 +605,11 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   const int h = hq / p.group;
   const int64_t pair = (int64_t)r * p.group + hq % p.group;
   const int pb = (int)(pair / p.ppb), j = (int)(pair % p.ppb);
-  const int ns = p.plan.pb_info[pb].z;
+  const bool uniform = p.plan.uniform_ns > 0;
+  const int ns = uniform ? p.plan.uniform_ns : p.plan.pb_info[pb].z;
   if (ns <= 1) return;  // written by the attention kernel
-  const int64_t slot0 = (int64_t)h * p.plan.hdr[1] + p.plan.pb_base[pb];
+  const int64_t slot0 = uniform ? ((int64_t)pb * (p.n_q_heads / p.group) + h) * ns
+                                : (int64_t)h * p.plan.hdr[1] + p.plan.pb_base[pb];
   if (slot0 + ns > p.plan.max_items) return;  // never for a plan within its bound
   float M = kNegInf;
   for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_m[(slot0 + s) * p.ppb + j]);
@@ -681,8 +703,44 @@ __global__ void lse_to_b_kernel(const float *lse, float *b, int n) {
 
 }  // namespace
 
-hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipStream_t s) {
+// Split count of the closed-form plan for rows at q_pos0 + r: about the
+// device plan's item target, at least kAttnPlanMinTiles tiles per split of
+// the shortest block, and no empty split in any block.
+static int uniform_split_count(const AttnParams &p, int ppb, int target) {
+  const int64_t n_pairs = (int64_t)p.n_rows * p.group;
+  const int n_pb = (int)((n_pairs + ppb - 1) / ppb);
+  int min_tiles = INT32_MAX;
+  auto tiles_of = [&](int b) {
+    const int64_t last = std::min<int64_t>((int64_t)(b + 1) * ppb, n_pairs) - 1;
+    const int maxpos = std::min(p.q_pos0 + (int)(last / p.group), p.n_ctx - 1);
+    return maxpos / KT + 1;
+  };
+  for (int b = 0; b < n_pb; ++b) min_tiles = std::min(min_tiles, tiles_of(b));
+  int ns = std::max(1, target / std::max(1, n_pb * p.n_kv_heads));
+  ns = std::min(ns, std::max(1, min_tiles / kAttnPlanMinTiles));
+  auto all_nonempty = [&](int n) {
+    for (int b = 0; b < n_pb; ++b) {
+      const int t = tiles_of(b);
+      if ((int64_t)((t + n - 1) / n) * (n - 1) >= t) return false;
+    }
+    return true;
+  };
+  while (ns > 1 && !all_nonempty(ns)) --ns;
+  return ns;
+}
+
+hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, hipStream_t s) {
   const int ppb = attn_pairs_per_block(with_values);
+  AttnParams p = p_in;
+  if (!p.row_pos && !with_values) {  // the scoring span: closed-form plan, no plan launch
+    const int ns = uniform_split_count(p, ppb, attn_grid(with_values) * attn_plan_rounds(with_values));
+    const int64_t n_pb = ((int64_t)p.n_rows * p.group + ppb - 1) / ppb;
+    p.plan.uniform_ns = ns;
+    p.plan.uniform_items = (int32_t)(n_pb * p.n_kv_heads * ns);
+  } else {
+    p.plan.uniform_ns = 0;
+    p.plan.uniform_items = 0;
+  }
   PlanArgs pa{};
   pa.row_pos = p.row_pos;
   pa.q_pos0 = p.q_pos0;
@@ -693,22 +751,27 @@ hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipS
   pa.ppb = ppb;
   pa.target_items = attn_grid(with_values) * attn_plan_rounds(with_values);
   pa.plan = p.plan;
-  {
+  hipError_t e = hipSuccess;
+  if (p.plan.uniform_ns == 0) {
     ProfScope ps("attn_plan", s);
     attn_plan_kernel<<<1, kPlanThreads, 0, s>>>(pa);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
 
   const int grid = attn_grid(with_values);
   {
     ProfScope ps(with_values ? "attn_values" : "attn_stats", s);
+    // the closed-form plan only serves the statistics of the scoring span
+    const bool uni = p.plan.uniform_ns > 0 && !with_values;
     if (head_dim == 128) {
-      if (with_values) attn_bf16_kernel<128, true, 8><<<grid, 8 * 64, 0, s>>>(p);
-      else attn_bf16_kernel<128, false, 4><<<grid, 4 * 64, 0, s>>>(p);
+      if (with_values) attn_bf16_kernel<128, true, 8, false><<<grid, 8 * 64, 0, s>>>(p);
+      else if (uni) attn_bf16_kernel<128, false, 4, true><<<grid, 4 * 64, 0, s>>>(p);
+      else attn_bf16_kernel<128, false, 4, false><<<grid, 4 * 64, 0, s>>>(p);
     } else {
-      if (with_values) attn_bf16_kernel<64, true, 8><<<grid, 8 * 64, 0, s>>>(p);
-      else attn_bf16_kernel<64, false, 4><<<grid, 4 * 64, 0, s>>>(p);
+      if (with_values) attn_bf16_kernel<64, true, 8, false><<<grid, 8 * 64, 0, s>>>(p);
+      else if (uni) attn_bf16_kernel<64, false, 4, true><<<grid, 4 * 64, 0, s>>>(p);
+      else attn_bf16_kernel<64, false, 4, false><<<grid, 4 * 64, 0, s>>>(p);
     }
   }
   e = hipGetLastError();

@@ -199,6 +199,12 @@ struct AttnPlan {
   int32_t *hdr;             // {n_items, slots per KV head}
   int32_t n_pb;
   int32_t max_items;
+  // Rows at q_pos0 + r (the scoring span): the plan is closed-form instead,
+  // every block cut into uniform_ns near-equal splits, item i = (block,
+  // KV head, split) = ((block * n_kv_heads + head) * uniform_ns + split),
+  // its own partial slot.  0 = the device-built plan above.
+  int32_t uniform_ns;
+  int32_t uniform_items;
 };
 
 // Causal attention of a set of query rows against one layer's cache.  Used for
