@@ -327,6 +327,8 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   float *row_b = reinterpret_cast<float *>(at(ws, L.row_b));
   const bool vis_only = norm == CONDUIT_NORM_VISUAL_ONLY;
 
+  int32_t lse_ns = 0;
+  bool fuse_lse = false;
   hipError_t e;
   if (row_lse_in) {
     e = launch_lse_to_b(row_lse_in, row_b, n_q * kv->n_q_heads, stream);
@@ -360,6 +362,12 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
       ap.plan = plan_at(ws, L.plan);
       ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
       ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
+      // With split rows the column-sum kernel merges the partials itself
+      // when its LDS holds every row of a KV head.
+      lse_ns = attn_uniform_splits(ap, attn_pairs_per_block(false),
+                                   attn_grid(false) * attn_plan_rounds(false));
+      fuse_lse = lse_ns > 1 && (int64_t)n_q * ap.group <= kColsumMaxLsePairs;
+      ap.skip_merge = fuse_lse ? 1 : 0;
       e = launch_attn(ap, D, false, stream);
       if (e != hipSuccess) return hip_fail(e, "row statistics");
     } else {
@@ -387,8 +395,6 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   cs.colsum_part = reinterpret_cast<float *>(at(ws, L.colsum));
   cs.vsq_part = reinterpret_cast<float *>(at(ws, L.vsq));
   cs.vnorm_in = vnorm_in;
-  e = launch_colsum(cs, D, bf16, agg == CONDUIT_AGG_RMS, stream);
-  if (e != hipSuccess) return hip_fail(e, "column sums");
 
   FinalizeParams fp{};
   fp.colsum_part = cs.colsum_part;
@@ -403,6 +409,16 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   fp.a_acc = a_acc;
   fp.a_out = a_out;
   fp.vnorm_out = vnorm_out;
+
+  if (fuse_lse) {
+    cs.lse_part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
+    cs.lse_part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
+    cs.lse_ns = lse_ns;
+    cs.lse_ppb = attn_pairs_per_block(false);
+    cs.lse_out = row_lse_out;
+  }
+  e = launch_colsum(cs, D, bf16, agg == CONDUIT_AGG_RMS, stream);
+  if (e != hipSuccess) return hip_fail(e, "column sums");
   e = launch_finalize(fp, stream);
   if (e != hipSuccess) return hip_fail(e, "finalize");
   return ok();

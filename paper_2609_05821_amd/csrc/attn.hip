@@ -326,6 +326,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   // UNI: the closed-form plan of contiguous rows (no plan loads at all).
   constexpr bool uniform = UNI;
   const int n_items = uniform ? p.plan.uniform_items : min(p.plan.hdr[0], p.plan.max_items);
+
   const int grid = gridDim.x, g = blockIdx.x;
   if (!PV && p.vis_only) {
     image_table_to_lds(p.tbl, sm.img, tid, kThreads);
@@ -706,7 +707,7 @@ __global__ void lse_to_b_kernel(const float *lse, float *b, int n) {
 // Split count of the closed-form plan for rows at q_pos0 + r: about the
 // device plan's item target, at least kAttnPlanMinTiles tiles per split of
 // the shortest block, and no empty split in any block.
-static int uniform_split_count(const AttnParams &p, int ppb, int target) {
+int attn_uniform_splits(const AttnParams &p, int ppb, int target) {
   const int64_t n_pairs = (int64_t)p.n_rows * p.group;
   const int n_pb = (int)((n_pairs + ppb - 1) / ppb);
   int min_tiles = INT32_MAX;
@@ -733,7 +734,7 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
   const int ppb = attn_pairs_per_block(with_values);
   AttnParams p = p_in;
   if (!p.row_pos && !with_values) {  // the scoring span: closed-form plan, no plan launch
-    const int ns = uniform_split_count(p, ppb, attn_grid(with_values) * attn_plan_rounds(with_values));
+    const int ns = attn_uniform_splits(p, ppb, attn_grid(with_values) * attn_plan_rounds(with_values));
     const int64_t n_pb = ((int64_t)p.n_rows * p.group + ppb - 1) / ppb;
     p.plan.uniform_ns = ns;
     p.plan.uniform_items = (int32_t)(n_pb * p.n_kv_heads * ns);
@@ -777,6 +778,7 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
   e = hipGetLastError();
   if (e != hipSuccess) return e;
 
+  if (p.skip_merge) return hipSuccess;  // merged by the caller's next kernel
   CombineParams cp{};
   cp.n_rows = p.n_rows;
   cp.n_q_heads = p.n_q_heads;

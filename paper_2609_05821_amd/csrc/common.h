@@ -235,6 +235,7 @@ struct AttnParams {
   float *lse_out;           // nullable [n_rows * H_q]: natural-log log-sum-exp
   void *o_out;              // [n_rows][H_q][D] bf16 (values only)
   ImageTable tbl;           // read when vis_only
+  int32_t skip_merge;       // host side: the split partials are merged by the caller's next kernel
 };
 
 // Merge of split partials into final outputs (blocks with n_s > 1).
@@ -259,6 +260,22 @@ struct DirectOut {
   float *o_out;
 };
 
+
+struct FinalizeParams {
+  const float *colsum_part;
+  const float *vsq_part;
+  const float *vnorm_in;    // nullable: value norms given
+  int32_t n_kv_heads;
+  int32_t n_vis;
+  float n_rows_f;           // n_q * n_q_heads, as float
+  int32_t rms;              // a = sqrt(colsum / n_rows) (Eq. 4) instead of the mean
+  int32_t accumulate;
+  float *s_acc;
+  float *a_acc;
+  float *a_out;             // nullable
+  float *vnorm_out;         // nullable
+};
+
 struct ColsumParams {
   const void *k;
   const void *v;
@@ -277,21 +294,14 @@ struct ColsumParams {
   float *colsum_part;       // [n_kv_heads][n_vis]: sum of alpha (or alpha^2 for RMS)
   float *vsq_part;          // [n_kv_heads][n_vis]
   const float *vnorm_in;    // nullable: value norms given, V not read
-};
-
-struct FinalizeParams {
-  const float *colsum_part;
-  const float *vsq_part;
-  const float *vnorm_in;    // nullable: value norms given
-  int32_t n_kv_heads;
-  int32_t n_vis;
-  float n_rows_f;           // n_q * n_q_heads, as float
-  int32_t rms;              // a = sqrt(colsum / n_rows) (Eq. 4) instead of the mean
-  int32_t accumulate;
-  float *s_acc;
-  float *a_acc;
-  float *a_out;             // nullable
-  float *vnorm_out;         // nullable
+  // Row log-sum-exp rebuilt from the statistics pass's split partials (its
+  // closed-form plan: lse_ns splits of lse_ppb-pair blocks) instead of read
+  // from row_b; the first key block also writes lse_out (natural log).
+  const float *lse_part_m;
+  const float *lse_part_l;
+  int32_t lse_ns;
+  int32_t lse_ppb;
+  float *lse_out;
 };
 
 struct SelectParams {
@@ -378,6 +388,9 @@ hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipS
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s);
 hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, hipStream_t s);
+// Split count of the closed-form plan the statistics pass uses for rows at
+// q_pos0 + r (pairs per block ppb), as launch_attn picks it.
+int attn_uniform_splits(const AttnParams &p, int ppb, int target);
 hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s);
 hipError_t launch_value_norms(const void *v, int64_t v_stride, const KvPages &pages, int32_t row_elems,
                               bool bf16, const ImageTable &tbl, float *out, hipStream_t s);
@@ -416,6 +429,7 @@ constexpr int64_t attn_max_items(int64_t n_pb, int64_t n_kv_heads, bool with_val
   return (int64_t)attn_grid(with_values) * attn_plan_rounds(with_values) + n_pb * n_kv_heads;
 }
 constexpr int kAttnKeyTile = 64;         // keys per LDS tile
-constexpr int kColsumKeysPerBlock = 256; // visual keys per workgroup
+constexpr int kColsumKeysPerBlock = 256;
+constexpr int kColsumMaxLsePairs = 4096;  // row LSEs a column-sum workgroup can rebuild in LDS // visual keys per workgroup
 
 }  // namespace conduit

@@ -31,8 +31,33 @@ constexpr int kColsumThreads = 512;   // 8 waves x 32 keys
 // value norms are fetched at the start and consumed at the end.
 constexpr int kQChunk = 256;
 
+// Finalize of one visual token: fixed-order sum over KV heads, the mean (or
+// RMS) over rows and heads, the value norm, s = a v and the layer
+// accumulation of Eq. 7.
+__device__ __forceinline__ void finalize_token(const FinalizeParams &p, int t) {
+  float cs = 0.f, sq = 0.f;
+  for (int h = 0; h < p.n_kv_heads; ++h) {
+    cs += p.colsum_part[(int64_t)h * p.n_vis + t];
+    if (!p.vnorm_in) sq += p.vsq_part[(int64_t)h * p.n_vis + t];
+  }
+  const float a = p.rms ? sqrtf(cs / p.n_rows_f) : cs / p.n_rows_f;
+  const float v = p.vnorm_in ? p.vnorm_in[t] : sqrtf(sq);
+  const float s = a * v;
+  if (p.accumulate) {
+    p.s_acc[t] += s;
+    p.a_acc[t] += a;
+  } else {
+    p.s_acc[t] = s;
+    p.a_acc[t] = a;
+  }
+  if (p.a_out) p.a_out[t] = a;
+  if (p.vnorm_out) p.vnorm_out[t] = v;
+}
+
 // RMS: accumulate alpha^2 (Eq. 4's surrogate) instead of alpha.
-template <int D, bool RMS>
+// FUSE: the row log-sum-exps are rebuilt from the statistics partials into
+// LDS (the split merge of the statistics pass, same order and arithmetic).
+template <int D, bool RMS, bool FUSE>
 __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParams p) {
   constexpr int KS = D / 16;
   constexpr int QCH = kQChunk * D / 8;       // 16-byte chunks in a Q chunk
@@ -42,6 +67,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   __shared__ alignas(16) u16 qs[2][kQChunk][D + 8];
   __shared__ alignas(16) float bs[2][kQChunk];
   __shared__ ImageLds img;
+  __shared__ float b_all[FUSE ? kColsumMaxLsePairs : 1];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
@@ -62,7 +88,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
       const int pr = min(c * kQChunk + cidx / (D / 8), n_pair - 1);
       qv[i] = ld16(Qg + ((int64_t)(pr / G) * p.n_q_heads + kvh * G + pr % G) * D + (cidx % (D / 8)) * 8);
     }
-    if (tid < kQChunk) {
+    if (!FUSE && tid < kQChunk) {
       const int pr = min(c * kQChunk + tid, n_pair - 1);
       bv = p.row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
     }
@@ -74,7 +100,10 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
       const bool live = c * kQChunk + cidx / (D / 8) < n_pair;
       st16(&qs[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], live ? qv[i] : u32x4{0, 0, 0, 0});
     }
-    if (tid < kQChunk) bs[buf][tid] = c * kQChunk + tid < n_pair ? bv : kInf;  // 2^-inf = 0
+    if (tid < kQChunk) {
+      const int pr = c * kQChunk + tid;
+      bs[buf][tid] = pr < n_pair ? (FUSE ? b_all[pr] : bv) : kInf;  // 2^-inf = 0
+    }
   };
 
   u32x4 qv[CPT];
@@ -82,6 +111,26 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   load_chunk(0, qv, bv);
 
   image_table_to_lds(p.tbl, img, tid, kColsumThreads);
+  if constexpr (FUSE) {
+    // b = M + log2(sum_s l_s 2^(m_s - M)) over the splits of the row's
+    // block, s ascending, exactly as the statistics merge computes it.
+    for (int pr = tid; pr < n_pair; pr += kColsumThreads) {
+      const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
+      const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * p.lse_ns;
+      float M = -kInf;
+#pragma unroll 8
+      for (int sp = 0; sp < p.lse_ns; ++sp) M = fmaxf(M, p.lse_part_m[(slot0 + sp) * p.lse_ppb + j]);
+      float L = 0.f;
+#pragma unroll 8
+      for (int sp = 0; sp < p.lse_ns; ++sp) {
+        const int64_t idx = (slot0 + sp) * p.lse_ppb + j;
+        L += fast_exp2(p.lse_part_m[idx] - M) * p.lse_part_l[idx];
+      }
+      const float b = M + __log2f(L);
+      b_all[pr] = b;
+      if (blockIdx.x == 0 && p.lse_out) p.lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
+    }
+  }
   __syncthreads();
   // This lane's key column, held as the B operand for every row tile.
   const int t = blockIdx.x * kColsumKeysPerBlock + wave * 32 + col;
@@ -148,9 +197,8 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   // dims (vi % (D/8))*8 .. +7 of key vi / (D/8); the D/8 items of a key sit
   // in consecutive lanes and are summed with lane shuffles.
   static_assert((D / 8) <= 64 && 64 % (D / 8) == 0, "key items within a wave");
-  if (!read_v) return;
 #pragma unroll
-  for (int i = 0; i < VPT; ++i) {
+  for (int i = 0; read_v && i < VPT; ++i) {
     float sq = 0.f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -202,24 +250,7 @@ __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p, bool rms
 
 __global__ void finalize_kernel(FinalizeParams p) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= p.n_vis) return;
-  float cs = 0.f, sq = 0.f;
-  for (int h = 0; h < p.n_kv_heads; ++h) {
-    cs += p.colsum_part[(int64_t)h * p.n_vis + t];
-    if (!p.vnorm_in) sq += p.vsq_part[(int64_t)h * p.n_vis + t];
-  }
-  const float a = p.rms ? sqrtf(cs / p.n_rows_f) : cs / p.n_rows_f;
-  const float v = p.vnorm_in ? p.vnorm_in[t] : sqrtf(sq);
-  const float s = a * v;
-  if (p.accumulate) {
-    p.s_acc[t] += s;
-    p.a_acc[t] += a;
-  } else {
-    p.s_acc[t] = s;
-    p.a_acc[t] = a;
-  }
-  if (p.a_out) p.a_out[t] = a;
-  if (p.vnorm_out) p.vnorm_out[t] = v;
+  if (t < p.n_vis) finalize_token(p, t);
 }
 
 // Value-norm table (Eq. 7's proxy, tabulated when the cache is built): one
@@ -270,12 +301,23 @@ hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rm
   if (bf16) {
     dim3 grid((p.n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock, p.n_kv_heads);
     ProfScope ps("colsum", s);
+    const bool fuse = p.lse_part_m != nullptr;
     if (head_dim == 128) {
-      if (rms) colsum_bf16_kernel<128, true><<<grid, kColsumThreads, 0, s>>>(p);
-      else colsum_bf16_kernel<128, false><<<grid, kColsumThreads, 0, s>>>(p);
+      if (fuse) {
+        if (rms) colsum_bf16_kernel<128, true, true><<<grid, kColsumThreads, 0, s>>>(p);
+        else colsum_bf16_kernel<128, false, true><<<grid, kColsumThreads, 0, s>>>(p);
+      } else {
+        if (rms) colsum_bf16_kernel<128, true, false><<<grid, kColsumThreads, 0, s>>>(p);
+        else colsum_bf16_kernel<128, false, false><<<grid, kColsumThreads, 0, s>>>(p);
+      }
     } else {
-      if (rms) colsum_bf16_kernel<64, true><<<grid, kColsumThreads, 0, s>>>(p);
-      else colsum_bf16_kernel<64, false><<<grid, kColsumThreads, 0, s>>>(p);
+      if (fuse) {
+        if (rms) colsum_bf16_kernel<64, true, true><<<grid, kColsumThreads, 0, s>>>(p);
+        else colsum_bf16_kernel<64, false, true><<<grid, kColsumThreads, 0, s>>>(p);
+      } else {
+        if (rms) colsum_bf16_kernel<64, true, false><<<grid, kColsumThreads, 0, s>>>(p);
+        else colsum_bf16_kernel<64, false, false><<<grid, kColsumThreads, 0, s>>>(p);
+      }
     }
   } else {
     dim3 grid((p.n_vis + 63) / 64, p.n_kv_heads);
