@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--budget", default="10%")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-scrub", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the supplementary measurements (variants, paged cache, text rows, "
+                         "residual diagnostic): only the step kernels run, e.g. under a kernel trace")
     ap.add_argument("--cpu-row-stride", type=int, default=8,
                     help="CPU baseline refreshes every n-th selected row and scales by n")
     return ap.parse_args()
@@ -197,86 +200,16 @@ def main():
     # Selection must be the same every step (deterministic).
     assert torch.equal(step.idx[:k], idx0), "selection changed between steps"
 
-    # Variants on the same workload: the value-norm table (built once per
-    # cache), scoring that reads the table instead of V, RMS aggregation, and
-    # the attention-only and explicit-quota selection rules.
-    table = torch.empty(w.n_vis, dtype=torch.float32, device=dev)
-    quota = torch.empty(w.n_images, dtype=torch.int32, device=dev)
-    variants_ms = {
-        "value_norms": timed(lambda: api.conduit_value_norms(kv, img, table)),
-        "score_vnorm_table": timed(lambda: api.conduit_score(kv, q, w.q_pos0, img, step.s_acc,
-                                                             step.a_acc, ws=step.ws_score,
-                                                             vnorm_in=table)),
-        "score_rms": timed(lambda: api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc,
-                                                     ws=step.ws_score, agg=api.AGG_RMS)),
-    }
-    api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score)
-    for name, rule in (("select_attention", api.RANK_ATTENTION), ("select_explicit", api.RANK_EXPLICIT)):
-        variants_ms[name] = timed(lambda rule=rule: api.conduit_select_topk(
-            step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos, mask_out=step.mask,
-            shat_out=step.shat, c_out=step.c, rule=rule, quota_out=quota))
-
-    # Paged cache (256-token pages, shuffled pool) and the recompute with the
-    # request's text rows in the same merge and attention launch.
-    page = 256
-    n_log = -(-w.n_ctx // page)
-    table_np = np.random.default_rng(7).permutation(n_log + 8)[:n_log].astype(np.int32)
-    table = torch.from_numpy(table_np).to(dev)
-    tok = np.arange(w.n_ctx)
-    rows_idx = torch.from_numpy(table_np[tok // page].astype(np.int64) * page + tok % page).to(dev)
-    k_pool = torch.zeros(((n_log + 8) * page, w.n_kv_heads, w.head_dim), dtype=kc.dtype, device=dev)
-    v_pool = torch.zeros_like(k_pool)
-    k_pool[rows_idx] = k_pristine
-    v_pool[rows_idx] = v_pristine
-    kv_paged = api.kv_desc_paged(k_pool.view(n_log + 8, page, w.n_kv_heads, w.head_dim),
-                                 v_pool.view(n_log + 8, page, w.n_kv_heads, w.head_dim), table,
-                                 w.n_ctx, w.n_q_heads)
-    text_np = w.text_positions()
-    rows_all = torch.cat([pos, torch.from_numpy(text_np.astype(np.int32)).to(dev)])
-    k_all = torch.cat([fresh["k_new"], up(L["k_text_star"])])
-    v_all = torch.cat([fresh["v_new"], up(L["v_text_star"])])
-    q_all = torch.cat([fresh["q_sel"], up(L["q_text_star"])])
-    n_all = rows_all.numel()
-    out_all = torch.empty((n_all, w.n_q_heads, w.head_dim), dtype=q_all.dtype, device=dev)
-    ws_all = torch.empty(api.refresh_workspace_bytes(kv, n_all), dtype=torch.uint8, device=dev)
-    variants_ms["score_paged256"] = timed(lambda: api.conduit_score(
-        kv_paged, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score))
-    api.conduit_scatter_kv(kv_paged, pos, fresh["k_new"], fresh["v_new"])
-    variants_ms["refresh_paged256"] = timed(lambda: api.conduit_refresh_attn(
-        kv_paged, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh))
-    variants_ms["recompute_with_text_rows"] = timed(lambda: (
-        api.conduit_scatter_kv(kv, rows_all, k_all, v_all),
-        api.conduit_refresh_attn(kv, q_all, rows_all, out_all, ws=ws_all)))
-    restore()
-
-    # Residual-error diagnostic: the isotropic estimate (M = 5) of the step's
-    # own 10% refresh set, timed, and the rule comparison table.
-    from paper_2609_05821_amd import diagnostics as D
-    n_samples = 5
-    z_dev = up(W.iso_directions(w, 0, n_samples))
-    err_iso = torch.empty((n_samples, w.n_q, w.n_q_heads), dtype=torch.float32, device=dev)
-    ws_res = torch.empty(api.residual_workspace_bytes(kv, w.n_q, img, n_samples, True), dtype=torch.uint8,
-                         device=dev)
-    variants_ms["residual_iso_m5"] = timed(lambda: api.conduit_residual_error(
-        kv, q, w.q_pos0, img, lse_rows, step.mask, err_iso, z=z_dev, ws=ws_res))
-    diag = D.rule_errors(kv, q, w.q_pos0, img, z_dev, seed=0)
-    del z_dev
-
     # Algorithmic work.
     H, d, hkv = w.n_q_heads, w.head_dim, w.n_kv_heads
     refresh_flops = 4.0 * H * d * float(np.sum(pos_np + 1))
     refresh_exps = H * float(np.sum(pos_np + 1))
-    text_flops = refresh_flops + 4.0 * H * d * float(np.sum(text_np + 1))
     e = 2  # bf16 bytes
-    res_flops = 2.0 * w.n_q * H * w.n_vis * d * (1 + n_samples)   # S once, then one product per sample
-    res_bytes = (n_samples + 2) * w.n_vis * hkv * d * e + w.n_q * H * d * e  # z, K and V rows, Q
     score_bytes = (w.n_q * H * d * e + w.n_ctx * hkv * d * e + w.n_vis * hkv * d * e
                    + w.n_vis * 4 * 4)
     score_flops = 2.0 * d * H * sum(w.q_pos0 + i + 1 for i in range(w.n_q)) + \
         2.0 * d * H * w.n_q * w.n_vis
     scatter_bytes = 2 * 2 * k * hkv * d * e
-    vnorm_bytes = w.n_vis * hkv * d * e + w.n_vis * 4
-    score_table_bytes = score_bytes - w.n_vis * hkv * d * e + w.n_vis * 4
     refresh_tflops = refresh_flops / (ms["refresh"] * 1e-3) / 1e12
     attn_ms = kernels_ms["attn_values"]["mean"]
     attn_tflops = refresh_flops / (attn_ms * 1e-3) / 1e12
@@ -337,34 +270,107 @@ def main():
             "hbm_frac": score_bytes / (ms["score"] * 1e-3) / 1e9 / PEAK_HBM_GBS,
             "mfma_frac": score_flops / (ms["score"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         },
-        "variants_ms": variants_ms,
-        "recompute_with_text_rows": {
-            "rows": n_all, "text_rows": int(len(text_np)),
-            "algorithmic_flops": text_flops,
-            "tflops_whole_call": text_flops / (variants_ms["recompute_with_text_rows"]["mean"] * 1e-3) / 1e12,
-            "note": "merge + refresh attention of the selected rows and every text row, one launch each",
-        },
-        "residual_iso_m5": {
-            "algorithmic_flops": res_flops, "algorithmic_bytes": res_bytes,
-            "tflops": res_flops / (variants_ms["residual_iso_m5"]["mean"] * 1e-3) / 1e12,
-            "gbs": res_bytes / (variants_ms["residual_iso_m5"]["mean"] * 1e-3) / 1e9,
-            "note": "conduit_residual_error, isotropic estimator, M = 5, the step's 10% set, all span rows",
-        },
-        "diagnostics": diag,
-        "paged": {"page_size": page, "pages": n_log + 8,
-                  "note": "same workload with K/V in a shuffled pool of 256-token pages"},
-        "variants_bytes": {
-            "value_norms": vnorm_bytes,
-            "value_norms_gbs": vnorm_bytes / (variants_ms["value_norms"]["mean"] * 1e-3) / 1e9,
-            "score_vnorm_table": score_table_bytes,
-            "score_vnorm_table_gbs": score_table_bytes /
-            (variants_ms["score_vnorm_table"]["mean"] * 1e-3) / 1e9,
-        },
         "scatter_gbs": scatter_bytes / (ms["scatter"] * 1e-3) / 1e9,
         "refresh_exps_per_s": refresh_exps / (ms["refresh"] * 1e-3),
         "wall_ms_per_step_incl_scrub_restore": t_wall / args.steps * 1e3,
         "gen_s": t_gen,
     }
+
+    if not args.no_extras:
+        # Variants on the same workload: the value-norm table (built once per
+        # cache), scoring that reads the table instead of V, RMS aggregation, and
+        # the attention-only and explicit-quota selection rules.
+        table = torch.empty(w.n_vis, dtype=torch.float32, device=dev)
+        quota = torch.empty(w.n_images, dtype=torch.int32, device=dev)
+        variants_ms = {
+            "value_norms": timed(lambda: api.conduit_value_norms(kv, img, table)),
+            "score_vnorm_table": timed(lambda: api.conduit_score(kv, q, w.q_pos0, img, step.s_acc,
+                                                                 step.a_acc, ws=step.ws_score,
+                                                                 vnorm_in=table)),
+            "score_rms": timed(lambda: api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc,
+                                                         ws=step.ws_score, agg=api.AGG_RMS)),
+        }
+        api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score)
+        for name, rule in (("select_attention", api.RANK_ATTENTION), ("select_explicit", api.RANK_EXPLICIT)):
+            variants_ms[name] = timed(lambda rule=rule: api.conduit_select_topk(
+                step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos, mask_out=step.mask,
+                shat_out=step.shat, c_out=step.c, rule=rule, quota_out=quota))
+
+        # Paged cache (256-token pages, shuffled pool) and the recompute with the
+        # request's text rows in the same merge and attention launch.
+        page = 256
+        n_log = -(-w.n_ctx // page)
+        table_np = np.random.default_rng(7).permutation(n_log + 8)[:n_log].astype(np.int32)
+        table = torch.from_numpy(table_np).to(dev)
+        tok = np.arange(w.n_ctx)
+        rows_idx = torch.from_numpy(table_np[tok // page].astype(np.int64) * page + tok % page).to(dev)
+        k_pool = torch.zeros(((n_log + 8) * page, w.n_kv_heads, w.head_dim), dtype=kc.dtype, device=dev)
+        v_pool = torch.zeros_like(k_pool)
+        k_pool[rows_idx] = k_pristine
+        v_pool[rows_idx] = v_pristine
+        kv_paged = api.kv_desc_paged(k_pool.view(n_log + 8, page, w.n_kv_heads, w.head_dim),
+                                     v_pool.view(n_log + 8, page, w.n_kv_heads, w.head_dim), table,
+                                     w.n_ctx, w.n_q_heads)
+        text_np = w.text_positions()
+        rows_all = torch.cat([pos, torch.from_numpy(text_np.astype(np.int32)).to(dev)])
+        k_all = torch.cat([fresh["k_new"], up(L["k_text_star"])])
+        v_all = torch.cat([fresh["v_new"], up(L["v_text_star"])])
+        q_all = torch.cat([fresh["q_sel"], up(L["q_text_star"])])
+        n_all = rows_all.numel()
+        out_all = torch.empty((n_all, w.n_q_heads, w.head_dim), dtype=q_all.dtype, device=dev)
+        ws_all = torch.empty(api.refresh_workspace_bytes(kv, n_all), dtype=torch.uint8, device=dev)
+        variants_ms["score_paged256"] = timed(lambda: api.conduit_score(
+            kv_paged, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score))
+        api.conduit_scatter_kv(kv_paged, pos, fresh["k_new"], fresh["v_new"])
+        variants_ms["refresh_paged256"] = timed(lambda: api.conduit_refresh_attn(
+            kv_paged, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh))
+        variants_ms["recompute_with_text_rows"] = timed(lambda: (
+            api.conduit_scatter_kv(kv, rows_all, k_all, v_all),
+            api.conduit_refresh_attn(kv, q_all, rows_all, out_all, ws=ws_all)))
+        restore()
+
+        # Residual-error diagnostic: the isotropic estimate (M = 5) of the step's
+        # own 10% refresh set, timed, and the rule comparison table.
+        from paper_2609_05821_amd import diagnostics as D
+        n_samples = 5
+        z_dev = up(W.iso_directions(w, 0, n_samples))
+        err_iso = torch.empty((n_samples, w.n_q, w.n_q_heads), dtype=torch.float32, device=dev)
+        ws_res = torch.empty(api.residual_workspace_bytes(kv, w.n_q, img, n_samples, True), dtype=torch.uint8,
+                             device=dev)
+        variants_ms["residual_iso_m5"] = timed(lambda: api.conduit_residual_error(
+            kv, q, w.q_pos0, img, lse_rows, step.mask, err_iso, z=z_dev, ws=ws_res))
+        diag = D.rule_errors(kv, q, w.q_pos0, img, z_dev, seed=0)
+        del z_dev
+        text_flops = refresh_flops + 4.0 * H * d * float(np.sum(text_np + 1))
+        res_flops = 2.0 * w.n_q * H * w.n_vis * d * (1 + n_samples)   # S once, then one product per sample
+        res_bytes = (n_samples + 2) * w.n_vis * hkv * d * e + w.n_q * H * d * e  # z, K and V rows, Q
+        vnorm_bytes = w.n_vis * hkv * d * e + w.n_vis * 4
+        score_table_bytes = score_bytes - w.n_vis * hkv * d * e + w.n_vis * 4
+        result.update({
+            "variants_ms": variants_ms,
+            "recompute_with_text_rows": {
+                "rows": n_all, "text_rows": int(len(text_np)),
+                "algorithmic_flops": text_flops,
+                "tflops_whole_call": text_flops / (variants_ms["recompute_with_text_rows"]["mean"] * 1e-3) / 1e12,
+                "note": "merge + refresh attention of the selected rows and every text row, one launch each",
+            },
+            "residual_iso_m5": {
+                "algorithmic_flops": res_flops, "algorithmic_bytes": res_bytes,
+                "tflops": res_flops / (variants_ms["residual_iso_m5"]["mean"] * 1e-3) / 1e12,
+                "gbs": res_bytes / (variants_ms["residual_iso_m5"]["mean"] * 1e-3) / 1e9,
+                "note": "conduit_residual_error, isotropic estimator, M = 5, the step's 10% set, all span rows",
+            },
+            "diagnostics": diag,
+            "paged": {"page_size": page, "pages": n_log + 8,
+                      "note": "same workload with K/V in a shuffled pool of 256-token pages"},
+            "variants_bytes": {
+                "value_norms": vnorm_bytes,
+                "value_norms_gbs": vnorm_bytes / (variants_ms["value_norms"]["mean"] * 1e-3) / 1e9,
+                "score_vnorm_table": score_table_bytes,
+                "score_vnorm_table_gbs": score_table_bytes /
+                (variants_ms["score_vnorm_table"]["mean"] * 1e-3) / 1e9,
+            },
+        })
 
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(w, L, q_sel_np, idx_np, pos_np, k,
