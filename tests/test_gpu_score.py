@@ -19,6 +19,12 @@ CASES = {
     "ragged_bf16_mha": lambda: W.custom(1, 4, 4, 128, 9, 1, [70], 0, "bf16", seed=5),
     "ragged_fp32_d128_gqa2": lambda: W.custom(1, 4, 2, 128, 5, 3, [20, 45, 11], 2, "f32", seed=6),
     "one_visual_token": lambda: W.custom(1, 28, 4, 128, 3, 2, [1], 0, "bf16", seed=8),
+    # statistics split into 2 per block, merged inside the column-sum kernel
+    "split_span_bf16_gqa7": lambda: W.custom(1, 28, 4, 128, 19, 1100, [300], 4, "bf16", n_sinks=3,
+                                             seed=9),
+    # 640 x 7 = 4,480 pairs per KV head: statistics split and merged by their own kernel
+    "long_span_bf16_gqa7": lambda: W.custom(1, 28, 4, 128, 640, 2000, [600, 600], 16, "bf16",
+                                            n_relevant=1, seed=10),
 }
 
 
