@@ -11,7 +11,7 @@
 //     passes with LDS histograms (integer atomics: exact);
 //  5. ordered compaction: everything above the threshold plus the first
 //     `need` entries equal to it in index order (ties to the lower index),
-//     with two block scans, so idx/pos come out ascending.
+//     with one block scan of both counts, so idx/pos come out ascending.
 // The explicit-quota rule (select_explicit_kernel) shares steps 1-2.
 #include "common.h"
 
@@ -51,6 +51,29 @@ __device__ int block_exclusive_scan(int x, int *s_wave, int &total) {
   total = s_wave[kWaves - 1];
   __syncthreads();
   return excl;
+}
+
+// Bitwise AND and OR of one value per thread over the block in one
+// exchange (every thread gets both).
+__device__ void block_and_or(uint32_t &a, uint32_t &o, int *s_a, int *s_o) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    a &= __shfl_xor(a, off, 64);
+    o |= __shfl_xor(o, off, 64);
+  }
+  if (lane == 0) {
+    s_a[w] = (int)a;
+    s_o[w] = (int)o;
+  }
+  __syncthreads();
+  a = 0xffffffffu;
+  o = 0;
+  for (int i = 0; i < kWaves; ++i) {
+    a &= (uint32_t)s_a[i];
+    o |= (uint32_t)s_o[i];
+  }
+  __syncthreads();
 }
 
 // Bitwise AND / OR of one value per thread over the block (every thread
@@ -206,8 +229,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Ima
 // image, lane-strided partial sums, butterfly reduction: a fixed order), then
 // g_bar and c_j = (1 - lambda) + lambda g_j / g_bar into s_c, exactly 1 where
 // g_j = g_bar or g_bar = 0.  All 1024 threads take part; ends synchronised.
-__device__ void image_coefficients(const SelectParams &p, int K, const int *s_off, float *s_g,
-                                   float *s_c, bool write_c) {
+// PRE: `pre` holds the first 16 x 64 values of image `wave`, loaded by the
+// caller at kernel start (the same values in the same order).
+template <bool PRE>
+__device__ __forceinline__ void image_coefficients(const SelectParams &p, int K, const int *s_off, float *s_g,
+                                                   float *s_c, bool write_c, const float (&pre)[16]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float n_layers = (float)p.n_layers;
   for (int j = wave; j < K; j += kWaves) {
@@ -215,10 +241,11 @@ __device__ void image_coefficients(const SelectParams &p, int K, const int *s_of
     float tot = 0.f;
     for (int t0 = a; t0 < b; t0 += 16 * 64) {  // 16 independent loads per round
       float v[16];
+      const bool use_pre = PRE && j == wave && t0 == a;
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const int t = t0 + 64 * u + lane;
-        v[u] = t < b ? p.a_acc[t] : 0.f;
+        v[u] = use_pre ? pre[u] : (t < b ? p.a_acc[t] : 0.f);
       }
 #pragma unroll
       for (int u = 0; u < 16; ++u) tot += v[u];
@@ -257,12 +284,27 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
   __shared__ int s_delta[kMaxImages];  // position - visual index, per image
   __shared__ int hist[kBins];
   __shared__ int s_wave[kWaves];
+  __shared__ int s_wave2[kWaves];
   __shared__ int s_bin, s_above;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = tbl.n_vis, K = tbl.n_images;
   const float n_layers = (float)p.n_layers;
   const float inv_layers = 1.f / n_layers;
+
+  // Image `wave`'s first attention values, in flight with the scores below.
+  float pre[16];
+  {
+    const int a = wave < K ? tbl.off[wave] : 0, b = wave < K ? tbl.off[wave + 1] : 0;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int t = a + 64 * u + lane;
+      pre[u] = t < b ? p.a_acc[t] : 0.f;
+    }
+  }
+  // The radix histogram starts cleared; afterwards each pass clears the bins
+  // it has read.
+  for (int b = tid; b < kBins; b += kSelThreads) hist[b] = 0;
 
   // The image table moves to LDS (per-lane lookups would otherwise be
   // dependent loads from the kernel-argument segment).
@@ -291,7 +333,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
   __syncthreads();
 
   // 1-2. per-image mean attention and coefficients
-  image_coefficients(p, K, s_off, s_g, s_c, true);
+  image_coefficients<true>(p, K, s_off, s_g, s_c, true, pre);
 
   // 3. composite scores (s / |L|) * c_pi(t) of this thread's tokens
   int j0 = 0;  // image of the first token
@@ -341,8 +383,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
       k_and &= key[e];
       k_or |= key[e];
     }
-  k_and = block_and(k_and, s_wave);
-  k_or = block_or(k_or, s_wave);
+  block_and_or(k_and, k_or, s_wave, s_wave2);
   const uint32_t varying = k_and ^ k_or;  // bits that differ between keys
   uint32_t prefix = k_and, pmask = 0xffffffffu;
   int kk = p.k;
@@ -352,8 +393,6 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
     prefix = k_and & pmask;
     for (int hi = top; hi >= 0; hi -= kBits) {  // digit = bits hi .. hi-10 (fewer at the end)
       const int sh = hi - (kBits - 1);
-      for (int b = tid; b < kBins; b += kSelThreads) hist[b] = 0;
-      __syncthreads();
 #pragma unroll
       for (int e = 0; e < PER; ++e)
         if (e < cnt && (key[e] & pmask) == prefix)
@@ -362,6 +401,8 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
       // thread tid owns bins kBins-1-2*tid, kBins-2-2*tid (descending)
       const int b0 = kBins - 1 - 2 * tid;
       const int h0 = hist[b0], h1 = hist[b0 - 1];
+      hist[b0] = 0;  // cleared for the next pass (only this thread reads them)
+      hist[b0 - 1] = 0;
       int total;
       const int run = block_exclusive_scan(h0 + h1, s_wave, total);
       if (run < kk && run + h0 >= kk) {
@@ -392,10 +433,13 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
     gt += (e < cnt) && key[e] > tau;
     eq += (e < cnt) && key[e] == tau;
   }
+  // One scan of both counts (each < 2^16 for n_vis <= 32,768): the equal
+  // entries taken before this thread are min(eq_before, need_eq).
   int total;
-  const int eq_before = block_exclusive_scan(eq, s_wave, total);
+  const int packed = block_exclusive_scan((eq << 16) | gt, s_wave, total);
+  const int eq_before = (int)((uint32_t)packed >> 16), gt_before = packed & 0xffff;
   const int take_eq = max(0, min(eq, need_eq - eq_before));
-  int out = block_exclusive_scan(gt + take_eq, s_wave, total);
+  int out = gt_before + min(eq_before, need_eq);
   int j = j0, next = cnt > 0 ? s_off[j0 + 1] : 0, delta = cnt > 0 ? s_delta[j0] : 0, eq_seen = 0;
   uint32_t mword[(PER + 3) / 4] = {};
 #pragma unroll
@@ -467,7 +511,8 @@ __global__ __launch_bounds__(kSelThreads) void select_explicit_kernel(SelectPara
   }
   if (tid == 0) s_left = p.k;
   __syncthreads();
-  image_coefficients(p, K, s_off, s_g, s_c, jimg == 0);
+  const float no_pre[16] = {};
+  image_coefficients<false>(p, K, s_off, s_g, s_c, jimg == 0, no_pre);
 
   // quotas
   for (;;) {
