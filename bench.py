@@ -56,7 +56,7 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "the benchmark measures one GPU (one process, one device); --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
 
