@@ -40,7 +40,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--cfg", type=int, default=4, help="workload id (4 = 16k tokens, 10%%)")
     ap.add_argument("--budget", default="10%")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -101,18 +101,20 @@ def main():
     pos = step.pos[:k]
     out, lse = step.out[0][:k], step.lse[0][:k]
 
-    def one_step(ev=None):
+    def one_step(ev=None, split=False):
+        # ev: 5 events; the step's two bracket it, the three inner ones (split)
+        # separate the calls for the per-call breakdown.
         if ev:
             ev[0].record(stream)
         api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score)
-        if ev:
+        if ev and split:
             ev[1].record(stream)
         api.conduit_select_topk(step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos,
                                 mask_out=step.mask, shat_out=step.shat, c_out=step.c)
-        if ev:
+        if ev and split:
             ev[2].record(stream)
         api.conduit_scatter_kv(kv, pos, fresh["k_new"], fresh["v_new"])
-        if ev:
+        if ev and split:
             ev[3].record(stream)
         api.conduit_refresh_attn(kv, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh)
         if ev:
@@ -127,16 +129,27 @@ def main():
         restore()
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    # Timed steps: events only around each step.
+    step_events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     for i in range(args.steps):
         if not args.no_scrub:
             scrub.fill_(i & 0xFF)
-        one_step(events[i])
+        one_step(step_events[i])
         restore()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
+
+    # The same steps again with events between the calls (per-call times;
+    # the extra events lengthen these steps slightly).
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        if not args.no_scrub:
+            scrub.fill_(i & 0xFF)
+        one_step(events[i], split=True)
+        restore()
+    torch.cuda.synchronize()
 
     # Second timed pass of the same steps with per-launch kernel timing (HIP
     # events recorded by the library around each launch, on this stream).
@@ -154,12 +167,14 @@ def main():
     kernels_ms = {name: {"calls_per_step": len(v) / args.steps, "mean": statistics.mean(v),
                          "p10": pct(v, 10), "p90": pct(v, 90)} for name, v in kern.items()}
 
-    per = {"score": [], "select": [], "scatter": [], "refresh": [], "step": []}
+    per = {"score": [], "select": [], "scatter": [], "refresh": [], "step": [], "step_with_call_events": []}
     for ev in events:
         per["score"].append(ev[0].elapsed_time(ev[1]))
         per["select"].append(ev[1].elapsed_time(ev[2]))
         per["scatter"].append(ev[2].elapsed_time(ev[3]))
         per["refresh"].append(ev[3].elapsed_time(ev[4]))
+        per["step_with_call_events"].append(ev[0].elapsed_time(ev[4]))
+    for ev in step_events:
         per["step"].append(ev[0].elapsed_time(ev[4]))
     ms_step = statistics.mean(per["step"])
     ms = {key: statistics.mean(v) for key, v in per.items()}
@@ -329,6 +344,37 @@ def main():
             api.conduit_refresh_attn(kv, q_all, rows_all, out_all, ws=ws_all)))
         restore()
 
+        # The step captured once in a HIP graph and replayed (same kernels, same
+        # buffers); replays, with eager steps between them, must reproduce the
+        # eager outputs bit for bit before their time is reported.
+        try:
+            restore()
+            one_step()
+            torch.cuda.synchronize()
+            ref = (out.clone(), lse.clone(), step.idx.clone(), kc.clone())
+            restore()
+            gstream = torch.cuda.Stream()
+            gstream.wait_stream(stream)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=gstream):
+                one_step()
+            torch.cuda.synchronize()
+            restore()
+            same = True
+            for _ in range(3):
+                graph.replay()
+                torch.cuda.synchronize()
+                same = same and all(torch.equal(a, b) for a, b in zip((out, lse, step.idx, kc), ref))
+                restore()
+                one_step()
+                restore()
+            torch.cuda.synchronize()
+            graph_info = {"ms_per_step": timed(graph.replay), "replays_equal_eager": bool(same),
+                          "note": "the timed step captured in a HIP graph (supplementary; value is eager)"}
+            restore()
+        except Exception as ex:  # noqa: BLE001 - reported, the eager figures stand
+            graph_info = {"error": repr(ex)}
+
         # Residual-error diagnostic: the isotropic estimate (M = 5) of the step's
         # own 10% refresh set, timed, and the rule comparison table.
         from paper_2609_05821_amd import diagnostics as D
@@ -347,6 +393,7 @@ def main():
         vnorm_bytes = w.n_vis * hkv * d * e + w.n_vis * 4
         score_table_bytes = score_bytes - w.n_vis * hkv * d * e + w.n_vis * 4
         result.update({
+            "graph_replay": graph_info,
             "variants_ms": variants_ms,
             "recompute_with_text_rows": {
                 "rows": n_all, "text_rows": int(len(text_np)),
