@@ -46,33 +46,6 @@ struct AttnSmem {
   ImageLds img;                      // visual-only statistics: the image table
 };
 
-// The A operand of O^T += V^T P^T for one 16-key MFMA step, read from the
-// row-major V tile with two transposing LDS reads (ds_read_b64_tr_b16): in
-// each group of 16 lanes, lane 4j + q reads 4 head dims of key j and lane
-// 4q + r receives dim 4q + r of keys 0..3.  Lane (m, h) of the wave ends up
-// with keys 4h + 0..3 and 8 + 4h + 0..3 of the step for head dim m, the
-// order in which the S^T accumulator holds them (so P needs no shuffle).
-typedef short short4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) short4 lds_short4;
-
-typedef short short8 __attribute__((ext_vector_type(8)));
-
-// Element offset, inside a V tile with row stride VS, of the 4 dims this
-// lane reads for the first half of an MFMA step (keys 0..7); the second
-// half (keys 8..15) is 8 rows further.
-template <int VS>
-__device__ __forceinline__ int v_operand_lane_offset(int lane) {
-  const int s = lane & 15, h = lane >> 5, dgrp = (lane >> 4) & 1;
-  return (4 * h + (s >> 2)) * VS + 16 * dgrp + 4 * (s & 3);
-}
-
-template <int VS>
-__device__ __forceinline__ bf16x8 v_operand(const u16 *at) {
-  const short4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(at));
-  const short4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(at + 8 * VS));
-  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-}
-
 __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, int r) {
   return row_pos ? row_pos[r] : q_pos0 + r;
 }

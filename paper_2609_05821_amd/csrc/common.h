@@ -164,14 +164,31 @@ __device__ __forceinline__ int64_t page_row(const KvPageReader &r, int page, int
   return ((int64_t)pg << r.shift) | (int64_t)((uint32_t)t & ((1u << r.shift) - 1u));
 }
 
-// Slot of key `kl` (0..63) of a tile inside a V^T row.  The S^T accumulator
-// gives lane half h, register v the key 8*(v/4) + 4*h + (v%4) of a 32-key
-// sub-tile; the PV product consumes registers 8*ks..8*ks+7 as one 16-deep
-// k-step, so those eight keys are stored contiguously per lane half.
-__device__ __forceinline__ int vt_slot(int kl) {
-  const int sub = kl >> 5, w = kl & 31, ks = w >> 4, r = w & 15;
-  const int h = (r & 7) >> 2, e = 4 * (r >> 3) + (r & 3);
-  return sub * 32 + ks * 16 + h * 8 + e;
+// The A operand of O^T += V^T P^T for one 16-key MFMA step, read from the
+// row-major V tile with two transposing LDS reads (ds_read_b64_tr_b16): in
+// each group of 16 lanes, lane 4j + q reads 4 head dims of key j and lane
+// 4q + r receives dim 4q + r of keys 0..3.  Lane (m, h) of the wave ends up
+// with keys 4h + 0..3 and 8 + 4h + 0..3 of the step for head dim m, the
+// order in which the S^T accumulator holds them (so P needs no shuffle).
+typedef short short4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) short4 lds_short4;
+
+typedef short short8 __attribute__((ext_vector_type(8)));
+
+// Element offset, inside a V tile with row stride VS, of the 4 dims this
+// lane reads for the first half of an MFMA step (keys 0..7); the second
+// half (keys 8..15) is 8 rows further.
+template <int VS>
+__device__ __forceinline__ int v_operand_lane_offset(int lane) {
+  const int s = lane & 15, h = lane >> 5, dgrp = (lane >> 4) & 1;
+  return (4 * h + (s >> 2)) * VS + 16 * dgrp + 4 * (s & 3);
+}
+
+template <int VS>
+__device__ __forceinline__ bf16x8 v_operand(const u16 *at) {
+  const short4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(at));
+  const short4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(at + 8 * VS));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 __device__ __forceinline__ float wave_sum(float x) {

@@ -12,8 +12,9 @@
 // The bf16 path is one MFMA pass per (key split, 256-pair block, KV head,
 // sample): S^T = K Q^T for 64 visual keys, alpha = 2^(c s - b) straight from
 // the known log-sum-exp (no running maximum), and y^T += Xi^T alpha^T with the
-// displacement tile staged transposed in LDS; refreshed keys and keys past
-// the last visual token get a zero displacement row at staging.  Partial y
+// displacement tile staged row-major in LDS (scaled at staging) and read
+// through transposing LDS reads; refreshed keys and keys past the last
+// visual token get a zero displacement row.  Partial y
 // per split go to the workspace; residual_sum_kernel adds them in split order
 // and squares.
 #include <type_traits>
@@ -29,7 +30,7 @@ constexpr int kThreads = 512;   // 8 waves, 32 pairs each
 template <int D>
 struct ResidualSmem {
   alignas(16) u16 k[2][KT][D + 8];   // K rows of the tile's visual keys
-  alignas(16) u16 xt[2][D][KT + 8];  // displacement tile, transposed (MFMA operand order)
+  alignas(16) u16 x[2][KT][D + 32];  // displacement tile, one row per key (PV operand reads transpose)
   int64_t row[kResidualMaxTiles * KT];   // cache row of each key of the split
   float scale[kResidualMaxTiles * KT];   // displacement scale: sigma_t, 1, or 0 (refreshed)
   ImageLds img;
@@ -39,10 +40,8 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualParams p) {
   constexpr int KS = D / 16;                     // MFMA k-steps over the head dim
   constexpr int DT = D / 32;                     // 32-row tiles of y^T
-  constexpr int KCH = KT * D / 8 / kThreads;     // 16-byte K chunks per thread
-  constexpr int XIT = (KT / 2) * (D / 8);        // (2 keys x 8 dims) items per tile
-  constexpr int XPT = XIT >= kThreads ? XIT / kThreads : 1;
-  static_assert(KCH >= 1 && KT * D / 8 == KCH * kThreads, "K staging covers the tile");
+  constexpr int KCH = KT * D / 8 / kThreads;     // 16-byte K (and displacement) chunks per thread
+  static_assert(KCH >= 1 && KT * D / 8 == KCH * kThreads, "staging covers the tile");
   __shared__ ResidualSmem<D> sm;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -55,6 +54,7 @@ __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualPara
   const u16 *Xg = static_cast<const u16 *>(p.disp);
   const float c = p.scale_log2;
   const bool iso = p.vnorm != nullptr;
+  const int v_lane = v_operand_lane_offset<D + 32>(lane);
 
   image_table_to_lds(p.tbl, sm.img, tid, kThreads);
 
@@ -88,8 +88,8 @@ __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualPara
   // Two register sets: tiles are loaded two ahead of the one computing, so
   // each load has two tiles' compute to arrive.
   u32x4 rk[2][KCH];
-  u32x4 rx[2][XPT][2];
-  float sx[2][XPT][2];
+  u32x4 rx[2][KCH];
+  float sx[2][KCH];
   // Global -> register set R for the tile of visual keys tv0 .. tv0 + 63.
   auto load_tile = [&](int tv0, auto set) __attribute__((always_inline)) {
     constexpr int R = decltype(set)::value;
@@ -97,26 +97,17 @@ __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualPara
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int cidx = tid + kThreads * i;
-      const int j = min(j0 + cidx / (D / 8), last);
-      rk[R][i] = ld16(Kg + sm.row[j] * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
-    }
-#pragma unroll
-    for (int it = 0; it < XPT; ++it) {
-      const int xi = min(tid + kThreads * it, XIT - 1);
-      const int kp = xi % (KT / 2), dc = xi / (KT / 2);
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int jr = j0 + 2 * kp + e;
-        const int j = min(jr, last);
-        const int64_t off = iso ? (((int64_t)m * p.n_vis + tv_beg + j) * p.n_kv_heads + kvh) * D
-                                : sm.row[j] * p.disp_stride + kvh * D;
-        rx[R][it][e] = ld16(Xg + off + dc * 8);
-        sx[R][it][e] = jr <= last && tid + kThreads * it < XIT ? sm.scale[j] : 0.f;
-      }
+      const int jr = j0 + cidx / (D / 8), j = min(jr, last);
+      const int dc = (cidx % (D / 8)) * 8;
+      rk[R][i] = ld16(Kg + sm.row[j] * p.k_stride + kvh * D + dc);
+      const int64_t off = iso ? (((int64_t)m * p.n_vis + tv_beg + j) * p.n_kv_heads + kvh) * D
+                              : sm.row[j] * p.disp_stride + kvh * D;
+      rx[R][i] = ld16(Xg + off + dc);
+      sx[R][i] = jr <= last ? sm.scale[j] : 0.f;
     }
   };
-  // Registers -> LDS: K rows as loaded; the displacement scaled, rounded to
-  // bf16 and written transposed, two keys per 32-bit word.
+  // Registers -> LDS: K rows as loaded; the displacement scaled and rounded
+  // to bf16, row-major.
   auto store_tile = [&](int buf, auto set) __attribute__((always_inline)) {
     constexpr int R = decltype(set)::value;
 #pragma unroll
@@ -125,25 +116,17 @@ __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualPara
       st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[R][i]);
     }
 #pragma unroll
-    for (int it = 0; it < XPT; ++it) {
-      const int xi = tid + kThreads * it;
-      if (xi >= XIT) continue;
-      const int kp = xi % (KT / 2), dc = xi / (KT / 2);
-      const int slot = vt_slot(2 * kp);
+    for (int i = 0; i < KCH; ++i) {
+      const int cidx = tid + kThreads * i;
+      u32x4 w;
 #pragma unroll
       for (int e2 = 0; e2 < 4; ++e2) {
-        uint32_t w[2];
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const uint32_t u = rx[R][it][e][e2];
-          const float lo = __builtin_bit_cast(float, u << 16) * sx[R][it][e];
-          const float hi = __builtin_bit_cast(float, u & 0xffff0000u) * sx[R][it][e];
-          w[e] = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
-        }
-        // dims 2*e2 (low halves) and 2*e2+1 (high halves) of the two keys
-        *reinterpret_cast<uint32_t *>(&sm.xt[buf][dc * 8 + 2 * e2][slot]) = (w[0] & 0xffffu) | (w[1] << 16);
-        *reinterpret_cast<uint32_t *>(&sm.xt[buf][dc * 8 + 2 * e2 + 1][slot]) = (w[0] >> 16) | (w[1] & 0xffff0000u);
+        const uint32_t u = rx[R][i][e2];
+        const float lo = __builtin_bit_cast(float, u << 16) * sx[R][i];
+        const float hi = __builtin_bit_cast(float, u & 0xffff0000u) * sx[R][i];
+        w[e2] = (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
       }
+      st16(&sm.x[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], w);
     }
   };
 
@@ -169,7 +152,7 @@ __global__ __launch_bounds__(kThreads, 1) void residual_bf16_kernel(ResidualPara
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const bf16x8 xa = as_bf16x8(ld16(&sm.xt[buf][dt * 32 + col][sub * 32 + ks * 16 + 8 * half]));
+          const bf16x8 xa = v_operand<D + 32>(&sm.x[buf][sub * 32 + ks * 16][dt * 32] + v_lane);
           y[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa, pk[ks], y[dt], 0, 0, 0);
         }
     }
