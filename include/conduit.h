@@ -38,7 +38,7 @@
  *     one.  Queries and outputs are dense
  *     [rows][n_q_heads][head_dim].  bf16 is IEEE binary32's top 16 bits.
  *     Device pointers must be 16-byte aligned and strides a multiple of
- *     16 bytes.
+ *     16 bytes and below 32 MiB (CONDUIT_ERR_UNSUPPORTED otherwise).
  *   - Query head h reads KV head h / (n_q_heads / n_kv_heads).
  *   - Supported: head_dim 64 or 128; n_kv_heads <= 256; CONDUIT_BF16 (MFMA
  *     kernels, fp32 accumulation) or CONDUIT_F32 (fp32 throughout).  The bf16

@@ -66,6 +66,9 @@ conduit_status check_kv(const conduit_kv *kv) {
                 (long long)kv->k_stride, (long long)kv->v_stride, (long long)row);
   if ((kv->k_stride * esize(kv->dtype)) % 16 || (kv->v_stride * esize(kv->dtype)) % 16)
     return fail(CONDUIT_ERR_INVALID_ARG, "token strides must be multiples of 16 bytes");
+  if (kv->k_stride * esize(kv->dtype) >= kMaxStrideBytes || kv->v_stride * esize(kv->dtype) >= kMaxStrideBytes)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "token strides of %lld / %lld bytes (supported: below 32 MiB)",
+                (long long)(kv->k_stride * esize(kv->dtype)), (long long)(kv->v_stride * esize(kv->dtype)));
   if (!kv->block_table) {
     if (kv->page_size != 0 || kv->n_pages != 0)
       return fail(CONDUIT_ERR_INVALID_ARG, "page_size and n_pages must be 0 without a block table");

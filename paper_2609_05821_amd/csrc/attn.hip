@@ -38,13 +38,45 @@ constexpr int KT = kAttnKeyTile;
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kMInit = -1e30f;  // initial running maximum (log2 units)
 
+// LDS tiles.  K rows are D + 8 elements apart (16 bytes of padding: the 16
+// lanes of an S^T operand read cover 16 rows in distinct banks); V rows are
+// D + 16 apart and read through transposing LDS reads.  Both pitches make a
+// tile a whole number of 1 KB direct-to-LDS transfers.
+template <int D>
+struct TileGeom {
+  static constexpr int kPitch = D + 8, vPitch = D + 16;
+  static constexpr int kXfer = KT * kPitch * 2 / 1024, vXfer = KT * vPitch * 2 / 1024;
+  static_assert(KT * kPitch * 2 % 1024 == 0 && KT * vPitch * 2 % 1024 == 0, "whole 1 KB transfers");
+};
+
+// With values: a four-stage ring of K and V tiles filled by direct-to-LDS
+// loads.  Statistics only: three register-staged K tiles and the image table.
 template <int D, bool PV>
 struct AttnSmem {
-  alignas(16) u16 k[2][KT][D + 8];   // K tiles, one row per key (+16 B pad against bank conflicts)
-  alignas(16) u16 v[2][PV ? KT : 1][D + 32];  // V tiles, one row per key; rows 16 words apart mod 64 banks
-  uint64_t okmask[2];                // key-domain filter per tile, bit = key
-  ImageLds img;                      // visual-only statistics: the image table
+  alignas(16) u16 k[PV ? 4 : 3][KT][TileGeom<D>::kPitch];
+  alignas(16) u16 v[PV ? 4 : 1][PV ? KT : 1][TileGeom<D>::vPitch];
+  uint64_t okmask[3];  // key-domain filter per K tile, bit = key
+  ImageLds img;        // visual-only statistics: the image table
 };
+
+// One 1 KB direct-to-LDS transfer: lane l's 16 bytes at byte voff of the
+// buffer land at LDS byte lds_addr + 16 l.  Written as assembly so that the
+// compiler's wait insertion does not make every later LDS read wait for it;
+// completion is awaited explicitly (vm_wait) before the barrier that
+// publishes a tile.
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t lds_addr, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(r)
+               : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N), expcnt and lgkmcnt left open (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 __device__ __forceinline__ int row_position(const int32_t *row_pos, int q_pos0, int r) {
   return row_pos ? row_pos[r] : q_pos0 + r;
@@ -293,7 +325,29 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const u16 *Kg = static_cast<const u16 *>(p.k);
   const u16 *Vg = static_cast<const u16 *>(p.v);
   const KvPageReader pr = page_reader(p.pages, p.n_ctx);
-  const int v_lane = v_operand_lane_offset<D + 32>(lane);  // PV operand reads
+  using Geo = TileGeom<D>;
+  const int v_lane = v_operand_lane_offset<Geo::vPitch>(lane);  // PV operand reads
+  // Direct-to-LDS staging (with values): a tile's K transfers are numbered
+  // 0..kXfer-1 and its V transfers kXfer..kXfer+vXfer-1; wave w issues
+  // transfers w, w + 8, ...  Lane l of transfer x fills LDS byte 16 l of it,
+  // i.e. one 16-byte chunk of a padded row; lanes that land in the padding
+  // re-read chunk 0 of their row.  xoff[s] is lane l's byte offset inside
+  // the tile for transfer wave + 8 s (head offset added per item).
+  constexpr int kXferAll = Geo::kXfer + Geo::vXfer;
+  constexpr int kSlots = PV ? (kXferAll + W - 1) / W : 1;
+  const int n_mine = PV ? (kXferAll - wave + W - 1) / W : 0;  // transfers of this wave per tile
+  uint32_t xoff0[kSlots];
+#pragma unroll
+  for (int sl = 0; sl < kSlots; ++sl) {
+    const int x = wave + W * sl;
+    const bool isk = x < Geo::kXfer;
+    const int pitch_b = 2 * (isk ? Geo::kPitch : Geo::vPitch);
+    const int b = (isk ? x : x - Geo::kXfer) * 1024 + 16 * lane;
+    const int row = b / pitch_b;
+    int ch = (b % pitch_b) / 16;
+    ch = ch < D / 8 ? ch : 0;
+    xoff0[sl] = (uint32_t)(((int64_t)row * (isk ? p.k_stride : p.v_stride) + 8 * ch) * 2);
+  }
   const u16 *Qg = static_cast<const u16 *>(p.q);
   const float c = p.scale_log2;
   // UNI: the closed-form plan of contiguous rows (no plan loads at all).
@@ -339,74 +393,85 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         qreg[ks] = as_bf16x8(valid ? ld16(qrow + ks * 16) : u32x4{0, 0, 0, 0});
     }
 
-    // Per-thread offsets of its staging chunks inside a key tile (16 lanes
-    // per key row, so K and V loads are coalesced); a tile's base moves by KT
-    // rows, and only a partial last tile clamps its rows.
-    int64_t koff[Regs::KCH], voff[Regs::KCH];
+    // Statistics only: register staging.  Per-thread byte offsets of its
+    // chunks inside a key tile (16 lanes per key row, so loads are
+    // coalesced), read through a buffer resource over the tile's KT rows
+    // (row strides stay below 32 MiB, so 32-bit offsets reach every row).
+    uint32_t koff[Regs::KCH];
 #pragma unroll
     for (int i = 0; i < Regs::KCH; ++i) {
       const int cidx = tid + kThreads * i;
-      koff[i] = (int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8;
-      voff[i] = (int64_t)(cidx / (D / 8)) * p.v_stride + kvh * D + (cidx % (D / 8)) * 8;
+      koff[i] = (uint32_t)(((int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8) * 2);
     }
-    u32x4 rk[Regs::KCH];
-    u32x4 rv[PV ? Regs::KCH : 1];
+    u32x4 rk[PV ? 1 : Regs::KCH];
     bool rok = false;
     // t0 is a multiple of the tile and a page holds a whole number of tiles,
-    // so a tile's rows are consecutive rows of the cache starting at row0.
-    auto load_tile = [&](int t0, int64_t row0) __attribute__((always_inline)) {
-      const u16 *kb = Kg + row0 * p.k_stride;
-      const u16 *vb = Vg + row0 * p.v_stride;
-      if (t0 + KT <= kend) {
+    // so a tile's rows are consecutive cache rows from row0; only a partial
+    // last tile clamps its rows (past kend they repeat the last row and are
+    // masked later).
+    auto load_k = [&](int t0, int64_t row0) __attribute__((always_inline)) {
+      if constexpr (!PV) {
+        const auto rs = buffer_rsrc(Kg + row0 * p.k_stride, (int)(KT * p.k_stride * 2));
+        if (t0 + KT <= kend) {
 #pragma unroll
-        for (int i = 0; i < Regs::KCH; ++i) rk[i] = ld16(kb + koff[i]);
-        if constexpr (PV) {
-#pragma unroll
-          for (int i = 0; i < Regs::KCH; ++i) rv[i] = ld16(vb + voff[i]);
-        }
-      } else {  // partial tile: rows past kend repeat the last row (masked later)
-#pragma unroll
-        for (int i = 0; i < Regs::KCH; ++i) {
-          const int cidx = tid + kThreads * i;
-          const int kp = min(t0 + cidx / (D / 8), kend - 1);
-          rk[i] = ld16(kb + (int64_t)(kp - t0) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8);
-        }
-        if constexpr (PV) {
+          for (int i = 0; i < Regs::KCH; ++i) rk[i] = buffer_ld16(rs, koff[i]);
+        } else {
 #pragma unroll
           for (int i = 0; i < Regs::KCH; ++i) {
             const int cidx = tid + kThreads * i;
             const int kp = min(t0 + cidx / (D / 8), kend - 1);
-            rv[i] = ld16(vb + (int64_t)(kp - t0) * p.v_stride + kvh * D + (cidx % (D / 8)) * 8);
+            rk[i] = buffer_ld16(rs, (uint32_t)(((int64_t)(kp - t0) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8) * 2));
           }
         }
-      }
-      if (!PV && p.vis_only && tid < KT) {
-        const int kp = t0 + tid;
-        rok = kp < kend && is_visual(sm.img, kp);
+        if (p.vis_only && tid < KT) {
+          const int kp = t0 + tid;
+          rok = kp < kend && is_visual(sm.img, kp);
+        }
       }
     };
-    auto store_tile = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-      for (int i = 0; i < Regs::KCH; ++i) {
-        const int cidx = tid + kThreads * i;
-        st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
-      }
-      if constexpr (PV) {
+    auto store_k = [&](int buf) __attribute__((always_inline)) {
+      if constexpr (!PV) {
 #pragma unroll
         for (int i = 0; i < Regs::KCH; ++i) {
           const int cidx = tid + kThreads * i;
-          st16(&sm.v[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rv[i]);
+          st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
+        }
+        if (p.vis_only && tid < KT) {  // wave 0: one bit per key of the tile
+          const uint64_t bits = __ballot(rok != 0);
+          if (tid == 0) sm.okmask[buf] = bits;
         }
       }
-      if (!PV && p.vis_only && tid < KT) {  // wave 0: one bit per key of the tile
-        const uint64_t bits = __ballot(rok != 0);
-        if (tid == 0) sm.okmask[buf] = bits;
+    };
+    // With values: this wave's transfers of the K tile at t0 (row0; rows at
+    // or past kend read as 0 through the resource bound) into K stage kst,
+    // or of the V tile into V stage vst.  A tile that does not exist still
+    // gets its transfers (zero-length resource), so every iteration issues
+    // the same count per wave.
+    const uint32_t head_b = (uint32_t)(kvh * D * 2);
+    auto dma_tile = [&](bool isk, int st, int t0, int64_t row0) __attribute__((always_inline)) {
+      if constexpr (PV) {
+        const int rows = min(max(kend - t0, 0), KT);
+        // the resource must sit in scalar registers: its inputs are uniform,
+        // which readfirstlane makes explicit
+        const uint64_t ga = (uint64_t)(uintptr_t)(isk ? Kg + row0 * p.k_stride : Vg + row0 * p.v_stride);
+        const uint64_t gu = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(ga >> 32)) << 32) |
+                            (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ga);
+        const int nbytes = __builtin_amdgcn_readfirstlane((int)(rows * (isk ? p.k_stride : p.v_stride) * 2));
+        const auto rs = buffer_rsrc(reinterpret_cast<const void *>((uintptr_t)gu), nbytes);
+        const uint32_t base = isk ? (uint32_t)(uintptr_t)&sm.k[st][0][0] : (uint32_t)(uintptr_t)&sm.v[st][0][0];
+#pragma unroll
+        for (int sl = 0; sl < kSlots; ++sl) {
+          const int x = wave + W * sl;
+          if (isk ? x < Geo::kXfer : (x >= Geo::kXfer && x < kXferAll))
+            lds_dma16(rs, __builtin_amdgcn_readfirstlane(base + (isk ? x : x - Geo::kXfer) * 1024),
+                      xoff0[sl] + head_b);
+        }
       }
     };
 
     // Running maximum (log2 units) starts finite, so exp2(c*s - m) needs no
-    // special case: masked logits are -inf and give 0; the first valid
-    // sub-tile always moves m.
+    // special case: masked logits are -inf and give 0; the first tile with a
+    // visible key always moves m.
     float m = kMInit, l = 0.f;
     f32x16 o[DT];
     if constexpr (PV) {
@@ -425,99 +490,153 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
       for (int ks = 0; ks < KS; ++ks) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qreg[ks], sc, 0, 0, 0);
       return sc;
     };
-
-    // Online softmax of one sub-tile, then O^T += V^T P^T.
-    auto softmax_pv = [&](f32x16 sc, int buf, int sub, int t0, bool masked) __attribute__((always_inline)) {
-      if (masked) {  // branch-free: causal / split end and the key domain
-        const int lim = min(kend - 1, rp) - t0;  // last visible key of the tile
+    // Tiles that need a key filter: causal / split end, and the key domain.
+    auto tile_masked = [&](int t0) __attribute__((always_inline)) {
+      return (!PV && p.vis_only) || t0 + KT > kend || t0 + KT - 1 > minpos;
+    };
+    // Key filter of sub-tile `sub` of the tile at t0 (K buffer buf).
+    auto mask_sub = [&](f32x16 &sc, int buf, int t0, int sub) __attribute__((always_inline)) {
+      const int lim = min(kend - 1, rp) - t0 - 4 * half;  // last visible key of the tile, lane-relative
+      // key-domain filter (statistics of visual-only scoring): the tile's
+      // bits from this lane's first key on
+      uint64_t dom = ~0ull;
+      if constexpr (!PV) dom = (sm.okmask[buf] | (p.vis_only ? 0ull : ~0ull)) >> (4 * half);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int kl = sub * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-          bool ok = kl <= lim;
-          if constexpr (!PV) {  // key-domain filter: statistics of visual-only scoring
-            const uint64_t dom = p.vis_only ? sm.okmask[buf] : ~0ull;
-            ok = ok & (((dom >> kl) & 1ull) != 0);
-          }
-          sc[v] = ok ? sc[v] : kNegInf;
-        }
-      }
-      float mx = kNegInf;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[v]);
-      mx = half_max(mx) * c;
-      const bool grow = mx > m + kRescaleSlack;
-      const float alpha = grow ? fast_exp2(m - mx) : 1.f;
-      m = grow ? mx : m;
-      const float neg_m = -m;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sc[v] = fast_exp2(fmaf(sc[v], c, neg_m));
-      if constexpr (PV) {
-        bf16x8 pk[2];
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pk[ks][e] = static_cast<__bf16>(sc[8 * ks + e]);
-        // fp32 row sum (the log-sum-exp output needs it to 1e-4; summing the
-        // bf16-rounded probabilities is off by up to 2^-9 when few terms dominate)
-        float psum = 0.f;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) psum += sc[v];
-        l = l * alpha + psum;
-        if (__ballot(grow)) {
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
-        }
-        bf16x8 va[2][DT];
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-            va[ks][dt] = v_operand<D + 32>(&sm.v[buf][sub * 32 + ks * 16][dt * 32] + v_lane);
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][dt], pk[ks], o[dt], 0, 0, 0);
-      } else {
-        float psum = 0.f;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) psum += sc[v];
-        l = l * alpha + psum;
+      for (int v = 0; v < 16; ++v) {
+        const int kl = sub * 32 + 8 * (v >> 2) + (v & 3);  // + 4 * half
+        bool ok = kl <= lim;
+        if constexpr (!PV) ok = ok & (((dom >> kl) & 1ull) != 0);
+        sc[v] = ok ? sc[v] : kNegInf;
       }
     };
+    auto sub_max = [&](const f32x16 &sc) __attribute__((always_inline)) {
+      float x = kNegInf;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) x = fmaxf(x, sc[v]);
+      return half_max(x) * c;
+    };
 
-    // Double-buffered main loop: the next tile's global loads are in flight
-    // while the current tile computes; one barrier per tile.  Both sub-tiles'
-    // S^T MFMAs are issued before the first softmax, so the VALU work of one
-    // sub-tile runs while the matrix core still works on the other.
+    // Software-pipelined main loop over 64-key tiles of two 32-key
+    // sub-tiles, one barrier per tile.  Each sub-step issues the S^T products
+    // of the next sub-tile while it exponentiates the current one
+    // (independent work in one instruction stream, so the matrix core and
+    // the VALU overlap), then O^T += V^T P^T of the current sub-tile while it
+    // takes the next one's maximum.  Iteration t reads K(t), K(t+1) and V(t).
+    // With values the tiles arrive by direct-to-LDS loads into a four-stage
+    // ring, K three tiles ahead and V two (each wave waits for the transfers
+    // it issued one iteration earlier before the barrier); statistics only
+    // stage K through registers one tile ahead (three K buffers).
     // Block-table entries of 64 consecutive tiles are read at once, one per
     // lane, and each tile takes its entry with a lane read; only every 64th
     // tile waits for the table.
-    int page_vec = 0, page_base = INT32_MIN;
+    int page_vec = 0, page_base = -64;
     auto tile_row = [&](int t0) __attribute__((always_inline)) {
       const int ti = t0 / KT;
       if (ti - page_base >= 64) {
         page_base = ti;
         page_vec = read_page(pr, (ti + (tid & 63)) * KT);
+        if constexpr (PV) vm_wait<0>();  // here, not before every lane read
       }
       return page_row(pr, __builtin_amdgcn_readlane(page_vec, ti - page_base), t0);
     };
-    load_tile(kbeg, tile_row(kbeg));
-    store_tile(0);
-    __syncthreads();
-    int buf = 0;
-    for (int t0 = kbeg; t0 < kend; t0 += KT) {
-      const bool more = t0 + KT < kend;
-      if (more) load_tile(t0 + KT, tile_row(t0 + KT));
-      const bool masked = (!PV && p.vis_only) || t0 + KT > kend || t0 + KT - 1 > minpos;
-      const f32x16 s0 = scores(buf, 0);
-      const f32x16 s1 = scores(buf, 1);
-      softmax_pv(s0, buf, 0, t0, masked);
-      softmax_pv(s1, buf, 1, t0, masked);
-      if (more) store_tile(buf ^ 1);
-      __syncthreads();
-      buf ^= 1;
+    auto row_of = [&](int t0) __attribute__((always_inline)) { return t0 < kend ? tile_row(t0) : (int64_t)0; };
+    if constexpr (PV) {
+      const int64_t r0 = tile_row(kbeg), r1 = row_of(kbeg + KT), r2 = row_of(kbeg + 2 * KT);
+      dma_tile(true, 0, kbeg, r0);
+      dma_tile(false, 0, kbeg, r0);
+      dma_tile(true, 1, kbeg + KT, r1);
+      dma_tile(false, 1, kbeg + KT, r1);
+      dma_tile(true, 2, kbeg + 2 * KT, r2);
+      vm_wait<0>();
+    } else {
+      const int64_t row0 = tile_row(kbeg);
+      load_k(kbeg, row0);
+      store_k(0);
+      if (kbeg + KT < kend) {
+        load_k(kbeg + KT, tile_row(kbeg + KT));
+        store_k(1);
+      }
     }
+    __syncthreads();
+    f32x16 sa = scores(0, 0), sb;
+    if (tile_masked(kbeg)) mask_sub(sa, 0, kbeg, 0);
+    float mx = sub_max(sa);
+    // One sub-step: cur holds S^T of the current sub-tile (V rows vsub*32..
+    // of V stage vst), nxt receives the next sub-tile's (K stage kbn, rows
+    // ksub*32.., of the tile at nt0; after the last sub-tile: discarded).
+    auto sub_step = [&](f32x16 &cur, f32x16 &nxt, int kbn, int ksub, int vst, int vsub, bool has_next, int nt0)
+                        __attribute__((always_inline)) {
+      const bool grow = mx > m + kRescaleSlack;
+      const float alpha = grow ? fast_exp2(m - mx) : 1.f;
+      m = grow ? mx : m;
+      if constexpr (PV) {
+        if (__ballot(grow)) {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        }
+      }
+      nxt = scores(kbn, ksub);
+      // probabilities of the current sub-tile; fp32 row sum (the
+      // log-sum-exp output needs it to 1e-4; summing the bf16-rounded
+      // probabilities is off by up to 2^-9 when few terms dominate)
+      const float neg_m = -m;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) cur[v] = fast_exp2(fmaf(cur[v], c, neg_m));
+      float psum = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) psum += cur[v];
+      l = l * alpha + psum;
+      if constexpr (PV) {
+        bf16x8 pk[2];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pk[ks][e] = static_cast<__bf16>(cur[8 * ks + e]);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          bf16x8 va[DT];
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            va[dt] = v_operand<Geo::vPitch>(&sm.v[vst][vsub * 32 + ks * 16][dt * 32] + v_lane);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[dt], pk[ks], o[dt], 0, 0, 0);
+        }
+      }
+      if (has_next) {
+        if (tile_masked(nt0)) mask_sub(nxt, kbn, nt0, ksub);
+        mx = sub_max(nxt);
+      }
+    };
+    constexpr int NKB = PV ? 4 : 3;
+    int t0 = kbeg, st = 0;  // K (and V) stage of tile t; stages follow mod NKB
+    for (;;) {
+      const bool more = t0 + KT < kend;
+      const int st1 = st + 1 == NKB ? 0 : st + 1;
+      if constexpr (PV) {
+        // V(t+2) and K(t+3); their stages last held tiles t-2 and t-1
+        const int st2 = st1 + 1 == NKB ? 0 : st1 + 1, st3 = st2 + 1 == NKB ? 0 : st2 + 1;
+        const int64_t rv2 = row_of(t0 + 2 * KT), rk3 = row_of(t0 + 3 * KT);
+        dma_tile(false, st2, t0 + 2 * KT, rv2);
+        dma_tile(true, st3, t0 + 3 * KT, rk3);
+      } else if (t0 + 2 * KT < kend) {
+        load_k(t0 + 2 * KT, tile_row(t0 + 2 * KT));
+      }
+      sub_step(sa, sb, st, 1, st, 0, true, t0);        // second half of tile t
+      sub_step(sb, sa, st1, 0, st, 1, more, t0 + KT);  // first half of tile t+1
+      if constexpr (PV) {
+        // the transfers issued one iteration ago (K(t+2), V(t+1)) have landed
+        if (n_mine == kSlots) vm_wait<kSlots>();
+        else vm_wait<kSlots - 1>();
+      } else if (t0 + 2 * KT < kend) {
+        store_k(st1 + 1 == NKB ? 0 : st1 + 1);
+      }
+      __syncthreads();
+      if (!more) break;
+      t0 += KT;
+      st = st1;
+    }
+    if constexpr (PV) vm_wait<0>();  // transfers of tiles past the end (zero-length) drained
 
     // ---- outputs: final values for a single-split block, else partials ----
     const float l_tot = l + __shfl_xor(l, 32, 64);

@@ -130,6 +130,20 @@ __device__ __forceinline__ int64_t kv_row(const KvPages &pg, int t) {
 // unconditional (no branch, hence no early wait on every load in flight).  A
 // contiguous cache gets 0 records and a 31-bit in-page mask, so the row is the
 // token itself.
+// gfx9 raw buffer resource, word 3: 32-bit data format, no swizzle.
+constexpr int kRawBufferWord3 = 0x00020000;
+
+// Buffer resource over `bytes` bytes from p: loads address it with 32-bit
+// per-lane byte offsets (one VGPR each, the base stays scalar), and a read
+// past the end returns 0 instead of touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, bytes, kRawBufferWord3);
+}
+
+__device__ __forceinline__ u32x4 buffer_ld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
 struct KvPageReader {
   __amdgpu_buffer_rsrc_t rsrc;
   int32_t shift;
@@ -138,15 +152,13 @@ struct KvPageReader {
 
 __device__ __forceinline__ KvPageReader page_reader(const KvPages &pg, int n_ctx) {
   KvPageReader r;
-  constexpr int kRsrcWord3 = 0x00020000;  // gfx9 raw buffer: 32-bit data format
   if (pg.table) {
     const int entries = ((n_ctx - 1) >> pg.shift) + 1;
-    r.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(pg.table), (short)0, entries * 4,
-                                               kRsrcWord3);
+    r.rsrc = buffer_rsrc(pg.table, entries * 4);
     r.shift = pg.shift;
     r.last_page = pg.n_pages - 1;
   } else {
-    r.rsrc = __builtin_amdgcn_make_buffer_rsrc(nullptr, (short)0, 0, kRsrcWord3);
+    r.rsrc = buffer_rsrc(nullptr, 0);
     r.shift = 31;
     r.last_page = 0;
   }
@@ -446,6 +458,7 @@ constexpr int64_t attn_max_items(int64_t n_pb, int64_t n_kv_heads, bool with_val
   return (int64_t)attn_grid(with_values) * attn_plan_rounds(with_values) + n_pb * n_kv_heads;
 }
 constexpr int kAttnKeyTile = 64;         // keys per LDS tile
+constexpr int64_t kMaxStrideBytes = int64_t(1) << 25;  // row strides below 32 MiB: a key tile spans < 2 GiB
 constexpr int kColsumKeysPerBlock = 256;
 constexpr int kColsumMaxLsePairs = 4096;  // row LSEs a column-sum workgroup can rebuild in LDS // visual keys per workgroup
 

@@ -80,6 +80,8 @@ def score(kvd=None, q=FAKE, n_q=64, q_pos0=1280, img=IMG, norm=0, agg=0, scale=0
     (dict(kvd=kv(dtype=7)), api.ERR_INVALID_ARG),
     (dict(kvd=kv(k_stride=100)), api.ERR_INVALID_ARG),
     (dict(kvd=kv(k_stride=516)), api.ERR_INVALID_ARG),
+    (dict(kvd=kv(k_stride=1 << 24)), api.ERR_UNSUPPORTED),                  # a 32 MiB row
+    (dict(kvd=kv(v_stride=(1 << 24) + 8)), api.ERR_UNSUPPORTED),
     (dict(q=0), api.ERR_INVALID_ARG),
     (dict(q=FAKE + 2), api.ERR_INVALID_ARG),
     (dict(n_q=0), api.ERR_INVALID_ARG),
