@@ -16,12 +16,15 @@
 //  2. attn_bf16_kernel runs a persistent grid (one 8-wave workgroup per CU
 //     with values, two 4-wave ones without) that walks the item list in
 //     snake order, so every CU gets a similar share of tiles.  Per 64-key
-//     tile, double-buffered in LDS with the next tile's global loads in
-//     flight, K is staged row-major and V transposed; each wave computes
+//     tile, K is staged row-major and V row-major (read back through
+//     transposing LDS reads); with values by direct-to-LDS loads into a
+//     four-stage ring, statistics only through registers.  Each wave computes
 //     S^T = K Q^T with v_mfma_f32_32x32x16_bf16 so that every lane holds 16
 //     keys of one pair column and the online softmax runs in-lane; the
 //     probabilities feed O^T = V^T P^T straight from the accumulator
-//     registers.  A block whose keys form a single split writes its final
+//     registers.  The loop is software-pipelined by 32-key sub-tiles: the S^T
+//     products of the next sub-tile are issued while the current one is
+//     exponentiated.  A block whose keys form a single split writes its final
 //     outputs; otherwise each split writes (m, l, O) partials in the log2
 //     domain.
 //  3. combine_kernel merges the partials of split blocks in a fixed order
