@@ -334,9 +334,11 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   // 0..kXfer-1 and its V transfers kXfer..kXfer+vXfer-1; wave w issues
   // transfers w, w + 8, ...  Lane l of transfer x fills LDS byte 16 l of it,
   // i.e. one 16-byte chunk of a padded row; lanes that land in the padding
-  // re-read chunk 0 of their row.  xoff[s] is lane l's byte offset inside
-  // the tile for transfer wave + 8 s (head offset added per item).
+  // point past the buffer's end, so they fetch nothing and write zeros.
+  // xoff[s] is lane l's byte offset inside the tile for transfer wave + 8 s
+  // (head offset added per item; the padding offset stays out of range).
   constexpr int kXferAll = Geo::kXfer + Geo::vXfer;
+  constexpr uint32_t kPadOff = 0x80000000u;  // beyond any tile resource (< 2 GiB): reads as 0
   constexpr int kSlots = PV ? (kXferAll + W - 1) / W : 1;
   const int n_mine = PV ? (kXferAll - wave + W - 1) / W : 0;  // transfers of this wave per tile
   uint32_t xoff0[kSlots];
@@ -346,10 +348,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     const bool isk = x < Geo::kXfer;
     const int pitch_b = 2 * (isk ? Geo::kPitch : Geo::vPitch);
     const int b = (isk ? x : x - Geo::kXfer) * 1024 + 16 * lane;
-    const int row = b / pitch_b;
-    int ch = (b % pitch_b) / 16;
-    ch = ch < D / 8 ? ch : 0;
-    xoff0[sl] = (uint32_t)(((int64_t)row * (isk ? p.k_stride : p.v_stride) + 8 * ch) * 2);
+    const int row = b / pitch_b, ch = (b % pitch_b) / 16;
+    xoff0[sl] = ch < D / 8 ? (uint32_t)(((int64_t)row * (isk ? p.k_stride : p.v_stride) + 8 * ch) * 2) : kPadOff;
   }
   const u16 *Qg = static_cast<const u16 *>(p.q);
   const float c = p.scale_log2;
@@ -467,7 +467,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
           const int x = wave + W * sl;
           if (isk ? x < Geo::kXfer : (x >= Geo::kXfer && x < kXferAll))
             lds_dma16(rs, __builtin_amdgcn_readfirstlane(base + (isk ? x : x - Geo::kXfer) * 1024),
-                      xoff0[sl] + head_b);
+                      xoff0[sl] == kPadOff ? kPadOff : xoff0[sl] + head_b);
         }
       }
     };
