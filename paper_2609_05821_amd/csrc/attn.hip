@@ -97,15 +97,6 @@ __device__ __forceinline__ int4 uniform_block_info(int pb, int ppb, int group, i
   return make_int4(maxpos, minpos, ns, ((tiles + ns - 1) / ns) * KT);
 }
 
-// Global -> register staging of one key tile (issued a tile ahead).
-template <int D, bool PV, int W>
-struct TileRegs {
-  static constexpr int kThreads = W * 64;
-  static constexpr int KCH = KT * D / 8 / kThreads;    // 16-byte K (and V) chunks per thread
-  u32x4 k[KCH];
-  u32x4 v[PV ? KCH : 1];
-  uint8_t ok;
-};
 
 // The running maximum only moves when a sub-tile's maximum exceeds it by more
 // than this many log2 units; probabilities stay below 2^8 and O, l are
@@ -318,7 +309,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   constexpr int kPairs = W * 32;  // (row, head) pairs per block
   constexpr int KS = D / 16;      // MFMA k-steps over the head dimension
   constexpr int DT = D / 32;      // 32-row tiles of O^T
-  using Regs = TileRegs<D, PV, W>;
+  constexpr int KCH = KT * D / 8 / kThreads;  // 16-byte K chunks per thread (register staging)
   __shared__ AttnSmem<D, PV> sm;
 
   const int G = p.group;
@@ -400,13 +391,13 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     // chunks inside a key tile (16 lanes per key row, so loads are
     // coalesced), read through a buffer resource over the tile's KT rows
     // (row strides stay below 32 MiB, so 32-bit offsets reach every row).
-    uint32_t koff[Regs::KCH];
+    uint32_t koff[KCH];
 #pragma unroll
-    for (int i = 0; i < Regs::KCH; ++i) {
+    for (int i = 0; i < KCH; ++i) {
       const int cidx = tid + kThreads * i;
       koff[i] = (uint32_t)(((int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8) * 2);
     }
-    u32x4 rk[PV ? 1 : Regs::KCH];
+    u32x4 rk[PV ? 1 : KCH];
     bool rok = false;
     // t0 is a multiple of the tile and a page holds a whole number of tiles,
     // so a tile's rows are consecutive cache rows from row0; only a partial
@@ -417,10 +408,10 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         const auto rs = buffer_rsrc(Kg + row0 * p.k_stride, (int)(KT * p.k_stride * 2));
         if (t0 + KT <= kend) {
 #pragma unroll
-          for (int i = 0; i < Regs::KCH; ++i) rk[i] = buffer_ld16(rs, koff[i]);
+          for (int i = 0; i < KCH; ++i) rk[i] = buffer_ld16(rs, koff[i]);
         } else {
 #pragma unroll
-          for (int i = 0; i < Regs::KCH; ++i) {
+          for (int i = 0; i < KCH; ++i) {
             const int cidx = tid + kThreads * i;
             const int kp = min(t0 + cidx / (D / 8), kend - 1);
             rk[i] = buffer_ld16(rs, (uint32_t)(((int64_t)(kp - t0) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8) * 2));
@@ -435,7 +426,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     auto store_k = [&](int buf) __attribute__((always_inline)) {
       if constexpr (!PV) {
 #pragma unroll
-        for (int i = 0; i < Regs::KCH; ++i) {
+        for (int i = 0; i < KCH; ++i) {
           const int cidx = tid + kThreads * i;
           st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
         }
