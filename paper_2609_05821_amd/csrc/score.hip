@@ -30,6 +30,7 @@ constexpr int kColsumThreads = 512;   // 8 waves x 32 keys
 // tiles and exponentials run, one barrier per chunk.  The V rows for the
 // value norms are fetched at the start and consumed at the end.
 constexpr int kQChunk = 256;
+constexpr int kLseRegSplits = 24;  // split partials of one row held in registers by the fused merge
 
 // Finalize of one visual token: fixed-order sum over KV heads, the mean (or
 // RMS) over rows and heads, the value norm, s = a v and the layer
@@ -111,26 +112,6 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   load_chunk(0, qv, bv);
 
   image_table_to_lds(p.tbl, img, tid, kColsumThreads);
-  if constexpr (FUSE) {
-    // b = M + log2(sum_s l_s 2^(m_s - M)) over the splits of the row's
-    // block, s ascending, exactly as the statistics merge computes it.
-    for (int pr = tid; pr < n_pair; pr += kColsumThreads) {
-      const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
-      const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * p.lse_ns;
-      float M = -kInf;
-#pragma unroll 8
-      for (int sp = 0; sp < p.lse_ns; ++sp) M = fmaxf(M, p.lse_part_m[(slot0 + sp) * p.lse_ppb + j]);
-      float L = 0.f;
-#pragma unroll 8
-      for (int sp = 0; sp < p.lse_ns; ++sp) {
-        const int64_t idx = (slot0 + sp) * p.lse_ppb + j;
-        L += fast_exp2(p.lse_part_m[idx] - M) * p.lse_part_l[idx];
-      }
-      const float b = M + __log2f(L);
-      b_all[pr] = b;
-      if (blockIdx.x == 0 && p.lse_out) p.lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
-    }
-  }
   __syncthreads();
   // This lane's key column, held as the B operand for every row tile.
   const int t = blockIdx.x * kColsumKeysPerBlock + wave * 32 + col;
@@ -142,7 +123,8 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     for (int ks = 0; ks < KS; ++ks) kreg[ks] = as_bf16x8(ld16(krow + ks * 16));
   }
   // V rows of the block's keys for the value norms, 16 bytes per item (not
-  // read when the norms are given).
+  // read when the norms are given).  Both reads are in flight while the row
+  // log-sum-exps are rebuilt below.
   const bool read_v = p.vnorm_in == nullptr;
   u32x4 vv[VPT];
 #pragma unroll
@@ -151,6 +133,43 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     const int tv = min(blockIdx.x * kColsumKeysPerBlock + vi / (D / 8), p.n_vis - 1);
     vv[i] = read_v ? ld16(Vg + kv_row(p.pages, vis_position(img, tv)) * p.v_stride + kvh * D + (vi % (D / 8)) * 8)
                    : u32x4{0, 0, 0, 0};
+  }
+  if constexpr (FUSE) {
+    // b = M + log2(sum_s l_s 2^(m_s - M)) over the splits of the row's
+    // block, s ascending, exactly as the statistics merge computes it.  Up
+    // to kLseRegSplits splits are read in one pass (indices clamped, so
+    // every read is issued unconditionally) and reduced from registers.
+    const int ns = p.lse_ns;
+    for (int pr = tid; pr < n_pair; pr += kColsumThreads) {
+      const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
+      const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns;
+      float M = -kInf, L = 0.f;
+      if (ns <= kLseRegSplits) {
+        float mv[kLseRegSplits], lv[kLseRegSplits];
+#pragma unroll
+        for (int sp = 0; sp < kLseRegSplits; ++sp) {
+          const int64_t idx = (slot0 + min(sp, ns - 1)) * p.lse_ppb + j;
+          mv[sp] = p.lse_part_m[idx];
+          lv[sp] = p.lse_part_l[idx];
+        }
+#pragma unroll
+        for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[sp]) : M;
+#pragma unroll
+        for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[sp] - M) * lv[sp] : L;
+      } else {
+#pragma unroll 8
+        for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, p.lse_part_m[(slot0 + sp) * p.lse_ppb + j]);
+#pragma unroll 8
+        for (int sp = 0; sp < ns; ++sp) {
+          const int64_t idx = (slot0 + sp) * p.lse_ppb + j;
+          L += fast_exp2(p.lse_part_m[idx] - M) * p.lse_part_l[idx];
+        }
+      }
+      const float b = M + __log2f(L);
+      b_all[pr] = b;
+      if (blockIdx.x == 0 && p.lse_out) p.lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
+    }
+    __syncthreads();
   }
   store_chunk(0, 0, qv, bv);
   __syncthreads();
@@ -161,7 +180,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     const bool more = c + 1 < nch;
     if (more) load_chunk(c + 1, qv, bv);
     const int rows = min(kQChunk, n_pair - c * kQChunk);
-    for (int r0 = 0; r0 < rows; r0 += 64) {
+    auto row_step = [&](int r0) __attribute__((always_inline)) {
       f32x16 acc0 = f32x16{}, acc1 = f32x16{};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -186,6 +205,14 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
         }
       }
       colsum += part0 + part1;
+    };
+    // A full chunk's row steps unrolled: one step's products are independent
+    // of the previous step's exponentials, so the two overlap.
+    if (rows == kQChunk) {
+#pragma unroll
+      for (int r0 = 0; r0 < kQChunk; r0 += 64) row_step(r0);
+    } else {
+      for (int r0 = 0; r0 < rows; r0 += 64) row_step(r0);
     }
     if (more) store_chunk(c + 1, buf ^ 1, qv, bv);
     __syncthreads();
