@@ -13,7 +13,9 @@ restored from a pristine copy.  Both happen outside the per-step HIP events.
 Prints one JSON line.  `value` is visual tokens scored and refreshed per
 second for the layer (N_vis / step time).  `roofline` covers the refresh
 attention (the dominant call): algorithmic FLOPs 4 * H_q * d * sum_i (p_i + 1)
-over its event-timed duration, against the bf16 dense MFMA peak.
+over its event-timed duration, against the bf16 dense MFMA peak; beside it the
+rate a reference loop of independent MFMAs on random operands sustains on this
+device in the same run (`sustained_mfma`).
 `cpu_baseline` times the float64 CPU oracle on a bounded sample of the same
 step on this host's cores.
 """
@@ -34,6 +36,54 @@ sys.path.insert(0, ROOT)
 METRIC = "visual tokens scored+refreshed/s per layer; refresh-step ms @16k tokens, 10%"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+
+
+def sustained_mfma(dev):
+    """Sustained bf16 matrix-core rate of this device on random operands: a
+    loop of independent v_mfma_f32_32x32x16_bf16 at two waves per SIMD
+    (paper_2609_05821_amd/csrc/ceiling.hip, built as libconduit_ceiling.so).
+    A reference for the attention kernel's rate: under matrix-core load the
+    shader clock drops below the one the nominal peak assumes."""
+    import ctypes
+    import torch
+    path = os.path.join(ROOT, "paper_2609_05821_amd", "libconduit_ceiling.so")
+    if not os.path.exists(path):
+        return {"error": "libconduit_ceiling.so is not built"}
+    lib = ctypes.CDLL(path)
+    lib.conduit_ceiling_ops_bytes.restype = ctypes.c_int64
+    lib.conduit_ceiling_ops_bytes.argtypes = [ctypes.c_int32]
+    lib.conduit_ceiling_flop.restype = ctypes.c_double
+    lib.conduit_ceiling_flop.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    lib.conduit_ceiling_mfma_bf16.restype = ctypes.c_int
+    lib.conduit_ceiling_mfma_bf16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                              ctypes.c_int32, ctypes.c_void_p]
+    blocks, iters = 512, 20000
+    gen = torch.Generator(device=dev).manual_seed(7)
+    ops = torch.randn(lib.conduit_ceiling_ops_bytes(blocks) // 2, generator=gen, device=dev).to(torch.bfloat16)
+    out = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def launch():
+        rc = lib.conduit_ceiling_mfma_bf16(ops.data_ptr(), out.data_ptr(), blocks, iters, stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"ceiling kernel launch failed ({rc})")
+
+    launch()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(3):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        launch()
+        b.record(stream)
+        b.synchronize()
+        times.append(a.elapsed_time(b))
+    t = statistics.median(times)
+    tflops = lib.conduit_ceiling_flop(blocks, iters) / (t * 1e-3) / 1e12
+    return {"tflops": tflops, "ms": t, "frac_of_nominal": tflops / PEAK_BF16_TFLOPS,
+            "what": "independent v_mfma_f32_32x32x16_bf16 on random bf16 operands, two waves per "
+                    f"SIMD, median of 3 launches of {lib.conduit_ceiling_flop(blocks, iters) / 1e12:.1f} "
+                    "TFLOP each (csrc/ceiling.hip)"}
 
 
 def parse():
@@ -229,6 +279,7 @@ def main():
     attn_ms = kernels_ms["attn_values"]["mean"]
     attn_tflops = refresh_flops / (attn_ms * 1e-3) / 1e12
     probe_bytes = (8 * H * d * e + w.n_ctx * hkv * d * e + w.n_vis * hkv * d * e + w.n_vis * 4 * 4)
+    ceiling = sustained_mfma(dev)  # after the timed passes
 
     result = {
         "metric": METRIC,
@@ -263,6 +314,8 @@ def main():
                       "timing), same steps as the timed region, second pass",
             "whole_call": {"ms": ms["refresh"], "tflops": refresh_tflops,
                            "note": "conduit_refresh_attn = plan + attention + split merge"},
+            "sustained_mfma": ceiling,
+            "frac_of_sustained": attn_tflops / ceiling["tflops"] if "tflops" in ceiling else None,
         },
         "per_call_ms_mean": ms,
         "per_call_ms_median": med,

@@ -1,4 +1,5 @@
-"""Build libconduit.so (gfx950) in-tree with hipcc.
+"""Build libconduit.so (gfx950) in-tree with hipcc, and the benchmark's
+matrix-core reference kernel as libconduit_ceiling.so.
 
     python -m paper_2609_05821_amd.build
 
@@ -20,6 +21,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libconduit.so")
 SOURCES = ["api.cpp", "attn.hip", "score.hip", "select.hip", "scatter.hip", "residual.hip"]
+CEILING_SRC = "ceiling.hip"  # measurement reference for bench.py, not part of the library
+CEILING_LIB = os.path.join(PKG, "libconduit_ceiling.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
@@ -40,16 +43,17 @@ def build(verbose: bool = False) -> str:
     if not shutil.which(HIPCC) and not os.path.exists(HIPCC):
         raise RuntimeError("hipcc not found; the ROCm toolchain is required")
     os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,--no-undefined", *objs, "-o", tmp]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError(f"link failed:\n{res.stderr}")
-    os.replace(tmp, LIB)
-    if verbose:
-        print(f"built {LIB}")
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES) + 1)) as ex:
+        objs = list(ex.map(_compile, SOURCES + [CEILING_SRC]))
+    for lib, parts in ((LIB, objs[:-1]), (CEILING_LIB, objs[-1:])):
+        tmp = lib + ".tmp"
+        cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,--no-undefined", *parts, "-o", tmp]
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError(f"link failed:\n{res.stderr}")
+        os.replace(tmp, lib)
+        if verbose:
+            print(f"built {lib}")
     return LIB
 
 

@@ -250,3 +250,26 @@ def test_residual_workspace_sizes():
     proj = L.conduit_residual_workspace_bytes(ctypes.byref(kvd), 64, ctypes.byref(IMG.desc), 1, 0)
     assert iso > proj > 64 * 28 * 4
     assert L.conduit_residual_workspace_bytes(ctypes.byref(kvd), 0, ctypes.byref(IMG.desc), 5, 1) == 0
+
+
+def test_ceiling_reference_library():
+    """The benchmark's matrix-core reference (a separate library, not part of
+    the C ABI): it loads, sizes its operands and counts its FLOP without a
+    GPU, and rejects bad arguments before launching."""
+    path = os.path.join(ROOT, "paper_2609_05821_amd", "libconduit_ceiling.so")
+    if not os.path.exists(path):
+        pytest.skip("libconduit_ceiling.so not built")
+    L = ctypes.CDLL(path)
+    L.conduit_ceiling_ops_bytes.restype = ctypes.c_int64
+    L.conduit_ceiling_ops_bytes.argtypes = [ctypes.c_int32]
+    L.conduit_ceiling_flop.restype = ctypes.c_double
+    L.conduit_ceiling_flop.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    L.conduit_ceiling_mfma_bf16.restype = ctypes.c_int
+    L.conduit_ceiling_mfma_bf16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_void_p]
+    assert L.conduit_ceiling_ops_bytes(2) == 2 * 256 * 16 * 16
+    # 4 waves x 16 products of 2*32*32*16 FLOP per iteration and workgroup
+    assert L.conduit_ceiling_flop(3, 5) == 3 * 4 * 5 * 16 * 32768.0
+    assert L.conduit_ceiling_mfma_bf16(None, FAKE, 1, 1, None) != 0
+    assert L.conduit_ceiling_mfma_bf16(FAKE + 8, FAKE, 1, 1, None) != 0
+    assert L.conduit_ceiling_mfma_bf16(FAKE, FAKE, 0, 1, None) != 0
