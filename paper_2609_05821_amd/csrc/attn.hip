@@ -17,8 +17,9 @@
 //     with values, two 4-wave ones without) that walks the item list in
 //     snake order, so every CU gets a similar share of tiles.  Per 64-key
 //     tile, K is staged row-major and V row-major (read back through
-//     transposing LDS reads); with values by direct-to-LDS loads into a
-//     four-stage ring, statistics only through registers.  Each wave computes
+//     transposing LDS reads); with values by direct-to-LDS loads into five K
+//     and four V stages, two tiles per barrier; statistics only through
+//     registers, one tile per barrier.  Each wave computes
 //     S^T = K Q^T with v_mfma_f32_32x32x16_bf16 so that every lane holds 16
 //     keys of one pair column and the online softmax runs in-lane; the
 //     probabilities feed O^T = V^T P^T straight from the accumulator
@@ -52,14 +53,21 @@ struct TileGeom {
   static_assert(KT * kPitch * 2 % 1024 == 0 && KT * vPitch * 2 % 1024 == 0, "whole 1 KB transfers");
 };
 
-// With values: a four-stage ring of K and V tiles filled by direct-to-LDS
-// loads.  Statistics only: three register-staged K tiles and the image table.
-template <int D, bool PV>
-struct AttnSmem {
-  alignas(16) u16 k[PV ? 4 : 3][KT][TileGeom<D>::kPitch];
-  alignas(16) u16 v[PV ? 4 : 1][PV ? KT : 1][TileGeom<D>::vPitch];
+// With values: five K and four V tile stages filled by direct-to-LDS loads
+// (160.8 KB at d = 128).  Statistics only: three register-staged K tiles, the
+// key-domain bits and the image table.
+template <bool Stats>
+struct StatsLds {
   uint64_t okmask[3];  // key-domain filter per K tile, bit = key
   ImageLds img;        // visual-only statistics: the image table
+};
+template <>
+struct StatsLds<false> {};
+
+template <int D, bool PV>
+struct AttnSmem : StatsLds<!PV> {
+  alignas(16) u16 k[PV ? 5 : 3][KT][TileGeom<D>::kPitch];
+  alignas(16) u16 v[PV ? 4 : 1][PV ? KT : 1][TileGeom<D>::vPitch];
 };
 
 // One 1 KB direct-to-LDS transfer: lane l's 16 bytes at byte voff of the
@@ -331,7 +339,6 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   constexpr int kXferAll = Geo::kXfer + Geo::vXfer;
   constexpr uint32_t kPadOff = 0x80000000u;  // beyond any tile resource (< 2 GiB): reads as 0
   constexpr int kSlots = PV ? (kXferAll + W - 1) / W : 1;
-  const int n_mine = PV ? (kXferAll - wave + W - 1) / W : 0;  // transfers of this wave per tile
   uint32_t xoff0[kSlots];
 #pragma unroll
   for (int sl = 0; sl < kSlots; ++sl) {
@@ -349,9 +356,11 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const int n_items = uniform ? p.plan.uniform_items : min(p.plan.hdr[0], p.plan.max_items);
 
   const int grid = gridDim.x, g = blockIdx.x;
-  if (!PV && p.vis_only) {
-    image_table_to_lds(p.tbl, sm.img, tid, kThreads);
-    __syncthreads();
+  if constexpr (!PV) {
+    if (p.vis_only) {
+      image_table_to_lds(p.tbl, sm.img, tid, kThreads);
+      __syncthreads();
+    }
   }
 
   for (int round = 0;; ++round) {
@@ -535,6 +544,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     };
     auto row_of = [&](int t0) __attribute__((always_inline)) { return t0 < kend ? tile_row(t0) : (int64_t)0; };
     if constexpr (PV) {
+      // K(0..2), V(0..1); tiles past kend arrive as zeros
       const int64_t r0 = tile_row(kbeg), r1 = row_of(kbeg + KT), r2 = row_of(kbeg + 2 * KT);
       dma_tile(true, 0, kbeg, r0);
       dma_tile(false, 0, kbeg, r0);
@@ -602,35 +612,50 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         mx = sub_max(nxt);
       }
     };
-    constexpr int NKB = PV ? 4 : 3;
-    int t0 = kbeg, st = 0;  // K (and V) stage of tile t; stages follow mod NKB
-    for (;;) {
-      const bool more = t0 + KT < kend;
-      const int st1 = st + 1 == NKB ? 0 : st + 1;
-      if constexpr (PV) {
-        // V(t+2) and K(t+3); their stages last held tiles t-2 and t-1
-        const int st2 = st1 + 1 == NKB ? 0 : st1 + 1, st3 = st2 + 1 == NKB ? 0 : st2 + 1;
-        const int64_t rv2 = row_of(t0 + 2 * KT), rk3 = row_of(t0 + 3 * KT);
-        dma_tile(false, st2, t0 + 2 * KT, rv2);
-        dma_tile(true, st3, t0 + 3 * KT, rk3);
-      } else if (t0 + 2 * KT < kend) {
-        load_k(t0 + 2 * KT, tile_row(t0 + 2 * KT));
+    if constexpr (PV) {
+      // Two tiles (t, t+1) per barrier.  K stages rotate mod 5 and V stages
+      // mod 4: the iteration reads K(t..t+2) and V(t..t+1) while K(t+3),
+      // K(t+4), V(t+2) and V(t+3) arrive; they are awaited before the
+      // barrier, one iteration after they were issued.  A tile t+1 past kend
+      // arrives as zeros and is masked whole.
+      int t0 = kbeg, ks = 0, vs = 0;  // stages of tile t
+      for (;;) {
+        const int k1 = ks + 1 == 5 ? 0 : ks + 1, k2 = k1 + 1 == 5 ? 0 : k1 + 1;
+        const int k3 = k2 + 1 == 5 ? 0 : k2 + 1, k4 = k3 + 1 == 5 ? 0 : k3 + 1;
+        const int v1 = (vs + 1) & 3, v2 = (vs + 2) & 3, v3 = (vs + 3) & 3;
+        const bool more2 = t0 + 2 * KT < kend;  // the next iteration exists
+        const int64_t r2 = row_of(t0 + 2 * KT), r3 = row_of(t0 + 3 * KT), r4 = row_of(t0 + 4 * KT);
+        dma_tile(false, v2, t0 + 2 * KT, r2);
+        dma_tile(false, v3, t0 + 3 * KT, r3);
+        dma_tile(true, k3, t0 + 3 * KT, r3);
+        dma_tile(true, k4, t0 + 4 * KT, r4);
+        sub_step(sa, sb, ks, 1, vs, 0, true, t0);                // S(t,1)   | P(t,0) V
+        sub_step(sb, sa, k1, 0, vs, 1, true, t0 + KT);           // S(t+1,0) | P(t,1) V
+        sub_step(sa, sb, k1, 1, v1, 0, true, t0 + KT);           // S(t+1,1) | P(t+1,0) V
+        sub_step(sb, sa, k2, 0, v1, 1, more2, t0 + 2 * KT);      // S(t+2,0) | P(t+1,1) V
+        vm_wait<0>();
+        __syncthreads();
+        if (!more2) break;
+        t0 += 2 * KT;
+        ks = k2;
+        vs = v2;
       }
-      sub_step(sa, sb, st, 1, st, 0, true, t0);        // second half of tile t
-      sub_step(sb, sa, st1, 0, st, 1, more, t0 + KT);  // first half of tile t+1
-      if constexpr (PV) {
-        // the transfers issued one iteration ago (K(t+2), V(t+1)) have landed
-        if (n_mine == kSlots) vm_wait<kSlots>();
-        else vm_wait<kSlots - 1>();
-      } else if (t0 + 2 * KT < kend) {
-        store_k(st1 + 1 == NKB ? 0 : st1 + 1);
+    } else {
+      constexpr int NKB = 3;
+      int t0 = kbeg, st = 0;  // K stage of tile t; stages follow mod NKB
+      for (;;) {
+        const bool more = t0 + KT < kend;
+        const int st1 = st + 1 == NKB ? 0 : st + 1;
+        if (t0 + 2 * KT < kend) load_k(t0 + 2 * KT, tile_row(t0 + 2 * KT));
+        sub_step(sa, sb, st, 1, 0, 0, true, t0);        // second half of tile t
+        sub_step(sb, sa, st1, 0, 0, 1, more, t0 + KT);  // first half of tile t+1
+        if (t0 + 2 * KT < kend) store_k(st1 + 1 == NKB ? 0 : st1 + 1);
+        __syncthreads();
+        if (!more) break;
+        t0 += KT;
+        st = st1;
       }
-      __syncthreads();
-      if (!more) break;
-      t0 += KT;
-      st = st1;
     }
-    if constexpr (PV) vm_wait<0>();  // transfers of tiles past the end (zero-length) drained
 
     // ---- outputs: final values for a single-split block, else partials ----
     const float l_tot = l + __shfl_xor(l, 32, 64);
