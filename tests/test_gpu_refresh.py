@@ -113,6 +113,23 @@ def test_refresh_is_deterministic():
     np.testing.assert_array_equal(bits(l1), bits(l2))
 
 
+def test_split_merge_is_deterministic_at_16k():
+    """The 16k-token multi-image workload at its 10% budget: nearly every pair
+    block is cut into several key splits.  Three calls give the same bits (the
+    split merge sums in split order, no atomics), and a few merged rows match
+    the oracle."""
+    w = W.config(4, n_layers=1)
+    L = w.layer(0)
+    k = w.budgets["10%"]
+    rng = np.random.default_rng(61)
+    sel = np.sort(rng.choice(w.n_vis, size=k, replace=False))
+    runs = [run_refresh(w, L, sel) for _ in range(3)]
+    for o, l, _, _ in runs[1:]:
+        np.testing.assert_array_equal(bits(o), bits(runs[0][0]))
+        np.testing.assert_array_equal(bits(l), bits(runs[0][1]))
+    check(w, L, sel, rows=[0, k // 3, k - 1])
+
+
 def test_zero_budget_refresh_enqueues_nothing():
     w = W.config(2)
     L = w.layer(0, fresh=False)
