@@ -16,8 +16,9 @@
 //  2. attn_bf16_kernel runs a persistent grid (one 8-wave workgroup per CU
 //     with values, two 4-wave ones without) that walks the item list in
 //     snake order, so every CU gets a similar share of tiles.  Per 64-key
-//     tile, K is staged row-major and V row-major (read back through
-//     transposing LDS reads); with values by direct-to-LDS loads into five K
+//     tile, K is staged row-major and V row-major with its rows interleaved
+//     within 16-key blocks (read back through transposing LDS reads free of
+//     bank conflicts); with values by direct-to-LDS loads into five K
 //     and four V stages, two tiles per barrier; statistics only through
 //     registers, one tile per barrier.  Each wave computes
 //     S^T = K Q^T with v_mfma_f32_32x32x16_bf16 so that every lane holds 16
@@ -328,7 +329,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const u16 *Vg = static_cast<const u16 *>(p.v);
   const KvPageReader pr = page_reader(p.pages, p.n_ctx);
   using Geo = TileGeom<D>;
-  const int v_lane = v_operand_lane_offset<Geo::vPitch>(lane);  // PV operand reads
+  const int v_lane = v_operand_lane_offset_il<Geo::vPitch>(lane);  // PV operand reads (interleaved V rows)
   // Direct-to-LDS staging (with values): a tile's K transfers are numbered
   // 0..kXfer-1 and its V transfers kXfer..kXfer+vXfer-1; wave w issues
   // transfers w, w + 8, ...  Lane l of transfer x fills LDS byte 16 l of it,
@@ -346,7 +347,9 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     const bool isk = x < Geo::kXfer;
     const int pitch_b = 2 * (isk ? Geo::kPitch : Geo::vPitch);
     const int b = (isk ? x : x - Geo::kXfer) * 1024 + 16 * lane;
-    const int row = b / pitch_b, ch = (b % pitch_b) / 16;
+    const int lrow = b / pitch_b, ch = (b % pitch_b) / 16;
+    // V rows are stored interleaved: LDS row lrow holds this key of the tile
+    const int row = isk ? lrow : (lrow & ~15) | v_interleaved_key(lrow & 15);
     xoff0[sl] = ch < D / 8 ? (uint32_t)(((int64_t)row * (isk ? p.k_stride : p.v_stride) + 8 * ch) * 2) : kPadOff;
   }
   const u16 *Qg = static_cast<const u16 *>(p.q);
@@ -601,7 +604,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
           bf16x8 va[DT];
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
-            va[dt] = v_operand<Geo::vPitch>(&sm.v[vst][vsub * 32 + ks * 16][dt * 32] + v_lane);
+            va[dt] = v_operand_il<Geo::vPitch>(&sm.v[vst][vsub * 32 + ks * 16][dt * 32] + v_lane);
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
             o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[dt], pk[ks], o[dt], 0, 0, 0);

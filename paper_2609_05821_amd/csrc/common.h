@@ -203,6 +203,29 @@ __device__ __forceinline__ bf16x8 v_operand(const u16 *at) {
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
+// Interleaved V tile: key 8a + 4b + c of every 16-key block (a, b in {0, 1},
+// c in 0..3) is stored in row 8b + 2c + a of the block.  The four rows that
+// one 32-lane half of a transposing read touches are then two rows apart, so
+// with a row stride of 8 (mod 32) dwords they start 16 banks apart and cover
+// the 64 banks once (with the plain order every bank is hit twice).  The
+// operand registers are the same as with the plain order.
+__device__ __forceinline__ int v_interleaved_key(int row16) {
+  return 8 * (row16 & 1) + 4 * ((row16 >> 3) & 1) + ((row16 >> 1) & 3);
+}
+
+template <int VS>
+__device__ __forceinline__ int v_operand_lane_offset_il(int lane) {
+  const int s = lane & 15, h = lane >> 5, dgrp = (lane >> 4) & 1;
+  return (8 * h + 2 * (s >> 2)) * VS + 16 * dgrp + 4 * (s & 3);
+}
+
+template <int VS>
+__device__ __forceinline__ bf16x8 v_operand_il(const u16 *at) {
+  const short4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(at));
+  const short4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(at + VS));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
