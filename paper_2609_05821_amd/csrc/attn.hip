@@ -707,9 +707,18 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
 
 // Merge split partials of blocks with n_s > 1: M = max m_s,
 // L = sum l_s 2^(m_s - M), O = sum O_s 2^(m_s - M) / L, splits in order.
+// With values a thread merges 16 head dims of one pair (the whole grid is
+// resident at once); statistics only, one thread per pair.  The m_s, l_s and
+// O_s of up to kMergeBatch splits are loaded together and folded into a
+// running maximum, so a thread waits on two round trips to memory for
+// n_s <= kMergeBatch (plan entry, then the partials); for such blocks the
+// sums are exactly those of the two-pass formula above.
+constexpr int kMergeBatch = 4;
+constexpr int kMergeDims = 16;
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
-  constexpr int NC = D / 4;
+  constexpr int NC = D / kMergeDims;
+  constexpr int NQ = kMergeDims / 4;
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const bool values = p.part_o != nullptr;
@@ -726,15 +735,42 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   const int64_t slot0 = uniform ? ((int64_t)pb * (p.n_q_heads / p.group) + h) * ns
                                 : (int64_t)h * p.plan.hdr[1] + p.plan.pb_base[pb];
   if (slot0 + ns > p.plan.max_items) return;  // never for a plan within its bound
-  float M = kNegInf;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_m[(slot0 + s) * p.ppb + j]);
-  float L = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < ns; ++s) {
-    const int64_t idx = (slot0 + s) * p.ppb + j;
-    const float w = fast_exp2(p.part_m[idx] - M);  // m >= kMInit is finite
-    L += w * p.part_l[idx];
-    if (values) acc += w * *reinterpret_cast<const f32x4 *>(p.part_o + idx * D + 4 * c);
+  const int64_t idx0 = slot0 * p.ppb + j;
+  float M = kNegInf, L = 0.f;
+  f32x4 acc[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < ns; s0 += kMergeBatch) {
+    float mb[kMergeBatch], lb[kMergeBatch];
+    f32x4 ob[kMergeBatch][NQ];
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const bool in = s0 + i < ns;
+      const int64_t idx = idx0 + (int64_t)(s0 + i) * p.ppb;
+      mb[i] = in ? p.part_m[idx] : kNegInf;
+      lb[i] = in ? p.part_l[idx] : 0.f;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        ob[i][q] = in && values ? *reinterpret_cast<const f32x4 *>(p.part_o + idx * D + kMergeDims * c + 4 * q)
+                                : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    float Mn = M;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) Mn = fmaxf(Mn, mb[i]);  // finite: split s0 exists
+    const float rs = fast_exp2(M - Mn);                             // 0 on the first batch
+    L *= rs;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) acc[q] *= rs;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      if (s0 + i < ns) {
+        const float w = fast_exp2(mb[i] - Mn);  // m >= kMInit is finite
+        L += w * lb[i];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) acc[q] += w * ob[i][q];
+      }
+    }
+    M = Mn;
   }
   const float b = M + __log2f(L);
   if (c == 0) {
@@ -743,11 +779,14 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   }
   if (values) {
     const float inv = 1.f / L;
-    u16 *out = static_cast<u16 *>(p.o_out) + gp * D + 4 * c;
-    uint2 w;
-    w.x = (uint32_t)f32_to_bf16(acc[0] * inv) | ((uint32_t)f32_to_bf16(acc[1] * inv) << 16);
-    w.y = (uint32_t)f32_to_bf16(acc[2] * inv) | ((uint32_t)f32_to_bf16(acc[3] * inv) << 16);
-    *reinterpret_cast<uint2 *>(out) = w;
+    u16 *out = static_cast<u16 *>(p.o_out) + gp * D + kMergeDims * c;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      uint2 w;
+      w.x = (uint32_t)f32_to_bf16(acc[q][0] * inv) | ((uint32_t)f32_to_bf16(acc[q][1] * inv) << 16);
+      w.y = (uint32_t)f32_to_bf16(acc[q][2] * inv) | ((uint32_t)f32_to_bf16(acc[q][3] * inv) << 16);
+      *reinterpret_cast<uint2 *>(out + 4 * q) = w;
+    }
   }
 }
 
@@ -906,7 +945,7 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
   cp.lse_out = p.lse_out;
   cp.o_out = with_values ? p.o_out : nullptr;
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
-  const int64_t n = with_values ? n_gp * (head_dim / 4) : n_gp;
+  const int64_t n = with_values ? n_gp * (head_dim / kMergeDims) : n_gp;
   const int blocks = (int)((n + 255) / 256);
   ProfScope ps("attn_merge", s);
   if (head_dim == 128) combine_kernel<128><<<blocks, 256, 0, s>>>(cp);
