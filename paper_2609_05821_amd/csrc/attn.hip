@@ -717,6 +717,7 @@ constexpr int kMergeBatch = 4;
 constexpr int kMergeDims = 16;
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
+  static_assert(D % kMergeDims == 0, "whole 16-dim slices");
   constexpr int NC = D / kMergeDims;
   constexpr int NQ = kMergeDims / 4;
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
