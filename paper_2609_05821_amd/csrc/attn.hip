@@ -904,7 +904,7 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
   pa.n_kv_heads = p.n_kv_heads;
   pa.n_ctx = p.n_ctx;
   pa.ppb = ppb;
-  pa.target_items = attn_grid(with_values) * attn_plan_rounds(with_values);
+  pa.target_items = (int32_t)attn_plan_target(p.plan.n_pb, p.n_kv_heads, with_values);
   pa.plan = p.plan;
   hipError_t e = hipSuccess;
   if (p.plan.uniform_ns == 0) {

@@ -475,10 +475,18 @@ constexpr int attn_grid(bool with_values) { return with_values ? 256 : 512; }
 constexpr int attn_plan_rounds(bool with_values) { return with_values ? 2 : 1; }
 constexpr int kAttnPlanMinTiles = 8;     // smallest split, in key tiles
 constexpr int kAttnPlanMaxBlocks = 4096; // pair blocks per KV head the planner holds
+// Items the plan aims at: `rounds` per grid slot; with values also at least
+// two per pair block and KV head, so that long causal ranges are always cut
+// (with more blocks than the grid takes per round and no splits, one block
+// longer than a workgroup's share of the tiles sets the kernel's time).
+constexpr int64_t attn_plan_target(int64_t n_pb, int64_t n_kv_heads, bool with_values) {
+  const int64_t base = (int64_t)attn_grid(with_values) * attn_plan_rounds(with_values);
+  return with_values && 2 * n_pb * n_kv_heads > base ? 2 * n_pb * n_kv_heads : base;
+}
 // Upper bound on the items of one plan: sum_b ceil(tiles_b / T) over blocks
-// and KV heads, with T >= total tiles / (grid * rounds).
+// and KV heads, with T >= total tiles / target.
 constexpr int64_t attn_max_items(int64_t n_pb, int64_t n_kv_heads, bool with_values) {
-  return (int64_t)attn_grid(with_values) * attn_plan_rounds(with_values) + n_pb * n_kv_heads;
+  return attn_plan_target(n_pb, n_kv_heads, with_values) + n_pb * n_kv_heads;
 }
 constexpr int kAttnKeyTile = 64;         // keys per LDS tile
 constexpr int64_t kMaxStrideBytes = int64_t(1) << 25;  // row strides below 32 MiB: a key tile spans < 2 GiB
