@@ -7,8 +7,9 @@
 //  2. g_bar and c_j = (1 - lambda) + lambda g_j / g_bar  (c_j = 1 if g_bar = 0);
 //  3. s_hat_t = (s_t / |L|) c_pi(t), written once;
 //  4. the k-th largest s_hat by radix select on the fp32 bit patterns
-//     (s_hat >= 0, so unsigned bit order is value order): 11 + 11 + 10 bit
-//     passes with LDS histograms (integer atomics: exact);
+//     (s_hat >= 0, so unsigned bit order is value order): the bits every key
+//     shares first (block AND/OR), then 11-bit passes over the rest with LDS
+//     histograms (integer atomics: exact);
 //  5. ordered compaction: everything above the threshold plus the first
 //     `need` entries equal to it in index order (ties to the lower index),
 //     with one block scan of both counts, so idx/pos come out ascending.
@@ -102,22 +103,32 @@ __device__ uint32_t block_or(uint32_t x, int *s_wave) {
   return r;
 }
 
+constexpr int kSelBatch = 8;  // strided scores loaded together per thread
+constexpr int kSelSeg = 16;   // consecutive scores loaded together in the compaction
 __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, ImageTable tbl) {
   __shared__ float s_g[kMaxImages];
   __shared__ float s_c[kMaxImages];
   __shared__ int hist[2048];
   __shared__ int s_wave[kWaves];
+  __shared__ int s_wave2[kWaves];
   __shared__ int s_bin, s_above;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = tbl.n_vis, K = tbl.n_images;
   const float n_layers = (float)p.n_layers;
 
-  // 1. per-image mean attention
+  // 1. per-image mean attention (each lane sums its tokens in order)
   for (int j = wave; j < K; j += kWaves) {
     const int lo = tbl.off[j], hi = tbl.off[j + 1];
     float acc = 0.f;
-    for (int t = lo + lane; t < hi; t += 64) acc += p.a_acc[t];
+    for (int t0 = lo + lane; t0 < hi; t0 += 64 * kSelBatch) {
+      float v[kSelBatch];
+#pragma unroll
+      for (int u = 0; u < kSelBatch; ++u) v[u] = t0 + 64 * u < hi ? p.a_acc[t0 + 64 * u] : 0.f;
+#pragma unroll
+      for (int u = 0; u < kSelBatch; ++u)
+        if (t0 + 64 * u < hi) acc += v[u];
+    }
     acc = wave_sum(acc);
     if (lane == 0) s_g[j] = acc / (n_layers * (float)(hi - lo));
   }
@@ -142,23 +153,60 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Ima
   for (int j = wave; j < K; j += kWaves) {
     const int lo = tbl.off[j], hi = tbl.off[j + 1];
     const float c = s_c[j];
-    for (int t = lo + lane; t < hi; t += 64) p.shat[t] = (p.s_acc[t] / n_layers) * c;
+    for (int t0 = lo + lane; t0 < hi; t0 += 64 * kSelBatch) {
+      float v[kSelBatch];
+#pragma unroll
+      for (int u = 0; u < kSelBatch; ++u) v[u] = t0 + 64 * u < hi ? p.s_acc[t0 + 64 * u] : 0.f;
+#pragma unroll
+      for (int u = 0; u < kSelBatch; ++u)
+        if (t0 + 64 * u < hi) p.shat[t0 + 64 * u] = (v[u] / n_layers) * c;
+    }
   }
   __syncthreads();
 
-  // 4. radix select of the k-th largest key
-  uint32_t prefix = 0, pmask = 0;
-  int kk = p.k;
-  const int shifts[3] = {21, 10, 0};
-  const int nbins[3] = {2048, 2048, 1024};
+  // 4. radix select of the k-th largest key.  The bits every key shares
+  // come first (block AND/OR); the rest are resolved 11 bits per pass, so
+  // the first digit spreads over the bits that vary (scores in a narrow
+  // range share their sign and high exponent bits, and a digit made of
+  // those would send nearly every LDS atomic to a few bins).
+  // Loops over the scores load kSelBatch of them before using any (one
+  // memory round trip per batch instead of one per score).
+  uint32_t k_and = 0xffffffffu, k_or = 0;
+  for (int t0 = tid; t0 < n; t0 += kSelBatch * kSelThreads) {
+    float v[kSelBatch];
 #pragma unroll
-  for (int pass = 0; pass < 3; ++pass) {
-    const int sh = shifts[pass], nb = nbins[pass];
+    for (int u = 0; u < kSelBatch; ++u) v[u] = t0 + u * kSelThreads < n ? p.shat[t0 + u * kSelThreads] : 0.f;
+#pragma unroll
+    for (int u = 0; u < kSelBatch; ++u)
+      if (t0 + u * kSelThreads < n) {
+        const uint32_t key = order_key(v[u]);
+        k_and &= key;
+        k_or |= key;
+      }
+  }
+  block_and_or(k_and, k_or, s_wave, s_wave2);
+  const uint32_t varying = k_and ^ k_or;
+  uint32_t prefix = k_and, pmask = 0xffffffffu;
+  int kk = p.k;
+  const int top = varying ? 31 - __builtin_clz(varying) : -1;
+  if (varying) {
+    pmask = top == 31 ? 0u : ~((2u << top) - 1u);  // shared high bits
+    prefix = k_and & pmask;
+  }
+  for (int hi = top; hi >= 0; hi -= 11) {  // digit = bits hi .. hi-10 (fewer at the end)
+    const int sh = hi - 10, nb = 2048;
     for (int b = tid; b < nb; b += kSelThreads) hist[b] = 0;
     __syncthreads();
-    for (int t = tid; t < n; t += kSelThreads) {
-      const uint32_t key = order_key(p.shat[t]);
-      if ((key & pmask) == prefix) atomicAdd(&hist[(key >> sh) & (nb - 1)], 1);
+    for (int t0 = tid; t0 < n; t0 += kSelBatch * kSelThreads) {
+      float v[kSelBatch];
+#pragma unroll
+      for (int u = 0; u < kSelBatch; ++u) v[u] = t0 + u * kSelThreads < n ? p.shat[t0 + u * kSelThreads] : 0.f;
+#pragma unroll
+      for (int u = 0; u < kSelBatch; ++u) {
+        const uint32_t key = order_key(v[u]);
+        if (t0 + u * kSelThreads < n && (key & pmask) == prefix)
+          atomicAdd(&hist[(sh >= 0 ? key >> sh : key << (-sh)) & (nb - 1)], 1);
+      }
     }
     __syncthreads();
     // thread tid owns bins in descending order: nb-1-per*tid .. nb-per*(tid+1)
@@ -177,8 +225,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Ima
       run += h;
     }
     __syncthreads();
-    prefix |= (uint32_t)s_bin << sh;
-    pmask |= (uint32_t)(nb - 1) << sh;
+    if (sh >= 0) {
+      prefix |= (uint32_t)s_bin << sh;
+      pmask |= (uint32_t)(nb - 1) << sh;
+    } else {  // last, partial digit
+      prefix |= (uint32_t)s_bin >> (-sh);
+      pmask |= (uint32_t)(nb - 1) >> (-sh);
+    }
     kk -= s_above;
     __syncthreads();
   }
@@ -189,10 +242,17 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Ima
   const int seg = (n + kSelThreads - 1) / kSelThreads;
   const int lo = min(n, tid * seg), hi = min(n, lo + seg);
   int gt = 0, eq = 0;
-  for (int t = lo; t < hi; ++t) {
-    const uint32_t key = order_key(p.shat[t]);
-    gt += key > tau;
-    eq += key == tau;
+  for (int t0 = lo; t0 < hi; t0 += kSelSeg) {
+    float v[kSelSeg];
+#pragma unroll
+    for (int u = 0; u < kSelSeg; ++u) v[u] = t0 + u < hi ? p.shat[t0 + u] : 0.f;
+#pragma unroll
+    for (int u = 0; u < kSelSeg; ++u)
+      if (t0 + u < hi) {
+        const uint32_t key = order_key(v[u]);
+        gt += key > tau;
+        eq += key == tau;
+      }
   }
   int total;
   const int eq_before = block_exclusive_scan(eq, s_wave, total);
@@ -208,19 +268,27 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p, Ima
     j = a;
   }
   int eq_seen = 0;
-  for (int t = lo; t < hi; ++t) {
-    while (t >= tbl.off[j + 1]) ++j;
-    const uint32_t key = order_key(p.shat[t]);
-    bool sel = key > tau;
-    if (key == tau) {
-      sel = eq_seen < take_eq;
-      ++eq_seen;
-    }
-    if (p.mask_out) p.mask_out[t] = sel ? 1 : 0;
-    if (sel && out < p.k) {
-      p.idx_out[out] = t;
-      p.pos_out[out] = tbl.pos[j] + (t - tbl.off[j]);
-      ++out;
+  for (int t0 = lo; t0 < hi; t0 += kSelSeg) {
+    float v[kSelSeg];
+#pragma unroll
+    for (int u = 0; u < kSelSeg; ++u) v[u] = t0 + u < hi ? p.shat[t0 + u] : 0.f;
+#pragma unroll
+    for (int u = 0; u < kSelSeg; ++u) {
+      const int t = t0 + u;
+      if (t >= hi) break;
+      while (t >= tbl.off[j + 1]) ++j;
+      const uint32_t key = order_key(v[u]);
+      bool sel = key > tau;
+      if (key == tau) {
+        sel = eq_seen < take_eq;
+        ++eq_seen;
+      }
+      if (p.mask_out) p.mask_out[t] = sel ? 1 : 0;
+      if (sel && out < p.k) {
+        p.idx_out[out] = t;
+        p.pos_out[out] = tbl.pos[j] + (t - tbl.off[j]);
+        ++out;
+      }
     }
   }
 }

@@ -97,6 +97,19 @@ def test_ties_go_to_lower_index(n):
         np.testing.assert_array_equal(got["idx"][:k], ref_idx)
 
 
+@pytest.mark.parametrize("n", [1000, 65536])
+def test_all_equal_scores_take_lowest_indices(n):
+    """No bit varies between the keys: the threshold is the common value and
+    the k lowest indices are taken (both the register-resident and the
+    streaming kernel)."""
+    img_pos, img_off = layout([n])
+    s = np.full(n, 0.25)
+    for k in (1, 100, n):
+        got = run_select(s, np.ones(n), 1, img_pos, img_off, 1.0, k)
+        np.testing.assert_array_equal(got["idx"][:k], np.arange(k))
+        assert got["mask"].sum() == k
+
+
 def test_single_image_coefficient_is_one():
     rng = np.random.default_rng(1)
     img_pos, img_off = layout([777])
