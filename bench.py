@@ -484,10 +484,18 @@ def pct(v, q):
     return xs[min(len(xs) - 1, max(0, int(round(q / 100.0 * (len(xs) - 1)))))]
 
 
-def source_digest(path):
+def source_digest(paths):
+    """First 16 hex digits of the SHA-256 of the files' bytes, in order."""
     import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+# Sources that decide the refresh kernel's code and tiling.
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_05821_amd", "csrc", f) for f in ("attn.hip", "common.h")]
 
 
 def traffic_from_profile():
@@ -496,7 +504,6 @@ def traffic_from_profile():
     recorded there; None when the summary is missing or was taken on another
     version of the kernel source."""
     path = os.path.join(ROOT, "profiles", "attn_values_16k_traffic.md")
-    src = os.path.join(ROOT, "paper_2609_05821_amd", "csrc", "attn.hip")
     try:
         text = open(path).read()
     except OSError:
@@ -506,7 +513,7 @@ def traffic_from_profile():
     if not m:
         return None
     rec = json.loads(m.group(1))
-    if rec.get("attn_hip_sha256_16") != source_digest(src):
+    if rec.get("kernel_sources_sha256_16") != source_digest(KERNEL_SOURCES):
         return None
     return rec.get("traffic_bytes_per_launch")
 

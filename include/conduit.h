@@ -200,7 +200,7 @@ conduit_status conduit_value_norms(const conduit_kv *kv, const conduit_images *i
  * rule          CONDUIT_RANK_COMPOSITE: the global top-k of
  *               s_hat_t = (s_acc_t / n_layers) * c_pi(t) (Eq. 10-11).
  *               CONDUIT_RANK_ATTENTION: the same with a_acc in place of s_acc
- *               (the value-norm factor dropped, Table 9's ablation).
+ *               (the value-norm factor dropped, Table 5's factor ablation).
  *               CONDUIT_RANK_EXPLICIT: quotas k_j proportional to c_j * n_j
  *               (largest remainder, float32 in image order, capped at n_j
  *               with the surplus re-apportioned, ties to the lower image; all

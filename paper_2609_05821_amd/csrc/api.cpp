@@ -595,7 +595,7 @@ conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32
     return ok();
   }
   SelectParams sp{};
-  // The attention-only rule ranks A where the composite ranks s (Table 9).
+  // The attention-only rule ranks A where the composite ranks s (Table 5's drop-value-norm ablation).
   sp.s_acc = rule == CONDUIT_RANK_ATTENTION ? a_acc : s_acc;
   sp.a_acc = a_acc;
   sp.n_layers = n_layers;

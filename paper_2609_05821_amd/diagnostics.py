@@ -71,7 +71,14 @@ def rule_errors(kv: api.KV, q: torch.Tensor, q_pos0: int, img: api.ImageTable,
                 z: Optional[torch.Tensor], ratios: Sequence = RATIOS, kappa: float = 0.5,
                 lam: float = 1.0, seed: int = 0) -> dict:
     """Projected error and isotropic estimate of every rule at every ratio,
-    and the reductions against random and TopK(||V||) selection."""
+    and the reductions against random and TopK(||V||) selection.
+
+    The library returns one residual per (sample, span row, query head).  The
+    two reductions over those entries are harness arithmetic on the host, in
+    float64 after the copy back: the projected error of App. D.3 sums the
+    final span row's heads, and the isotropic estimate of App. D.1 is the mean
+    over samples, rows and heads.  They are a few thousand additions per rule
+    and ratio and are not part of the refresh step."""
     n_q = q.shape[0]
     sc = layer_scores(kv, q, q_pos0, img)
     q_last = q[n_q - 1:].contiguous()
@@ -88,10 +95,12 @@ def rule_errors(kv: api.KV, q: torch.Tensor, q_pos0: int, img: api.ImageTable,
         masks = rule_masks(kv, q, q_pos0, img, k, sc, seed=seed * 1000 + ri, lam=lam)
         for name in RULES:
             api.conduit_residual_error(kv, q_last, q_pos0 + n_q - 1, img, lse_last, masks[name], err_p)
+            # host-side harness reduction (App. D.3): sum over the final row's heads
             res["projected"][name].append(float(err_p.cpu().numpy().astype(np.float64).sum()))
             if err_i is not None:
                 api.conduit_residual_error(kv, q, q_pos0, img, sc["lse"], masks[name], err_i, z=z,
                                            kappa=kappa)
+                # host-side harness reduction (App. D.1): mean over samples, rows, heads
                 res["iso"][name].append(float(err_i.cpu().numpy().astype(np.float64).mean()))
     for est in ("projected", "iso"):
         e = res[est]

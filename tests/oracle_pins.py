@@ -5,6 +5,9 @@ any exception) when the oracle is wrong, so the same pins can be run against
 deliberately broken copies of the oracle (see test_oracle_mutations.py).
 
 What pins what:
+  * bf16 inputs          hand-worked bit patterns (sign, exponent, mantissa
+                          fields; subnormal, largest finite, infinities) and
+                          random patterns against torch's bfloat16 decoder;
   * budget (Eq. 2)       exact rational floor via fractions.Fraction, and the
                           hand-computed budgets of the workloads;
   * scoring (Eq. 6)      a hand-worked example, closed forms for equal keys,
@@ -114,6 +117,40 @@ def _sdpa_out(q, k, v, mask):
 
 
 # ---------------------------------------------------------------------------
+
+def pin_bf16_decode(o):
+    """bf16 inputs are decoded by the oracle itself (uint16 bit patterns: the
+    top half of an IEEE binary32).  Hand-worked patterns (sign, 8 exponent
+    bits, 7 mantissa bits) and random patterns against torch's own bfloat16
+    decoder."""
+    cases = {
+        0x3F80: 1.0,                          # exponent 127, mantissa 0
+        0xC040: -3.0,                         # sign, exponent 128, mantissa 1/2 -> -1.5 * 2
+        0x3E80: 0.25,                         # exponent 125
+        0x4049: 3.140625,                     # exponent 128, mantissa 73/128
+        0x0001: 2.0 ** -133,                  # smallest subnormal: 2^-7 * 2^-126
+        0x7F7F: (2.0 - 2.0 ** -7) * 2.0 ** 127,  # largest finite
+        0x0080: 2.0 ** -126,                  # smallest normal
+        0x7F80: math.inf,
+        0xFF80: -math.inf,
+    }
+    bits = np.array(list(cases), dtype=np.uint16)
+    got = o.to_f64(bits)
+    assert got.dtype == np.float64
+    for b, want, g in zip(cases, cases.values(), got):
+        assert g == want, (hex(b), g, want)
+    neg_zero = o.to_f64(np.array([0x8000], dtype=np.uint16))[0]
+    assert neg_zero == 0.0 and math.copysign(1.0, neg_zero) < 0
+    rng = np.random.default_rng(11)
+    r = rng.integers(0, 1 << 16, size=(64, 3, 8), dtype=np.uint16)
+    r = np.where((r & 0x7F80) == 0x7F80, r & 0x807F, r)  # no inf/NaN patterns
+    ref = torch.from_numpy(r.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    got = o.to_f64(r)
+    assert got.shape == r.shape
+    assert np.array_equal(got, ref)
+    f = rng.standard_normal(17).astype(np.float32)
+    assert np.array_equal(o.to_f64(f), f.astype(np.float64))
+
 
 def pin_budget(o):
     gold = _golden()["budget"]["cases"]

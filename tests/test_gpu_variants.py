@@ -1,6 +1,6 @@
 """The scoring and selection variants on the GPU against the CPU oracle:
 RMS aggregation (Eq. 4), the value-norm table (Sec. 4.3), the attention-only
-and explicit-quota rules (Table 9, App. D), and scored-layer subsets."""
+and explicit-quota rules (Table 5 for attention only, App. D for explicit quotas), and scored-layer subsets."""
 import zlib
 
 import numpy as np

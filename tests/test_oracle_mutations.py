@@ -14,6 +14,10 @@ from oracle import conduit_oracle
 from tests import oracle_pins
 
 MUTATIONS = {
+    "bf16_shift_15": ("return (x.astype(np.uint32) << 16).view(np.float32)",
+                      "return (x.astype(np.uint32) << 15).view(np.float32)"),
+    "bf16_as_float16": ("return (x.astype(np.uint32) << 16).view(np.float32).astype(np.float64)",
+                        "return x.view(np.float16).astype(np.float64)"),
     "scale_1_over_d": ("scale = 1.0 / np.sqrt(d)", "scale = 1.0 / d", 3),
     "gqa_modulo_mapping": ("kv = h // group", "kv = h % n_kv_heads", 3),
     "causal_excludes_self": ("k_cache[: p + 1, kv, :], scale)\n                alpha = alpha[P_vis]",
