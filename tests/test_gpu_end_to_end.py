@@ -7,7 +7,7 @@ import torch
 from oracle import conduit_oracle as O
 from paper_2609_05821_amd import api, workloads as W
 from tests.gpu_helpers import (DEV, assert_attention, assert_scores, assert_selection, bits,
-                               to_dev, to_f64)
+                               oracle_refresh_rows, to_dev, to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -26,10 +26,12 @@ def run_step(w, layers_np, k, lam=1.0, norm=O.NORM_CAUSAL_ROW):
     return step, layers, idx
 
 
-@pytest.mark.parametrize("cfg,n_layers,budget,sample",
-                         [(1, 1, "10%", None), (1, 1, "10%-stated", None), (2, 1, "10%", None),
-                          (3, 3, "20%", 12), (4, 1, "10%", 24)])
-def test_refresh_step_matches_oracle(cfg, n_layers, budget, sample):
+@pytest.mark.parametrize("cfg,n_layers,budget",
+                         [(1, 1, "10%"), (1, 1, "10%-stated"), (2, 1, "10%"),
+                          (3, 3, "5%"), (3, 3, "10%"), (3, 3, "20%"), (4, 1, "10%")])
+def test_refresh_step_matches_oracle(cfg, n_layers, budget):
+    """Every refreshed row of every layer is compared with the oracle (the
+    16k workload: all 1,638 rows, in the benchmark's launch configuration)."""
     w = W.config(cfg, n_layers=n_layers)
     k = w.budgets[budget]
     layers_np = [w.layer(li) for li in range(n_layers)]
@@ -44,16 +46,11 @@ def test_refresh_step_matches_oracle(cfg, n_layers, budget, sample):
     mask = np.zeros(w.n_vis, np.uint8)
     mask[idx] = 1
     np.testing.assert_array_equal(step.mask.cpu().numpy(), mask)
-    rows = None
-    if sample:
-        rng = np.random.default_rng(cfg)
-        rows = sorted(set([0, k - 1] + rng.choice(k, size=sample, replace=False).tolist()))
     for li, L in enumerate(layers_np):
-        km, vm, o_ref, lse_ref = O.refresh_layer(L["k"], L["v"], P[idx], L["k_star"][idx],
-                                                 L["v_star"][idx], L["q_star"][idx], rows=rows)
-        r = slice(None) if rows is None else np.asarray(rows)
-        assert_attention(to_f64(step.out[li][:k])[r], o_ref[r], w.dtype, what=f"O layer {li}")
-        assert_scores(to_f64(step.lse[li][:k])[r], lse_ref[r], what=f"lse layer {li}")
+        km, vm, o_ref, lse_ref = oracle_refresh_rows(L["k"], L["v"], P[idx], L["k_star"][idx],
+                                                     L["v_star"][idx], L["q_star"][idx], range(k))
+        assert_attention(to_f64(step.out[li][:k]), o_ref, w.dtype, what=f"O layer {li}")
+        assert_scores(to_f64(step.lse[li][:k]), lse_ref, what=f"lse layer {li}")
         np.testing.assert_array_equal(to_f64(layers[li]["k"]), km)
         np.testing.assert_array_equal(to_f64(layers[li]["v"]), vm)
 

@@ -6,7 +6,8 @@ import torch
 
 from oracle import conduit_oracle as O
 from paper_2609_05821_amd import api, workloads as W
-from tests.gpu_helpers import DEV, assert_attention, assert_scores, bits, to_dev, to_f64
+from tests.gpu_helpers import (DEV, assert_attention, assert_scores, bits, oracle_refresh_rows, to_dev,
+                               to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -29,8 +30,8 @@ def run_refresh(w, L, sel):
 def check(w, L, sel, rows=None):
     out, lse, kc, vc = run_refresh(w, L, sel)
     P = w.vis_positions()
-    km, vm, o_ref, lse_ref = O.refresh_layer(L["k"], L["v"], P[sel], L["k_star"][sel],
-                                             L["v_star"][sel], L["q_star"][sel], rows=rows)
+    km, vm, o_ref, lse_ref = oracle_refresh_rows(L["k"], L["v"], P[sel], L["k_star"][sel], L["v_star"][sel],
+                                                 L["q_star"][sel], range(len(sel)) if rows is None else rows)
     r = slice(None) if rows is None else np.asarray(rows)
     assert_attention(to_f64(out)[r], o_ref[r], w.dtype, what="O")
     assert_scores(to_f64(lse)[r], lse_ref[r], what="lse")
@@ -86,9 +87,9 @@ def test_full_budget_equals_full_prefill(case):
     assert_attention(to_f64(out), dense[P], w.dtype, what="O vs full prefill")
 
 
-def test_refresh_16k_workload_sampled_rows():
+def test_refresh_16k_workload_every_row():
     """The 16,384-visual-token layer at a 10% budget in the benchmark's launch
-    shape; rows checked one by one by the oracle on a sample."""
+    shape; every one of the 1,638 rows checked by the oracle."""
     w = W.config(4)
     L = w.layer(0)
     rng = np.random.default_rng(44)
@@ -99,8 +100,20 @@ def test_refresh_16k_workload_sampled_rows():
     sel = np.sort(np.concatenate([rng.choice(pool, size=k // 2, replace=False),
                                   rng.choice(np.setdiff1d(np.arange(w.n_vis), pool), size=k - k // 2,
                                              replace=False)]))
-    rows = sorted(set([0, 1, k // 2, k - 2, k - 1] + rng.choice(k, size=27, replace=False).tolist()))
-    check(w, L, sel, rows=rows)
+    check(w, L, sel)
+
+
+@pytest.mark.parametrize("k", [2400, 3000])
+def test_refresh_many_blocks_short_context(k):
+    """More pair blocks than the persistent grid takes per round (k * 7 / 256 >
+    64 blocks per KV head): the plan then aims at two items per block and KV
+    head, so even short causal ranges are cut into splits and merged.  Every
+    row is checked by the oracle."""
+    w = W.custom(1, 28, 4, 128, 8, 96, [1024, 1024, 1024, 1024], 16, "bf16", n_relevant=1, seed=71)
+    L = w.layer(0)
+    rng = np.random.default_rng(k)
+    sel = np.sort(rng.choice(w.n_vis, size=k, replace=False))
+    check(w, L, sel)
 
 
 def test_refresh_is_deterministic():

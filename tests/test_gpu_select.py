@@ -51,6 +51,9 @@ SIZES = {
     "single_image_ragged": [1000],
     "three_images": [37, 250, 301],
     "sixteen_images": [1024] * 16,
+    # 16,385 .. 32,768 keys: 32 keys per thread in registers
+    "twenty_four_images_ragged": [1024] * 23 + [999],
+    "thirty_two_images": [1024] * 32,
     "long_document": [1024] * 64,
     "many_small": [7] * 256,
 }
@@ -84,7 +87,7 @@ def test_select_matches_oracle(name, lam):
         np.testing.assert_array_equal(got["mask"], m)
 
 
-@pytest.mark.parametrize("n", [5, 1000, 16384, 65536, 100000])
+@pytest.mark.parametrize("n", [5, 1000, 16384, 16385, 24576, 32767, 32768, 65536, 100000])
 def test_ties_go_to_lower_index(n):
     """Heavy ties: few distinct scores, so the boundary value repeats often."""
     rng = np.random.default_rng(n)
@@ -97,14 +100,14 @@ def test_ties_go_to_lower_index(n):
         np.testing.assert_array_equal(got["idx"][:k], ref_idx)
 
 
-@pytest.mark.parametrize("n", [1000, 65536])
+@pytest.mark.parametrize("n", [1000, 16385, 32768, 65536])
 def test_all_equal_scores_take_lowest_indices(n):
     """No bit varies between the keys: the threshold is the common value and
     the k lowest indices are taken (both the register-resident and the
     streaming kernel)."""
     img_pos, img_off = layout([n])
     s = np.full(n, 0.25)
-    for k in (1, 100, n):
+    for k in sorted({1, 100, n - 1, n}):
         got = run_select(s, np.ones(n), 1, img_pos, img_off, 1.0, k)
         np.testing.assert_array_equal(got["idx"][:k], np.arange(k))
         assert got["mask"].sum() == k
