@@ -176,6 +176,35 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
                              void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ *
+ * Allocation-free scoring pass: conduit_score with the library's own fixed
+ * device scratch in place of (ws, ws_bytes).  For callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the call itself makes no hipMalloc,
+ * hipFree or other allocating call; every other argument, the kernels and
+ * the results are those of conduit_score, bit for bit.
+ *
+ * The scratch is one array of CONDUIT_SCORE_NOALLOC_MAX_BYTES per GPU the
+ * library is loaded on, held until the process ends; its address is looked
+ * up on the first call on each device (with that device current).  Every
+ * call on a GPU shares that GPU's array and leaves its contents behind (no
+ * part of it needs to start at zero: each launch writes what the next one
+ * reads), so calls that overlap on one GPU (on different streams, or from
+ * different threads) race and must be serialised by the caller.
+ *
+ * Errors: those of conduit_score, and CONDUIT_ERR_UNSUPPORTED when
+ * conduit_score_workspace_bytes(kv, n_q, img) exceeds
+ * CONDUIT_SCORE_NOALLOC_MAX_BYTES (nothing is enqueued; use conduit_score).
+ * With kernel timing enabled, the timing events are created on first use.
+ * ------------------------------------------------------------------------ */
+#define CONDUIT_SCORE_NOALLOC_MAX_BYTES ((size_t)16 << 20)
+
+conduit_status conduit_score_noalloc(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
+                                     const conduit_images *img, conduit_norm norm, conduit_agg agg,
+                                     float scale, const float *row_lse_in, float *row_lse_out,
+                                     const float *vnorm_in, float *s_acc, float *a_acc, int32_t accumulate,
+                                     float *a_out, float *vnorm_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ *
  * Value-norm table of one layer (Eq. 7's proxy; Sec. 4.3: the norms depend on
  * the cache only, so storing one scalar per visual token and layer when the
  * cache is built preserves the scores exactly and removes the V reads from

@@ -31,8 +31,9 @@ EXPORTS = [
     "conduit_refresh_workspace_bytes", "conduit_refresh_attn", "conduit_status_str",
     "conduit_last_error", "conduit_version", "conduit_profile_enable", "conduit_profile_count",
     "conduit_profile_read", "conduit_value_norms", "conduit_residual_workspace_bytes",
-    "conduit_residual_error",
+    "conduit_residual_error", "conduit_score_noalloc",
 ]
+SCORE_NOALLOC_MAX_BYTES = 16 << 20
 
 
 class ConduitError(RuntimeError):
@@ -76,6 +77,9 @@ def lib() -> ctypes.CDLL:
         L.conduit_score.argtypes = [pkv, vp, i32, i32, pimg, ctypes.c_int, ctypes.c_int, f32, vp, vp,
                                     vp, vp, vp, i32, vp, vp, vp, sz, vp]
         L.conduit_score.restype = ctypes.c_int
+        L.conduit_score_noalloc.argtypes = [pkv, vp, i32, i32, pimg, ctypes.c_int, ctypes.c_int, f32, vp,
+                                            vp, vp, vp, vp, i32, vp, vp, vp]
+        L.conduit_score_noalloc.restype = ctypes.c_int
         L.conduit_select_workspace_bytes.argtypes = [i32, i32]
         L.conduit_select_workspace_bytes.restype = sz
         L.conduit_select_topk.argtypes = [vp, vp, i32, pimg, f32, ctypes.c_int, i32, vp, vp, vp, vp,
@@ -231,6 +235,23 @@ def conduit_score(kv: KV, q: torch.Tensor, q_pos0: int, img: ImageTable, s_acc: 
                                norm, agg, scale, _ptr(row_lse_in), _ptr(row_lse_out), _ptr(vnorm_in),
                                s_acc.data_ptr(), a_acc.data_ptr(), int(accumulate), _ptr(a_out),
                                _ptr(vnorm_out), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def conduit_score_noalloc(kv: KV, q: torch.Tensor, q_pos0: int, img: ImageTable, s_acc: torch.Tensor,
+                          a_acc: torch.Tensor, accumulate: bool = False, norm: int = NORM_CAUSAL_ROW,
+                          scale: Optional[float] = None, row_lse_in: Optional[torch.Tensor] = None,
+                          row_lse_out: Optional[torch.Tensor] = None, a_out: Optional[torch.Tensor] = None,
+                          vnorm_out: Optional[torch.Tensor] = None, stream=None, agg: int = AGG_MEAN,
+                          vnorm_in: Optional[torch.Tensor] = None) -> None:
+    """conduit_score on the library's fixed device scratch (no workspace, no
+    allocation); see conduit_score_noalloc in conduit.h."""
+    n_q = q.shape[0]
+    if scale is None:
+        scale = 1.0 / math.sqrt(kv.head_dim)
+    _check(lib().conduit_score_noalloc(ctypes.byref(kv), q.data_ptr(), n_q, q_pos0, ctypes.byref(img.desc),
+                                       norm, agg, scale, _ptr(row_lse_in), _ptr(row_lse_out),
+                                       _ptr(vnorm_in), s_acc.data_ptr(), a_acc.data_ptr(), int(accumulate),
+                                       _ptr(a_out), _ptr(vnorm_out), _stream(stream)))
 
 
 def conduit_value_norms(kv: KV, img: ImageTable, vnorm_out: torch.Tensor, stream=None) -> None:

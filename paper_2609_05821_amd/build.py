@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libconduit.so")
-SOURCES = ["api.cpp", "attn.hip", "score.hip", "select.hip", "scatter.hip", "residual.hip"]
+SOURCES = ["api.cpp", "attn.hip", "score.hip", "select.hip", "scatter.hip", "residual.hip", "static_ws.hip"]
 CEILING_SRC = "ceiling.hip"  # measurement reference for bench.py, not part of the library
 CEILING_LIB = os.path.join(PKG, "libconduit_ceiling.so")
 

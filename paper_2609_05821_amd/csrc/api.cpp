@@ -427,6 +427,31 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   return ok();
 }
 
+conduit_status conduit_score_noalloc(const conduit_kv *kv, const void *q, int32_t n_q, int32_t q_pos0,
+                                     const conduit_images *img, conduit_norm norm, conduit_agg agg, float scale,
+                                     const float *row_lse_in, float *row_lse_out, const float *vnorm_in,
+                                     float *s_acc, float *a_acc, int32_t accumulate, float *a_out,
+                                     float *vnorm_out, hipStream_t stream) {
+  static_assert(kStaticScoreScratchBytes == CONDUIT_SCORE_NOALLOC_MAX_BYTES, "scratch size");
+  // A size query of 0 means an argument conduit_score rejects on its own
+  // (a valid call always needs scratch, so with none it cannot pass the
+  // checks); otherwise the call must fit the fixed scratch.
+  const size_t need = conduit_score_workspace_bytes(kv, n_q, img);
+  if (need == 0)
+    return conduit_score(kv, q, n_q, q_pos0, img, norm, agg, scale, row_lse_in, row_lse_out, vnorm_in, s_acc,
+                         a_acc, accumulate, a_out, vnorm_out, nullptr, 0, stream);
+  if (need > kStaticScoreScratchBytes)
+    return fail(CONDUIT_ERR_UNSUPPORTED,
+                "this scoring call needs %zu bytes of scratch; conduit_score_noalloc holds at most %zu "
+                "(use conduit_score with a caller workspace)",
+                need, kStaticScoreScratchBytes);
+  void *scratch = nullptr;
+  const hipError_t e = static_score_scratch(&scratch);
+  if (e != hipSuccess) return hip_fail(e, "static scratch address");
+  return conduit_score(kv, q, n_q, q_pos0, img, norm, agg, scale, row_lse_in, row_lse_out, vnorm_in, s_acc, a_acc,
+                       accumulate, a_out, vnorm_out, scratch, kStaticScoreScratchBytes, stream);
+}
+
 conduit_status conduit_value_norms(const conduit_kv *kv, const conduit_images *img, float *vnorm_out,
                                    hipStream_t stream) {
   conduit_status st = check_kv(kv);

@@ -453,6 +453,13 @@ hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
 hipError_t launch_residual(const ResidualParams &p, int head_dim, bool bf16, hipStream_t s);
 
+// Size of the fixed device scratch behind conduit_score_noalloc (must equal
+// CONDUIT_SCORE_NOALLOC_MAX_BYTES of conduit.h).
+constexpr size_t kStaticScoreScratchBytes = size_t(16) << 20;
+// Device address of that scratch on the current device, resolved with
+// hipGetSymbolAddress on the first call per device and kept.
+hipError_t static_score_scratch(void **out);
+
 // Residual-error tiling: 256 pairs of one KV head per workgroup (8 waves),
 // 64 visual keys per tile, at least this many tiles per key split.
 constexpr int kResidualPairs = 256;

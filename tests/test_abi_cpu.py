@@ -273,3 +273,25 @@ def test_ceiling_reference_library():
     assert L.conduit_ceiling_mfma_bf16(None, FAKE, 1, 1, None) != 0
     assert L.conduit_ceiling_mfma_bf16(FAKE + 8, FAKE, 1, 1, None) != 0
     assert L.conduit_ceiling_mfma_bf16(FAKE, FAKE, 0, 1, None) != 0
+
+
+def test_noalloc_rejects_calls_beyond_its_scratch():
+    """conduit_score_noalloc refuses, before any HIP call, a call whose
+    workspace exceeds its fixed scratch (256 KV heads: the per-head column sums
+    alone need 2 * 256 * 4 bytes per visual token)."""
+    import ctypes
+    L = api.lib()
+    fake = 1 << 20  # aligned, never dereferenced: the call is refused first
+    n_vis = 9000
+    kv = api.KV(fake, fake, 256 * 64, 256 * 64, n_vis + 64, 256, 256, 64, api.BF16, 0, None, 0)
+    img = api.ImageTable([16], [0, n_vis])
+    need = api.score_workspace_bytes(kv, 8, img)
+    assert need > api.SCORE_NOALLOC_MAX_BYTES
+    st = L.conduit_score_noalloc(ctypes.byref(kv), fake, 8, n_vis + 16, ctypes.byref(img.desc), 0, 0, 0.125,
+                                 None, None, None, fake, fake, 0, None, None, None)
+    assert st == api.ERR_UNSUPPORTED
+    assert b"conduit_score_noalloc holds at most" in L.conduit_last_error()
+    # an invalid argument is still reported as such
+    st = L.conduit_score_noalloc(None, fake, 8, 0, ctypes.byref(img.desc), 0, 0, 0.125,
+                                 None, None, None, fake, fake, 0, None, None, None)
+    assert st == api.ERR_INVALID_ARG
