@@ -155,7 +155,7 @@ PlanLayout plan_layout(const conduit_kv *kv, int64_t n_rows, bool with_values, T
   P.hdr = take(16);
   P.part_m = take((size_t)slots * 4);
   P.part_l = take((size_t)slots * 4);
-  P.part_o = take(with_values ? (size_t)slots * kv->head_dim * 4 : 0);
+  P.part_o = take(with_values ? (size_t)slots * kv->head_dim * 2 : 0);  // bf16
   return P;
 }
 
@@ -715,7 +715,7 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
     ap.plan = plan_at(ws, L.plan);
     ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
     ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
-    ap.part_o = reinterpret_cast<float *>(at(ws, L.plan.part_o));
+    ap.part_o = reinterpret_cast<u16 *>(at(ws, L.plan.part_o));
     e = launch_attn(ap, kv->head_dim, true, stream);
     if (e != hipSuccess) return hip_fail(e, "refresh attention");
   } else {

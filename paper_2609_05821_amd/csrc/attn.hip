@@ -320,6 +320,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   constexpr int DT = D / 32;      // 32-row tiles of O^T
   constexpr int KCH = KT * D / 8 / kThreads;  // 16-byte K chunks per thread (register staging)
   __shared__ AttnSmem<D, PV> sm;
+  __shared__ int s_restart;  // attempt id of the item being restarted (values only; see kHeadroom)
 
   const int G = p.group;
   const int n_pairs = p.n_rows * G;
@@ -359,6 +360,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const int n_items = uniform ? p.plan.uniform_items : min(p.plan.hdr[0], p.plan.max_items);
 
   const int grid = gridDim.x, g = blockIdx.x;
+  if (tid == 0) s_restart = 0;
+  int attempt_id = 0;
   if constexpr (!PV) {
     if (p.vis_only) {
       image_table_to_lds(p.tbl, sm.img, tid, kThreads);
@@ -480,10 +483,6 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     // visible key always moves m.
     float m = kMInit, l = 0.f;
     f32x16 o[DT];
-    if constexpr (PV) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
-    }
 
     // S^T of one 32-key sub-tile: K operands from LDS, 8 chained MFMAs.
     auto scores = [&](int buf, int sub) __attribute__((always_inline)) {
@@ -546,6 +545,31 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
       return page_row(pr, __builtin_amdgcn_readlane(page_vec, ti - page_base), t0);
     };
     auto row_of = [&](int t0) __attribute__((always_inline)) { return t0 < kend ? tile_row(t0) : (int64_t)0; };
+
+    // With values, the probabilities of an item are taken against one
+    // reference maximum per pair column, fixed for the item: the first
+    // sub-tile's maximum (kMInit if none of its keys is visible: then no key
+    // of the split is).  The result is exact for any reference (O, l and the
+    // final normaliser share it); the reference only has to keep
+    // 2^(c s - m) in range.  A later sub-tile whose maximum exceeds the
+    // reference by more than kHeadroom (2^32: sums over any key range stay
+    // far inside fp32) marks the workgroup for a restart of the item with
+    // the largest maximum seen so far as the reference.  A restart is taken
+    // at a barrier, so every wave takes it; each restart is triggered by a
+    // sub-tile beyond the previous trigger, so an item restarts at most once
+    // per iteration.  Without a running-maximum rescale the sub-steps have no
+    // branch on the probabilities, and O^T is written by matrix products only.
+    // Statistics only keep the online maximum (their rescale is one multiply).
+    constexpr float kHeadroom = 32.f;
+    float m_seen = kMInit;
+    bool over = false;
+    for (int attempt = 0;; ++attempt) {
+    l = 0.f;
+    if constexpr (PV) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
+      page_base = -64;
+    }
     if constexpr (PV) {
       // K(0..2), V(0..1); tiles past kend arrive as zeros
       const int64_t r0 = tile_row(kbeg), r1 = row_of(kbeg + KT), r2 = row_of(kbeg + 2 * KT);
@@ -568,19 +592,21 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     f32x16 sa = scores(0, 0), sb;
     if (tile_masked(kbeg)) mask_sub(sa, 0, kbeg, 0);
     float mx = sub_max(sa);
+    if constexpr (PV) {
+      m = fmaxf(fmaxf(mx, m_seen), kMInit);
+      m_seen = m;
+      over = false;
+    }
     // One sub-step: cur holds S^T of the current sub-tile (V rows vsub*32..
     // of V stage vst), nxt receives the next sub-tile's (K stage kbn, rows
     // ksub*32.., of the tile at nt0; after the last sub-tile: discarded).
     auto sub_step = [&](f32x16 &cur, f32x16 &nxt, int kbn, int ksub, int vst, int vsub, bool has_next, int nt0)
                         __attribute__((always_inline)) {
-      const bool grow = mx > m + kRescaleSlack;
-      const float alpha = grow ? fast_exp2(m - mx) : 1.f;
-      m = grow ? mx : m;
-      if constexpr (PV) {
-        if (__ballot(grow)) {
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
-        }
+      float alpha = 1.f;
+      if constexpr (!PV) {
+        const bool grow = mx > m + kRescaleSlack;
+        alpha = grow ? fast_exp2(m - mx) : 1.f;
+        m = grow ? mx : m;
       }
       nxt = scores(kbn, ksub);
       // probabilities of the current sub-tile; fp32 row sum (the
@@ -592,7 +618,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
       float psum = 0.f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) psum += cur[v];
-      l = l * alpha + psum;
+      l = PV ? l + psum : l * alpha + psum;
       if constexpr (PV) {
         bf16x8 pk[2];
 #pragma unroll
@@ -613,8 +639,14 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
       if (has_next) {
         if (tile_masked(nt0)) mask_sub(nxt, kbn, nt0, ksub);
         mx = sub_max(nxt);
+        if constexpr (PV) {
+          m_seen = fmaxf(m_seen, mx);
+          over = over || mx > m + kHeadroom;
+        }
       }
     };
+    const int gen = ++attempt_id;  // the workgroup's attempts in order (uniform, never repeats)
+    bool restart = false;
     if constexpr (PV) {
       // Two tiles (t, t+1) per barrier.  K stages rotate mod 5 and V stages
       // mod 4: the iteration reads K(t..t+2) and V(t..t+1) while K(t+3),
@@ -636,9 +668,11 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         sub_step(sb, sa, k1, 0, vs, 1, true, t0 + KT);           // S(t+1,0) | P(t,1) V
         sub_step(sa, sb, k1, 1, v1, 0, true, t0 + KT);           // S(t+1,1) | P(t+1,0) V
         sub_step(sb, sa, k2, 0, v1, 1, more2, t0 + 2 * KT);      // S(t+2,0) | P(t+1,1) V
+        if (__ballot(over) != 0 && lane == 0) s_restart = gen;
         vm_wait<0>();
         __syncthreads();
-        if (!more2) break;
+        restart = s_restart == gen;
+        if (!more2 || restart) break;
         t0 += 2 * KT;
         ks = k2;
         vs = v2;
@@ -659,6 +693,9 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         st = st1;
       }
     }
+
+    if (!restart) break;
+    }  // attempts
 
     // ---- outputs: final values for a single-split block, else partials ----
     const float l_tot = l + __shfl_xor(l, 32, 64);
@@ -691,13 +728,20 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
           p.part_l[idx2] = l_tot;
         }
         if constexpr (PV) {
-          float *dst = p.part_o + idx2 * D;
+          // the split's own attention output O_s / l_s (a convex combination
+          // of V rows) in bf16; l = 0 (no visible key in the split) gives 0
+          const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+          u16 *dst = p.part_o + idx2 * D;
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
             for (int g4 = 0; g4 < 4; ++g4) {
-              f32x4 w = {o[dt][4 * g4], o[dt][4 * g4 + 1], o[dt][4 * g4 + 2], o[dt][4 * g4 + 3]};
-              *reinterpret_cast<f32x4 *>(dst + dt * 32 + 8 * g4 + 4 * half) = w;
+              uint2 w;
+              w.x = (uint32_t)f32_to_bf16(o[dt][4 * g4] * inv) |
+                    ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 1] * inv) << 16);
+              w.y = (uint32_t)f32_to_bf16(o[dt][4 * g4 + 2] * inv) |
+                    ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 3] * inv) << 16);
+              *reinterpret_cast<uint2 *>(dst + dt * 32 + 8 * g4 + 4 * half) = w;
             }
         }
       }
@@ -706,10 +750,13 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
 }
 
 // Merge split partials of blocks with n_s > 1: M = max m_s,
-// L = sum l_s 2^(m_s - M), O = sum O_s 2^(m_s - M) / L, splits in order.
+// L = sum l_s 2^(m_s - M), O = sum l_s 2^(m_s - M) Ohat_s / L, splits in
+// order, where Ohat_s = O_s / l_s is the split's own output, kept in bf16 (a
+// convex combination of V rows, so its relative rounding error stays 2^-9
+// and the merged row, a convex combination of the Ohat_s, keeps it).
 // With values a thread merges 16 head dims of one pair (the whole grid is
 // resident at once); statistics only, one thread per pair.  The m_s, l_s and
-// O_s of up to kMergeBatch splits are loaded together and folded into a
+// Ohat_s of up to kMergeBatch splits are loaded together and folded into a
 // running maximum, so a thread waits on two round trips to memory for
 // n_s <= kMergeBatch (plan entry, then the partials); for such blocks the
 // sums are exactly those of the two-pass formula above.
@@ -719,7 +766,6 @@ template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   static_assert(D % kMergeDims == 0, "whole 16-dim slices");
   constexpr int NC = D / kMergeDims;
-  constexpr int NQ = kMergeDims / 4;
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const bool values = p.part_o != nullptr;
@@ -737,13 +783,15 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
                                 : (int64_t)h * p.plan.hdr[1] + p.plan.pb_base[pb];
   if (slot0 + ns > p.plan.max_items) return;  // never for a plan within its bound
   const int64_t idx0 = slot0 * p.ppb + j;
+  // Split s contributes W_s = 2^(m_s - M) l_s and W_s * Ohat_s, with Ohat_s
+  // its normalised output (bf16) and M the running maximum of the m_s.
   float M = kNegInf, L = 0.f;
-  f32x4 acc[NQ];
+  float acc[kMergeDims];
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int e = 0; e < kMergeDims; ++e) acc[e] = 0.f;
   for (int s0 = 0; s0 < ns; s0 += kMergeBatch) {
     float mb[kMergeBatch], lb[kMergeBatch];
-    f32x4 ob[kMergeBatch][NQ];
+    u32x4 ob[kMergeBatch][2];
 #pragma unroll
     for (int i = 0; i < kMergeBatch; ++i) {
       const bool in = s0 + i < ns;
@@ -751,9 +799,8 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
       mb[i] = in ? p.part_m[idx] : kNegInf;
       lb[i] = in ? p.part_l[idx] : 0.f;
 #pragma unroll
-      for (int q = 0; q < NQ; ++q)
-        ob[i][q] = in && values ? *reinterpret_cast<const f32x4 *>(p.part_o + idx * D + kMergeDims * c + 4 * q)
-                                : f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int q = 0; q < 2; ++q)
+        ob[i][q] = in && values ? ld16(p.part_o + idx * D + kMergeDims * c + 8 * q) : u32x4{0, 0, 0, 0};
     }
     float Mn = M;
 #pragma unroll
@@ -761,14 +808,20 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
     const float rs = fast_exp2(M - Mn);                             // 0 on the first batch
     L *= rs;
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) acc[q] *= rs;
+    for (int e = 0; e < kMergeDims; ++e) acc[e] *= rs;
 #pragma unroll
     for (int i = 0; i < kMergeBatch; ++i) {
       if (s0 + i < ns) {
-        const float w = fast_exp2(mb[i] - Mn);  // m >= kMInit is finite
-        L += w * lb[i];
+        const float w = fast_exp2(mb[i] - Mn) * lb[i];  // m >= kMInit is finite
+        L += w;
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) acc[q] += w * ob[i][q];
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const uint32_t x = ob[i][q][u];
+            acc[8 * q + 2 * u] += w * __builtin_bit_cast(float, x << 16);
+            acc[8 * q + 2 * u + 1] += w * __builtin_bit_cast(float, x & 0xffff0000u);
+          }
       }
     }
     M = Mn;
@@ -782,10 +835,10 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
     const float inv = 1.f / L;
     u16 *out = static_cast<u16 *>(p.o_out) + gp * D + kMergeDims * c;
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
+    for (int q = 0; q < kMergeDims / 4; ++q) {
       uint2 w;
-      w.x = (uint32_t)f32_to_bf16(acc[q][0] * inv) | ((uint32_t)f32_to_bf16(acc[q][1] * inv) << 16);
-      w.y = (uint32_t)f32_to_bf16(acc[q][2] * inv) | ((uint32_t)f32_to_bf16(acc[q][3] * inv) << 16);
+      w.x = (uint32_t)f32_to_bf16(acc[4 * q] * inv) | ((uint32_t)f32_to_bf16(acc[4 * q + 1] * inv) << 16);
+      w.y = (uint32_t)f32_to_bf16(acc[4 * q + 2] * inv) | ((uint32_t)f32_to_bf16(acc[4 * q + 3] * inv) << 16);
       *reinterpret_cast<uint2 *>(out + 4 * q) = w;
     }
   }

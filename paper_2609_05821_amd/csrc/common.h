@@ -281,7 +281,7 @@ struct AttnParams {
   AttnPlan plan;            // bf16 path
   float *part_m;            // [max_items][ppb] running max (log2 units)
   float *part_l;            // [max_items][ppb] softmax denominator
-  float *part_o;            // [max_items][ppb][D] unnormalised output (values only)
+  u16 *part_o;              // [max_items][ppb][D] bf16: the split's output O_s / l_s (values only)
   // Final outputs, written directly by blocks whose keys form one split.
   float *row_b;             // nullable [n_rows * H_q]: log2-domain log-sum-exp
   float *lse_out;           // nullable [n_rows * H_q]: natural-log log-sum-exp
@@ -299,7 +299,7 @@ struct CombineParams {
   AttnPlan plan;
   const float *part_m;
   const float *part_l;
-  const float *part_o;      // nullable (statistics only)
+  const u16 *part_o;        // nullable (statistics only): bf16 O_s / l_s
   float *row_b;             // nullable [n_rows * H_q]: log2-domain log-sum-exp
   float *lse_out;           // nullable [n_rows * H_q]: natural-log log-sum-exp
   void *o_out;              // nullable [n_rows][H_q][D] bf16
