@@ -42,6 +42,10 @@ namespace {
 constexpr int KT = kAttnKeyTile;
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kMInit = -1e30f;  // initial running maximum (log2 units)
+// Statistics: the running maximum only moves when a sub-tile's maximum
+// exceeds it by more than this many log2 units; probabilities stay below 2^8
+// and l is rescaled rarely.  Exact: l and the final normaliser share it.
+constexpr float kRescaleSlack = 8.f;
 
 // LDS tiles.  K rows are D + 8 elements apart (16 bytes of padding: the 16
 // lanes of an S^T operand read cover 16 rows in distinct banks); V rows are
@@ -59,7 +63,7 @@ struct TileGeom {
 // key-domain bits and the image table.
 template <bool Stats>
 struct StatsLds {
-  uint64_t okmask[3];  // key-domain filter per K tile, bit = key
+  uint64_t okmask[4];  // key-domain filter per K stage, bit = key
   ImageLds img;        // visual-only statistics: the image table
 };
 template <>
@@ -67,7 +71,7 @@ struct StatsLds<false> {};
 
 template <int D, bool PV>
 struct AttnSmem : StatsLds<!PV> {
-  alignas(16) u16 k[PV ? 5 : 3][KT][TileGeom<D>::kPitch];
+  alignas(16) u16 k[PV ? 5 : 4][KT][TileGeom<D>::kPitch];
   alignas(16) u16 v[PV ? 4 : 1][PV ? KT : 1][TileGeom<D>::vPitch];
 };
 
@@ -107,10 +111,6 @@ __device__ __forceinline__ int4 uniform_block_info(int pb, int ppb, int group, i
 }
 
 
-// The running maximum only moves when a sub-tile's maximum exceeds it by more
-// than this many log2 units; probabilities stay below 2^8 and O, l are
-// rescaled rarely.  Exact: O, l and the final normaliser share the reference.
-constexpr float kRescaleSlack = 8.f;
 
 // Builds the work plan from the row positions (see AttnPlan).  One
 // workgroup of 1024 threads; blocks and histogram bins live in LDS.
@@ -318,9 +318,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   constexpr int kPairs = W * 32;  // (row, head) pairs per block
   constexpr int KS = D / 16;      // MFMA k-steps over the head dimension
   constexpr int DT = D / 32;      // 32-row tiles of O^T
-  constexpr int KCH = KT * D / 8 / kThreads;  // 16-byte K chunks per thread (register staging)
   __shared__ AttnSmem<D, PV> sm;
-  __shared__ int s_restart;  // attempt id of the item being restarted (values only; see kHeadroom)
+  __shared__ int s_restart;  // attempt id of the item being restarted (see kHeadroom)
 
   const int G = p.group;
   const int n_pairs = p.n_rows * G;
@@ -340,7 +339,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   // (head offset added per item; the padding offset stays out of range).
   constexpr int kXferAll = Geo::kXfer + Geo::vXfer;
   constexpr uint32_t kPadOff = 0x80000000u;  // beyond any tile resource (< 2 GiB): reads as 0
-  constexpr int kSlots = PV ? (kXferAll + W - 1) / W : 1;
+  constexpr int kXferUsed = PV ? kXferAll : Geo::kXfer;  // statistics only: K tiles alone
+  constexpr int kSlots = (kXferUsed + W - 1) / W;
   uint32_t xoff0[kSlots];
 #pragma unroll
   for (int sl = 0; sl < kSlots; ++sl) {
@@ -402,63 +402,25 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         qreg[ks] = as_bf16x8(valid ? ld16(qrow + ks * 16) : u32x4{0, 0, 0, 0});
     }
 
-    // Statistics only: register staging.  Per-thread byte offsets of its
-    // chunks inside a key tile (16 lanes per key row, so loads are
-    // coalesced), read through a buffer resource over the tile's KT rows
-    // (row strides stay below 32 MiB, so 32-bit offsets reach every row).
-    uint32_t koff[KCH];
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int cidx = tid + kThreads * i;
-      koff[i] = (uint32_t)(((int64_t)(cidx / (D / 8)) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8) * 2);
-    }
-    u32x4 rk[PV ? 1 : KCH];
-    bool rok = false;
-    // t0 is a multiple of the tile and a page holds a whole number of tiles,
-    // so a tile's rows are consecutive cache rows from row0; only a partial
-    // last tile clamps its rows (past kend they repeat the last row and are
-    // masked later).
-    auto load_k = [&](int t0, int64_t row0) __attribute__((always_inline)) {
+    // Statistics only (visual-only domain): one bit per key of the tile at
+    // t0 in K stage st, set by wave 0 beside the tile's transfers.
+    auto okmask_tile = [&](int st, int t0) __attribute__((always_inline)) {
       if constexpr (!PV) {
-        const auto rs = buffer_rsrc(Kg + row0 * p.k_stride, (int)(KT * p.k_stride * 2));
-        if (t0 + KT <= kend) {
-#pragma unroll
-          for (int i = 0; i < KCH; ++i) rk[i] = buffer_ld16(rs, koff[i]);
-        } else {
-#pragma unroll
-          for (int i = 0; i < KCH; ++i) {
-            const int cidx = tid + kThreads * i;
-            const int kp = min(t0 + cidx / (D / 8), kend - 1);
-            rk[i] = buffer_ld16(rs, (uint32_t)(((int64_t)(kp - t0) * p.k_stride + kvh * D + (cidx % (D / 8)) * 8) * 2));
-          }
-        }
-        if (p.vis_only && tid < KT) {
-          const int kp = t0 + tid;
-          rok = kp < kend && is_visual(sm.img, kp);
+        if (p.vis_only && wave == 0) {
+          const int kp = t0 + lane;
+          const uint64_t bits = __ballot(kp < kend && is_visual(sm.img, kp));
+          if (lane == 0) sm.okmask[st] = bits;
         }
       }
     };
-    auto store_k = [&](int buf) __attribute__((always_inline)) {
-      if constexpr (!PV) {
-#pragma unroll
-        for (int i = 0; i < KCH; ++i) {
-          const int cidx = tid + kThreads * i;
-          st16(&sm.k[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], rk[i]);
-        }
-        if (p.vis_only && tid < KT) {  // wave 0: one bit per key of the tile
-          const uint64_t bits = __ballot(rok != 0);
-          if (tid == 0) sm.okmask[buf] = bits;
-        }
-      }
-    };
-    // With values: this wave's transfers of the K tile at t0 (row0; rows at
-    // or past kend read as 0 through the resource bound) into K stage kst,
-    // or of the V tile into V stage vst.  A tile that does not exist still
+    // This wave's transfers of the K tile at t0 (row0; rows at or past kend
+    // read as 0 through the resource bound) into K stage st, or (with values)
+    // of the V tile into V stage st.  A tile that does not exist still
     // gets its transfers (zero-length resource), so every iteration issues
     // the same count per wave.
     const uint32_t head_b = (uint32_t)(kvh * D * 2);
     auto dma_tile = [&](bool isk, int st, int t0, int64_t row0) __attribute__((always_inline)) {
-      if constexpr (PV) {
+      {
         const int rows = min(max(kend - t0, 0), KT);
         // the resource must sit in scalar registers: its inputs are uniform,
         // which readfirstlane makes explicit
@@ -467,7 +429,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
                             (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ga);
         const int nbytes = __builtin_amdgcn_readfirstlane((int)(rows * (isk ? p.k_stride : p.v_stride) * 2));
         const auto rs = buffer_rsrc(reinterpret_cast<const void *>((uintptr_t)gu), nbytes);
-        const uint32_t base = isk ? (uint32_t)(uintptr_t)&sm.k[st][0][0] : (uint32_t)(uintptr_t)&sm.v[st][0][0];
+        const uint32_t base = isk ? (uint32_t)(uintptr_t)&sm.k[st][0][0] : (uint32_t)(uintptr_t)&sm.v[PV ? st : 0][0][0];
 #pragma unroll
         for (int sl = 0; sl < kSlots; ++sl) {
           const int x = wave + W * sl;
@@ -540,7 +502,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
       if (ti - page_base >= 64) {
         page_base = ti;
         page_vec = read_page(pr, (ti + (tid & 63)) * KT);
-        if constexpr (PV) vm_wait<0>();  // here, not before every lane read
+        vm_wait<0>();  // here, not before every lane read (the tile transfers are invisible to the compiler)
       }
       return page_row(pr, __builtin_amdgcn_readlane(page_vec, ti - page_base), t0);
     };
@@ -558,17 +520,19 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     // at a barrier, so every wave takes it; each restart is triggered by a
     // sub-tile beyond the previous trigger, so an item restarts at most once
     // per iteration.  Without a running-maximum rescale the sub-steps have no
-    // branch on the probabilities, and O^T is written by matrix products only.
-    // Statistics only keep the online maximum (their rescale is one multiply).
+    // branch on the probabilities, and O^T is written by matrix products
+    // only.  Statistics only keep an online maximum (their rescale is one
+    // multiply; with the visual-only domain the first keys of a split are
+    // often outside it, which a fixed reference would turn into restarts).
     constexpr float kHeadroom = 32.f;
     float m_seen = kMInit;
     bool over = false;
     for (int attempt = 0;; ++attempt) {
     l = 0.f;
+    page_base = -64;
     if constexpr (PV) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
-      page_base = -64;
     }
     if constexpr (PV) {
       // K(0..2), V(0..1); tiles past kend arrive as zeros
@@ -580,35 +544,45 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
       dma_tile(true, 2, kbeg + 2 * KT, r2);
       vm_wait<0>();
     } else {
-      const int64_t row0 = tile_row(kbeg);
-      load_k(kbeg, row0);
-      store_k(0);
-      if (kbeg + KT < kend) {
-        load_k(kbeg + KT, tile_row(kbeg + KT));
-        store_k(1);
-      }
+      // K(0..2); tiles past kend arrive as zeros
+      const int64_t r0 = tile_row(kbeg), r1 = row_of(kbeg + KT), r2 = row_of(kbeg + 2 * KT);
+      dma_tile(true, 0, kbeg, r0);
+      okmask_tile(0, kbeg);
+      dma_tile(true, 1, kbeg + KT, r1);
+      okmask_tile(1, kbeg + KT);
+      dma_tile(true, 2, kbeg + 2 * KT, r2);
+      okmask_tile(2, kbeg + 2 * KT);
+      vm_wait<0>();
     }
     __syncthreads();
     f32x16 sa = scores(0, 0), sb;
-    if (tile_masked(kbeg)) mask_sub(sa, 0, kbeg, 0);
-    float mx = sub_max(sa);
     if constexpr (PV) {
-      m = fmaxf(fmaxf(mx, m_seen), kMInit);
+      if (tile_masked(kbeg)) mask_sub(sa, 0, kbeg, 0);
+      m = fmaxf(fmaxf(sub_max(sa), m_seen), kMInit);
       m_seen = m;
       over = false;
     }
-    // One sub-step: cur holds S^T of the current sub-tile (V rows vsub*32..
-    // of V stage vst), nxt receives the next sub-tile's (K stage kbn, rows
-    // ksub*32.., of the tile at nt0; after the last sub-tile: discarded).
-    auto sub_step = [&](f32x16 &cur, f32x16 &nxt, int kbn, int ksub, int vst, int vsub, bool has_next, int nt0)
-                        __attribute__((always_inline)) {
+    // One sub-step.  cur holds S^T of the current sub-tile (sub-tile csub of
+    // the tile at ct0, K stage cbuf; its V rows are vsub*32.. of V stage
+    // vst); the S^T products of the next sub-tile (K stage kbn, rows
+    // ksub*32..; after the last sub-tile: discarded) are issued into nxt.
+    // The key filter of cur comes first, so everything after it is one basic
+    // block: the compiler then places the exponentials of cur among the
+    // matrix products of nxt instead of sinking them past a later branch.
+    auto sub_step = [&](f32x16 &cur, f32x16 &nxt, int kbn, int ksub, int vst, int vsub, bool cur_masked, int cbuf,
+                        int ct0, int csub) __attribute__((always_inline)) {
+      if (cur_masked) mask_sub(cur, cbuf, ct0, csub);
+      nxt = scores(kbn, ksub);
+      const float mx = sub_max(cur);
       float alpha = 1.f;
-      if constexpr (!PV) {
+      if constexpr (PV) {
+        m_seen = fmaxf(m_seen, mx);
+        over = over || mx > m + kHeadroom;
+      } else {
         const bool grow = mx > m + kRescaleSlack;
         alpha = grow ? fast_exp2(m - mx) : 1.f;
         m = grow ? mx : m;
       }
-      nxt = scores(kbn, ksub);
       // probabilities of the current sub-tile; fp32 row sum (the
       // log-sum-exp output needs it to 1e-4; summing the bf16-rounded
       // probabilities is off by up to 2^-9 when few terms dominate)
@@ -619,6 +593,10 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
 #pragma unroll
       for (int v = 0; v < 16; ++v) psum += cur[v];
       l = PV ? l + psum : l * alpha + psum;
+      // l is needed only after the loop; this empty statement makes it (and
+      // so this sub-tile's exponentials) due here, so the compiler does not
+      // sink them past the next sub-step's key filter.
+      asm volatile("" ::"v"(l));
       if constexpr (PV) {
         bf16x8 pk[2];
 #pragma unroll
@@ -634,14 +612,6 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
             o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[dt], pk[ks], o[dt], 0, 0, 0);
-        }
-      }
-      if (has_next) {
-        if (tile_masked(nt0)) mask_sub(nxt, kbn, nt0, ksub);
-        mx = sub_max(nxt);
-        if constexpr (PV) {
-          m_seen = fmaxf(m_seen, mx);
-          over = over || mx > m + kHeadroom;
         }
       }
     };
@@ -664,10 +634,11 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         dma_tile(false, v3, t0 + 3 * KT, r3);
         dma_tile(true, k3, t0 + 3 * KT, r3);
         dma_tile(true, k4, t0 + 4 * KT, r4);
-        sub_step(sa, sb, ks, 1, vs, 0, true, t0);                // S(t,1)   | P(t,0) V
-        sub_step(sb, sa, k1, 0, vs, 1, true, t0 + KT);           // S(t+1,0) | P(t,1) V
-        sub_step(sa, sb, k1, 1, v1, 0, true, t0 + KT);           // S(t+1,1) | P(t+1,0) V
-        sub_step(sb, sa, k2, 0, v1, 1, more2, t0 + 2 * KT);      // S(t+2,0) | P(t+1,1) V
+        const bool m0 = tile_masked(t0), m1 = tile_masked(t0 + KT);
+        sub_step(sa, sb, ks, 1, vs, 0, m0, ks, t0, 0);           // S(t,1)   | P(t,0) V
+        sub_step(sb, sa, k1, 0, vs, 1, m0, ks, t0, 1);           // S(t+1,0) | P(t,1) V
+        sub_step(sa, sb, k1, 1, v1, 0, m1, k1, t0 + KT, 0);      // S(t+1,1) | P(t+1,0) V
+        sub_step(sb, sa, k2, 0, v1, 1, m1, k1, t0 + KT, 1);      // S(t+2,0) | P(t+1,1) V
         if (__ballot(over) != 0 && lane == 0) s_restart = gen;
         vm_wait<0>();
         __syncthreads();
@@ -678,20 +649,26 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
         vs = v2;
       }
     } else {
-      constexpr int NKB = 3;
-      int t0 = kbeg, st = 0;  // K stage of tile t; stages follow mod NKB
+      // One tile per barrier, K stages mod 4: iteration t reads K(t) and
+      // K(t+1) while K(t+2) is complete and K(t+3) arrives.  Before the
+      // barrier a wave waits until at most kSlots of its transfers are
+      // outstanding: all of K(t+2)'s, so only K(t+3)'s may remain.
+      int t0 = kbeg, st = 0;  // K stage of tile t
       for (;;) {
         const bool more = t0 + KT < kend;
-        const int st1 = st + 1 == NKB ? 0 : st + 1;
-        if (t0 + 2 * KT < kend) load_k(t0 + 2 * KT, tile_row(t0 + 2 * KT));
-        sub_step(sa, sb, st, 1, 0, 0, true, t0);        // second half of tile t
-        sub_step(sb, sa, st1, 0, 0, 1, more, t0 + KT);  // first half of tile t+1
-        if (t0 + 2 * KT < kend) store_k(st1 + 1 == NKB ? 0 : st1 + 1);
+        const int st1 = (st + 1) & 3, st3 = (st + 3) & 3;
+        dma_tile(true, st3, t0 + 3 * KT, row_of(t0 + 3 * KT));
+        okmask_tile(st3, t0 + 3 * KT);
+        const bool m0 = tile_masked(t0);
+        sub_step(sa, sb, st, 1, 0, 0, m0, st, t0, 0);   // S(t,1)   | P(t,0)
+        sub_step(sb, sa, st1, 0, 0, 0, m0, st, t0, 1);  // S(t+1,0) | P(t,1)
+        vm_wait<kSlots - 1>();
         __syncthreads();
         if (!more) break;
         t0 += KT;
         st = st1;
       }
+      vm_wait<0>();  // the last transfers (zero tiles) land before the stages are reused
     }
 
     if (!restart) break;
