@@ -98,8 +98,10 @@ def parse():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the supplementary measurements (variants, paged cache, text rows, "
                          "residual diagnostic): only the step kernels run, e.g. under a kernel trace")
-    ap.add_argument("--cpu-row-stride", type=int, default=8,
+    ap.add_argument("--cpu-row-stride", type=int, default=1,
                     help="CPU baseline refreshes every n-th selected row and scales by n")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the other workloads (single image, 28-layer multi-image, long document)")
     return ap.parse_args()
 
 
@@ -258,6 +260,32 @@ def main():
 
     score_lse_in = timed(lambda: api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc,
                                                    row_lse_in=lse_rows, ws=step.ws_score))
+
+    def one_step_lse_in():
+        api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, row_lse_in=lse_rows,
+                          ws=step.ws_score)
+        api.conduit_select_topk(step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos,
+                                mask_out=step.mask, shat_out=step.shat, c_out=step.c)
+        api.conduit_scatter_kv(kv, pos, fresh["k_new"], fresh["v_new"])
+        api.conduit_refresh_attn(kv, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh)
+
+    def timed_restored(fn):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
+        for _ in range(args.warmup):
+            fn()
+            restore()
+        for i in range(args.steps):
+            if not args.no_scrub:
+                scrub.fill_(i & 0xFF)
+            ev[2 * i].record(stream)
+            fn()
+            ev[2 * i + 1].record(stream)
+            restore()
+        torch.cuda.synchronize()
+        out_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)]
+        return {"mean": statistics.mean(out_ms), "p10": pct(out_ms, 10), "p90": pct(out_ms, 90)}
+
+    step_lse_in = timed_restored(one_step_lse_in)
     probe = timed(lambda: api.conduit_score(kv, q8, w.q_pos0, img, step.s_acc, step.a_acc, ws=ws8))
     tiny = torch.empty(1, dtype=torch.float32, device=dev)
     launch_floor = timed(lambda: tiny.fill_(0.0))
@@ -323,6 +351,10 @@ def main():
         "per_call_ms_p90": p90,
         "kernels_ms": kernels_ms,
         "score_row_lse_in_ms": score_lse_in,
+        "step_row_lse_in": {
+            "ms": step_lse_in, "value": w.n_vis / (step_lse_in["mean"] * 1e-3),
+            "note": "the same step with the span rows' log-sum-exp supplied to conduit_score (e.g. "
+                    "from the model's own attention of the span): the row-statistics pass is skipped"},
         "bandwidth_probe": {
             "what": "conduit_score at n_q = 8 on the same cache (supplementary; not a benchmark "
                     "config): HBM-bound",
@@ -472,6 +504,10 @@ def main():
             },
         })
 
+    del scrub, step, fresh
+    torch.cuda.empty_cache()
+    if not args.no_workloads:
+        result["workloads"] = other_workloads(args, dev)
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(w, L, q_sel_np, idx_np, pos_np, k,
                                               args.cpu_row_stride)
@@ -516,6 +552,173 @@ def traffic_from_profile():
     if rec.get("kernel_sources_sha256_16") != source_digest(KERNEL_SOURCES):
         return None
     return rec.get("traffic_bytes_per_launch")
+
+
+def other_workloads(args, dev):
+    """The other workloads, each step timed on this GPU (HIP events around
+    the whole step, cold caches) beside its CPU oracle timing.
+
+    A step is the refresh step of the workload: conduit_score for every
+    scored layer (layer sums accumulated), one conduit_select_topk, then
+    conduit_scatter_kv + conduit_refresh_attn for every layer.  The 28-layer
+    workloads hold 28 per-layer caches, span queries and fresh rows in device
+    memory; their contents are one generated layer copied into each (so the
+    selection is that of one layer; every layer still reads and writes its own
+    buffers).  Throughput is visual tokens per second per layer:
+    N_vis / (step time / layers)."""
+    import torch
+
+    from paper_2609_05821_amd import api, workloads as W
+
+    stream = torch.cuda.current_stream()
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    out = {}
+    plan = [(1, ["10%", "10%-stated"], 1), (2, ["10%"], 1), (3, ["5%", "10%", "20%"], 28),
+            (5, ["10%", "10%-stated"], 28)]
+    for cfg, labels, n_layers in plan:
+        w = W.config(cfg, n_layers=1)
+        L = w.layer(0)
+
+        def up(x):
+            if x.dtype == np.uint16:
+                return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+            return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+        k0, v0, q0 = up(L["k"]), up(L["v"]), up(L["q"])
+        caches = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_layers - 1)]
+        qs = [q0] + [q0.clone() for _ in range(n_layers - 1)]
+        kvs = [api.kv_desc(kc, vc, w.n_q_heads) for kc, vc in caches]
+        img = api.ImageTable(w.img_pos, w.img_off)
+        f32 = dict(dtype=torch.float32, device=dev)
+        s_acc, a_acc = torch.zeros(w.n_vis, **f32), torch.zeros(w.n_vis, **f32)
+        shat, cj = torch.zeros(w.n_vis, **f32), torch.zeros(w.n_images, **f32)
+        mask = torch.zeros(w.n_vis, dtype=torch.uint8, device=dev)
+        ws_score = torch.empty(api.score_workspace_bytes(kvs[0], w.n_q, img), dtype=torch.uint8, device=dev)
+        entry = {"workload": w.name, "layers": n_layers, "n_vis": w.n_vis, "n_ctx": w.n_ctx,
+                 "dtype": w.dtype, "budgets": {}}
+        for label in labels:
+            k = w.budgets[label]
+            idx = torch.zeros(k, dtype=torch.int32, device=dev)
+            pos = torch.zeros(k, dtype=torch.int32, device=dev)
+
+            def score_select():
+                for li in range(n_layers):
+                    api.conduit_score(kvs[li], qs[li], w.q_pos0, img, s_acc, a_acc, accumulate=li > 0,
+                                      ws=ws_score)
+                api.conduit_select_topk(s_acc, a_acc, n_layers, img, 1.0, k, idx, pos, mask_out=mask,
+                                        shat_out=shat, c_out=cj)
+
+            score_select()
+            torch.cuda.synchronize()
+            idx_np = idx.cpu().numpy()
+            pos_np = pos.cpu().numpy().astype(np.int64)
+            kn, vn, qn = (up(L[x][idx_np]) for x in ("k_star", "v_star", "q_star"))
+            k_new = [kn] + [kn.clone() for _ in range(n_layers - 1)]
+            v_new = [vn] + [vn.clone() for _ in range(n_layers - 1)]
+            q_sel = [qn] + [qn.clone() for _ in range(n_layers - 1)]
+            pos_l = pos.long()
+            stale = [(kc[pos_l].clone(), vc[pos_l].clone()) for kc, vc in caches]
+            o = torch.empty((k, w.n_q_heads, w.head_dim), dtype=k0.dtype, device=dev)
+            ws_ref = torch.empty(max(1, api.refresh_workspace_bytes(kvs[0], k)), dtype=torch.uint8, device=dev)
+
+            def step_fn():
+                score_select()
+                for li in range(n_layers):
+                    api.conduit_scatter_kv(kvs[li], pos, k_new[li], v_new[li])
+                    api.conduit_refresh_attn(kvs[li], q_sel[li], pos, o, ws=ws_ref)
+
+            def restore():
+                for (kc, vc), (ks, vs) in zip(caches, stale):
+                    kc[pos_l] = ks
+                    vc[pos_l] = vs
+
+            n_steps, n_warm = max(3, args.steps // 4), 2
+            for _ in range(n_warm):
+                step_fn()
+                restore()
+            torch.cuda.synchronize()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * n_steps)]
+            for i in range(n_steps):
+                if not args.no_scrub:
+                    scrub.fill_(i & 0xFF)
+                ev[2 * i].record(stream)
+                step_fn()
+                ev[2 * i + 1].record(stream)
+                restore()
+            torch.cuda.synchronize()
+            ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(n_steps)]
+            assert torch.equal(pos[:k].long(), pos_l), "selection changed between steps"
+            api.profile_enable(True)
+            step_fn()
+            torch.cuda.synchronize()
+            api.profile_enable(False)
+            restore()
+            kern = {}
+            for name, t in api.profile_records():
+                kern.setdefault(name, []).append(t)
+            ms_step = statistics.mean(ms)
+            rec = {"k": k, "ms_per_step": ms_step, "p10": pct(ms, 10), "p90": pct(ms, 90), "steps": n_steps,
+                   "value": w.n_vis / (ms_step * 1e-3 / n_layers),
+                   "kernels_ms_per_step": {n: sum(v) for n, v in kern.items()}}
+            if "attn_values" in kern:
+                fl = 4.0 * w.n_q_heads * w.head_dim * float(np.sum(pos_np + 1))
+                t_att = statistics.mean(kern["attn_values"])
+                rec["refresh_kernel"] = {"algorithmic_flops_per_launch": fl, "avg_launch_ms": t_att,
+                                         "tflops": fl / (t_att * 1e-3) / 1e12,
+                                         "frac_of_bf16_peak": fl / (t_att * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+            if not args.no_cpu and not (cfg == 5 and label != labels[0]):
+                # (the long document's two budgets differ by one row: its CPU leg runs once)
+                rec["cpu_baseline"] = cpu_workload(w, L, idx_np, pos_np, k, n_layers)
+            entry["budgets"][label] = rec
+            del k_new, v_new, q_sel, stale, o, ws_ref, kn, vn, qn
+        out[f"cfg{cfg}"] = entry
+        del caches, qs, kvs, k0, v0, q0, L
+        torch.cuda.empty_cache()
+    return out
+
+
+def cpu_workload(w, L, idx, pos, k, n_layers):
+    """The float64 oracle on this host for one workload: scoring, reweighting,
+    top-k and merge of one layer plus the refresh attention of its selected
+    rows.  The single-image workloads run in full, with all host threads and
+    again single-threaded; the 28-layer ones time one layer (the long
+    document on a sample of span rows and refreshed rows, scaled) and report
+    the step as 28 such layers, labelled as an extrapolation."""
+    import threadpoolctl
+
+    from oracle import conduit_oracle as O
+
+    def run(score_rows, ref_stride):
+        layer = {"q": L["q"][:score_rows], "k": L["k"], "v": L["v"]}
+        t0 = time.perf_counter()
+        O.select([layer], w.q_pos0, w.img_pos, w.img_off, k, lam=1.0)
+        t1 = time.perf_counter()
+        rows = list(range(0, k, ref_stride))
+        O.refresh_layer(L["k"], L["v"], pos, L["k_star"][idx], L["v_star"][idx], L["q_star"][idx], rows=rows)
+        t2 = time.perf_counter()
+        return (t1 - t0) * (w.n_q / score_rows) + (t2 - t1) * (k / len(rows)), t1 - t0, t2 - t1, len(rows)
+
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info] or [1])
+    if w.cfg_id == 5:
+        score_rows, stride = 16, 64
+    else:
+        score_rows, stride = w.n_q, 1
+    t_layer, ts, tr, nr = run(score_rows, stride)
+    rec = {"value": w.n_vis / t_layer, "unit": "visual tokens/s per layer", "cores": threads,
+           "kind": "oracle", "seconds_per_layer": t_layer,
+           "sample": (f"one layer: scoring of {score_rows} of {w.n_q} span rows ({ts:.2f} s"
+                      + (f", scaled x{w.n_q / score_rows:.0f}" if score_rows < w.n_q else "")
+                      + f"), reweighting, top-k and merge, refresh attention of {nr} of {k} rows "
+                      f"({tr:.2f} s" + (f", scaled x{k / nr:.1f}" if nr < k else "") + "); float64 numpy")}
+    if n_layers > 1:
+        rec["seconds_per_step_extrapolated"] = t_layer * n_layers
+        rec["note"] = f"per-layer rate; the {n_layers}-layer step is extrapolated as {n_layers} x one layer"
+    if w.n_vis <= 1024:
+        with threadpoolctl.threadpool_limits(1):
+            t1, _, _, _ = run(score_rows, stride)
+        rec["single_thread"] = {"value": w.n_vis / t1, "seconds_per_layer": t1, "cores": 1}
+    return rec
 
 
 def provenance():

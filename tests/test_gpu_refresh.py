@@ -175,3 +175,24 @@ def test_kernel_timing_records_each_launch():
     api.profile_enable(True)  # enabling clears the record
     assert api.lib().conduit_profile_count() == 0
     api.profile_enable(False)
+
+
+@pytest.mark.parametrize("norms", [(300.0,), (300.0, 3000.0)], ids=["one_jump", "two_jumps"])
+def test_refresh_large_logit_jumps(norms):
+    """Keys far larger than the rest, placed at separator positions after the
+    first images: for rows that see them, a later key tile's maximum exceeds
+    the reference maximum taken from the split's first keys by far more than
+    2^32, so the attention restarts those items (twice for two jumps).  Every
+    row is checked by the oracle."""
+    w = W.custom(1, 28, 4, 128, 8, 64, [512, 512, 512, 512], 16, "bf16", seed=81)
+    L = w.layer(0)
+    text = O.text_positions(w.n_ctx, w.img_pos, w.img_off)
+    rng = np.random.default_rng(82)
+    for j, nrm in enumerate(norms):
+        p = int(w.img_pos[1 + j]) - 1  # the separator token just before image 1 + j
+        assert p in set(text.tolist())
+        u = rng.standard_normal((w.n_kv_heads, w.head_dim))
+        u /= np.linalg.norm(u, axis=1, keepdims=True)
+        L["k"][p] = w._cast((nrm * u).astype(np.float32))
+    sel = np.sort(rng.choice(w.n_vis, size=240, replace=False))
+    check(w, L, sel)
