@@ -821,53 +821,100 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
   }
 }
 
-// fp32 path: one wave per (row, head) pair over the whole causal key range,
-// 64 keys per step (one per lane), written straight to the final outputs.
+// fp32 path.  A workgroup of four waves takes four consecutive rows of one
+// query head (one wave per (row, head) pair); they share every 64-key tile of
+// K (and V), which is staged in LDS by coalesced 16-byte loads.  For the
+// logits, lane j of a wave takes key t0 + j of the tile: its K row is read
+// from LDS (rows padded to D + 4 floats, so the lanes' rows start in
+// different banks) and the query is held in registers.  The probabilities go
+// through LDS, so that lane e accumulates output dims e, e + 64, ... over the
+// tile's V rows.  Online softmax in the log2 domain, fp32 throughout; the
+// final outputs are written directly (no splits).
+constexpr int kF32Rows = 4;
 template <int D, bool PV>
-__global__ __launch_bounds__(64) void attn_f32_kernel(AttnParams p, DirectOut out) {
+__global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, DirectOut out) {
+  constexpr int KP = D + 4;
   constexpr int PER = D / 64;
-  __shared__ float qs[D];
-  const int64_t gp = blockIdx.x;
-  const int lane = threadIdx.x;
-  const int r = (int)(gp / p.n_q_heads), hq = (int)(gp % p.n_q_heads), kvh = hq / p.group;
-  const int rpos = min(row_position(p.row_pos, p.q_pos0, r), p.n_ctx - 1);
+  constexpr int CH = KT * D / 4 / (kF32Rows * 64);  // 16-byte chunks per thread and tile
+  static_assert(CH * kF32Rows * 64 * 4 == KT * D, "whole chunks");
+  __shared__ alignas(16) float ks[KT][KP];
+  __shared__ alignas(16) float vsm[PV ? KT : 1][PV ? D : 4];
+  __shared__ float ps[kF32Rows][KT];
+  __shared__ int s_maxpos;
+  __shared__ ImageLds img;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int r = blockIdx.x * kF32Rows + wave, hq = blockIdx.y, kvh = hq / p.group;
+  const bool valid = r < p.n_rows;
+  const int rpos = valid ? min(row_position(p.row_pos, p.q_pos0, r), p.n_ctx - 1) : -1;
+  const int64_t gp = (int64_t)(valid ? r : 0) * p.n_q_heads + hq;
   const float *Kg = static_cast<const float *>(p.k);
   const float *Vg = static_cast<const float *>(p.v);
-  const float *q = static_cast<const float *>(p.q) + gp * D;
-  for (int e = lane; e < D; e += 64) qs[e] = q[e];
+  if (tid == 0) s_maxpos = -1;
+  if (p.vis_only) image_table_to_lds(p.tbl, img, tid, kF32Rows * 64);
   __syncthreads();
+  if (lane == 0) atomicMax(&s_maxpos, rpos);
+  float qv[D];
+  {
+    const float *q = static_cast<const float *>(p.q) + gp * D;
+#pragma unroll
+    for (int e = 0; e < D; e += 4) {
+      const f32x4 x = valid ? *reinterpret_cast<const f32x4 *>(q + e) : f32x4{0.f, 0.f, 0.f, 0.f};
+      qv[e] = x[0];
+      qv[e + 1] = x[1];
+      qv[e + 2] = x[2];
+      qv[e + 3] = x[3];
+    }
+  }
+  __syncthreads();
+  const int maxpos = s_maxpos;
   float m = kNegInf, l = 0.f, o[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) o[i] = 0.f;
-  for (int base = 0; base <= rpos; base += 64) {
-    const int kp = base + lane;
-    const bool ok = kp <= rpos && (!p.vis_only || is_visual(p.tbl, kp));
-    float z = kNegInf;
-    if (ok) {
-      const float *kr = Kg + kv_row(p.pages, kp) * p.k_stride + kvh * D;
-      float dot = 0.f;
-#pragma unroll 8
-      for (int e = 0; e < D; ++e) dot = fmaf(qs[e], kr[e], dot);
-      z = dot * p.scale_log2;
+  for (int t0 = 0; t0 <= maxpos; t0 += KT) {
+    // stage the tile (rows past the cache repeat its last row; they are masked)
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int cidx = tid + kF32Rows * 64 * i;
+      const int row = cidx / (D / 4), c4 = cidx % (D / 4);
+      const int64_t src = kv_row(p.pages, min(t0 + row, p.n_ctx - 1));
+      *reinterpret_cast<f32x4 *>(&ks[row][4 * c4]) =
+          *reinterpret_cast<const f32x4 *>(Kg + src * p.k_stride + kvh * D + 4 * c4);
+      if constexpr (PV)
+        *reinterpret_cast<f32x4 *>(&vsm[row][4 * c4]) =
+            *reinterpret_cast<const f32x4 *>(Vg + src * p.v_stride + kvh * D + 4 * c4);
     }
+    __syncthreads();
+    const int key = t0 + lane;
+    const bool vis = key <= rpos && (!p.vis_only || is_visual(img, key));
+    float d4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int e = 0; e < D; e += 4) {
+      const f32x4 kk = *reinterpret_cast<const f32x4 *>(&ks[lane][e]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) d4[u] = fmaf(qv[e + u], kk[u], d4[u]);
+    }
+    const float dot = (d4[0] + d4[1]) + (d4[2] + d4[3]);
+    const float z = vis ? dot * p.scale_log2 : kNegInf;
     const float m_new = fmaxf(m, wave_max(z));
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
+    const float m_use = m_new == kNegInf ? 0.f : m_new;
     const float alpha = fast_exp2(m - m_use);
-    const float e = fast_exp2(z - m_use);
-    l = l * alpha + wave_sum(e);
+    const float pj = fast_exp2(z - m_use);
+    l = l * alpha + wave_sum(pj);
     m = m_new;
     if constexpr (PV) {
+      ps[wave][lane] = pj;  // read back by this wave only; LDS keeps a wave's accesses in order
 #pragma unroll
       for (int i = 0; i < PER; ++i) o[i] *= alpha;
-      const int nk = min(64, rpos - base + 1);
-      for (int j = 0; j < nk; ++j) {
-        const float pj = __shfl(e, j, 64);
-        const float *vr = Vg + kv_row(p.pages, base + j) * p.v_stride + kvh * D;
+#pragma unroll 8
+      for (int j = 0; j < KT; ++j) {
+        const float pjj = ps[wave][j];
 #pragma unroll
-        for (int i = 0; i < PER; ++i) o[i] = fmaf(pj, vr[lane + 64 * i], o[i]);
+        for (int i = 0; i < PER; ++i) o[i] = fmaf(pjj, vsm[j][lane + 64 * i], o[i]);
       }
     }
+    __syncthreads();
   }
+  if (!valid) return;
   const float b = m + __log2f(l);
   if (lane == 0) {
     if (out.row_b) out.row_b[gp] = b;
@@ -986,14 +1033,14 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
 
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s) {
-  const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   ProfScope ps("attn_f32", s);
+  const dim3 grid((p.n_rows + kF32Rows - 1) / kF32Rows, p.n_q_heads);
   if (head_dim == 128) {
-    if (with_values) attn_f32_kernel<128, true><<<n_gp, 64, 0, s>>>(p, out);
-    else attn_f32_kernel<128, false><<<n_gp, 64, 0, s>>>(p, out);
+    if (with_values) attn_f32_kernel<128, true><<<grid, kF32Rows * 64, 0, s>>>(p, out);
+    else attn_f32_kernel<128, false><<<grid, kF32Rows * 64, 0, s>>>(p, out);
   } else {
-    if (with_values) attn_f32_kernel<64, true><<<n_gp, 64, 0, s>>>(p, out);
-    else attn_f32_kernel<64, false><<<n_gp, 64, 0, s>>>(p, out);
+    if (with_values) attn_f32_kernel<64, true><<<grid, kF32Rows * 64, 0, s>>>(p, out);
+    else attn_f32_kernel<64, false><<<grid, kF32Rows * 64, 0, s>>>(p, out);
   }
   return hipGetLastError();
 }

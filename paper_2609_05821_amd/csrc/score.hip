@@ -242,36 +242,71 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   }
 }
 
-// fp32 path: one thread per (visual key, KV head).
+// fp32 path: one wave per 64 visual keys of one KV head.  Lane j holds the
+// K row of key j in registers; the (span token, grouped head) query rows and
+// their log-sum-exps pass through LDS in chunks of 64 (loaded coalesced, read
+// as broadcasts), and the lane sums 2^(c z - b) (or its square) over them.
+// The lane's V row gives its share of ||V_t||^2.
 template <int D>
 __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p, bool rms) {
-  const int t = blockIdx.x * 64 + threadIdx.x;
+  __shared__ alignas(16) float qs[64][D];
+  __shared__ float bs[64];
+  const int lane = threadIdx.x;
+  const int t = blockIdx.x * 64 + lane;
   const int kvh = blockIdx.y;
-  if (t >= p.n_vis) return;
+  const bool tvalid = t < p.n_vis;
   const float *Kg = static_cast<const float *>(p.k);
   const float *Vg = static_cast<const float *>(p.v);
   const float *Qg = static_cast<const float *>(p.q);
-  const int64_t pos = kv_row(p.pages, vis_position(p.tbl, t));  // cache row
+  const int64_t pos = kv_row(p.pages, vis_position(p.tbl, tvalid ? t : p.n_vis - 1));  // cache row
   float kr[D];
 #pragma unroll
-  for (int e = 0; e < D; ++e) kr[e] = Kg[pos * p.k_stride + kvh * D + e];
-  float colsum = 0.f;
-  const int n_pair = p.n_q * p.group;
-  for (int pr = 0; pr < n_pair; ++pr) {
-    const int i = pr / p.group, hq = kvh * p.group + pr % p.group;
-    const float *q = Qg + ((int64_t)i * p.n_q_heads + hq) * D;
-    float dot = 0.f;
-#pragma unroll
-    for (int e = 0; e < D; ++e) dot = fmaf(q[e], kr[e], dot);
-    const float z = fmaf(dot, p.scale_log2, -p.row_b[(int64_t)i * p.n_q_heads + hq]);
-    colsum += fast_exp2(rms ? 2.f * z : z);
+  for (int e = 0; e < D; e += 4) {
+    const f32x4 x = *reinterpret_cast<const f32x4 *>(Kg + pos * p.k_stride + kvh * D + e);
+    kr[e] = x[0];
+    kr[e + 1] = x[1];
+    kr[e + 2] = x[2];
+    kr[e + 3] = x[3];
   }
+  const int G = p.group, n_pair = p.n_q * G;
+  float colsum = 0.f;
+  for (int c0 = 0; c0 < n_pair; c0 += 64) {
+    const int rows = min(64, n_pair - c0);
+    for (int cidx = lane; cidx < rows * (D / 4); cidx += 64) {
+      const int rr = cidx / (D / 4), c4 = cidx % (D / 4), pr = c0 + rr;
+      const int64_t qrow = (int64_t)(pr / G) * p.n_q_heads + kvh * G + pr % G;
+      *reinterpret_cast<f32x4 *>(&qs[rr][4 * c4]) = *reinterpret_cast<const f32x4 *>(Qg + qrow * D + 4 * c4);
+    }
+    if (lane < rows) {
+      const int pr = c0 + lane;
+      bs[lane] = p.row_b[(int64_t)(pr / G) * p.n_q_heads + kvh * G + pr % G];
+    }
+    __syncthreads();
+    for (int rr = 0; rr < rows; ++rr) {
+      float d4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int e = 0; e < D; e += 4) {
+        const f32x4 qq = *reinterpret_cast<const f32x4 *>(&qs[rr][e]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) d4[u] = fmaf(qq[u], kr[e + u], d4[u]);
+      }
+      const float dot = (d4[0] + d4[1]) + (d4[2] + d4[3]);
+      const float z = fmaf(dot, p.scale_log2, -bs[rr]);
+      colsum += fast_exp2(rms ? 2.f * z : z);
+    }
+    __syncthreads();
+  }
+  if (!tvalid) return;
   p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
   if (p.vnorm_in) return;
   float sq = 0.f;
   const float *vr = Vg + pos * p.v_stride + kvh * D;
-#pragma unroll 8
-  for (int e = 0; e < D; ++e) sq = fmaf(vr[e], vr[e], sq);
+#pragma unroll
+  for (int e = 0; e < D; e += 4) {
+    const f32x4 x = *reinterpret_cast<const f32x4 *>(vr + e);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) sq = fmaf(x[u], x[u], sq);
+  }
   p.vsq_part[(int64_t)kvh * p.n_vis + t] = sq;
 }
 
