@@ -828,8 +828,10 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
 // from LDS (rows padded to D + 4 floats, so the lanes' rows start in
 // different banks) and the query is held in registers.  The probabilities go
 // through LDS, so that lane e accumulates output dims e, e + 64, ... over the
-// tile's V rows.  Online softmax in the log2 domain, fp32 throughout; the
-// final outputs are written directly (no splits).
+// tile's V rows.  The next tile's K/V chunks are loaded into registers while
+// the current one is used, and the queries sit in LDS (read as broadcasts).
+// Online softmax in the log2 domain, fp32 throughout; the final outputs are
+// written directly (no splits).
 constexpr int kF32Rows = 4;
 template <int D, bool PV>
 __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, DirectOut out) {
@@ -840,6 +842,7 @@ __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, D
   __shared__ alignas(16) float ks[KT][KP];
   __shared__ alignas(16) float vsm[PV ? KT : 1][PV ? D : 4];
   __shared__ float ps[kF32Rows][KT];
+  __shared__ alignas(16) float qsm[kF32Rows][D];
   __shared__ int s_maxpos;
   __shared__ ImageLds img;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -853,45 +856,49 @@ __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, D
   if (p.vis_only) image_table_to_lds(p.tbl, img, tid, kF32Rows * 64);
   __syncthreads();
   if (lane == 0) atomicMax(&s_maxpos, rpos);
-  float qv[D];
-  {
+  if (lane < D / 4) {
     const float *q = static_cast<const float *>(p.q) + gp * D;
-#pragma unroll
-    for (int e = 0; e < D; e += 4) {
-      const f32x4 x = valid ? *reinterpret_cast<const f32x4 *>(q + e) : f32x4{0.f, 0.f, 0.f, 0.f};
-      qv[e] = x[0];
-      qv[e + 1] = x[1];
-      qv[e + 2] = x[2];
-      qv[e + 3] = x[3];
-    }
+    *reinterpret_cast<f32x4 *>(&qsm[wave][4 * lane]) =
+        valid ? *reinterpret_cast<const f32x4 *>(q + 4 * lane) : f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  __syncthreads();
-  const int maxpos = s_maxpos;
-  float m = kNegInf, l = 0.f, o[PER];
-#pragma unroll
-  for (int i = 0; i < PER; ++i) o[i] = 0.f;
-  for (int t0 = 0; t0 <= maxpos; t0 += KT) {
-    // stage the tile (rows past the cache repeat its last row; they are masked)
+  // A tile's chunks (rows past the cache repeat its last row; they are
+  // masked), loaded into registers one tile ahead.
+  f32x4 kq[CH], vq[PV ? CH : 1];
+  auto load_tile = [&](int t0) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int cidx = tid + kF32Rows * 64 * i;
       const int row = cidx / (D / 4), c4 = cidx % (D / 4);
       const int64_t src = kv_row(p.pages, min(t0 + row, p.n_ctx - 1));
-      *reinterpret_cast<f32x4 *>(&ks[row][4 * c4]) =
-          *reinterpret_cast<const f32x4 *>(Kg + src * p.k_stride + kvh * D + 4 * c4);
-      if constexpr (PV)
-        *reinterpret_cast<f32x4 *>(&vsm[row][4 * c4]) =
-            *reinterpret_cast<const f32x4 *>(Vg + src * p.v_stride + kvh * D + 4 * c4);
+      kq[i] = *reinterpret_cast<const f32x4 *>(Kg + src * p.k_stride + kvh * D + 4 * c4);
+      if constexpr (PV) vq[i] = *reinterpret_cast<const f32x4 *>(Vg + src * p.v_stride + kvh * D + 4 * c4);
+    }
+  };
+  __syncthreads();
+  const int maxpos = s_maxpos;
+  float m = kNegInf, l = 0.f, o[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) o[i] = 0.f;
+  load_tile(0);
+  for (int t0 = 0; t0 <= maxpos; t0 += KT) {
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int cidx = tid + kF32Rows * 64 * i;
+      const int row = cidx / (D / 4), c4 = cidx % (D / 4);
+      *reinterpret_cast<f32x4 *>(&ks[row][4 * c4]) = kq[i];
+      if constexpr (PV) *reinterpret_cast<f32x4 *>(&vsm[row][4 * c4]) = vq[i];
     }
     __syncthreads();
+    if (t0 + KT <= maxpos) load_tile(t0 + KT);
     const int key = t0 + lane;
     const bool vis = key <= rpos && (!p.vis_only || is_visual(img, key));
     float d4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int e = 0; e < D; e += 4) {
       const f32x4 kk = *reinterpret_cast<const f32x4 *>(&ks[lane][e]);
+      const f32x4 qq = *reinterpret_cast<const f32x4 *>(&qsm[wave][e]);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) d4[u] = fmaf(qv[e + u], kk[u], d4[u]);
+      for (int u = 0; u < 4; ++u) d4[u] = fmaf(qq[u], kk[u], d4[u]);
     }
     const float dot = (d4[0] + d4[1]) + (d4[2] + d4[3]);
     const float z = vis ? dot * p.scale_log2 : kNegInf;

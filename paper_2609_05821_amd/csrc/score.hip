@@ -268,6 +268,18 @@ __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p, bool rms
     kr[e + 2] = x[2];
     kr[e + 3] = x[3];
   }
+  // The V row's share of ||V_t||^2, loaded with the K row (in flight during
+  // the first query chunk).
+  float sq = 0.f;
+  if (!p.vnorm_in) {
+    const float *vr = Vg + pos * p.v_stride + kvh * D;
+#pragma unroll
+    for (int e = 0; e < D; e += 4) {
+      const f32x4 x = *reinterpret_cast<const f32x4 *>(vr + e);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sq = fmaf(x[u], x[u], sq);
+    }
+  }
   const int G = p.group, n_pair = p.n_q * G;
   float colsum = 0.f;
   for (int c0 = 0; c0 < n_pair; c0 += 64) {
@@ -298,16 +310,7 @@ __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p, bool rms
   }
   if (!tvalid) return;
   p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
-  if (p.vnorm_in) return;
-  float sq = 0.f;
-  const float *vr = Vg + pos * p.v_stride + kvh * D;
-#pragma unroll
-  for (int e = 0; e < D; e += 4) {
-    const f32x4 x = *reinterpret_cast<const f32x4 *>(vr + e);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) sq = fmaf(x[u], x[u], sq);
-  }
-  p.vsq_part[(int64_t)kvh * p.n_vis + t] = sq;
+  if (!p.vnorm_in) p.vsq_part[(int64_t)kvh * p.n_vis + t] = sq;
 }
 
 __global__ void finalize_kernel(FinalizeParams p) {
