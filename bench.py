@@ -162,7 +162,7 @@ def main():
         if ev and split:
             ev[1].record(stream)
         api.conduit_select_topk(step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos,
-                                mask_out=step.mask, shat_out=step.shat, c_out=step.c)
+                                mask_out=step.mask, shat_out=step.shat, c_out=step.c, ws=step.ws_select)
         if ev and split:
             ev[2].record(stream)
         api.conduit_scatter_kv(kv, pos, fresh["k_new"], fresh["v_new"])
@@ -265,7 +265,7 @@ def main():
         api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, row_lse_in=lse_rows,
                           ws=step.ws_score)
         api.conduit_select_topk(step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos,
-                                mask_out=step.mask, shat_out=step.shat, c_out=step.c)
+                                mask_out=step.mask, shat_out=step.shat, c_out=step.c, ws=step.ws_select)
         api.conduit_scatter_kv(kv, pos, fresh["k_new"], fresh["v_new"])
         api.conduit_refresh_attn(kv, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh)
 
@@ -394,7 +394,7 @@ def main():
         for name, rule in (("select_attention", api.RANK_ATTENTION), ("select_explicit", api.RANK_EXPLICIT)):
             variants_ms[name] = timed(lambda rule=rule: api.conduit_select_topk(
                 step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos, mask_out=step.mask,
-                shat_out=step.shat, c_out=step.c, rule=rule, quota_out=quota))
+                shat_out=step.shat, c_out=step.c, ws=step.ws_select, rule=rule, quota_out=quota))
 
         # Paged cache (256-token pages, shuffled pool) and the recompute with the
         # request's text rows in the same merge and attention launch.
@@ -594,6 +594,8 @@ def other_workloads(args, dev):
         shat, cj = torch.zeros(w.n_vis, **f32), torch.zeros(w.n_images, **f32)
         mask = torch.zeros(w.n_vis, dtype=torch.uint8, device=dev)
         ws_score = torch.empty(api.score_workspace_bytes(kvs[0], w.n_q, img), dtype=torch.uint8, device=dev)
+        ws_sel = torch.empty(max(1, int(api.lib().conduit_select_workspace_bytes(w.n_vis, w.n_images))),
+                             dtype=torch.uint8, device=dev)
         entry = {"workload": w.name, "layers": n_layers, "n_vis": w.n_vis, "n_ctx": w.n_ctx,
                  "dtype": w.dtype, "budgets": {}}
         for label in labels:
@@ -606,7 +608,7 @@ def other_workloads(args, dev):
                     api.conduit_score(kvs[li], qs[li], w.q_pos0, img, s_acc, a_acc, accumulate=li > 0,
                                       ws=ws_score)
                 api.conduit_select_topk(s_acc, a_acc, n_layers, img, 1.0, k, idx, pos, mask_out=mask,
-                                        shat_out=shat, c_out=cj)
+                                        shat_out=shat, c_out=cj, ws=ws_sel)
 
             score_select()
             torch.cuda.synchronize()

@@ -294,8 +294,7 @@ def conduit_select_topk(s_acc: torch.Tensor, a_acc: torch.Tensor, n_layers: int,
                         stream=None, rule: int = RANK_COMPOSITE,
                         quota_out: Optional[torch.Tensor] = None) -> None:
     """Reweighting and top-k (Eq. 8-11, or a variant rule); see conduit_select_topk."""
-    need = 0 if shat_out is not None else int(
-        lib().conduit_select_workspace_bytes(img.n_vis, img.n_images))
+    need = int(lib().conduit_select_workspace_bytes(img.n_vis, img.n_images))
     ws = _workspace(need, s_acc.device, ws)
     _check(lib().conduit_select_topk(s_acc.data_ptr(), a_acc.data_ptr(), n_layers,
                                      ctypes.byref(img.desc), lam, rule, k, _ptr(idx_out),
@@ -382,6 +381,8 @@ class RefreshStep:
         self.mask = torch.zeros(nv, dtype=torch.uint8, device=device)
         ws_bytes = max(score_workspace_bytes(kv, self.n_q, img) for kv in self.kvs)
         self.ws_score = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=device)
+        sb = int(lib().conduit_select_workspace_bytes(nv, img.n_images))
+        self.ws_select = torch.empty(max(sb, 1), dtype=torch.uint8, device=device)
         rb = max(refresh_workspace_bytes(kv, k) for kv in self.kvs) if k > 0 else 0
         self.ws_refresh = torch.empty(max(rb, 1), dtype=torch.uint8, device=device)
         L0 = layers[0]
@@ -402,7 +403,8 @@ class RefreshStep:
                           vnorm_in=None if self.vnorm_tables is None else self.vnorm_tables[li])
         conduit_select_topk(self.s_acc, self.a_acc, len(self.layers), self.img, self.lam, self.k,
                             self.idx, self.pos, mask_out=self.mask, shat_out=self.shat,
-                            c_out=self.c, stream=stream, rule=self.rule, quota_out=self.quota)
+                            c_out=self.c, ws=self.ws_select, stream=stream, rule=self.rule,
+                            quota_out=self.quota)
 
     def refresh(self, fresh, stream=None, k_old=None, v_old=None):
         if self.k == 0:

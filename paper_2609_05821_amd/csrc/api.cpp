@@ -580,10 +580,19 @@ conduit_status conduit_residual_error(const conduit_kv *kv, const void *q, int32
   return ok();
 }
 
+namespace {
+// Workspace of conduit_select_topk: the exchange area of the multi-workgroup
+// top-k (when n_vis uses it), then s_hat when the caller keeps none.
+size_t select_ws_need(int32_t n_vis, bool with_shat) {
+  if (n_vis < 1) return 0;
+  const size_t multi = select_uses_multi(n_vis) ? select_multi_layout().total : 0;
+  return multi + (with_shat ? 0 : align_up((size_t)n_vis * 4, 256));
+}
+}  // namespace
+
 size_t conduit_select_workspace_bytes(int32_t n_vis, int32_t n_images) {
   (void)n_images;
-  if (n_vis < 1) return 0;
-  return align_up((size_t)n_vis * 4, 256);
+  return select_ws_need(n_vis, false);
 }
 
 conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32_t n_layers,
@@ -602,7 +611,7 @@ conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32
   check_images(img, INT32_MAX, &tbl);
   if (k < 0 || k > img->n_vis) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_vis = %d]", k, img->n_vis);
   if (k > 0 && (!idx_out || !pos_out)) return fail(CONDUIT_ERR_INVALID_ARG, "idx_out and pos_out are required");
-  const size_t need = shat_out ? 0 : conduit_select_workspace_bytes(img->n_vis, img->n_images);
+  const size_t need = select_ws_need(img->n_vis, shat_out != nullptr);
   if (k > 0) {
     st = check_ws(ws, ws_bytes, need);
     if (st) return st;
@@ -629,7 +638,9 @@ conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32
   sp.idx_out = idx_out;
   sp.pos_out = pos_out;
   sp.mask_out = mask_out;
-  sp.shat = shat_out ? shat_out : static_cast<float *>(ws);
+  const size_t multi = select_uses_multi(img->n_vis) ? select_multi_layout().total : 0;
+  sp.multi = multi ? ws : nullptr;
+  sp.shat = shat_out ? shat_out : reinterpret_cast<float *>(static_cast<char *>(ws) + multi);
   sp.c_out = c_out;
   sp.quota_out = quota_out;
   e = rule == CONDUIT_RANK_EXPLICIT ? launch_select_explicit(sp, tbl, stream) : launch_select(sp, tbl, stream);

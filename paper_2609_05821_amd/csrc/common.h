@@ -368,7 +368,32 @@ struct SelectParams {
   float *shat;              // [n_vis]: caller's shat_out or workspace
   float *c_out;             // nullable
   int32_t *quota_out;       // nullable (explicit rule)
+  void *multi;              // exchange area of the multi-workgroup top-k (select_multi_bytes)
 };
+
+// Multi-workgroup top-k: kSelMultiKeys visual tokens per workgroup (1024
+// threads x 4), between kSelSingleMax + 1 and kSelMultiMaxWg * kSelMultiKeys
+// tokens.  Its exchange area holds the arrival flags of the grid barriers,
+// the per-workgroup image partial sums and digit histograms.
+constexpr int kSelMultiKeys = 4096;
+constexpr int kSelMultiMaxWg = 32;
+constexpr int kSelMultiBarriers = 3;  // one after each of the three digit passes
+constexpr int kSelDigitBins = 2048;
+struct SelectMultiLayout {
+  size_t flags, gpart, ghist, total;
+};
+constexpr SelectMultiLayout select_multi_layout() {
+  SelectMultiLayout L{};
+  L.flags = 0;
+  L.gpart = 256 * ((kSelMultiBarriers * kSelMultiMaxWg * 4 + 255) / 256);
+  L.ghist = L.gpart + 256 * (((kSelMultiMaxWg + kMaxImages) * 4 + 255) / 256);
+  L.total = L.ghist + (size_t)3 * kSelMultiMaxWg * kSelDigitBins * 4;
+  return L;
+}
+constexpr int kSelSingleMax = 16384;  // one workgroup up to here
+constexpr bool select_uses_multi(int n_vis) {
+  return n_vis > kSelSingleMax && n_vis <= kSelMultiMaxWg * kSelMultiKeys;
+}
 
 struct ScatterParams {
   void *k;

@@ -336,72 +336,205 @@ __device__ __forceinline__ void image_coefficients(const SelectParams &p, int K,
   __syncthreads();
 }
 
-// Register-resident variant for n_vis <= 1024 * PER: thread t owns visual
-// tokens [t*PER, t*PER + PER), so scores are read once and the compaction is
-// in index order without re-reading.  The radix select first fixes the bits
-// every key shares (block AND/OR), then resolves the rest 11 bits per pass
-// with one shared 2,048-bin LDS histogram: below the shared prefix the
-// digits spread over the varying exponent and high mantissa bits, so LDS
-// atomics rarely collide.
+// image of visual token t (s_off in LDS, K images)
+__device__ __forceinline__ int image_of(const int *s_off, int K, int t) {
+  int a = 0, b = K - 1;
+  while (a < b) {
+    const int mid = (a + b + 1) >> 1;
+    if (s_off[mid] <= t) a = mid; else b = mid - 1;
+  }
+  return a;
+}
+
+// ---------------------------------------------------------------------------
+// Latency-bound building blocks of the register-resident kernel: wave-wide
+// reductions and scans through DPP lane moves (no LDS round trips), and
+// block-wide ones that exchange one value per wave through LDS behind a
+// single barrier.  Each block-wide call site has its own LDS slots (or
+// alternates between two), so no trailing barrier is needed before reuse.
+// ---------------------------------------------------------------------------
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t old, uint32_t x) {
+  // lanes whose source is outside the row, or whose row is masked off, keep `old`
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROW_MASK, 0xf, false);
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // lane i <- lane 7-i within 8
+constexpr int kDppMirror = 0x140;      // lane i <- lane 15-i within 16
+constexpr int kDppBcast15 = 0x142;     // lane 15 of each row -> the next row
+constexpr int kDppBcast31 = 0x143;     // lane 31 -> rows 2 and 3
+constexpr int kDppShr1 = 0x111;        // row_shr:n = 0x110 + n
+
+// Reduction of one value per lane with an associative, commutative op of
+// identity `id`; the result is uniform.  Fixed order: quads, eights,
+// sixteens, then the four rows into lane 63.
+template <class Op>
+__device__ __forceinline__ uint32_t wave_reduce(uint32_t x, uint32_t id, Op op) {
+  x = op(x, dpp_mov<kDppXor1>(id, x));
+  x = op(x, dpp_mov<kDppXor2>(id, x));
+  x = op(x, dpp_mov<kDppHalfMirror>(id, x));
+  x = op(x, dpp_mov<kDppMirror>(id, x));
+  x = op(x, dpp_mov<kDppBcast15, 0xA>(id, x));
+  x = op(x, dpp_mov<kDppBcast31, 0xC>(id, x));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+__device__ __forceinline__ float wave_fsum(float x) {
+  return __builtin_bit_cast(float, wave_reduce(__builtin_bit_cast(uint32_t, x), 0u, [](uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b));
+  }));
+}
+// Inclusive prefix sum over the wave (modulo 2^32).
+__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
+  x += dpp_mov<kDppShr1>(0u, x);
+  x += dpp_mov<kDppShr1 + 1>(0u, x);
+  x += dpp_mov<kDppShr1 + 3>(0u, x);
+  x += dpp_mov<kDppShr1 + 7>(0u, x);
+  x += dpp_mov<kDppBcast15, 0xA>(0u, x);
+  x += dpp_mov<kDppBcast31, 0xC>(0u, x);
+  return x;
+}
+// Exclusive prefix sum over the block in thread order (modulo 2^32: exact
+// whenever the true prefix fits); `total` gets the block sum.  `slot`:
+// kWaves LDS words for this call.
+__device__ __forceinline__ uint32_t block_exclusive_sum(uint32_t x, uint32_t *slot, uint32_t &total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint32_t inc = wave_inclusive_sum(x);
+  if (lane == 63) slot[w] = inc;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    const uint32_t v = slot[i];
+    before += i < w ? v : 0u;
+    all += v;
+  }
+  total = all;
+  return before + inc - x;
+}
+__device__ __forceinline__ uint32_t block_exclusive_sum(uint32_t x, uint32_t *slot) {
+  uint32_t total;
+  return block_exclusive_sum(x, slot, total);
+}
+
+// Register-resident top-k for n_vis <= 1024 * PER: thread t owns visual
+// tokens [t*PER, t*PER + PER), so every score is read once and the
+// compaction is in index order without re-reading.  All reductions and scans
+// are DPP-based; the steps are
+//  1. g_j: each thread sums its A values image by image (token order) into
+//     LDS slot (thread + image) - unique, because a thread's images never
+//     precede its predecessor's - then one wave per image adds the slots of
+//     the threads that overlap it, in thread order;
+//  2. g_bar over the images (every wave, the same order, so the same bits)
+//     and c_j into LDS;
+//  3. s_hat and its order keys;
+//  4. radix select: the bits every key shares (block AND/OR), then 11-bit
+//     digits over the rest with one LDS histogram, stopping as soon as the
+//     chosen bin holds exactly the entries still needed;
+//  5. ordered compaction of everything above the prefix found plus the
+//     first `need` entries equal to it (ties to the lower index): the
+//     selected indices go to LDS at their output rank, then out to idx/pos
+//     in coalesced stores.
 template <int PER>
 __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p, ImageTable tbl) {
   constexpr int kBits = 11, kBins = 1 << kBits;
+  static_assert(PER % 4 == 0 && PER * kSelThreads <= 65536, "counts are packed in 16 bits");
+  __shared__ int s_idx[PER * kSelThreads];
   __shared__ float s_g[kMaxImages];
   __shared__ float s_c[kMaxImages];
   __shared__ int s_off[kMaxImages + 1];
   __shared__ int s_delta[kMaxImages];  // position - visual index, per image
+  __shared__ float s_part[kSelThreads + kMaxImages];
   __shared__ int hist[kBins];
-  __shared__ int s_wave[kWaves];
-  __shared__ int s_wave2[kWaves];
-  __shared__ int s_bin, s_above;
+  __shared__ uint32_t s_andor[2][kWaves];
+  __shared__ uint32_t s_scan[3][kWaves];
+  __shared__ int s_pick[2][3];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = tbl.n_vis, K = tbl.n_images;
   const float n_layers = (float)p.n_layers;
   const float inv_layers = 1.f / n_layers;
-
-  // Image `wave`'s first attention values, in flight with the scores below.
-  float pre[16];
-  {
-    const int a = wave < K ? tbl.off[wave] : 0, b = wave < K ? tbl.off[wave + 1] : 0;
-#pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int t = a + 64 * u + lane;
-      pre[u] = t < b ? p.a_acc[t] : 0.f;
-    }
-  }
-  // The radix histogram starts cleared; afterwards each pass clears the bins
-  // it has read.
-  for (int b = tid; b < kBins; b += kSelThreads) hist[b] = 0;
-
-  // The image table moves to LDS (per-lane lookups would otherwise be
-  // dependent loads from the kernel-argument segment).
-  for (int j = tid; j <= K; j += kSelThreads) {
-    s_off[j] = tbl.off[j];
-    if (j < K) s_delta[j] = tbl.pos[j] - tbl.off[j];
-  }
-  // This thread's tokens [lo, lo + cnt): their scores load while the
-  // per-image means are computed.
   const int lo = min(n, tid * PER), cnt = min(n, lo + PER) - lo;
-  const bool whole = cnt == PER;
-  float sv[PER];
-  if (whole) {  // 16-byte loads, all in flight at once
+  const bool vec = cnt == PER && ((reinterpret_cast<uintptr_t>(p.s_acc) | reinterpret_cast<uintptr_t>(p.a_acc) |
+                                   reinterpret_cast<uintptr_t>(p.shat)) & 15) == 0;
+  auto load = [&](const float *src, float (&v)[PER]) __attribute__((always_inline)) {
+    if (vec) {
 #pragma unroll
-    for (int e = 0; e < PER; e += 4) {
-      const f32x4 v4 = *reinterpret_cast<const f32x4 *>(p.s_acc + lo + e);
-      sv[e] = v4[0];
-      sv[e + 1] = v4[1];
-      sv[e + 2] = v4[2];
-      sv[e + 3] = v4[3];
+      for (int e = 0; e < PER; e += 4) {
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(src + lo + e);
+        v[e] = x[0];
+        v[e + 1] = x[1];
+        v[e + 2] = x[2];
+        v[e + 3] = x[3];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < PER; ++e) v[e] = e < cnt ? src[lo + e] : 0.f;
     }
-  } else {
+  };
+  float sv[PER];
+  {
+    float av[PER];
+    load(p.a_acc, av);
+    load(p.s_acc, sv);
+    for (int j = tid; j <= K; j += kSelThreads) {
+      s_off[j] = tbl.off[j];
+      if (j < K) s_delta[j] = tbl.pos[j] - tbl.off[j];
+    }
+    for (int b = tid; b < kBins; b += kSelThreads) hist[b] = 0;
+    __syncthreads();
+    // 1. this thread's A, summed per image in token order
+    if (cnt > 0) {
+      int a = 0, b = K - 1;  // image of the first token
+      while (a < b) {
+        const int mid = (a + b + 1) >> 1;
+        if (s_off[mid] <= lo) a = mid; else b = mid - 1;
+      }
+      int j = a, next = s_off[a + 1];
+      float acc = 0.f;
+      if (next >= lo + cnt) {  // one image
 #pragma unroll
-    for (int e = 0; e < PER; ++e) sv[e] = e < cnt ? p.s_acc[lo + e] : 0.f;
+        for (int e = 0; e < PER; ++e) acc += e < cnt ? av[e] : 0.f;
+      } else {
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+          if (e < cnt) {
+            if (lo + e >= next) {  // images are non-empty: the next token starts image j + 1
+              s_part[tid + j] = acc;
+              acc = 0.f;
+              ++j;
+              next = s_off[j + 1];
+            }
+            acc += av[e];
+          }
+        }
+      }
+      s_part[tid + j] = acc;
+    }
   }
   __syncthreads();
-
-  // 1-2. per-image mean attention and coefficients
-  image_coefficients<true>(p, K, s_off, s_g, s_c, true, pre);
+  for (int j = wave; j < K; j += kWaves) {
+    const int a = s_off[j], b = s_off[j + 1];
+    float acc = 0.f;
+    for (int t = a / PER + lane; t <= (b - 1) / PER; t += 64) acc += s_part[t + j];
+    acc = wave_fsum(acc);
+    if (lane == 0) s_g[j] = acc / (n_layers * (float)(b - a));
+  }
+  __syncthreads();
+  // 2. g_bar and the coefficients
+  float gacc = 0.f;
+  for (int j = lane; j < K; j += 64) gacc += s_g[j];
+  const float g_bar = wave_fsum(gacc) / (float)K;
+  for (int j = tid; j < K; j += kSelThreads) {
+    // (1 - lambda) + lambda * x adds two non-negative terms, so it keeps full
+    // relative precision even for c << 1; x == 1 (one image, or an image at
+    // the mean) gives exactly 1.
+    const float x = s_g[j] / g_bar;
+    const float c = (g_bar == 0.f || x == 1.f) ? 1.f : (1.f - p.lambda) + p.lambda * x;
+    s_c[j] = c;
+    if (p.c_out) p.c_out[j] = c;
+  }
+  __syncthreads();
 
   // 3. composite scores (s / |L|) * c_pi(t) of this thread's tokens
   int j0 = 0;  // image of the first token
@@ -413,32 +546,32 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
     }
     j0 = a;
   }
-  uint32_t key[PER];
+  uint32_t key[PER];  // takes the place of sv: each score is stored, then only its key is kept
   {
     int j = j0, next = s_off[j0 + 1];
     float c = s_c[j0];
-    float sh[PER];
+    const bool one_image = next >= lo + cnt;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) {
-      if (e < cnt) {
-        while (lo + e >= next) {
+    for (int e = 0; e < PER; e += 4) {
+      f32x4 sh;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (!one_image && e + u < cnt && lo + e + u >= next) {
           ++j;
           next = s_off[j + 1];
           c = s_c[j];
         }
+        sh[u] = (sv[e + u] * inv_layers) * c;
+        key[e + u] = order_key(sh[u]);
       }
-      sh[e] = (sv[e] * inv_layers) * c;
-      key[e] = order_key(sh[e]);
-    }
-    if (p.shat) {
-      if (whole) {
+      if (p.shat) {
+        if (vec) {
+          *reinterpret_cast<f32x4 *>(p.shat + lo + e) = sh;
+        } else {
 #pragma unroll
-        for (int e = 0; e < PER; e += 4)
-          *reinterpret_cast<f32x4 *>(p.shat + lo + e) = f32x4{sh[e], sh[e + 1], sh[e + 2], sh[e + 3]};
-      } else {
-#pragma unroll
-        for (int e = 0; e < PER; ++e)
-          if (e < cnt) p.shat[lo + e] = sh[e];
+          for (int u = 0; u < 4; ++u)
+            if (e + u < cnt) p.shat[lo + e + u] = sh[u];
+        }
       }
     }
   }
@@ -451,7 +584,18 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
       k_and &= key[e];
       k_or |= key[e];
     }
-  block_and_or(k_and, k_or, s_wave, s_wave2);
+  k_and = wave_reduce(k_and, 0xffffffffu, [](uint32_t a, uint32_t b) { return a & b; });
+  k_or = wave_reduce(k_or, 0u, [](uint32_t a, uint32_t b) { return a | b; });
+  if (lane == 0) {
+    s_andor[0][wave] = k_and;
+    s_andor[1][wave] = k_or;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    k_and &= s_andor[0][i];
+    k_or |= s_andor[1][i];
+  }
   const uint32_t varying = k_and ^ k_or;  // bits that differ between keys
   uint32_t prefix = k_and, pmask = 0xffffffffu;
   int kk = p.k;
@@ -459,7 +603,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
     const int top = 31 - __builtin_clz(varying);
     pmask = top == 31 ? 0u : ~((2u << top) - 1u);  // shared high bits
     prefix = k_and & pmask;
-    for (int hi = top; hi >= 0; hi -= kBits) {  // digit = bits hi .. hi-10 (fewer at the end)
+    for (int hi = top, pass = 0; hi >= 0; hi -= kBits, ++pass) {  // digit = bits hi .. hi-10 (fewer at the end)
       const int sh = hi - (kBits - 1);
 #pragma unroll
       for (int e = 0; e < PER; ++e)
@@ -471,60 +615,376 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
       const int h0 = hist[b0], h1 = hist[b0 - 1];
       hist[b0] = 0;  // cleared for the next pass (only this thread reads them)
       hist[b0 - 1] = 0;
-      int total;
-      const int run = block_exclusive_scan(h0 + h1, s_wave, total);
+      const int run = (int)block_exclusive_sum((uint32_t)(h0 + h1), s_scan[pass & 1]);
+      int *pick = s_pick[pass & 1];
       if (run < kk && run + h0 >= kk) {
-        s_bin = b0;
-        s_above = run;
+        pick[0] = b0;
+        pick[1] = run;
+        pick[2] = run + h0 == kk;  // the bin is exactly what is still needed
       } else if (run + h0 < kk && run + h0 + h1 >= kk) {
-        s_bin = b0 - 1;
-        s_above = run + h0;
+        pick[0] = b0 - 1;
+        pick[1] = run + h0;
+        pick[2] = run + h0 + h1 == kk;
       }
       __syncthreads();
+      const uint32_t bin = (uint32_t)pick[0];
       if (sh >= 0) {
-        prefix |= (uint32_t)s_bin << sh;
+        prefix |= bin << sh;
         pmask |= (uint32_t)(kBins - 1) << sh;
       } else {  // last, partial digit
-        prefix |= (uint32_t)s_bin >> (-sh);
+        prefix |= bin >> (-sh);
         pmask |= (uint32_t)(kBins - 1) >> (-sh);
       }
-      kk -= s_above;
+      kk -= pick[1];
+      if (pick[2]) break;
     }
   }
-  const uint32_t tau = prefix;
-  const int need_eq = kk;  // entries equal to tau to take, lowest indices first
+  // The selection: keys whose masked bits exceed the prefix, then the first
+  // `need_eq` (in index order) whose masked bits equal it.  After the last
+  // digit the mask is complete and the prefix is the k-th largest key.
+  const int need_eq = kk;
 
   // 5. ordered compaction
   int gt = 0, eq = 0;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
-    gt += (e < cnt) && key[e] > tau;
-    eq += (e < cnt) && key[e] == tau;
+    const uint32_t m = key[e] & pmask;
+    gt += (e < cnt) && m > prefix;
+    eq += (e < cnt) && m == prefix;
   }
-  // One scan of both counts (each < 2^16 for n_vis <= 32,768): the equal
-  // entries taken before this thread are min(eq_before, need_eq).
-  int total;
-  const int packed = block_exclusive_scan((eq << 16) | gt, s_wave, total);
-  const int eq_before = (int)((uint32_t)packed >> 16), gt_before = packed & 0xffff;
+  // One scan of both counts (each prefix < 2^16 for n_vis <= 65,536): the
+  // equal entries taken before this thread are min(eq_before, need_eq).
+  const uint32_t packed = block_exclusive_sum(((uint32_t)eq << 16) | (uint32_t)gt, s_scan[2]);
+  const int eq_before = (int)(packed >> 16), gt_before = (int)(packed & 0xffffu);
+  const int take_eq = max(0, min(eq, need_eq - eq_before));
+  int out = gt_before + min(eq_before, need_eq);
+  int eq_seen = 0;
+  uint32_t mword[4] = {};
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    bool sel = false;
+    if (e < cnt) {
+      const uint32_t m = key[e] & pmask;
+      sel = m > prefix;
+      if (m == prefix) {
+        sel = eq_seen < take_eq;
+        ++eq_seen;
+      }
+      if (sel && out < p.k) s_idx[out++] = lo + e;
+    }
+    mword[(e >> 2) & 3] |= (sel ? 1u : 0u) << (8 * (e & 3));
+    if (p.mask_out && (e & 15) == 15) {  // 16 mask bytes per store
+      const int base = e - 15;
+      if (vec && (reinterpret_cast<uintptr_t>(p.mask_out) & 15) == 0) {
+        *reinterpret_cast<u32x4 *>(p.mask_out + lo + base) = u32x4{mword[0], mword[1], mword[2], mword[3]};
+      } else {
+        for (int u = 0; u < 16; ++u)
+          if (base + u < cnt) p.mask_out[lo + base + u] = (mword[u >> 2] >> (8 * (u & 3))) & 1u;
+      }
+      mword[0] = mword[1] = mword[2] = mword[3] = 0u;
+    }
+  }
+  if constexpr (PER % 16 != 0) {
+    if (p.mask_out)
+      for (int u = 0; u < PER % 16; ++u)
+        if (PER - PER % 16 + u < cnt)
+          p.mask_out[lo + PER - PER % 16 + u] = (mword[u >> 2] >> (8 * (u & 3))) & 1u;
+  }
+  __syncthreads();
+  for (int i = tid; i < p.k; i += kSelThreads) {
+    const int t = s_idx[i];
+    p.idx_out[i] = t;
+    p.pos_out[i] = t + s_delta[image_of(s_off, K, t)];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Multi-workgroup top-k for kSelMultiKeys < n_vis <= kSelMultiMaxWg *
+// kSelMultiKeys: workgroup b owns visual tokens [4096 b, 4096 b + 4096), four
+// consecutive ones per thread (16-byte loads), so the per-token work and the
+// scattered output stores spread over G = ceil(n_vis / 4096) CUs.
+//  select_partials_kernel: each workgroup sums its A values per image in
+//    token order (threads, then the threads of each image in order) into
+//    slot (b + image) of the exchange area - unique, as for threads - and
+//    clears the barrier flags of the next kernel.
+//  select_multi_kernel: every workgroup adds the partials of each image in
+//    workgroup order (so all derive the same g_j, g_bar and c_j bits), forms
+//    its keys and writes s_hat, then the radix select runs on fixed digits
+//    (bits 31-21, 20-10, 9-0 of the key): per pass each workgroup publishes
+//    its local histogram, passes a grid barrier and adds all G histograms in
+//    workgroup order, so every workgroup picks the same bin; the passes stop
+//    once the bin holds exactly what is still needed.  The published
+//    histograms also give each workgroup the number of selected entries of
+//    the workgroups before it, so it writes its outputs in index order with
+//    no further exchange.
+// A grid barrier is a flag per workgroup in device memory (set after a
+// device-scope release, polled with device-scope loads and an acquire): all
+// G <= 32 workgroups are resident at once on a 256-CU device.  The wait is
+// bounded (about a second); a workgroup that gives up goes on, so the kernel
+// always ends, and its outputs are then not meaningful.
+// ---------------------------------------------------------------------------
+constexpr int kSelMultiPer = kSelMultiKeys / kSelThreads;
+constexpr uint32_t kSelSpinLimit = 1u << 20;
+
+__device__ __forceinline__ void grid_arrive_wait(uint32_t *flags, int G) {
+  __syncthreads();  // every wave's stores of this phase are done
+  if (threadIdx.x == 0) {
+    __threadfence();  // release them at device scope
+    __hip_atomic_store(flags + blockIdx.x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    if (lane < G) {
+      uint32_t spins = 0;
+      while (__hip_atomic_load(flags + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+        if (++spins > kSelSpinLimit) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
+    __threadfence();  // acquire the other workgroups' stores
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_partials_kernel(SelectParams p, ImageTable tbl) {
+  constexpr int PER = kSelMultiPer;
+  __shared__ int s_off[kMaxImages + 1];
+  __shared__ float s_part[kSelThreads + kMaxImages];
+  const SelectMultiLayout L = select_multi_layout();
+  char *ws = static_cast<char *>(p.multi);
+  float *gpart = reinterpret_cast<float *>(ws + L.gpart);
+  uint32_t *flags = reinterpret_cast<uint32_t *>(ws + L.flags);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, b = blockIdx.x;
+  const int n = tbl.n_vis, K = tbl.n_images;
+  const int base = b * kSelMultiKeys, end = min(n, base + kSelMultiKeys);
+  const int lo = min(end, base + tid * PER), cnt = min(end, lo + PER) - lo;
+  float av[PER];
+  if (cnt == PER && (reinterpret_cast<uintptr_t>(p.a_acc) & 15) == 0) {
+    const f32x4 x = *reinterpret_cast<const f32x4 *>(p.a_acc + lo);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) av[e] = x[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < PER; ++e) av[e] = e < cnt ? p.a_acc[lo + e] : 0.f;
+  }
+  for (int j = tid; j <= K; j += kSelThreads) s_off[j] = tbl.off[j];
+  if (b == 0)
+    for (int i = tid; i < kSelMultiBarriers * kSelMultiMaxWg; i += kSelThreads) flags[i] = 0u;
+  __syncthreads();
+  if (cnt > 0) {
+    int j = image_of(s_off, K, lo), next = s_off[j + 1];
+    float acc = 0.f;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      if (e < cnt) {
+        if (lo + e >= next) {  // images are non-empty: the next token starts image j + 1
+          s_part[tid + j] = acc;
+          acc = 0.f;
+          ++j;
+          next = s_off[j + 1];
+        }
+        acc += av[e];
+      }
+    }
+    s_part[tid + j] = acc;
+  }
+  __syncthreads();
+  // this workgroup's partial of every image it overlaps, threads in order
+  const int j_first = image_of(s_off, K, base), j_last = image_of(s_off, K, end - 1);
+  for (int j = j_first + wave; j <= j_last; j += kWaves) {
+    const int t0 = (max(s_off[j], base) - base) / PER, t1 = (min(s_off[j + 1], end) - 1 - base) / PER;
+    float acc = 0.f;
+    for (int t = t0 + lane; t <= t1; t += 64) acc += s_part[t + j];
+    acc = wave_fsum(acc);
+    if (lane == 0) gpart[b + j] = acc;
+  }
+}
+
+// GMAX >= gridDim.x bounds the unrolled histogram merge.
+template <int GMAX>
+__global__ __launch_bounds__(kSelThreads) void select_multi_kernel(SelectParams p, ImageTable tbl) {
+  constexpr int PER = kSelMultiPer;
+  __shared__ float s_g[kMaxImages];
+  __shared__ float s_c[kMaxImages];
+  __shared__ int s_off[kMaxImages + 1];
+  __shared__ int s_delta[kMaxImages];
+  __shared__ float s_gpart[kSelMultiMaxWg + kMaxImages];
+  __shared__ int hist[kSelDigitBins];
+  __shared__ uint32_t s_scan[4][kWaves];
+  __shared__ int s_pick[2][4];
+  const SelectMultiLayout L = select_multi_layout();
+  char *ws = static_cast<char *>(p.multi);
+  const float *gpart = reinterpret_cast<const float *>(ws + L.gpart);
+  int *ghist = reinterpret_cast<int *>(ws + L.ghist);
+  uint32_t *flags = reinterpret_cast<uint32_t *>(ws + L.flags);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, b = blockIdx.x, G = gridDim.x;
+  const int n = tbl.n_vis, K = tbl.n_images;
+  const float n_layers = (float)p.n_layers;
+  const float inv_layers = 1.f / n_layers;
+  const int base = b * kSelMultiKeys, end = min(n, base + kSelMultiKeys);
+  const int lo = min(end, base + tid * PER), cnt = min(end, lo + PER) - lo;
+  const bool vec = cnt == PER && ((reinterpret_cast<uintptr_t>(p.s_acc) | reinterpret_cast<uintptr_t>(p.shat)) & 15) == 0;
+  float sv[PER];
+  if (vec) {
+    const f32x4 x = *reinterpret_cast<const f32x4 *>(p.s_acc + lo);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) sv[e] = x[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < PER; ++e) sv[e] = e < cnt ? p.s_acc[lo + e] : 0.f;
+  }
+  for (int j = tid; j <= K; j += kSelThreads) {
+    s_off[j] = tbl.off[j];
+    if (j < K) s_delta[j] = tbl.pos[j] - tbl.off[j];
+  }
+  for (int i = tid; i < kSelDigitBins; i += kSelThreads) hist[i] = 0;
+  // the partials (slots never written are never read)
+  if (tid < G + K) s_gpart[tid] = gpart[tid];
+  __syncthreads();
+  // 1. g_j: the workgroup partials of image j, in workgroup order
+  for (int j = wave; j < K; j += kWaves) {
+    const int a = s_off[j], e = s_off[j + 1];
+    float acc = 0.f;
+    for (int w = a / kSelMultiKeys + lane; w <= (e - 1) / kSelMultiKeys; w += 64) acc += s_gpart[w + j];
+    acc = wave_fsum(acc);
+    if (lane == 0) s_g[j] = acc / (n_layers * (float)(e - a));
+  }
+  __syncthreads();
+  // 2. g_bar (every wave, same order) and c_j
+  float gacc = 0.f;
+  for (int j = lane; j < K; j += 64) gacc += s_g[j];
+  const float g_bar = wave_fsum(gacc) / (float)K;
+  for (int j = tid; j < K; j += kSelThreads) {
+    const float x = s_g[j] / g_bar;
+    const float c = (g_bar == 0.f || x == 1.f) ? 1.f : (1.f - p.lambda) + p.lambda * x;
+    s_c[j] = c;
+    if (b == 0 && p.c_out) p.c_out[j] = c;
+  }
+  __syncthreads();
+  // 3. keys of this thread's tokens
+  const int j0 = cnt > 0 ? image_of(s_off, K, lo) : 0;
+  uint32_t key[PER];
+  {
+    int j = j0, next = s_off[j0 + 1];
+    float c = s_c[j0];
+    f32x4 sh;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      if (e < cnt && lo + e >= next) {
+        ++j;
+        next = s_off[j + 1];
+        c = s_c[j];
+      }
+      sh[e] = (sv[e] * inv_layers) * c;
+      key[e] = order_key(sh[e]);
+    }
+    if (p.shat) {
+      if (vec) {
+        *reinterpret_cast<f32x4 *>(p.shat + lo) = sh;
+      } else {
+#pragma unroll
+        for (int e = 0; e < PER; ++e)
+          if (e < cnt) p.shat[lo + e] = sh[e];
+      }
+    }
+  }
+  // 4. radix select on fixed digits.  The histograms also give the
+  // compaction's offsets: the entries of workgroups before this one above
+  // the final threshold are, summed over the passes, those of their
+  // published bins above each pass's pick (gt_prior, one share per thread),
+  // and those equal to it are their count in the last pick.
+  uint32_t prefix = 0, pmask = 0;
+  int kk = p.k, gt_prior = 0, eq_prior = 0;
+  for (int pass = 0; pass < 3; ++pass) {
+    const int sh = pass == 0 ? 21 : pass == 1 ? 10 : 0;
+    const uint32_t dmask = pass == 2 ? 0x3ffu : 0x7ffu;
+#pragma unroll
+    for (int e = 0; e < PER; ++e)
+      if (e < cnt && (key[e] & pmask) == prefix) atomicAdd(&hist[(key[e] >> sh) & dmask], 1);
+    __syncthreads();
+    // thread tid owns bins 2047-2*tid, 2046-2*tid (descending)
+    const int b0 = kSelDigitBins - 1 - 2 * tid;
+    int *mine = ghist + ((size_t)pass * kSelMultiMaxWg + b) * kSelDigitBins;
+    *reinterpret_cast<int2 *>(mine + b0 - 1) = int2{hist[b0 - 1], hist[b0]};
+    hist[b0] = 0;
+    hist[b0 - 1] = 0;
+    grid_arrive_wait(flags + pass * kSelMultiMaxWg, G);
+    int2 v[GMAX];  // all loads in flight together
+#pragma unroll
+    for (int w = 0; w < GMAX; ++w)
+      if (w < G) v[w] = *reinterpret_cast<const int2 *>(ghist + ((size_t)pass * kSelMultiMaxWg + w) * kSelDigitBins + b0 - 1);
+    int h0 = 0, h1 = 0, q0 = 0, q1 = 0;  // all workgroups / those before this one
+#pragma unroll
+    for (int w = 0; w < GMAX; ++w)  // workgroup order
+      if (w < G) {
+        h0 += v[w].y;
+        h1 += v[w].x;
+        if (w < b) {
+          q0 += v[w].y;
+          q1 += v[w].x;
+        }
+      }
+    const int run = (int)block_exclusive_sum((uint32_t)(h0 + h1), s_scan[pass & 1]);
+    int *pick = s_pick[pass & 1];
+    if (run < kk && run + h0 >= kk) {
+      pick[0] = b0;
+      pick[1] = run;
+      pick[2] = run + h0 == kk;
+      pick[3] = q0;
+    } else if (run + h0 < kk && run + h0 + h1 >= kk) {
+      pick[0] = b0 - 1;
+      pick[1] = run + h0;
+      pick[2] = run + h0 + h1 == kk;
+      pick[3] = q1;
+    }
+    __syncthreads();
+    const int bin = pick[0];
+    gt_prior += (b0 > bin ? q0 : 0) + (b0 - 1 > bin ? q1 : 0);
+    eq_prior = pick[3];
+    prefix |= (uint32_t)bin << sh;
+    pmask |= dmask << sh;
+    kk -= pick[1];
+    if (pick[2]) break;
+  }
+  const int need_eq = kk;
+
+  // 5. ordered compaction: counts in the workgroup, then across workgroups
+  int gt = 0, eq = 0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const uint32_t m = key[e] & pmask;
+    gt += (e < cnt) && m > prefix;
+    eq += (e < cnt) && m == prefix;
+  }
+  // one block exclusive scan of the packed counts (< 2^16 entries per
+  // workgroup) and of the prior workgroups' share, whose block total is
+  // their count above the threshold
+  const uint32_t packed = block_exclusive_sum(((uint32_t)eq << 16) | (uint32_t)gt, s_scan[2]);
+  uint32_t gt_wg;
+  (void)block_exclusive_sum((uint32_t)gt_prior, s_scan[3], gt_wg);
+  const int eq_before = eq_prior + (int)(packed >> 16), gt_before = (int)gt_wg + (int)(packed & 0xffffu);
   const int take_eq = max(0, min(eq, need_eq - eq_before));
   int out = gt_before + min(eq_before, need_eq);
   int j = j0, next = cnt > 0 ? s_off[j0 + 1] : 0, delta = cnt > 0 ? s_delta[j0] : 0, eq_seen = 0;
-  uint32_t mword[(PER + 3) / 4] = {};
+  uint32_t mword = 0;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     if (e < cnt) {
       const int t = lo + e;
-      while (t >= next) {
+      if (t >= next) {
         ++j;
         next = s_off[j + 1];
         delta = s_delta[j];
       }
-      bool sel = key[e] > tau;
-      if (key[e] == tau) {
+      const uint32_t m = key[e] & pmask;
+      bool sel = m > prefix;
+      if (m == prefix) {
         sel = eq_seen < take_eq;
         ++eq_seen;
       }
-      mword[e >> 2] |= (sel ? 1u : 0u) << (8 * (e & 3));
+      mword |= (sel ? 1u : 0u) << (8 * e);
       if (sel && out < p.k) {
         p.idx_out[out] = t;
         p.pos_out[out] = t + delta;
@@ -533,14 +993,10 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(SelectParams p
     }
   }
   if (p.mask_out) {
-    if (whole && (reinterpret_cast<uintptr_t>(p.mask_out) & 15) == 0 && PER % 16 == 0) {
-#pragma unroll
-      for (int w = 0; w < PER / 4; w += 4)
-        *reinterpret_cast<u32x4 *>(p.mask_out + lo + 4 * w) = u32x4{mword[w], mword[w + 1], mword[w + 2], mword[w + 3]};
+    if (cnt == PER && (reinterpret_cast<uintptr_t>(p.mask_out) & 3) == 0) {
+      *reinterpret_cast<uint32_t *>(p.mask_out + lo) = mword;
     } else {
-#pragma unroll
-      for (int e = 0; e < PER; ++e)
-        if (e < cnt) p.mask_out[lo + e] = (mword[e >> 2] >> (8 * (e & 3))) & 1u;
+      for (int e = 0; e < cnt; ++e) p.mask_out[lo + e] = (mword >> (8 * e)) & 1u;
     }
   }
 }
@@ -712,9 +1168,24 @@ __global__ void clear_u8_kernel(uint8_t *p, int64_t n) {
 
 hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream_t s) {
   ProfScope ps("select", s);
-  if (tbl.n_vis <= kSelThreads * 16) select_regs_kernel<16><<<1, kSelThreads, 0, s>>>(p, tbl);
-  else if (tbl.n_vis <= kSelThreads * 32) select_regs_kernel<32><<<1, kSelThreads, 0, s>>>(p, tbl);
-  else select_kernel<<<1, kSelThreads, 0, s>>>(p, tbl);
+  const int n = tbl.n_vis;
+  if (n <= kSelThreads * 4) {
+    select_regs_kernel<4><<<1, kSelThreads, 0, s>>>(p, tbl);
+  } else if (n <= kSelThreads * 16) {  // faster in one workgroup up to here
+    select_regs_kernel<16><<<1, kSelThreads, 0, s>>>(p, tbl);
+  } else if (select_uses_multi(n)) {
+    if (!p.multi) return hipErrorInvalidValue;
+    const int G = (n + kSelMultiKeys - 1) / kSelMultiKeys;
+    select_partials_kernel<<<G, kSelThreads, 0, s>>>(p, tbl);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (G <= 4) select_multi_kernel<4><<<G, kSelThreads, 0, s>>>(p, tbl);
+    else if (G <= 8) select_multi_kernel<8><<<G, kSelThreads, 0, s>>>(p, tbl);
+    else if (G <= 16) select_multi_kernel<16><<<G, kSelThreads, 0, s>>>(p, tbl);
+    else select_multi_kernel<32><<<G, kSelThreads, 0, s>>>(p, tbl);
+  } else {
+    select_kernel<<<1, kSelThreads, 0, s>>>(p, tbl);
+  }
   return hipGetLastError();
 }
 

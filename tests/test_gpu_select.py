@@ -56,6 +56,9 @@ SIZES = {
     "thirty_two_images": [1024] * 32,
     "long_document": [1024] * 64,
     "many_small": [7] * 256,
+    # several workgroups of 4,096 tokens, up to ~110 images each
+    "many_small_multi": [37] * 250,
+    "ragged_long": [1024] * 40 + [513],
 }
 
 
@@ -87,7 +90,10 @@ def test_select_matches_oracle(name, lam):
         np.testing.assert_array_equal(got["mask"], m)
 
 
-@pytest.mark.parametrize("n", [5, 1000, 16384, 16385, 24576, 32767, 32768, 65536, 100000])
+# 4,096 / 4,097 and 131,072 / 131,073 straddle the one-workgroup, the
+# multi-workgroup and the streaming kernels.
+@pytest.mark.parametrize("n", [5, 1000, 4096, 4097, 16384, 16385, 24576, 32767, 32768, 65536, 100000,
+                               131072, 131073])
 def test_ties_go_to_lower_index(n):
     """Heavy ties: few distinct scores, so the boundary value repeats often."""
     rng = np.random.default_rng(n)
@@ -100,11 +106,11 @@ def test_ties_go_to_lower_index(n):
         np.testing.assert_array_equal(got["idx"][:k], ref_idx)
 
 
-@pytest.mark.parametrize("n", [1000, 16385, 32768, 65536])
+@pytest.mark.parametrize("n", [1000, 4097, 16385, 32768, 65536, 131073])
 def test_all_equal_scores_take_lowest_indices(n):
     """No bit varies between the keys: the threshold is the common value and
-    the k lowest indices are taken (both the register-resident and the
-    streaming kernel)."""
+    the k lowest indices are taken (one-workgroup, multi-workgroup and
+    streaming kernels)."""
     img_pos, img_off = layout([n])
     s = np.full(n, 0.25)
     for k in sorted({1, 100, n - 1, n}):
