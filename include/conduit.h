@@ -246,6 +246,13 @@ conduit_status conduit_value_norms(const conduit_kv *kv, const conduit_images *i
  * c_out         nullable device [n_images] fp32: the coefficients c_j.
  * quota_out     nullable device [n_images] int32: the quotas k_j
  *               (CONDUIT_RANK_EXPLICIT only; ignored otherwise).
+ * ws            256-byte aligned device workspace of at least
+ *               conduit_select_workspace_bytes(n_vis, n_images) bytes when
+ *               k > 0 (it holds s_hat when shat_out is NULL, and for
+ *               16,384 < n_vis <= 131,072 the exchange area of the
+ *               multi-workgroup top-k: barrier flags, which the call clears
+ *               itself, partial sums and histograms).  Its contents need no
+ *               initialisation and are not meaningful afterwards.
  * ------------------------------------------------------------------------ */
 size_t conduit_select_workspace_bytes(int32_t n_vis, int32_t n_images);
 
