@@ -130,30 +130,22 @@ constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / 64;
 constexpr int kPlanBins = 2048;  // (size class, KV head) bins; larger sizes share the top class
 
+// Exclusive prefix sum over the block (one call per kernel: s_wave is not
+// reused, so no trailing barrier).
 __device__ int plan_exclusive_scan(int x, int *s_wave, int &total) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int inc = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += y;
-  }
+  const int inc = (int)wave_inclusive_sum((uint32_t)x);
   if (lane == 63) s_wave[w] = inc;
   __syncthreads();
-  if (w == 0) {
-    int v = lane < kPlanWaves ? s_wave[lane] : 0;
+  int before = 0, all = 0;
 #pragma unroll
-    for (int o = 1; o < kPlanWaves; o <<= 1) {
-      const int y = __shfl_up(v, o, 64);
-      if (lane >= o) v += y;
-    }
-    if (lane < kPlanWaves) s_wave[lane] = v;
+  for (int i = 0; i < kPlanWaves; ++i) {
+    const int v = s_wave[i];
+    before += i < w ? v : 0;
+    all += v;
   }
-  __syncthreads();
-  const int excl = inc - x + (w > 0 ? s_wave[w - 1] : 0);
-  total = s_wave[kPlanWaves - 1];
-  __syncthreads();
-  return excl;
+  total = all;
+  return before + inc - x;
 }
 
 __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
@@ -210,8 +202,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
     const int b0 = min(lane * per, n_pb), b1 = min(b0 + per, n_pb);
     int max_tiles = 0;
     for (int b = b0; b < b1; ++b) max_tiles = max(max_tiles, s_max[b] / kAttnKeyTile + 1);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) max_tiles = max(max_tiles, __shfl_xor(max_tiles, o, 64));
+    max_tiles = (int)wave_reduce((uint32_t)max_tiles, 0u, [](uint32_t x, uint32_t y) { return x > y ? x : y; });
 
     // Split size T: the smallest T >= kAttnPlanMinTiles whose item count
     // n_kv * sum_b ceil(tiles_b / T) fits the target (bisection; the count
@@ -219,8 +210,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
     auto count_items = [&](int T) {
       int my = 0;
       for (int b = b0; b < b1; ++b) my += (s_max[b] / kAttnKeyTile + T) / T;  // ceil(tiles / T)
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) my += __shfl_xor(my, o, 64);
+      my = (int)wave_reduce((uint32_t)my, 0u, [](uint32_t x, uint32_t y) { return x + y; });
       return (long long)my * a.n_kv_heads;
     };
     int lo = kAttnPlanMinTiles, hi = max(kAttnPlanMinTiles, max_tiles);
@@ -236,12 +226,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
     // go into a histogram (one count per KV head).
     int my_ns = 0;
     for (int b = b0; b < b1; ++b) my_ns += (s_max[b] / kAttnKeyTile + T) / T;
-    int inc = my_ns;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(inc, o, 64);
-      if (lane >= o) inc += y;
-    }
+    const int inc = (int)wave_inclusive_sum((uint32_t)my_ns);
     int base = inc - my_ns;
     for (int b = b0; b < b1; ++b) {
       const int tiles = s_max[b] / kAttnKeyTile + 1;

@@ -226,6 +226,49 @@ __device__ __forceinline__ bf16x8 v_operand_il(const u16 *at) {
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
+// Wave-wide reductions and scans through DPP lane moves (no LDS round trip,
+// unlike a shuffle).
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t old, uint32_t x) {
+  // lanes whose source is outside the row, or whose row is masked off, keep `old`
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROW_MASK, 0xf, false);
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // lane i <- lane 7-i within 8
+constexpr int kDppMirror = 0x140;      // lane i <- lane 15-i within 16
+constexpr int kDppBcast15 = 0x142;     // lane 15 of each row -> the next row
+constexpr int kDppBcast31 = 0x143;     // lane 31 -> rows 2 and 3
+constexpr int kDppShr1 = 0x111;        // row_shr:n = 0x110 + n
+
+// Reduction of one value per lane with an associative, commutative op of
+// identity `id`; the result is uniform.  Fixed order: quads, eights,
+// sixteens, then the four rows into lane 63.
+template <class Op>
+__device__ __forceinline__ uint32_t wave_reduce(uint32_t x, uint32_t id, Op op) {
+  x = op(x, dpp_mov<kDppXor1>(id, x));
+  x = op(x, dpp_mov<kDppXor2>(id, x));
+  x = op(x, dpp_mov<kDppHalfMirror>(id, x));
+  x = op(x, dpp_mov<kDppMirror>(id, x));
+  x = op(x, dpp_mov<kDppBcast15, 0xA>(id, x));
+  x = op(x, dpp_mov<kDppBcast31, 0xC>(id, x));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+__device__ __forceinline__ float wave_fsum(float x) {
+  return __builtin_bit_cast(float, wave_reduce(__builtin_bit_cast(uint32_t, x), 0u, [](uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b));
+  }));
+}
+// Inclusive prefix sum over the wave (modulo 2^32).
+__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
+  x += dpp_mov<kDppShr1>(0u, x);
+  x += dpp_mov<kDppShr1 + 1>(0u, x);
+  x += dpp_mov<kDppShr1 + 3>(0u, x);
+  x += dpp_mov<kDppShr1 + 7>(0u, x);
+  x += dpp_mov<kDppBcast15, 0xA>(0u, x);
+  x += dpp_mov<kDppBcast31, 0xC>(0u, x);
+  return x;
+}
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);

@@ -28,7 +28,7 @@ constexpr int kColsumThreads = 512;   // 8 waves x 32 keys
 // double-buffered: the next chunk's global loads (unconditional, clamped
 // addresses) are in flight while the current chunk's kQChunk / 32 MFMA row
 // tiles and exponentials run, one barrier per chunk.  The V rows for the
-// value norms are fetched at the start and consumed at the end.
+// value norms are fetched during the last chunk and consumed at the end.
 constexpr int kQChunk = 256;
 constexpr int kLseRegSplits = 24;  // split partials of one row held in registers by the fused merge
 
@@ -123,17 +123,25 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     for (int ks = 0; ks < KS; ++ks) kreg[ks] = as_bf16x8(ld16(krow + ks * 16));
   }
   // V rows of the block's keys for the value norms, 16 bytes per item (not
-  // read when the norms are given).  Both reads are in flight while the row
-  // log-sum-exps are rebuilt below.
+  // read when the norms are given).  They are loaded during the last Q
+  // chunk, so that they do not compete with the K rows and the first chunk
+  // for memory bandwidth at the start.
+  // The rows (page lookups included) are resolved here, so that the loads
+  // inside the chunk loop wait on nothing.
   const bool read_v = p.vnorm_in == nullptr;
   u32x4 vv[VPT];
+  const u16 *vsrc[VPT];
 #pragma unroll
   for (int i = 0; i < VPT; ++i) {
     const int vi = tid + kColsumThreads * i;
     const int tv = min(blockIdx.x * kColsumKeysPerBlock + vi / (D / 8), p.n_vis - 1);
-    vv[i] = read_v ? ld16(Vg + kv_row(p.pages, vis_position(img, tv)) * p.v_stride + kvh * D + (vi % (D / 8)) * 8)
-                   : u32x4{0, 0, 0, 0};
+    vsrc[i] = Vg + kv_row(p.pages, vis_position(img, tv)) * p.v_stride + kvh * D + (vi % (D / 8)) * 8;
   }
+  auto load_v = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) vv[i] = read_v ? ld16(vsrc[i]) : u32x4{0, 0, 0, 0};
+  };
+  const int v_chunk = nch - 1;  // no chunk load (and wait) follows
   if constexpr (FUSE) {
     // b = M + log2(sum_s l_s 2^(m_s - M)) over the splits of the row's
     // block, s ascending, exactly as the statistics merge computes it.  Up
@@ -179,6 +187,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     const int buf = c & 1;
     const bool more = c + 1 < nch;
     if (more) load_chunk(c + 1, qv, bv);
+    if (c == v_chunk) load_v();
     const int rows = min(kQChunk, n_pair - c * kQChunk);
     auto row_step = [&](int r0) __attribute__((always_inline)) {
       f32x16 acc0 = f32x16{}, acc1 = f32x16{};
