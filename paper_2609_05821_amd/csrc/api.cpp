@@ -162,7 +162,7 @@ PlanLayout plan_layout(const conduit_kv *kv, int64_t n_rows, bool with_values, T
 AttnPlan plan_at(void *ws, const PlanLayout &P);
 
 struct ScoreLayout {
-  size_t row_b, colsum, vsq, total;
+  size_t row_b, colsum, vsq, done, total;
   PlanLayout plan;
 };
 
@@ -176,6 +176,7 @@ ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis) {
   if (bf16) L.plan = plan_layout(kv, n_q, false, take);
   L.colsum = take((size_t)kv->n_kv_heads * n_vis * 4);
   L.vsq = take((size_t)kv->n_kv_heads * n_vis * 4);
+  if (bf16) L.done = take((size_t)(n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock * 4);
   L.total = off;
   return L;
 }
@@ -333,8 +334,12 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   int32_t lse_ns = 0;
   bool fuse_lse = false;
   hipError_t e;
+  // bf16: the column-sum workgroups count their arrivals per key block and
+  // the last one finalizes it; the kernel before them clears the counters.
+  int32_t *done = bf16 ? reinterpret_cast<int32_t *>(at(ws, L.done)) : nullptr;
+  const int32_t n_done = (img->n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock;
   if (row_lse_in) {
-    e = launch_lse_to_b(row_lse_in, row_b, n_q * kv->n_q_heads, stream);
+    e = launch_lse_to_b(row_lse_in, row_b, n_q * kv->n_q_heads, done, bf16 ? n_done : 0, stream);
     if (e != hipSuccess) return hip_fail(e, "lse_to_b");
     if (row_lse_out) {
       e = hipMemcpyAsync(row_lse_out, row_lse_in, (size_t)n_q * kv->n_q_heads * 4, hipMemcpyDeviceToDevice,
@@ -371,6 +376,8 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
                                    attn_grid(false) * attn_plan_rounds(false));
       fuse_lse = lse_ns > 1 && (int64_t)n_q * ap.group <= kColsumMaxLsePairs;
       ap.skip_merge = fuse_lse ? 1 : 0;
+      ap.zero_i32 = done;
+      ap.zero_n = n_done;
       e = launch_attn(ap, D, false, stream);
       if (e != hipSuccess) return hip_fail(e, "row statistics");
     } else {
@@ -420,10 +427,14 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
     cs.lse_ppb = attn_pairs_per_block(false);
     cs.lse_out = row_lse_out;
   }
+  cs.done = done;
+  cs.fin = fp;
   e = launch_colsum(cs, D, bf16, agg == CONDUIT_AGG_RMS, stream);
   if (e != hipSuccess) return hip_fail(e, "column sums");
-  e = launch_finalize(fp, stream);
-  if (e != hipSuccess) return hip_fail(e, "finalize");
+  if (!done) {
+    e = launch_finalize(fp, stream);
+    if (e != hipSuccess) return hip_fail(e, "finalize");
+  }
   return ok();
 }
 
@@ -568,7 +579,8 @@ conduit_status conduit_residual_error(const conduit_kv *kv, const void *q, int32
   rp.pairs_pad = L.pairs_pad;
   rp.part = bf16 ? reinterpret_cast<float *>(w + L.part) : nullptr;
   rp.err_out = err_out;
-  hipError_t e = launch_lse_to_b(row_lse_in, reinterpret_cast<float *>(w + L.row_b), n_q * kv->n_q_heads, stream);
+  hipError_t e = launch_lse_to_b(row_lse_in, reinterpret_cast<float *>(w + L.row_b), n_q * kv->n_q_heads, nullptr, 0,
+                                 stream);
   if (e != hipSuccess) return hip_fail(e, "row statistics");
   if (iso) {
     e = launch_value_norms(kv->v, kv->v_stride, pages_of(kv), kv->n_kv_heads * kv->head_dim, bf16, tbl,

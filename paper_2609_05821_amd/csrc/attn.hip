@@ -310,6 +310,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   const int n_pairs = p.n_rows * G;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
+  if (p.zero_i32)
+    for (int i = blockIdx.x * kThreads + tid; i < p.zero_n; i += gridDim.x * kThreads) p.zero_i32[i] = 0;
   const u16 *Kg = static_cast<const u16 *>(p.k);
   const u16 *Vg = static_cast<const u16 *>(p.v);
   const KvPageReader pr = page_reader(p.pages, p.n_ctx);
@@ -920,9 +922,11 @@ __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, D
   }
 }
 
-__global__ void lse_to_b_kernel(const float *lse, float *b, int n) {
+__global__ void lse_to_b_kernel(const float *lse, float *b, int n, int32_t *zero_i32, int zero_n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) b[i] = lse[i] * kLog2e;
+  if (zero_i32)
+    for (int z = i; z < zero_n; z += gridDim.x * blockDim.x) zero_i32[z] = 0;
 }
 
 }  // namespace
@@ -1037,9 +1041,10 @@ hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_d
   return hipGetLastError();
 }
 
-hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, hipStream_t s) {
+hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, int32_t *zero_i32, int32_t zero_n,
+                           hipStream_t s) {
   ProfScope ps("lse_to_b", s);
-  lse_to_b_kernel<<<(n + 255) / 256, 256, 0, s>>>(lse_in, row_b, n);
+  lse_to_b_kernel<<<(n + 255) / 256, 256, 0, s>>>(lse_in, row_b, n, zero_i32, zero_n);
   return hipGetLastError();
 }
 

@@ -331,6 +331,8 @@ struct AttnParams {
   void *o_out;              // [n_rows][H_q][D] bf16 (values only)
   ImageTable tbl;           // read when vis_only
   int32_t skip_merge;       // host side: the split partials are merged by the caller's next kernel
+  int32_t *zero_i32;        // nullable: cleared by the kernel (counters of a later kernel)
+  int32_t zero_n;
 };
 
 // Merge of split partials into final outputs (blocks with n_s > 1).
@@ -397,6 +399,10 @@ struct ColsumParams {
   int32_t lse_ns;
   int32_t lse_ppb;
   float *lse_out;
+  // nullable: arrival counters, one per key block, cleared beforehand; the
+  // last KV head's workgroup of a key block finalizes its keys (fin).
+  int32_t *done;
+  FinalizeParams fin;
 };
 
 struct SelectParams {
@@ -507,7 +513,9 @@ class ProfScope {
 hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipStream_t s);
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s);
-hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, hipStream_t s);
+// lse_in (natural log) to the log2 domain; also clears zero_i32[0, zero_n).
+hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, int32_t *zero_i32, int32_t zero_n,
+                           hipStream_t s);
 // Split count of the closed-form plan the statistics pass uses for rows at
 // q_pos0 + r (pairs per block ppb), as launch_attn picks it.
 int attn_uniform_splits(const AttnParams &p, int ppb, int target);

@@ -35,11 +35,17 @@ constexpr int kLseRegSplits = 24;  // split partials of one row held in register
 // Finalize of one visual token: fixed-order sum over KV heads, the mean (or
 // RMS) over rows and heads, the value norm, s = a v and the layer
 // accumulation of Eq. 7.
+// COHERENT: the partials were written by other workgroups of the running
+// kernel with device-coherent stores, and are read the same way.
+template <bool COHERENT = false>
 __device__ __forceinline__ void finalize_token(const FinalizeParams &p, int t) {
+  auto ld = [](const float *q) {
+    return COHERENT ? __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : *q;
+  };
   float cs = 0.f, sq = 0.f;
   for (int h = 0; h < p.n_kv_heads; ++h) {
-    cs += p.colsum_part[(int64_t)h * p.n_vis + t];
-    if (!p.vnorm_in) sq += p.vsq_part[(int64_t)h * p.n_vis + t];
+    cs += ld(p.colsum_part + (int64_t)h * p.n_vis + t);
+    if (!p.vnorm_in) sq += ld(p.vsq_part + (int64_t)h * p.n_vis + t);
   }
   const float a = p.rms ? sqrtf(cs / p.n_rows_f) : cs / p.n_rows_f;
   const float v = p.vnorm_in ? p.vnorm_in[t] : sqrtf(sq);
@@ -53,6 +59,36 @@ __device__ __forceinline__ void finalize_token(const FinalizeParams &p, int t) {
   }
   if (p.a_out) p.a_out[t] = a;
   if (p.vnorm_out) p.vnorm_out[t] = v;
+}
+
+// Device-coherent store of a partial (written through to where every XCD
+// reads it), so that a later workgroup of the same kernel can read it without
+// a device-scope cache write-back.
+__device__ __forceinline__ void store_coherent(float *q, float v) {
+  __hip_atomic_store(q, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The workgroups of the n_kv_heads KV heads of one key block each count
+// their arrival once their partials are stored (device-coherent stores,
+// waited for before the count); the last to arrive finalizes the block's
+// keys, reading every head's partials in head order with device-coherent
+// loads, as the finalize kernel does.  The counters are cleared by the kernel
+// that runs before this one.  (A device-scope release/acquire fence pair per
+// workgroup would write back and invalidate the XCD's L2 each time, which
+// costs more than the separate finalize launch.)
+__device__ __forceinline__ void finalize_when_last(const ColsumParams &p, int tid, int n_threads) {
+  __shared__ int s_last;
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are complete
+  __syncthreads();
+  if (tid == 0)
+    s_last = __hip_atomic_fetch_add(p.done + blockIdx.x, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+             p.n_kv_heads - 1;
+  __syncthreads();
+  if (!s_last) return;
+  for (int i = tid; i < kColsumKeysPerBlock; i += n_threads) {
+    const int t = blockIdx.x * kColsumKeysPerBlock + i;
+    if (t < p.n_vis) finalize_token<true>(p.fin, t);
+  }
 }
 
 // RMS: accumulate alpha^2 (Eq. 4's surrogate) instead of alpha.
@@ -227,7 +263,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     __syncthreads();
   }
   colsum += __shfl_xor(colsum, 32, 64);
-  if (half == 0 && tvalid) p.colsum_part[(int64_t)kvh * p.n_vis + t] = colsum;
+  if (half == 0 && tvalid) store_coherent(p.colsum_part + (int64_t)kvh * p.n_vis + t, colsum);
 
   // Value-norm proxy: this head's share of ||V_t||^2.  Item vi covers
   // dims (vi % (D/8))*8 .. +7 of key vi / (D/8); the D/8 items of a key sit
@@ -247,8 +283,9 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     for (int o = 1; o < D / 8; o <<= 1) sq += __shfl_xor(sq, o, 64);
     const int vi = tid + kColsumThreads * i;
     const int tv = blockIdx.x * kColsumKeysPerBlock + vi / (D / 8);
-    if (vi % (D / 8) == 0 && tv < p.n_vis) p.vsq_part[(int64_t)kvh * p.n_vis + tv] = sq;
+    if (vi % (D / 8) == 0 && tv < p.n_vis) store_coherent(p.vsq_part + (int64_t)kvh * p.n_vis + tv, sq);
   }
+  if (p.done) finalize_when_last(p, tid, kColsumThreads);
 }
 
 // fp32 path: one wave per 64 visual keys of one KV head.  Lane j holds the
@@ -324,7 +361,7 @@ __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p, bool rms
 
 __global__ void finalize_kernel(FinalizeParams p) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < p.n_vis) finalize_token(p, t);
+  if (t < p.n_vis) finalize_token<false>(p, t);
 }
 
 // Value-norm table (Eq. 7's proxy, tabulated when the cache is built): one
