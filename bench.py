@@ -535,9 +535,10 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_05821_amd", "csrc", f) for f in
 
 
 def traffic_from_profile():
-    """HBM bytes per launch of the refresh attention kernel from the committed
-    FETCH_SIZE / WRITE_SIZE counter summary, scaled by the plain-copy factor
-    recorded there; None when the summary is missing or was taken on another
+    """Bytes per launch of the refresh attention kernel between its L2s and the
+    memory fabric, from the committed counter summary (read requests counted
+    by size, 128 x RDREQ_128B + 64 x RDREQ_64B + 32 x RDREQ_32B, plus the
+    WRITE_SIZE bytes); None when the summary is missing or was taken on another
     version of the kernel source."""
     path = os.path.join(ROOT, "profiles", "attn_values_16k_traffic.md")
     try:
