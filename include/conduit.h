@@ -310,6 +310,39 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
                                     void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ *
+ * The merge and the refresh attention of several layers of one request at
+ * once (the recompute of Sec. 3 runs in every layer with the same selection
+ * M, Algorithm 1).  The merged caches equal those of conduit_scatter_kv called
+ * layer by layer, bit for bit; the attention computes what
+ * conduit_refresh_attn computes per layer, to the same tolerance but not bit
+ * for bit (with many layers in one launch the plan cuts the key ranges into
+ * fewer splits).  The work of up to 16 layers goes into each launch, and the
+ * refresh builds its work plan once (it depends on the rows only).
+ *
+ * kvs        HOST [n_layers] descriptors, 1 <= n_layers <= CONDUIT_MAX_LAYERS;
+ *            every layer shaped like kvs[0] (dtype, heads, head_dim, n_ctx,
+ *            strides, block table, page size and pool): only k and v differ,
+ *            else CONDUIT_ERR_INVALID_ARG.
+ * k_new, v_new, q_sel, o_out  HOST [n_layers] arrays of the per-layer device
+ *            buffers described above (16-byte aligned).
+ * lse_out    nullable HOST [n_layers] array; entries may be NULL.
+ * pos, k     shared by every layer, as above.
+ * ws         conduit_refresh_layers_workspace_bytes(kvs, k, n_layers) bytes
+ *            (the plan and the split partials of 16 layers).
+ * ------------------------------------------------------------------------ */
+#define CONDUIT_MAX_LAYERS 1024
+conduit_status conduit_scatter_kv_layers(const conduit_kv *kvs, int32_t n_layers, const int32_t *pos, int32_t k,
+                                         const void *const *k_new, const void *const *v_new,
+                                         hipStream_t stream);
+
+size_t conduit_refresh_layers_workspace_bytes(const conduit_kv *kv, int32_t k, int32_t n_layers);
+
+conduit_status conduit_refresh_attn_layers(const conduit_kv *kvs, int32_t n_layers, const void *const *q_sel,
+                                           const int32_t *pos, int32_t k, float scale, void *const *o_out,
+                                           float *const *lse_out, void *ws, size_t ws_bytes,
+                                           hipStream_t stream);
+
+/* ------------------------------------------------------------------------ *
  * Residual value-write error of a refresh set, a quality diagnostic of a
  * selection (the local model of Eq. 3; App. D.1 isotropic Monte Carlo
  * estimator; App. D.3 projected error).  For displacement sample m, span row i

@@ -31,7 +31,8 @@ EXPORTS = [
     "conduit_refresh_workspace_bytes", "conduit_refresh_attn", "conduit_status_str",
     "conduit_last_error", "conduit_version", "conduit_profile_enable", "conduit_profile_count",
     "conduit_profile_read", "conduit_value_norms", "conduit_residual_workspace_bytes",
-    "conduit_residual_error", "conduit_score_noalloc",
+    "conduit_residual_error", "conduit_score_noalloc", "conduit_scatter_kv_layers",
+    "conduit_refresh_layers_workspace_bytes", "conduit_refresh_attn_layers",
 ]
 SCORE_NOALLOC_MAX_BYTES = 16 << 20
 
@@ -98,6 +99,13 @@ def lib() -> ctypes.CDLL:
         L.conduit_refresh_workspace_bytes.restype = sz
         L.conduit_refresh_attn.argtypes = [pkv, vp, vp, i32, f32, vp, vp, vp, sz, vp]
         L.conduit_refresh_attn.restype = ctypes.c_int
+        pvp = ctypes.POINTER(ctypes.c_void_p)
+        L.conduit_scatter_kv_layers.argtypes = [pkv, i32, vp, i32, pvp, pvp, vp]
+        L.conduit_scatter_kv_layers.restype = ctypes.c_int
+        L.conduit_refresh_layers_workspace_bytes.argtypes = [pkv, i32, i32]
+        L.conduit_refresh_layers_workspace_bytes.restype = sz
+        L.conduit_refresh_attn_layers.argtypes = [pkv, i32, pvp, vp, i32, f32, pvp, pvp, vp, sz, vp]
+        L.conduit_refresh_attn_layers.restype = ctypes.c_int
         L.conduit_status_str.argtypes = [ctypes.c_int]
         L.conduit_status_str.restype = ctypes.c_char_p
         L.conduit_last_error.argtypes = []
@@ -315,6 +323,35 @@ def refresh_workspace_bytes(kv: KV, k: int) -> int:
     return int(lib().conduit_refresh_workspace_bytes(ctypes.byref(kv), k))
 
 
+def _ptr_array(ts) -> ctypes.Array:
+    return (ctypes.c_void_p * len(ts))(*[None if t is None else t.data_ptr() for t in ts])
+
+
+def conduit_scatter_kv_layers(kvs, pos: torch.Tensor, k_new, v_new, stream=None) -> None:
+    """Cache merge of several layers with the same rows; see conduit_scatter_kv_layers."""
+    arr = (KV * len(kvs))(*kvs)
+    _check(lib().conduit_scatter_kv_layers(arr, len(kvs), pos.data_ptr(), pos.numel(), _ptr_array(k_new),
+                                           _ptr_array(v_new), _stream(stream)))
+
+
+def refresh_layers_workspace_bytes(kv: KV, k: int, n_layers: int) -> int:
+    return int(lib().conduit_refresh_layers_workspace_bytes(ctypes.byref(kv), k, n_layers))
+
+
+def conduit_refresh_attn_layers(kvs, q_sel, pos: torch.Tensor, o_out, lse_out=None,
+                                scale: Optional[float] = None, ws: Optional[torch.Tensor] = None,
+                                stream=None) -> None:
+    """Refresh attention of the same rows in several layers; see conduit_refresh_attn_layers."""
+    k, n = pos.numel(), len(kvs)
+    if scale is None:
+        scale = 1.0 / math.sqrt(kvs[0].head_dim)
+    ws = _workspace(refresh_layers_workspace_bytes(kvs[0], k, n), q_sel[0].device, ws)
+    arr = (KV * n)(*kvs)
+    lse = None if lse_out is None else ctypes.cast(_ptr_array(lse_out), ctypes.POINTER(ctypes.c_void_p))
+    _check(lib().conduit_refresh_attn_layers(arr, n, _ptr_array(q_sel), pos.data_ptr(), k, scale,
+                                             _ptr_array(o_out), lse, _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
 def conduit_refresh_attn(kv: KV, q_sel: torch.Tensor, pos: torch.Tensor, o_out: torch.Tensor,
                          lse_out: Optional[torch.Tensor] = None, scale: Optional[float] = None,
                          ws: Optional[torch.Tensor] = None, stream=None) -> None:
@@ -383,7 +420,7 @@ class RefreshStep:
         self.ws_score = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=device)
         sb = int(lib().conduit_select_workspace_bytes(nv, img.n_images))
         self.ws_select = torch.empty(max(sb, 1), dtype=torch.uint8, device=device)
-        rb = max(refresh_workspace_bytes(kv, k) for kv in self.kvs) if k > 0 else 0
+        rb = refresh_layers_workspace_bytes(self.kvs[0], k, len(self.kvs)) if k > 0 else 0
         self.ws_refresh = torch.empty(max(rb, 1), dtype=torch.uint8, device=device)
         L0 = layers[0]
         self.out = [torch.empty((max(k, 1), n_q_heads, L0["k"].shape[2]), dtype=L0["k"].dtype,
@@ -410,6 +447,14 @@ class RefreshStep:
         if self.k == 0:
             return
         pos = self.pos[: self.k]
+        if len(self.kvs) > 1 and k_old is None and v_old is None:
+            # every layer in a few launches: one merge and one plan for up to 16 layers
+            conduit_scatter_kv_layers(self.kvs, pos, [F["k_new"] for F in fresh], [F["v_new"] for F in fresh],
+                                      stream=stream)
+            conduit_refresh_attn_layers(self.kvs, [F["q_sel"] for F in fresh], pos,
+                                        [o[: self.k] for o in self.out], lse_out=[x[: self.k] for x in self.lse],
+                                        ws=self.ws_refresh, stream=stream)
+            return
         for li, (kv, F) in enumerate(zip(self.kvs, fresh)):
             conduit_scatter_kv(kv, pos, F["k_new"], F["v_new"],
                                None if k_old is None else k_old[li],

@@ -141,12 +141,12 @@ int64_t attn_blocks(int64_t n_rows, int32_t group, bool with_values) {
 }
 
 template <typename Take>
-PlanLayout plan_layout(const conduit_kv *kv, int64_t n_rows, bool with_values, Take &&take) {
+PlanLayout plan_layout(const conduit_kv *kv, int64_t n_rows, bool with_values, Take &&take, int32_t layers = 1) {
   PlanLayout P{};
   const int32_t group = kv->n_q_heads / kv->n_kv_heads;
   const int64_t n_pb = attn_blocks(n_rows, group, with_values);
   const int64_t max_items = attn_max_items(n_pb, kv->n_kv_heads, with_values);
-  const int64_t slots = max_items * attn_pairs_per_block(with_values);
+  const int64_t slots = max_items * attn_pairs_per_block(with_values) * layers;  // layer l's partials l * max_items slots on
   P.n_pb = (int32_t)n_pb;
   P.max_items = (int32_t)max_items;
   P.pb_info = take((size_t)n_pb * 16);
@@ -186,12 +186,13 @@ struct RefreshLayout {
   PlanLayout plan;
 };
 
-RefreshLayout refresh_layout(const conduit_kv *kv, int32_t k) {
+// layers: the layers one attention launch covers (the multi-layer refresh).
+RefreshLayout refresh_layout(const conduit_kv *kv, int32_t k, int32_t layers = 1) {
   RefreshLayout L{};
   if (kv->dtype != CONDUIT_BF16 || k <= 0) return L;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
-  L.plan = plan_layout(kv, k, true, take);
+  L.plan = plan_layout(kv, k, true, take, layers);
   L.total = off;
   return L;
 }
@@ -744,6 +745,149 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
   } else {
     DirectOut out{nullptr, lse_out, static_cast<float *>(o_out)};
     e = launch_attn_f32(ap, out, kv->head_dim, true, stream);
+    if (e != hipSuccess) return hip_fail(e, "refresh attention");
+  }
+  return ok();
+}
+
+namespace {
+
+// The layers of one request: every descriptor valid and shaped like kvs[0]
+// (only the k and v pointers may differ).
+conduit_status check_layers(const conduit_kv *kvs, int32_t n_layers) {
+  if (!kvs) return fail(CONDUIT_ERR_INVALID_ARG, "kvs is NULL");
+  if (n_layers < 1 || n_layers > CONDUIT_MAX_LAYERS)
+    return fail(CONDUIT_ERR_INVALID_ARG, "n_layers = %d outside [1, %d]", n_layers, CONDUIT_MAX_LAYERS);
+  for (int32_t l = 0; l < n_layers; ++l) {
+    const conduit_status st = check_kv(&kvs[l]);
+    if (st) return st;
+    const conduit_kv &a = kvs[0], &b = kvs[l];
+    if (a.dtype != b.dtype || a.n_kv_heads != b.n_kv_heads || a.n_q_heads != b.n_q_heads ||
+        a.head_dim != b.head_dim || a.n_ctx != b.n_ctx || a.k_stride != b.k_stride || a.v_stride != b.v_stride ||
+        a.block_table != b.block_table || a.page_size != b.page_size || a.n_pages != b.n_pages)
+      return fail(CONDUIT_ERR_INVALID_ARG, "layer %d's cache is not shaped like layer 0's", l);
+  }
+  return CONDUIT_OK;
+}
+
+conduit_status check_layer_ptrs(const void *const *ptrs, int32_t n_layers, const char *what, bool nullable) {
+  if (!ptrs) return nullable ? CONDUIT_OK : fail(CONDUIT_ERR_INVALID_ARG, "%s is NULL", what);
+  for (int32_t l = 0; l < n_layers; ++l) {
+    if (!ptrs[l] && nullable) continue;
+    if (!ptrs[l] || !aligned16(ptrs[l]))
+      return fail(CONDUIT_ERR_INVALID_ARG, "%s[%d] must be non-NULL and 16-byte aligned", what, l);
+  }
+  return CONDUIT_OK;
+}
+
+}  // namespace
+
+conduit_status conduit_scatter_kv_layers(const conduit_kv *kvs, int32_t n_layers, const int32_t *pos, int32_t k,
+                                         const void *const *k_new, const void *const *v_new, hipStream_t stream) {
+  conduit_status st = check_layers(kvs, n_layers);
+  if (st) return st;
+  const conduit_kv *kv = &kvs[0];
+  if (k < 0 || k > kv->n_ctx) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_ctx]", k);
+  if (k == 0) return ok();
+  if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
+  st = check_layer_ptrs(k_new, n_layers, "k_new", false);
+  if (st) return st;
+  st = check_layer_ptrs(v_new, n_layers, "v_new", false);
+  if (st) return st;
+  ScatterParams sp{};
+  sp.k_stride_bytes = kv->k_stride * esize(kv->dtype);
+  sp.v_stride_bytes = kv->v_stride * esize(kv->dtype);
+  sp.pages = pages_of(kv);
+  sp.n_ctx = kv->n_ctx;
+  sp.row_bytes = kv->n_kv_heads * kv->head_dim * esize(kv->dtype);
+  sp.pos = pos;
+  sp.n_rows = k;
+  for (int32_t l0 = 0; l0 < n_layers; l0 += kMaxLayerBatch) {
+    ScatterLayers sl{};
+    sl.n = std::min<int32_t>(kMaxLayerBatch, n_layers - l0);
+    for (int32_t i = 0; i < sl.n; ++i) {
+      sl.k[i] = kvs[l0 + i].k;
+      sl.v[i] = kvs[l0 + i].v;
+      sl.k_new[i] = k_new[l0 + i];
+      sl.v_new[i] = v_new[l0 + i];
+    }
+    const hipError_t e = launch_scatter_layers(sp, sl, stream);
+    if (e != hipSuccess) return hip_fail(e, "scatter");
+  }
+  return ok();
+}
+
+size_t conduit_refresh_layers_workspace_bytes(const conduit_kv *kv, int32_t k, int32_t n_layers) {
+  if (n_layers < 1 || n_layers > CONDUIT_MAX_LAYERS) return 0;
+  const size_t one = conduit_refresh_workspace_bytes(kv, k);
+  if (one == 0 || n_layers == 1) return one;
+  return refresh_layout(kv, k, std::min<int32_t>(n_layers, kMaxLayerBatch)).total;
+}
+
+conduit_status conduit_refresh_attn_layers(const conduit_kv *kvs, int32_t n_layers, const void *const *q_sel,
+                                           const int32_t *pos, int32_t k, float scale, void *const *o_out,
+                                           float *const *lse_out, void *ws, size_t ws_bytes, hipStream_t stream) {
+  conduit_status st = check_layers(kvs, n_layers);
+  if (st) return st;
+  const conduit_kv *kv = &kvs[0];
+  if (k < 0 || k > kv->n_ctx) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_ctx]", k);
+  if (!(scale > 0.f) || scale == __builtin_inff()) return fail(CONDUIT_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (k == 0) return ok();
+  if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
+  st = check_layer_ptrs(q_sel, n_layers, "q_sel", false);
+  if (st) return st;
+  st = check_layer_ptrs(reinterpret_cast<const void *const *>(o_out), n_layers, "o_out", false);
+  if (st) return st;
+  if (n_layers == 1)
+    return conduit_refresh_attn(kv, q_sel[0], pos, k, scale, o_out[0], lse_out ? lse_out[0] : nullptr, ws, ws_bytes,
+                                stream);
+  if (kv->dtype == CONDUIT_BF16 && attn_blocks(k, kv->n_q_heads / kv->n_kv_heads, true) > kAttnPlanMaxBlocks)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "k * n_q_heads / n_kv_heads = %lld exceeds %lld",
+                (long long)k * (kv->n_q_heads / kv->n_kv_heads),
+                (long long)kAttnPlanMaxBlocks * attn_pairs_per_block(true));
+  const RefreshLayout L = refresh_layout(kv, k, std::min<int32_t>(n_layers, kMaxLayerBatch));
+  st = check_ws(ws, ws_bytes, L.total);
+  if (st) return st;
+  if (kv->dtype != CONDUIT_BF16) {  // fp32: the per-layer kernel, which needs no workspace
+    for (int32_t l = 0; l < n_layers; ++l) {
+      st = conduit_refresh_attn(&kvs[l], q_sel[l], pos, k, scale, o_out[l], lse_out ? lse_out[l] : nullptr, ws,
+                                ws_bytes, stream);
+      if (st) return st;
+    }
+    return ok();
+  }
+  AttnParams ap{};
+  ap.k = kv->k;
+  ap.v = kv->v;
+  ap.k_stride = kv->k_stride;
+  ap.v_stride = kv->v_stride;
+  ap.pages = pages_of(kv);
+  ap.n_kv_heads = kv->n_kv_heads;
+  ap.group = kv->n_q_heads / kv->n_kv_heads;
+  ap.n_q_heads = kv->n_q_heads;
+  ap.n_ctx = kv->n_ctx;
+  ap.q = q_sel[0];
+  ap.n_rows = k;
+  ap.row_pos = pos;
+  ap.scale_log2 = scale * kLog2e;
+  ap.o_out = o_out[0];
+  ap.plan = plan_at(ws, L.plan);
+  ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
+  ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
+  ap.part_o = reinterpret_cast<u16 *>(at(ws, L.plan.part_o));
+  // One plan (it depends on the rows only), then one attention and one
+  // merge launch per kMaxLayerBatch layers.
+  for (int32_t l0 = 0; l0 < n_layers; l0 += kMaxLayerBatch) {
+    LayerTable lt{};
+    lt.n = std::min<int32_t>(kMaxLayerBatch, n_layers - l0);
+    for (int32_t i = 0; i < lt.n; ++i) {
+      lt.k[i] = kvs[l0 + i].k;
+      lt.v[i] = kvs[l0 + i].v;
+      lt.q[i] = q_sel[l0 + i];
+      lt.o[i] = o_out[l0 + i];
+      lt.lse[i] = lse_out ? lse_out[l0 + i] : nullptr;
+    }
+    const hipError_t e = launch_attn(ap, kv->head_dim, true, stream, &lt, l0 > 0);
     if (e != hipSuccess) return hip_fail(e, "refresh attention");
   }
   return ok();

@@ -297,8 +297,12 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
 // tile; statistics only W = 4 with two workgroups per CU.  The grid is
 // persistent: workgroup g takes items g, 2G' - 1 - g, 2G' + g, ... of the
 // plan (G' = grid size), i.e. snake order over a largest-first list.
-template <int D, bool PV, int W, bool UNI>
-__global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) {
+// ML: several layers per launch (LayerTable); item i of the launch is plan
+// item i mod n of layer i / n (n plan items): layer after layer, each largest
+// item first, so the running workgroups share one or two layers' K/V in the
+// last-level cache.
+template <int D, bool PV, int W, bool UNI, bool ML = false>
+__global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, LayerTable lt) {
   constexpr int kThreads = W * 64;
   constexpr int kPairs = W * 32;  // (row, head) pairs per block
   constexpr int KS = D / 16;      // MFMA k-steps over the head dimension
@@ -314,6 +318,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     for (int i = blockIdx.x * kThreads + tid; i < p.zero_n; i += gridDim.x * kThreads) p.zero_i32[i] = 0;
   const u16 *Kg = static_cast<const u16 *>(p.k);
   const u16 *Vg = static_cast<const u16 *>(p.v);
+  const int n_layers = ML ? lt.n : 1;
   const KvPageReader pr = page_reader(p.pages, p.n_ctx);
   using Geo = TileGeom<D>;
   const int v_lane = v_operand_lane_offset_il<Geo::vPitch>(lane);  // PV operand reads (interleaved V rows)
@@ -341,10 +346,13 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
     xoff0[sl] = ch < D / 8 ? (uint32_t)(((int64_t)row * (isk ? p.k_stride : p.v_stride) + 8 * ch) * 2) : kPadOff;
   }
   const u16 *Qg = static_cast<const u16 *>(p.q);
+  void *o_out = p.o_out;
+  float *lse_out = p.lse_out;
   const float c = p.scale_log2;
   // UNI: the closed-form plan of contiguous rows (no plan loads at all).
   constexpr bool uniform = UNI;
-  const int n_items = uniform ? p.plan.uniform_items : min(p.plan.hdr[0], p.plan.max_items);
+  const int n_plan_items = uniform ? p.plan.uniform_items : min(p.plan.hdr[0], p.plan.max_items);
+  const int n_items = n_plan_items * n_layers;
 
   const int grid = gridDim.x, g = blockIdx.x;
   if (tid == 0) s_restart = 0;
@@ -357,8 +365,19 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
   }
 
   for (int round = 0;; ++round) {
-    const int idx = round * grid + ((round & 1) ? grid - 1 - g : g);
-    if (idx >= n_items) break;
+    const int lidx = round * grid + ((round & 1) ? grid - 1 - g : g);
+    if (lidx >= n_items) break;
+    const int idx = ML ? lidx % n_plan_items : lidx;  // plan item
+    int64_t slot_off = 0;  // partial slots of this item's layer
+    if constexpr (ML) {
+      const int layer = lidx / n_plan_items;
+      Kg = static_cast<const u16 *>(lt.k[layer]);
+      Vg = static_cast<const u16 *>(lt.v[layer]);
+      Qg = static_cast<const u16 *>(lt.q[layer]);
+      o_out = lt.o[layer];
+      lse_out = lt.lse[layer];
+      slot_off = (int64_t)layer * p.plan.max_items;
+    }
     const int uns = p.plan.uniform_ns;
     const int4 item = uniform ? make_int4((idx / uns) % p.n_kv_heads, idx / (uns * p.n_kv_heads), idx % uns, idx)
                               : p.plan.items[idx];  // {kv head, block, split, slot}
@@ -667,12 +686,12 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
       if (single) {
         const float b = m + __log2f(l_tot);
         if (half == 0) {
-          if (p.row_b) p.row_b[gpair] = b;
-          if (p.lse_out) p.lse_out[gpair] = b * kLn2;
+          if (!ML && p.row_b) p.row_b[gpair] = b;
+          if (lse_out) lse_out[gpair] = b * kLn2;
         }
         if constexpr (PV) {
           const float inv = 1.f / l_tot;
-          u16 *dst = static_cast<u16 *>(p.o_out) + (int64_t)gpair * D;
+          u16 *dst = static_cast<u16 *>(o_out) + (int64_t)gpair * D;
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -686,7 +705,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
             }
         }
       } else {
-        const int64_t idx2 = (int64_t)item.w * kPairs + wave * 32 + col;
+        const int64_t idx2 = (item.w + slot_off) * kPairs + wave * 32 + col;
         if (half == 0) {
           p.part_m[idx2] = m;
           p.part_l[idx2] = l_tot;
@@ -727,9 +746,19 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p) 
 constexpr int kMergeBatch = 4;
 constexpr int kMergeDims = 16;
 template <int D>
-__global__ __launch_bounds__(256) void combine_kernel(CombineParams p) {
+__global__ __launch_bounds__(256) void combine_kernel(CombineParams p, LayerTable lt) {
   static_assert(D % kMergeDims == 0, "whole 16-dim slices");
   constexpr int NC = D / kMergeDims;
+  if (lt.n > 0) {  // layer blockIdx.y of a multi-layer launch
+    const int l = blockIdx.y;
+    const int64_t off = (int64_t)l * p.plan.max_items * p.ppb;
+    p.part_m += off;
+    p.part_l += off;
+    if (p.part_o) p.part_o += off * D;
+    p.o_out = lt.o[l];
+    p.lse_out = lt.lse[l];
+    p.row_b = nullptr;
+  }
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const bool values = p.part_o != nullptr;
@@ -957,7 +986,10 @@ int attn_uniform_splits(const AttnParams &p, int ppb, int target) {
   return ns;
 }
 
-hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, hipStream_t s) {
+hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, hipStream_t s, const LayerTable *lt,
+                       bool plan_ready) {
+  const LayerTable lt0 = lt ? *lt : LayerTable{};
+  const bool ml = lt0.n > 0;
   const int ppb = attn_pairs_per_block(with_values);
   AttnParams p = p_in;
   if (!p.row_pos && !with_values) {  // the scoring span: closed-form plan, no plan launch
@@ -977,10 +1009,19 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
   pa.n_kv_heads = p.n_kv_heads;
   pa.n_ctx = p.n_ctx;
   pa.ppb = ppb;
-  pa.target_items = (int32_t)attn_plan_target(p.plan.n_pb, p.n_kv_heads, with_values);
+  // With several layers per launch every plan item runs once per layer, so
+  // when one layer's unsplit items do not fill the grid the plan needs
+  // proportionally fewer splits.  Layers that fill it on their own keep the
+  // one-layer plan: the launch then walks the layers one after the other
+  // like separate launches would (their K/V do not all fit in the last-level
+  // cache at once; unsplit items of very different lengths would spread the
+  // workgroups over several layers).
+  const int64_t one_layer = attn_plan_target(p.plan.n_pb, p.n_kv_heads, with_values);
+  pa.target_items = (int32_t)(ml && (int64_t)p.plan.n_pb * p.n_kv_heads < attn_grid(with_values)
+                                  ? std::max<int64_t>(1, one_layer / lt0.n) : one_layer);
   pa.plan = p.plan;
   hipError_t e = hipSuccess;
-  if (p.plan.uniform_ns == 0) {
+  if (p.plan.uniform_ns == 0 && !plan_ready) {
     ProfScope ps("attn_plan", s);
     attn_plan_kernel<<<1, kPlanThreads, 0, s>>>(pa);
     e = hipGetLastError();
@@ -992,14 +1033,17 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
     ProfScope ps(with_values ? "attn_values" : "attn_stats", s);
     // the closed-form plan only serves the statistics of the scoring span
     const bool uni = p.plan.uniform_ns > 0 && !with_values;
+    if (ml && !with_values) return hipErrorInvalidValue;  // several layers: refresh only
     if (head_dim == 128) {
-      if (with_values) attn_bf16_kernel<128, true, 8, false><<<grid, 8 * 64, 0, s>>>(p);
-      else if (uni) attn_bf16_kernel<128, false, 4, true><<<grid, 4 * 64, 0, s>>>(p);
-      else attn_bf16_kernel<128, false, 4, false><<<grid, 4 * 64, 0, s>>>(p);
+      if (ml) attn_bf16_kernel<128, true, 8, false, true><<<grid, 8 * 64, 0, s>>>(p, lt0);
+      else if (with_values) attn_bf16_kernel<128, true, 8, false><<<grid, 8 * 64, 0, s>>>(p, lt0);
+      else if (uni) attn_bf16_kernel<128, false, 4, true><<<grid, 4 * 64, 0, s>>>(p, lt0);
+      else attn_bf16_kernel<128, false, 4, false><<<grid, 4 * 64, 0, s>>>(p, lt0);
     } else {
-      if (with_values) attn_bf16_kernel<64, true, 8, false><<<grid, 8 * 64, 0, s>>>(p);
-      else if (uni) attn_bf16_kernel<64, false, 4, true><<<grid, 4 * 64, 0, s>>>(p);
-      else attn_bf16_kernel<64, false, 4, false><<<grid, 4 * 64, 0, s>>>(p);
+      if (ml) attn_bf16_kernel<64, true, 8, false, true><<<grid, 8 * 64, 0, s>>>(p, lt0);
+      else if (with_values) attn_bf16_kernel<64, true, 8, false><<<grid, 8 * 64, 0, s>>>(p, lt0);
+      else if (uni) attn_bf16_kernel<64, false, 4, true><<<grid, 4 * 64, 0, s>>>(p, lt0);
+      else attn_bf16_kernel<64, false, 4, false><<<grid, 4 * 64, 0, s>>>(p, lt0);
     }
   }
   e = hipGetLastError();
@@ -1020,10 +1064,10 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
   cp.o_out = with_values ? p.o_out : nullptr;
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   const int64_t n = with_values ? n_gp * (head_dim / kMergeDims) : n_gp;
-  const int blocks = (int)((n + 255) / 256);
+  const dim3 blocks((unsigned)((n + 255) / 256), ml ? (unsigned)lt0.n : 1u);
   ProfScope ps("attn_merge", s);
-  if (head_dim == 128) combine_kernel<128><<<blocks, 256, 0, s>>>(cp);
-  else combine_kernel<64><<<blocks, 256, 0, s>>>(cp);
+  if (head_dim == 128) combine_kernel<128><<<blocks, 256, 0, s>>>(cp, lt0);
+  else combine_kernel<64><<<blocks, 256, 0, s>>>(cp, lt0);
   return hipGetLastError();
 }
 

@@ -335,6 +335,20 @@ struct AttnParams {
   int32_t zero_n;
 };
 
+// Per-layer pointers of a launch that covers several layers of one request
+// (the same rows, shapes and plan in every layer).  n = 0: one layer, the
+// pointers of the parameter block are used.  Split partials of layer l sit
+// l * max_items slots further on.
+constexpr int kMaxLayerBatch = 16;
+struct LayerTable {
+  const void *k[kMaxLayerBatch];
+  const void *v[kMaxLayerBatch];
+  const void *q[kMaxLayerBatch];
+  void *o[kMaxLayerBatch];
+  float *lse[kMaxLayerBatch];
+  int32_t n;
+};
+
 // Merge of split partials into final outputs (blocks with n_s > 1).
 struct CombineParams {
   int32_t n_rows;
@@ -460,6 +474,15 @@ struct ScatterParams {
   void *v_old;              // nullable
 };
 
+// Per-layer cache and fresh-row pointers of a multi-layer merge.
+struct ScatterLayers {
+  void *k[kMaxLayerBatch];
+  void *v[kMaxLayerBatch];
+  const void *k_new[kMaxLayerBatch];
+  const void *v_new[kMaxLayerBatch];
+  int32_t n;
+};
+
 // Residual value-write error of a refresh set: for each displacement sample
 // m and (span row, query head) pair, || sum over non-refreshed visual t of
 // alpha_t xi_t ||^2 with alpha from the row's known log-sum-exp.  The bf16
@@ -510,7 +533,11 @@ class ProfScope {
 // status of the launch.
 // ---------------------------------------------------------------------------
 // bf16 attention: plan, persistent attention over the plan's items, merge.
-hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipStream_t s);
+// lt (nullable): several layers in one launch of each kernel; plan_ready:
+// the device plan was built by an earlier call on the same rows and
+// workspace, so no plan launch.
+hipError_t launch_attn(const AttnParams &p, int head_dim, bool with_values, hipStream_t s,
+                       const LayerTable *lt = nullptr, bool plan_ready = false);
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s);
 // lse_in (natural log) to the log2 domain; also clears zero_i32[0, zero_n).
@@ -527,6 +554,7 @@ hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream
 hipError_t launch_select_explicit(const SelectParams &p, const ImageTable &tbl, hipStream_t s);
 hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
+hipError_t launch_scatter_layers(const ScatterParams &p, const ScatterLayers &sl, hipStream_t s);
 hipError_t launch_residual(const ResidualParams &p, int head_dim, bool bf16, hipStream_t s);
 
 // Size of the fixed device scratch behind conduit_score_noalloc (must equal

@@ -295,3 +295,36 @@ def test_noalloc_rejects_calls_beyond_its_scratch():
     st = L.conduit_score_noalloc(None, fake, 8, 0, ctypes.byref(img.desc), 0, 0, 0.125,
                                  None, None, None, fake, fake, 0, None, None, None)
     assert st == api.ERR_INVALID_ARG
+
+
+def test_layer_calls_reject_and_size():
+    """The multi-layer merge and refresh validate every layer before anything
+    is enqueued; the refresh workspace covers the split partials of 16 layers."""
+    L = api.lib()
+    good = (api.KV * 3)(kv(), kv(k=FAKE + 4096, v=FAKE + 8192), kv())
+    ptrs = (ctypes.c_void_p * 3)(FAKE, FAKE, FAKE)
+    bad_shape = (api.KV * 2)(kv(), kv(n_ctx=1000))
+    bad_align = (ctypes.c_void_p * 3)(FAKE, FAKE + 4, FAKE)
+    null_entry = (ctypes.c_void_p * 3)(FAKE, None, FAKE)
+    sc = L.conduit_scatter_kv_layers
+    assert sc(good, 0, FAKE, 3, ptrs, ptrs, None) == api.ERR_INVALID_ARG
+    assert sc(None, 1, FAKE, 3, ptrs, ptrs, None) == api.ERR_INVALID_ARG
+    assert sc(bad_shape, 2, FAKE, 3, ptrs, ptrs, None) == api.ERR_INVALID_ARG
+    assert sc(good, 3, FAKE, 3, bad_align, ptrs, None) == api.ERR_INVALID_ARG
+    assert sc(good, 3, FAKE, 3, ptrs, null_entry, None) == api.ERR_INVALID_ARG
+    assert sc(good, 3, None, 3, ptrs, ptrs, None) == api.ERR_INVALID_ARG
+    assert sc(good, 3, None, 0, None, None, None) == api.OK  # k = 0: nothing to do
+    rf = L.conduit_refresh_attn_layers
+    one = L.conduit_refresh_workspace_bytes(ctypes.byref(good[0]), 300)
+    many = L.conduit_refresh_layers_workspace_bytes(ctypes.byref(good[0]), 300, 20)
+    assert L.conduit_refresh_layers_workspace_bytes(ctypes.byref(good[0]), 300, 1) == one
+    assert many > one
+    assert L.conduit_refresh_layers_workspace_bytes(ctypes.byref(good[0]), 300, 16) == many
+    assert L.conduit_refresh_layers_workspace_bytes(ctypes.byref(good[0]), 300, 0) == 0
+    assert rf(bad_shape, 2, ptrs, FAKE, 300, 0.1, ptrs, None, FAKE, many, None) == api.ERR_INVALID_ARG
+    assert rf(good, 3, ptrs, FAKE, 300, 0.1, bad_align, None, FAKE, many, None) == api.ERR_INVALID_ARG
+    assert rf(good, 3, ptrs, FAKE, 300, -1.0, ptrs, None, FAKE, many, None) == api.ERR_INVALID_ARG
+    need3 = L.conduit_refresh_layers_workspace_bytes(ctypes.byref(good[0]), 300, 3)
+    assert one < need3 < many
+    assert rf(good, 3, ptrs, FAKE, 300, 0.1, ptrs, None, FAKE, need3 - 256, None) == api.ERR_WORKSPACE
+    assert rf(good, 3, ptrs, None, 0, 0.1, ptrs, None, None, 0, None) == api.OK

@@ -1,0 +1,129 @@
+"""The multi-layer merge and refresh (conduit_scatter_kv_layers,
+conduit_refresh_attn_layers) on the GPU against the CPU oracle, layer by
+layer: the same selection M refreshed in every layer (Sec. 3, Algorithm 1)."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_05821_amd import api, workloads as W
+from tests.gpu_helpers import (DEV, assert_attention, assert_scores, bits, oracle_refresh_rows, to_dev,
+                               to_f64)
+from tests.test_gpu_paged_text import Paged
+
+pytestmark = pytest.mark.gpu
+
+
+def run_layers(w, layers_np, sel, paged=None):
+    P = w.vis_positions()
+    pos = torch.from_numpy(P[sel].astype(np.int32)).to(DEV)
+    if paged is None:
+        caches = [(to_dev(L["k"]), to_dev(L["v"])) for L in layers_np]
+        kvs = [api.kv_desc(kc, vc, w.n_q_heads) for kc, vc in caches]
+    else:
+        caches = [(pg.k, pg.v) for pg in paged]
+        kvs = [pg.kv for pg in paged]
+    k = len(sel)
+    kn = [to_dev(np.ascontiguousarray(L["k_star"][sel])) for L in layers_np]
+    vn = [to_dev(np.ascontiguousarray(L["v_star"][sel])) for L in layers_np]
+    qn = [to_dev(np.ascontiguousarray(L["q_star"][sel])) for L in layers_np]
+    dt = qn[0].dtype
+    out = [torch.empty((k, w.n_q_heads, w.head_dim), dtype=dt, device=DEV) for _ in layers_np]
+    lse = [torch.empty((k, w.n_q_heads), dtype=torch.float32, device=DEV) for _ in layers_np]
+    api.conduit_scatter_kv_layers(kvs, pos, kn, vn)
+    api.conduit_refresh_attn_layers(kvs, qn, pos, out, lse_out=lse)
+    torch.cuda.synchronize()
+    return caches, out, lse
+
+
+def check_layers(w, layers_np, sel, rows=None, paged=None):
+    caches, out, lse = run_layers(w, layers_np, sel, paged)
+    P = w.vis_positions()
+    rows = range(len(sel)) if rows is None else rows
+    r = np.asarray(list(rows))
+    for li, L in enumerate(layers_np):
+        km, vm, o_ref, lse_ref = oracle_refresh_rows(L["k"], L["v"], P[sel], L["k_star"][sel], L["v_star"][sel],
+                                                     L["q_star"][sel], rows)
+        assert_attention(to_f64(out[li])[r], o_ref[r], w.dtype, what=f"O layer {li}")
+        assert_scores(to_f64(lse[li])[r], lse_ref[r], what=f"lse layer {li}")
+        kc, vc = caches[li]
+        if paged is None:
+            np.testing.assert_array_equal(to_f64(kc), km)
+            np.testing.assert_array_equal(to_f64(vc), vm)
+        else:
+            np.testing.assert_array_equal(to_f64(paged[li].logical(kc)), km)
+            np.testing.assert_array_equal(to_f64(paged[li].logical(vc)), vm)
+    return out, lse
+
+
+def small(n_layers, dtype="bf16", seed=81):
+    return W.custom(n_layers, 28, 4, 128, 24, 40, [300, 220, 180], 8, dtype, n_sinks=4, n_relevant=1, seed=seed)
+
+
+@pytest.mark.parametrize("n_layers", [2, 16, 20])
+def test_layers_refresh_matches_oracle(n_layers):
+    """Every row of every layer; 20 layers cross the 16-layer launch batch."""
+    w = small(n_layers)
+    layers_np = [w.layer(li) for li in range(n_layers)]
+    rng = np.random.default_rng(n_layers)
+    sel = np.sort(rng.choice(w.n_vis, size=w.n_vis // 10, replace=False))
+    check_layers(w, layers_np, sel)
+
+
+def test_layers_refresh_28_layer_workload_sampled_rows():
+    """The 28-layer multi-image workload's shape at its 10% budget, three of its
+    layers in one call; every 8th refreshed row of each checked."""
+    w = W.config(3, n_layers=3)
+    layers_np = [w.layer(li) for li in range(3)]
+    k = w.budgets["10%"]
+    rng = np.random.default_rng(33)
+    sel = np.sort(rng.choice(w.n_vis, size=k, replace=False))
+    check_layers(w, layers_np, sel, rows=range(0, k, 8))
+
+
+def test_layers_refresh_fp32():
+    w = W.config(1, n_layers=2)
+    layers_np = [w.layer(li) for li in range(2)]
+    sel = np.arange(0, w.n_vis, 10)
+    check_layers(w, layers_np, sel)
+
+
+def test_layers_refresh_paged():
+    """Two layers in shuffled pools of 64-token pages sharing one block table."""
+    w = small(2, seed=82)
+    layers_np = [w.layer(li) for li in range(2)]
+    pg0 = Paged(w, layers_np[0], 64, seed=5)
+    pg1 = Paged(w, layers_np[1], 64, seed=5)  # same seed: the same table
+    assert torch.equal(pg0.table, pg1.table)
+    pg1.table = pg0.table
+    pg1.kv = api.kv_desc_paged(pg1.k, pg1.v, pg0.table, w.n_ctx, w.n_q_heads)
+    sel = np.arange(3, w.n_vis, 9)
+    check_layers(w, layers_np, sel, paged=[pg0, pg1])
+
+
+def test_layers_equal_single_layer_calls_when_one_layer():
+    """n_layers = 1 is conduit_refresh_attn itself (bit for bit)."""
+    w = small(1, seed=83)
+    L = w.layer(0)
+    sel = np.arange(0, w.n_vis, 5)
+    _, out_m, lse_m = run_layers(w, [L], sel)
+    P = w.vis_positions()
+    kc, vc = to_dev(L["k"]), to_dev(L["v"])
+    kv = api.kv_desc(kc, vc, w.n_q_heads)
+    pos = torch.from_numpy(P[sel].astype(np.int32)).to(DEV)
+    api.conduit_scatter_kv(kv, pos, to_dev(L["k_star"][sel]), to_dev(L["v_star"][sel]))
+    out = torch.empty_like(out_m[0])
+    lse = torch.empty_like(lse_m[0])
+    api.conduit_refresh_attn(kv, to_dev(L["q_star"][sel]), pos, out, lse_out=lse)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(bits(out), bits(out_m[0]))
+    np.testing.assert_array_equal(bits(lse), bits(lse_m[0]))
+
+
+def test_layers_refresh_is_deterministic():
+    w = small(18, seed=84)
+    layers_np = [w.layer(li) for li in range(18)]
+    sel = np.arange(1, w.n_vis, 6)
+    _, o1, l1 = run_layers(w, layers_np, sel)
+    _, o2, l2 = run_layers(w, layers_np, sel)
+    for a, b in zip(o1 + l1, o2 + l2):
+        np.testing.assert_array_equal(bits(a), bits(b))
