@@ -595,7 +595,8 @@ def other_workloads(args, dev):
         s_acc, a_acc = torch.zeros(w.n_vis, **f32), torch.zeros(w.n_vis, **f32)
         shat, cj = torch.zeros(w.n_vis, **f32), torch.zeros(w.n_images, **f32)
         mask = torch.zeros(w.n_vis, dtype=torch.uint8, device=dev)
-        ws_score = torch.empty(api.score_workspace_bytes(kvs[0], w.n_q, img), dtype=torch.uint8, device=dev)
+        ws_score = torch.empty(api.score_layers_workspace_bytes(kvs[0], w.n_q, img, n_layers), dtype=torch.uint8,
+                               device=dev)
         ws_sel = torch.empty(max(1, int(api.lib().conduit_select_workspace_bytes(w.n_vis, w.n_images))),
                              dtype=torch.uint8, device=dev)
         entry = {"workload": w.name, "layers": n_layers, "n_vis": w.n_vis, "n_ctx": w.n_ctx,
@@ -606,9 +607,8 @@ def other_workloads(args, dev):
             pos = torch.zeros(k, dtype=torch.int32, device=dev)
 
             def score_select():
-                for li in range(n_layers):
-                    api.conduit_score(kvs[li], qs[li], w.q_pos0, img, s_acc, a_acc, accumulate=li > 0,
-                                      ws=ws_score)
+                # every layer's scoring in two launches per 16 layers, summed in layer order
+                api.conduit_score_layers(kvs, qs, w.q_pos0, img, s_acc, a_acc, ws=ws_score)
                 api.conduit_select_topk(s_acc, a_acc, n_layers, img, 1.0, k, idx, pos, mask_out=mask,
                                         shat_out=shat, c_out=cj, ws=ws_sel)
 

@@ -89,6 +89,7 @@ typedef enum {
 } conduit_rule;
 
 #define CONDUIT_MAX_IMAGES 256
+#define CONDUIT_MAX_LAYERS 1024  /* layers of one multi-layer call */
 
 /* One layer's KV cache, contiguous or paged.
  *
@@ -203,6 +204,29 @@ conduit_status conduit_score_noalloc(const conduit_kv *kv, const void *q, int32_
                                      float scale, const float *row_lse_in, float *row_lse_out,
                                      const float *vnorm_in, float *s_acc, float *a_acc, int32_t accumulate,
                                      float *a_out, float *vnorm_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ *
+ * The scoring pass over several layers of one request (Eq. 6-7 summed over
+ * the scored layers L of Algorithm 1): conduit_score of every layer in turn,
+ * accumulating into s_acc and a_acc, with the layers' work in a few launches
+ * (up to 16 layers in each).  The results equal those of the per-layer calls
+ * bit for bit (the same arithmetic, layers added in order).
+ *
+ * kvs       HOST [n_layers] descriptors shaped alike (see the multi-layer
+ *           merge below); q: HOST [n_layers] span queries, each as q above.
+ * vnorm_in  nullable HOST [n_layers] array of nullable value-norm tables.
+ * accumulate  0: the first layer overwrites s_acc / a_acc; 1: all add.
+ * ws        conduit_score_layers_workspace_bytes(kvs, n_q, img, n_layers).
+ * No row LSE, per-layer a_t or norm outputs (use conduit_score for those).
+ * ------------------------------------------------------------------------ */
+size_t conduit_score_layers_workspace_bytes(const conduit_kv *kv, int32_t n_q, const conduit_images *img,
+                                           int32_t n_layers);
+
+conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, const void *const *q, int32_t n_q,
+                                    int32_t q_pos0, const conduit_images *img, conduit_norm norm,
+                                    conduit_agg agg, float scale, const float *const *vnorm_in, float *s_acc,
+                                    float *a_acc, int32_t accumulate, void *ws, size_t ws_bytes,
+                                    hipStream_t stream);
 
 /* ------------------------------------------------------------------------ *
  * Value-norm table of one layer (Eq. 7's proxy; Sec. 4.3: the norms depend on
@@ -330,7 +354,6 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
  * ws         conduit_refresh_layers_workspace_bytes(kvs, k, n_layers) bytes
  *            (the plan and the split partials of 16 layers).
  * ------------------------------------------------------------------------ */
-#define CONDUIT_MAX_LAYERS 1024
 conduit_status conduit_scatter_kv_layers(const conduit_kv *kvs, int32_t n_layers, const int32_t *pos, int32_t k,
                                          const void *const *k_new, const void *const *v_new,
                                          hipStream_t stream);

@@ -33,6 +33,7 @@ EXPORTS = [
     "conduit_profile_read", "conduit_value_norms", "conduit_residual_workspace_bytes",
     "conduit_residual_error", "conduit_score_noalloc", "conduit_scatter_kv_layers",
     "conduit_refresh_layers_workspace_bytes", "conduit_refresh_attn_layers",
+    "conduit_score_layers_workspace_bytes", "conduit_score_layers",
 ]
 SCORE_NOALLOC_MAX_BYTES = 16 << 20
 
@@ -106,6 +107,11 @@ def lib() -> ctypes.CDLL:
         L.conduit_refresh_layers_workspace_bytes.restype = sz
         L.conduit_refresh_attn_layers.argtypes = [pkv, i32, pvp, vp, i32, f32, pvp, pvp, vp, sz, vp]
         L.conduit_refresh_attn_layers.restype = ctypes.c_int
+        L.conduit_score_layers_workspace_bytes.argtypes = [pkv, i32, pimg, i32]
+        L.conduit_score_layers_workspace_bytes.restype = sz
+        L.conduit_score_layers.argtypes = [pkv, i32, pvp, i32, i32, pimg, ctypes.c_int, ctypes.c_int, f32, pvp,
+                                           vp, vp, i32, vp, sz, vp]
+        L.conduit_score_layers.restype = ctypes.c_int
         L.conduit_status_str.argtypes = [ctypes.c_int]
         L.conduit_status_str.restype = ctypes.c_char_p
         L.conduit_last_error.argtypes = []
@@ -243,6 +249,26 @@ def conduit_score(kv: KV, q: torch.Tensor, q_pos0: int, img: ImageTable, s_acc: 
                                norm, agg, scale, _ptr(row_lse_in), _ptr(row_lse_out), _ptr(vnorm_in),
                                s_acc.data_ptr(), a_acc.data_ptr(), int(accumulate), _ptr(a_out),
                                _ptr(vnorm_out), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def score_layers_workspace_bytes(kv: KV, n_q: int, img: "ImageTable", n_layers: int) -> int:
+    return int(lib().conduit_score_layers_workspace_bytes(ctypes.byref(kv), n_q, ctypes.byref(img.desc), n_layers))
+
+
+def conduit_score_layers(kvs, qs, q_pos0: int, img: "ImageTable", s_acc: torch.Tensor, a_acc: torch.Tensor,
+                         accumulate: bool = False, norm: int = NORM_CAUSAL_ROW, scale: Optional[float] = None,
+                         agg: int = AGG_MEAN, vnorm_in=None, ws: Optional[torch.Tensor] = None,
+                         stream=None) -> None:
+    """Scoring pass over several layers, accumulated (Eq. 6-7); see conduit_score_layers."""
+    n, n_q = len(kvs), qs[0].shape[0]
+    if scale is None:
+        scale = 1.0 / math.sqrt(kvs[0].head_dim)
+    ws = _workspace(score_layers_workspace_bytes(kvs[0], n_q, img, n), qs[0].device, ws)
+    arr = (KV * n)(*kvs)
+    vn = None if vnorm_in is None else _ptr_array(vnorm_in)
+    _check(lib().conduit_score_layers(arr, n, _ptr_array(qs), n_q, q_pos0, ctypes.byref(img.desc), norm, agg,
+                                      scale, vn, s_acc.data_ptr(), a_acc.data_ptr(), int(accumulate), _ptr(ws),
+                                      _nbytes(ws), _stream(stream)))
 
 
 def conduit_score_noalloc(kv: KV, q: torch.Tensor, q_pos0: int, img: ImageTable, s_acc: torch.Tensor,
@@ -416,7 +442,7 @@ class RefreshStep:
         self.idx = torch.zeros(max(k, 1), dtype=torch.int32, device=device)
         self.pos = torch.zeros(max(k, 1), dtype=torch.int32, device=device)
         self.mask = torch.zeros(nv, dtype=torch.uint8, device=device)
-        ws_bytes = max(score_workspace_bytes(kv, self.n_q, img) for kv in self.kvs)
+        ws_bytes = score_layers_workspace_bytes(self.kvs[0], self.n_q, img, len(self.kvs))
         self.ws_score = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=device)
         sb = int(lib().conduit_select_workspace_bytes(nv, img.n_images))
         self.ws_select = torch.empty(max(sb, 1), dtype=torch.uint8, device=device)
@@ -433,11 +459,14 @@ class RefreshStep:
                                 self.idx, self.pos, mask_out=self.mask, stream=stream,
                                 rule=self.rule)
             return
-        for li, (L, kv) in enumerate(zip(self.layers, self.kvs)):
-            conduit_score(kv, L["q"], self.q_pos0, self.img, self.s_acc, self.a_acc,
-                          accumulate=li > 0, norm=self.norm, ws=self.ws_score, stream=stream,
-                          agg=self.agg,
-                          vnorm_in=None if self.vnorm_tables is None else self.vnorm_tables[li])
+        if len(self.kvs) > 1:  # every layer in a few launches, summed in layer order
+            conduit_score_layers(self.kvs, [L["q"] for L in self.layers], self.q_pos0, self.img, self.s_acc,
+                                 self.a_acc, norm=self.norm, agg=self.agg, vnorm_in=self.vnorm_tables,
+                                 ws=self.ws_score, stream=stream)
+        else:
+            conduit_score(self.kvs[0], self.layers[0]["q"], self.q_pos0, self.img, self.s_acc, self.a_acc,
+                          norm=self.norm, ws=self.ws_score, stream=stream, agg=self.agg,
+                          vnorm_in=None if self.vnorm_tables is None else self.vnorm_tables[0])
         conduit_select_topk(self.s_acc, self.a_acc, len(self.layers), self.img, self.lam, self.k,
                             self.idx, self.pos, mask_out=self.mask, shat_out=self.shat,
                             c_out=self.c, ws=self.ws_select, stream=stream, rule=self.rule,

@@ -160,22 +160,25 @@ PlanLayout plan_layout(const conduit_kv *kv, int64_t n_rows, bool with_values, T
 }
 
 AttnPlan plan_at(void *ws, const PlanLayout &P);
+conduit_status check_layers(const conduit_kv *kvs, int32_t n_layers);
 
 struct ScoreLayout {
   size_t row_b, colsum, vsq, done, total;
   PlanLayout plan;
 };
 
-ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis) {
+// layers: the layers one launch covers (the multi-layer scoring); each has
+// its own row LSEs, statistics partials, column sums and norms.
+ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis, int32_t layers = 1) {
   ScoreLayout L{};
   const int64_t rows = (int64_t)n_q * kv->n_q_heads;
   const bool bf16 = kv->dtype == CONDUIT_BF16;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
-  L.row_b = take((size_t)rows * 4);
-  if (bf16) L.plan = plan_layout(kv, n_q, false, take);
-  L.colsum = take((size_t)kv->n_kv_heads * n_vis * 4);
-  L.vsq = take((size_t)kv->n_kv_heads * n_vis * 4);
+  L.row_b = take((size_t)rows * 4 * layers);
+  if (bf16) L.plan = plan_layout(kv, n_q, false, take, layers);
+  L.colsum = take((size_t)kv->n_kv_heads * n_vis * 4 * layers);
+  L.vsq = take((size_t)kv->n_kv_heads * n_vis * 4 * layers);
   if (bf16) L.done = take((size_t)(n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock * 4);
   L.total = off;
   return L;
@@ -435,6 +438,152 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   if (!done) {
     e = launch_finalize(fp, stream);
     if (e != hipSuccess) return hip_fail(e, "finalize");
+  }
+  return ok();
+}
+
+size_t conduit_score_layers_workspace_bytes(const conduit_kv *kv, int32_t n_q, const conduit_images *img,
+                                           int32_t n_layers) {
+  if (n_layers < 1 || n_layers > CONDUIT_MAX_LAYERS) return 0;
+  const size_t one = conduit_score_workspace_bytes(kv, n_q, img);
+  if (one == 0 || n_layers == 1 || kv->dtype != CONDUIT_BF16) return one;
+  return score_layout(kv, n_q, img->n_vis, std::min<int32_t>(n_layers, kMaxLayerBatch)).total;
+}
+
+conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, const void *const *q, int32_t n_q,
+                                    int32_t q_pos0, const conduit_images *img, conduit_norm norm,
+                                    conduit_agg agg, float scale, const float *const *vnorm_in, float *s_acc,
+                                    float *a_acc, int32_t accumulate, void *ws, size_t ws_bytes,
+                                    hipStream_t stream) {
+  conduit_status st = check_layers(kvs, n_layers);
+  if (st) return st;
+  const conduit_kv *kv = &kvs[0];
+  if (!q) return fail(CONDUIT_ERR_INVALID_ARG, "q is NULL");
+  for (int32_t l = 0; l < n_layers; ++l)
+    if (!q[l] || !aligned16(q[l])) return fail(CONDUIT_ERR_INVALID_ARG, "q[%d] must be non-NULL and 16-byte aligned", l);
+  if (n_q < 1) return fail(CONDUIT_ERR_INVALID_ARG, "n_q = %d < 1", n_q);
+  if (q_pos0 < 0 || (int64_t)q_pos0 + n_q > kv->n_ctx)
+    return fail(CONDUIT_ERR_INVALID_ARG, "span [%d, %lld) outside the cache of %d tokens", q_pos0,
+                (long long)q_pos0 + n_q, kv->n_ctx);
+  if (norm != CONDUIT_NORM_CAUSAL_ROW && norm != CONDUIT_NORM_VISUAL_ONLY)
+    return fail(CONDUIT_ERR_INVALID_ARG, "norm %d is not a conduit_norm", (int)norm);
+  if (agg != CONDUIT_AGG_MEAN && agg != CONDUIT_AGG_RMS)
+    return fail(CONDUIT_ERR_INVALID_ARG, "agg %d is not a conduit_agg", (int)agg);
+  if (!(scale > 0.f) || scale == __builtin_inff()) return fail(CONDUIT_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (!s_acc || !a_acc) return fail(CONDUIT_ERR_INVALID_ARG, "s_acc and a_acc are required");
+  if (accumulate != 0 && accumulate != 1) return fail(CONDUIT_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  ImageTable tbl;
+  st = check_images(img, q_pos0, &tbl);
+  if (st) return st;
+  const bool bf16 = kv->dtype == CONDUIT_BF16;
+  if (n_layers == 1 || !bf16) {  // fp32 (or one layer): the per-layer calls
+    const size_t need = conduit_score_workspace_bytes(kv, n_q, img);
+    st = check_ws(ws, ws_bytes, need);
+    if (st) return st;
+    for (int32_t l = 0; l < n_layers; ++l) {
+      st = conduit_score(&kvs[l], q[l], n_q, q_pos0, img, norm, agg, scale, nullptr, nullptr,
+                         vnorm_in ? vnorm_in[l] : nullptr, s_acc, a_acc, l > 0 ? 1 : accumulate, nullptr, nullptr, ws,
+                         ws_bytes, stream);
+      if (st) return st;
+    }
+    return ok();
+  }
+  if (attn_blocks(n_q, kv->n_q_heads / kv->n_kv_heads, false) > kAttnPlanMaxBlocks)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "n_q * n_q_heads / n_kv_heads = %lld exceeds %lld",
+                (long long)n_q * (kv->n_q_heads / kv->n_kv_heads),
+                (long long)kAttnPlanMaxBlocks * attn_pairs_per_block(false));
+  const int32_t nb_max = std::min<int32_t>(n_layers, kMaxLayerBatch);
+  const ScoreLayout L = score_layout(kv, n_q, img->n_vis, nb_max);
+  st = check_ws(ws, ws_bytes, L.total);
+  if (st) return st;
+
+  const int D = kv->head_dim;
+  const int64_t rows = (int64_t)n_q * kv->n_q_heads;
+  const float scale_log2 = scale * kLog2e;
+  float *row_b = reinterpret_cast<float *>(at(ws, L.row_b));
+  int32_t *done = reinterpret_cast<int32_t *>(at(ws, L.done));
+  const int32_t n_done = (img->n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock;
+
+  AttnParams ap{};
+  ap.k = kv->k;
+  ap.v = kv->v;
+  ap.k_stride = kv->k_stride;
+  ap.v_stride = kv->v_stride;
+  ap.pages = pages_of(kv);
+  ap.n_kv_heads = kv->n_kv_heads;
+  ap.group = kv->n_q_heads / kv->n_kv_heads;
+  ap.n_q_heads = kv->n_q_heads;
+  ap.n_ctx = kv->n_ctx;
+  ap.q = q[0];
+  ap.n_rows = n_q;
+  ap.q_pos0 = q_pos0;
+  ap.vis_only = norm == CONDUIT_NORM_VISUAL_ONLY ? 1 : 0;
+  ap.tbl = tbl;
+  ap.scale_log2 = scale_log2;
+  ap.plan = plan_at(ws, L.plan);
+  ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
+  ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
+  const int32_t lse_ns = attn_uniform_splits(ap, attn_pairs_per_block(false),
+                                             attn_grid(false) * attn_plan_rounds(false));
+  const bool fuse_lse = lse_ns > 1 && (int64_t)n_q * ap.group <= kColsumMaxLsePairs;
+  ap.skip_merge = fuse_lse ? 1 : 0;
+  ap.zero_i32 = done;
+  ap.zero_n = n_done;
+
+  ColsumParams cs{};
+  cs.k = kv->k;
+  cs.v = kv->v;
+  cs.k_stride = kv->k_stride;
+  cs.v_stride = kv->v_stride;
+  cs.pages = pages_of(kv);
+  cs.n_kv_heads = kv->n_kv_heads;
+  cs.group = ap.group;
+  cs.n_q_heads = kv->n_q_heads;
+  cs.q = q[0];
+  cs.n_q = n_q;
+  cs.row_b = row_b;
+  cs.tbl = tbl;
+  cs.n_vis = img->n_vis;
+  cs.scale_log2 = scale_log2;
+  cs.colsum_part = reinterpret_cast<float *>(at(ws, L.colsum));
+  cs.vsq_part = reinterpret_cast<float *>(at(ws, L.vsq));
+  if (fuse_lse) {
+    cs.lse_part_m = ap.part_m;
+    cs.lse_part_l = ap.part_l;
+    cs.lse_ns = lse_ns;
+    cs.lse_ppb = attn_pairs_per_block(false);
+    cs.lse_layer_stride = (int64_t)L.plan.max_items * attn_pairs_per_block(false);
+  }
+  cs.done = done;
+  FinalizeParams fp{};
+  fp.colsum_part = cs.colsum_part;
+  fp.vsq_part = cs.vsq_part;
+  fp.rms = agg == CONDUIT_AGG_RMS;
+  fp.n_kv_heads = kv->n_kv_heads;
+  fp.n_vis = img->n_vis;
+  fp.n_rows_f = (float)rows;
+  fp.s_acc = s_acc;
+  fp.a_acc = a_acc;
+
+  // Per batch of up to 16 layers: one statistics launch (which also clears
+  // the finalize counters) and one column-sum launch whose last workgroup per
+  // key block finalizes the batch's layers in order onto s_acc and A.
+  for (int32_t l0 = 0; l0 < n_layers; l0 += kMaxLayerBatch) {
+    LayerTable lt{};
+    lt.n = std::min<int32_t>(kMaxLayerBatch, n_layers - l0);
+    for (int32_t i = 0; i < lt.n; ++i) {
+      lt.k[i] = kvs[l0 + i].k;
+      lt.v[i] = kvs[l0 + i].v;
+      lt.q[i] = q[l0 + i];
+      lt.rowb[i] = row_b + i * rows;
+      lt.vnorm[i] = vnorm_in ? vnorm_in[l0 + i] : nullptr;
+    }
+    hipError_t e = launch_attn(ap, D, false, stream, &lt);
+    if (e != hipSuccess) return hip_fail(e, "row statistics");
+    fp.accumulate = (l0 > 0 || accumulate) ? 1 : 0;
+    cs.fin = fp;
+    e = launch_colsum(cs, D, true, agg == CONDUIT_AGG_RMS, stream, &lt);
+    if (e != hipSuccess) return hip_fail(e, "column sums");
   }
   return ok();
 }

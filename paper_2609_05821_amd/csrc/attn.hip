@@ -348,6 +348,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
   const u16 *Qg = static_cast<const u16 *>(p.q);
   void *o_out = p.o_out;
   float *lse_out = p.lse_out;
+  float *row_b = p.row_b;
   const float c = p.scale_log2;
   // UNI: the closed-form plan of contiguous rows (no plan loads at all).
   constexpr bool uniform = UNI;
@@ -376,6 +377,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
       Qg = static_cast<const u16 *>(lt.q[layer]);
       o_out = lt.o[layer];
       lse_out = lt.lse[layer];
+      row_b = lt.rowb[layer];
       slot_off = (int64_t)layer * p.plan.max_items;
     }
     const int uns = p.plan.uniform_ns;
@@ -686,7 +688,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
       if (single) {
         const float b = m + __log2f(l_tot);
         if (half == 0) {
-          if (!ML && p.row_b) p.row_b[gpair] = b;
+          if (row_b) row_b[gpair] = b;
           if (lse_out) lse_out[gpair] = b * kLn2;
         }
         if constexpr (PV) {
@@ -757,7 +759,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p, LayerTabl
     if (p.part_o) p.part_o += off * D;
     p.o_out = lt.o[l];
     p.lse_out = lt.lse[l];
-    p.row_b = nullptr;
+    p.row_b = lt.rowb[l];
   }
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -1033,14 +1035,16 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
     ProfScope ps(with_values ? "attn_values" : "attn_stats", s);
     // the closed-form plan only serves the statistics of the scoring span
     const bool uni = p.plan.uniform_ns > 0 && !with_values;
-    if (ml && !with_values) return hipErrorInvalidValue;  // several layers: refresh only
+    if (ml && !with_values && !uni) return hipErrorInvalidValue;  // several layers: refresh or scoring span
     if (head_dim == 128) {
-      if (ml) attn_bf16_kernel<128, true, 8, false, true><<<grid, 8 * 64, 0, s>>>(p, lt0);
+      if (ml && !with_values) attn_bf16_kernel<128, false, 4, true, true><<<grid, 4 * 64, 0, s>>>(p, lt0);
+      else if (ml) attn_bf16_kernel<128, true, 8, false, true><<<grid, 8 * 64, 0, s>>>(p, lt0);
       else if (with_values) attn_bf16_kernel<128, true, 8, false><<<grid, 8 * 64, 0, s>>>(p, lt0);
       else if (uni) attn_bf16_kernel<128, false, 4, true><<<grid, 4 * 64, 0, s>>>(p, lt0);
       else attn_bf16_kernel<128, false, 4, false><<<grid, 4 * 64, 0, s>>>(p, lt0);
     } else {
-      if (ml) attn_bf16_kernel<64, true, 8, false, true><<<grid, 8 * 64, 0, s>>>(p, lt0);
+      if (ml && !with_values) attn_bf16_kernel<64, false, 4, true, true><<<grid, 4 * 64, 0, s>>>(p, lt0);
+      else if (ml) attn_bf16_kernel<64, true, 8, false, true><<<grid, 8 * 64, 0, s>>>(p, lt0);
       else if (with_values) attn_bf16_kernel<64, true, 8, false><<<grid, 8 * 64, 0, s>>>(p, lt0);
       else if (uni) attn_bf16_kernel<64, false, 4, true><<<grid, 4 * 64, 0, s>>>(p, lt0);
       else attn_bf16_kernel<64, false, 4, false><<<grid, 4 * 64, 0, s>>>(p, lt0);

@@ -344,10 +344,24 @@ struct LayerTable {
   const void *k[kMaxLayerBatch];
   const void *v[kMaxLayerBatch];
   const void *q[kMaxLayerBatch];
-  void *o[kMaxLayerBatch];
-  float *lse[kMaxLayerBatch];
+  void *o[kMaxLayerBatch];           // refresh outputs
+  float *lse[kMaxLayerBatch];        // nullable: natural-log LSE outputs
+  float *rowb[kMaxLayerBatch];       // nullable: log2-domain row LSE (statistics)
+  const float *vnorm[kMaxLayerBatch];  // nullable: value-norm tables (column sums)
   int32_t n;
 };
+
+// Entry l of one of a LayerTable's pointer arrays, as a chain of selects.  An
+// index that is not a compile-time constant into an array of a kernel
+// parameter makes the compiler copy the whole parameter to per-lane scratch
+// memory (2 KB per lane here, reloaded all through the kernel).
+template <class T>
+__device__ __forceinline__ T layer_entry(T const (&a)[kMaxLayerBatch], int l) {
+  T r = a[0];
+#pragma unroll
+  for (int i = 1; i < kMaxLayerBatch; ++i) r = l == i ? a[i] : r;
+  return r;
+}
 
 // Merge of split partials into final outputs (blocks with n_s > 1).
 struct CombineParams {
@@ -413,6 +427,7 @@ struct ColsumParams {
   int32_t lse_ns;
   int32_t lse_ppb;
   float *lse_out;
+  int64_t lse_layer_stride;  // several layers: statistics partial slots per layer
   // nullable: arrival counters, one per key block, cleared beforehand; the
   // last KV head's workgroup of a key block finalizes its keys (fin).
   int32_t *done;
@@ -546,7 +561,9 @@ hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, int32_t
 // Split count of the closed-form plan the statistics pass uses for rows at
 // q_pos0 + r (pairs per block ppb), as launch_attn picks it.
 int attn_uniform_splits(const AttnParams &p, int ppb, int target);
-hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s);
+// lt (nullable, bf16 only): several layers in one launch (grid z = layer).
+hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s,
+                         const LayerTable *lt = nullptr);
 hipError_t launch_value_norms(const void *v, int64_t v_stride, const KvPages &pages, int32_t row_elems,
                               bool bf16, const ImageTable &tbl, float *out, hipStream_t s);
 hipError_t launch_finalize(const FinalizeParams &p, hipStream_t s);

@@ -76,27 +76,82 @@ __device__ __forceinline__ void store_coherent(float *q, float v) {
 // that runs before this one.  (A device-scope release/acquire fence pair per
 // workgroup would write back and invalidate the XCD's L2 each time, which
 // costs more than the separate finalize launch.)
-__device__ __forceinline__ void finalize_when_last(const ColsumParams &p, int tid, int n_threads) {
+// With several layers in the launch (nb > 0) the last of the nb * n_kv_heads
+// workgroups of a key block finalizes every layer in layer order: the same
+// fp32 additions, in the same order, as one finalize per layer.
+__device__ __forceinline__ void finalize_layers_token(const FinalizeParams &p, const LayerTable &lt, int nb, int t) {
+  const int64_t stride = (int64_t)p.n_kv_heads * p.n_vis;
+  float s_acc = 0.f, a_acc = 0.f;
+  for (int l = 0; l < nb; ++l) {
+    float cs = 0.f, sq = 0.f;
+    const float *vn = layer_entry(lt.vnorm, l);
+    for (int h = 0; h < p.n_kv_heads; ++h) {
+      const int64_t i = l * stride + (int64_t)h * p.n_vis + t;
+      cs += __hip_atomic_load(const_cast<float *>(p.colsum_part + i), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (!vn) sq += __hip_atomic_load(const_cast<float *>(p.vsq_part + i), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const float a = p.rms ? sqrtf(cs / p.n_rows_f) : cs / p.n_rows_f;
+    const float v = vn ? vn[t] : sqrtf(sq);
+    const float sv = a * v;
+    if (l == 0 && !p.accumulate) {
+      s_acc = sv;
+      a_acc = a;
+    } else {
+      if (l == 0) {
+        s_acc = p.s_acc[t];
+        a_acc = p.a_acc[t];
+      }
+      s_acc += sv;
+      a_acc += a;
+    }
+  }
+  p.s_acc[t] = s_acc;
+  p.a_acc[t] = a_acc;
+}
+
+__device__ __forceinline__ void finalize_when_last(const ColsumParams &p, const LayerTable &lt, int tid,
+                                                   int n_threads) {
   __shared__ int s_last;
   __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are complete
   __syncthreads();
+  const int arrivals = p.n_kv_heads * (lt.n > 0 ? lt.n : 1);
   if (tid == 0)
     s_last = __hip_atomic_fetch_add(p.done + blockIdx.x, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-             p.n_kv_heads - 1;
+             arrivals - 1;
   __syncthreads();
   if (!s_last) return;
   for (int i = tid; i < kColsumKeysPerBlock; i += n_threads) {
     const int t = blockIdx.x * kColsumKeysPerBlock + i;
-    if (t < p.n_vis) finalize_token<true>(p.fin, t);
+    if (t >= p.n_vis) continue;
+    if (lt.n > 0) finalize_layers_token(p.fin, lt, lt.n, t);
+    else finalize_token<true>(p.fin, t);
   }
 }
 
 // RMS: accumulate alpha^2 (Eq. 4's surrogate) instead of alpha.
 // FUSE: the row log-sum-exps are rebuilt from the statistics partials into
 // LDS (the split merge of the statistics pass, same order and arithmetic).
+// lt.n > 0: several layers, layer blockIdx.z (the statistics partials, column
+// sums and norms of layer l sit l strides further on).
 template <int D, bool RMS, bool FUSE>
-__global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParams p) {
+__global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParams p, LayerTable lt) {
   constexpr int KS = D / 16;
+  // This layer's pointers, in locals: p itself stays unwritten (a written
+  // kernel parameter holding the image table would be copied to scratch).
+  const bool ml = lt.n > 0;
+  const int layer = ml ? (int)blockIdx.z : 0;
+  const int64_t part_off = (int64_t)layer * p.n_kv_heads * p.n_vis;
+  const int64_t lse_off = p.lse_part_m ? layer * p.lse_layer_stride : 0;
+  const void *k_l = ml ? layer_entry(lt.k, layer) : p.k;
+  const void *v_l = ml ? layer_entry(lt.v, layer) : p.v;
+  const void *q_l = ml ? layer_entry(lt.q, layer) : p.q;
+  const float *row_b = ml ? layer_entry(lt.rowb, layer) : p.row_b;
+  const float *vnorm_in = ml ? layer_entry(lt.vnorm, layer) : p.vnorm_in;
+  float *colsum_part = p.colsum_part + part_off;
+  float *vsq_part = p.vsq_part + part_off;
+  const float *lse_part_m = p.lse_part_m ? p.lse_part_m + lse_off : nullptr;
+  const float *lse_part_l = p.lse_part_m ? p.lse_part_l + lse_off : nullptr;
+  float *lse_out = ml ? nullptr : p.lse_out;
   constexpr int QCH = kQChunk * D / 8;       // 16-byte chunks in a Q chunk
   constexpr int CPT = QCH / kColsumThreads;  // per thread
   constexpr int VPT = kColsumKeysPerBlock * D / 8 / kColsumThreads;  // V chunks per thread
@@ -112,9 +167,9 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   const int G = p.group;
   const int n_pair = p.n_q * G;
   const int nch = (n_pair + kQChunk - 1) / kQChunk;
-  const u16 *Kg = static_cast<const u16 *>(p.k);
-  const u16 *Vg = static_cast<const u16 *>(p.v);
-  const u16 *Qg = static_cast<const u16 *>(p.q);
+  const u16 *Kg = static_cast<const u16 *>(k_l);
+  const u16 *Vg = static_cast<const u16 *>(v_l);
+  const u16 *Qg = static_cast<const u16 *>(q_l);
 
   // Chunk c into registers: rows past n_pair load row n_pair - 1 and are
   // zeroed (b = +inf) when stored.
@@ -127,7 +182,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     }
     if (!FUSE && tid < kQChunk) {
       const int pr = min(c * kQChunk + tid, n_pair - 1);
-      bv = p.row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
+      bv = row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
     }
   };
   auto store_chunk = [&](int c, int buf, const u32x4 (&qv)[CPT], float bv) __attribute__((always_inline)) {
@@ -164,7 +219,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   // for memory bandwidth at the start.
   // The rows (page lookups included) are resolved here, so that the loads
   // inside the chunk loop wait on nothing.
-  const bool read_v = p.vnorm_in == nullptr;
+  const bool read_v = vnorm_in == nullptr;
   u32x4 vv[VPT];
   const u16 *vsrc[VPT];
 #pragma unroll
@@ -193,8 +248,8 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
 #pragma unroll
         for (int sp = 0; sp < kLseRegSplits; ++sp) {
           const int64_t idx = (slot0 + min(sp, ns - 1)) * p.lse_ppb + j;
-          mv[sp] = p.lse_part_m[idx];
-          lv[sp] = p.lse_part_l[idx];
+          mv[sp] = lse_part_m[idx];
+          lv[sp] = lse_part_l[idx];
         }
 #pragma unroll
         for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[sp]) : M;
@@ -202,16 +257,16 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
         for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[sp] - M) * lv[sp] : L;
       } else {
 #pragma unroll 8
-        for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, p.lse_part_m[(slot0 + sp) * p.lse_ppb + j]);
+        for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, lse_part_m[(slot0 + sp) * p.lse_ppb + j]);
 #pragma unroll 8
         for (int sp = 0; sp < ns; ++sp) {
           const int64_t idx = (slot0 + sp) * p.lse_ppb + j;
-          L += fast_exp2(p.lse_part_m[idx] - M) * p.lse_part_l[idx];
+          L += fast_exp2(lse_part_m[idx] - M) * lse_part_l[idx];
         }
       }
       const float b = M + __log2f(L);
       b_all[pr] = b;
-      if (blockIdx.x == 0 && p.lse_out) p.lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
+      if (blockIdx.x == 0 && lse_out) lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
     }
     __syncthreads();
   }
@@ -263,7 +318,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     __syncthreads();
   }
   colsum += __shfl_xor(colsum, 32, 64);
-  if (half == 0 && tvalid) store_coherent(p.colsum_part + (int64_t)kvh * p.n_vis + t, colsum);
+  if (half == 0 && tvalid) store_coherent(colsum_part + (int64_t)kvh * p.n_vis + t, colsum);
 
   // Value-norm proxy: this head's share of ||V_t||^2.  Item vi covers
   // dims (vi % (D/8))*8 .. +7 of key vi / (D/8); the D/8 items of a key sit
@@ -283,9 +338,9 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     for (int o = 1; o < D / 8; o <<= 1) sq += __shfl_xor(sq, o, 64);
     const int vi = tid + kColsumThreads * i;
     const int tv = blockIdx.x * kColsumKeysPerBlock + vi / (D / 8);
-    if (vi % (D / 8) == 0 && tv < p.n_vis) store_coherent(p.vsq_part + (int64_t)kvh * p.n_vis + tv, sq);
+    if (vi % (D / 8) == 0 && tv < p.n_vis) store_coherent(vsq_part + (int64_t)kvh * p.n_vis + tv, sq);
   }
-  if (p.done) finalize_when_last(p, tid, kColsumThreads);
+  if (p.done) finalize_when_last(p, lt, tid, kColsumThreads);
 }
 
 // fp32 path: one wave per 64 visual keys of one KV head.  Lane j holds the
@@ -408,26 +463,28 @@ hipError_t launch_value_norms(const void *v, int64_t v_stride, const KvPages &pa
   return hipGetLastError();
 }
 
-hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s) {
+hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s,
+                         const LayerTable *lt) {
+  const LayerTable lt0 = lt ? *lt : LayerTable{};
   if (bf16) {
-    dim3 grid((p.n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock, p.n_kv_heads);
+    dim3 grid((p.n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock, p.n_kv_heads, lt0.n > 0 ? lt0.n : 1);
     ProfScope ps("colsum", s);
     const bool fuse = p.lse_part_m != nullptr;
     if (head_dim == 128) {
       if (fuse) {
-        if (rms) colsum_bf16_kernel<128, true, true><<<grid, kColsumThreads, 0, s>>>(p);
-        else colsum_bf16_kernel<128, false, true><<<grid, kColsumThreads, 0, s>>>(p);
+        if (rms) colsum_bf16_kernel<128, true, true><<<grid, kColsumThreads, 0, s>>>(p, lt0);
+        else colsum_bf16_kernel<128, false, true><<<grid, kColsumThreads, 0, s>>>(p, lt0);
       } else {
-        if (rms) colsum_bf16_kernel<128, true, false><<<grid, kColsumThreads, 0, s>>>(p);
-        else colsum_bf16_kernel<128, false, false><<<grid, kColsumThreads, 0, s>>>(p);
+        if (rms) colsum_bf16_kernel<128, true, false><<<grid, kColsumThreads, 0, s>>>(p, lt0);
+        else colsum_bf16_kernel<128, false, false><<<grid, kColsumThreads, 0, s>>>(p, lt0);
       }
     } else {
       if (fuse) {
-        if (rms) colsum_bf16_kernel<64, true, true><<<grid, kColsumThreads, 0, s>>>(p);
-        else colsum_bf16_kernel<64, false, true><<<grid, kColsumThreads, 0, s>>>(p);
+        if (rms) colsum_bf16_kernel<64, true, true><<<grid, kColsumThreads, 0, s>>>(p, lt0);
+        else colsum_bf16_kernel<64, false, true><<<grid, kColsumThreads, 0, s>>>(p, lt0);
       } else {
-        if (rms) colsum_bf16_kernel<64, true, false><<<grid, kColsumThreads, 0, s>>>(p);
-        else colsum_bf16_kernel<64, false, false><<<grid, kColsumThreads, 0, s>>>(p);
+        if (rms) colsum_bf16_kernel<64, true, false><<<grid, kColsumThreads, 0, s>>>(p, lt0);
+        else colsum_bf16_kernel<64, false, false><<<grid, kColsumThreads, 0, s>>>(p, lt0);
       }
     }
   } else {

@@ -328,3 +328,42 @@ def test_layer_calls_reject_and_size():
     assert one < need3 < many
     assert rf(good, 3, ptrs, FAKE, 300, 0.1, ptrs, None, FAKE, need3 - 256, None) == api.ERR_WORKSPACE
     assert rf(good, 3, ptrs, None, 0, 0.1, ptrs, None, None, 0, None) == api.OK
+
+
+def test_score_layers_reject_and_size():
+    """The multi-layer scoring validates every layer and argument before
+    anything is enqueued; its workspace covers 16 layers' partials (bf16) or
+    one layer's (fp32, which runs the per-layer calls)."""
+    L = api.lib()
+    good = (api.KV * 3)(kv(), kv(k=FAKE + 4096, v=FAKE + 8192), kv())
+    qs = (ctypes.c_void_p * 3)(FAKE, FAKE, FAKE)
+    img = ctypes.byref(IMG.desc)
+    one = L.conduit_score_workspace_bytes(ctypes.byref(good[0]), 64, img)
+    sz = lambda n, k=good[0]: L.conduit_score_layers_workspace_bytes(ctypes.byref(k), 64, img, n)
+    assert sz(1) == one
+    assert sz(0) == 0
+    assert one < sz(3) < sz(16)
+    assert sz(16) == sz(20)
+    f32 = kv(dtype=api.F32, n_q_heads=8, n_kv_heads=8, head_dim=64, k_stride=512, v_stride=512)
+    assert sz(5, f32) == L.conduit_score_workspace_bytes(ctypes.byref(f32), 64, img)
+    need = sz(3)
+    sc = L.conduit_score_layers
+
+    def call(kvs=good, n=3, q=qs, n_q=64, q_pos0=1280, norm=api.NORM_CAUSAL_ROW, agg=api.AGG_MEAN, scale=0.1,
+             s_acc=FAKE, acc=0, nbytes=need):
+        return sc(kvs, n, q, n_q, q_pos0, img, norm, agg, scale, None, s_acc, FAKE, acc, FAKE, nbytes, None)
+
+    assert call(n=0) == api.ERR_INVALID_ARG
+    assert call(kvs=None) == api.ERR_INVALID_ARG
+    assert call(kvs=(api.KV * 2)(kv(), kv(n_ctx=1000)), n=2) == api.ERR_INVALID_ARG
+    assert call(q=None) == api.ERR_INVALID_ARG
+    assert call(q=(ctypes.c_void_p * 3)(FAKE, FAKE + 4, FAKE)) == api.ERR_INVALID_ARG
+    assert call(q=(ctypes.c_void_p * 3)(FAKE, None, FAKE)) == api.ERR_INVALID_ARG
+    assert call(n_q=0) == api.ERR_INVALID_ARG
+    assert call(q_pos0=1300) == api.ERR_INVALID_ARG
+    assert call(norm=7) == api.ERR_INVALID_ARG
+    assert call(agg=9) == api.ERR_INVALID_ARG
+    assert call(scale=0.0) == api.ERR_INVALID_ARG
+    assert call(s_acc=None) == api.ERR_INVALID_ARG
+    assert call(acc=2) == api.ERR_INVALID_ARG
+    assert call(nbytes=need - 256) == api.ERR_WORKSPACE

@@ -1,6 +1,8 @@
-"""The multi-layer merge and refresh (conduit_scatter_kv_layers,
-conduit_refresh_attn_layers) on the GPU against the CPU oracle, layer by
-layer: the same selection M refreshed in every layer (Sec. 3, Algorithm 1)."""
+"""The multi-layer calls on the GPU: the merge and refresh
+(conduit_scatter_kv_layers, conduit_refresh_attn_layers) against the CPU
+oracle layer by layer, the same selection M refreshed in every layer (Sec. 3,
+Algorithm 1); the scoring (conduit_score_layers) bit for bit against the
+per-layer calls and against the oracle's layer sums (Eq. 7)."""
 import numpy as np
 import pytest
 import torch
@@ -127,3 +129,76 @@ def test_layers_refresh_is_deterministic():
     _, o2, l2 = run_layers(w, layers_np, sel)
     for a, b in zip(o1 + l1, o2 + l2):
         np.testing.assert_array_equal(bits(a), bits(b))
+
+
+# ---------------------------------------------------------------------------
+# Scoring over several layers (conduit_score_layers)
+# ---------------------------------------------------------------------------
+
+def score_both(w, layers_np, norm=api.NORM_CAUSAL_ROW, agg=api.AGG_MEAN, tables=False, accumulate=False):
+    """The multi-layer call and the per-layer calls on the same inputs."""
+    caches = [(to_dev(L["k"]), to_dev(L["v"])) for L in layers_np]
+    kvs = [api.kv_desc(kc, vc, w.n_q_heads) for kc, vc in caches]
+    qs = [to_dev(L["q"]) for L in layers_np]
+    img = api.ImageTable(w.img_pos, w.img_off)
+    vn = None
+    if tables:
+        vn = [torch.empty(w.n_vis, dtype=torch.float32, device=DEV) for _ in layers_np]
+        for kv, t in zip(kvs, vn):
+            api.conduit_value_norms(kv, img, t)
+    f32 = dict(dtype=torch.float32, device=DEV)
+    init = torch.rand(w.n_vis, **f32)
+    s_m, a_m = init.clone(), init.clone()
+    api.conduit_score_layers(kvs, qs, w.q_pos0, img, s_m, a_m, accumulate=accumulate, norm=norm, agg=agg,
+                             vnorm_in=vn)
+    s_p, a_p = init.clone(), init.clone()
+    for li, (kv, q) in enumerate(zip(kvs, qs)):
+        api.conduit_score(kv, q, w.q_pos0, img, s_p, a_p, accumulate=accumulate or li > 0, norm=norm, agg=agg,
+                          vnorm_in=None if vn is None else vn[li])
+    torch.cuda.synchronize()
+    return (s_m, a_m), (s_p, a_p)
+
+
+@pytest.mark.parametrize("n_layers", [2, 17])
+@pytest.mark.parametrize("norm", [api.NORM_CAUSAL_ROW, api.NORM_VISUAL_ONLY], ids=["causal", "visual"])
+def test_score_layers_equal_per_layer_calls(n_layers, norm):
+    """Bit for bit the per-layer calls with the layer sums accumulated in
+    order; 17 layers cross the 16-layer launch batch."""
+    w = small(n_layers, seed=90 + n_layers)
+    layers_np = [w.layer(li, fresh=False) for li in range(n_layers)]
+    (s_m, a_m), (s_p, a_p) = score_both(w, layers_np, norm=norm)
+    np.testing.assert_array_equal(bits(s_m), bits(s_p))
+    np.testing.assert_array_equal(bits(a_m), bits(a_p))
+
+
+@pytest.mark.parametrize("case", ["rms", "tables", "accumulate"])
+def test_score_layers_variants(case):
+    w = small(3, seed=95)
+    layers_np = [w.layer(li, fresh=False) for li in range(3)]
+    kw = {"rms": dict(agg=api.AGG_RMS), "tables": dict(tables=True), "accumulate": dict(accumulate=True)}[case]
+    (s_m, a_m), (s_p, a_p) = score_both(w, layers_np, **kw)
+    np.testing.assert_array_equal(bits(s_m), bits(s_p))
+    np.testing.assert_array_equal(bits(a_m), bits(a_p))
+
+
+def test_score_layers_matches_oracle():
+    """The 28-layer multi-image workload's shape, four layers, against the
+    oracle's layer sums (Eq. 7)."""
+    from oracle import conduit_oracle as O
+    w = W.config(3, n_layers=4)
+    layers_np = [w.layer(li, fresh=False) for li in range(4)]
+    caches = [(to_dev(L["k"]), to_dev(L["v"])) for L in layers_np]
+    kvs = [api.kv_desc(kc, vc, w.n_q_heads) for kc, vc in caches]
+    img = api.ImageTable(w.img_pos, w.img_off)
+    s = torch.zeros(w.n_vis, device=DEV)
+    a = torch.zeros(w.n_vis, device=DEV)
+    api.conduit_score_layers(kvs, [to_dev(L["q"]) for L in layers_np], w.q_pos0, img, s, a)
+    torch.cuda.synchronize()
+    a_l, v_l = [], []
+    for L in layers_np:
+        a_o, v_o, _ = O.score_layer(L["q"], L["k"], L["v"], w.q_pos0, w.img_pos, w.img_off)
+        a_l.append(a_o)
+        v_l.append(v_o)
+    s_ref, A_ref = O.aggregate_layers(a_l, v_l)
+    assert_scores(to_f64(s), s_ref * 4, what="sum over layers of a v")
+    assert_scores(to_f64(a), A_ref, what="sum over layers of a")
