@@ -33,6 +33,7 @@
 //     (deterministic, no atomics).
 #include <algorithm>
 #include <climits>
+#include <type_traits>
 
 #include "common.h"
 
@@ -533,6 +534,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
     // multiply; with the visual-only domain the first keys of a split are
     // often outside it, which a fixed reference would turn into restarts).
     constexpr float kHeadroom = 32.f;
+    constexpr float kHeadroomSum = 4294967296.f;  // 2^kHeadroom
     float m_seen = kMInit;
     bool over = false;
     for (int attempt = 0;; ++attempt) {
@@ -577,16 +579,25 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
     // The key filter of cur comes first, so everything after it is one basic
     // block: the compiler then places the exponentials of cur among the
     // matrix products of nxt instead of sinking them past a later branch.
-    auto sub_step = [&](f32x16 &cur, f32x16 &nxt, int kbn, int ksub, int vst, int vsub, bool cur_masked, int cbuf,
-                        int ct0, int csub) __attribute__((always_inline)) {
+    // exact_tag (values only): std::true_type tracks every sub-tile's
+    // maximum against the reference (the attempts after a restart);
+    // std::false_type, the first attempt, only checks that the sub-tile's
+    // probabilities stay below 2^kHeadroom in sum, which any sub-tile
+    // exceeding the reference by more than kHeadroom violates.
+    auto sub_step = [&](auto exact_tag, f32x16 &cur, f32x16 &nxt, int kbn, int ksub, int vst, int vsub,
+                        bool cur_masked, int cbuf, int ct0, int csub) __attribute__((always_inline)) {
+      constexpr bool kExact = decltype(exact_tag)::value;
       if (cur_masked) mask_sub(cur, cbuf, ct0, csub);
       nxt = scores(kbn, ksub);
-      const float mx = sub_max(cur);
       float alpha = 1.f;
       if constexpr (PV) {
-        m_seen = fmaxf(m_seen, mx);
-        over = over || mx > m + kHeadroom;
+        if constexpr (kExact) {
+          const float mx = sub_max(cur);
+          m_seen = fmaxf(m_seen, mx);
+          over = over || mx > m + kHeadroom;
+        }
       } else {
+        const float mx = sub_max(cur);
         const bool grow = mx > m + kRescaleSlack;
         alpha = grow ? fast_exp2(m - mx) : 1.f;
         m = grow ? mx : m;
@@ -600,6 +611,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
       float psum = 0.f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) psum += cur[v];
+      if constexpr (PV && !kExact) over = over || !(psum <= kHeadroomSum);  // inf included
       l = PV ? l + psum : l * alpha + psum;
       // l is needed only after the loop; this empty statement makes it (and
       // so this sub-tile's exponentials) due here, so the compiler does not
@@ -631,6 +643,9 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
       // K(t+4), V(t+2) and V(t+3) arrive; they are awaited before the
       // barrier, one iteration after they were issued.  A tile t+1 past kend
       // arrives as zeros and is masked whole.
+      // The first attempt checks the probability sums, a restart tracks the
+      // maxima (below).
+      auto tiles = [&](auto exact_tag) __attribute__((always_inline)) {
       int t0 = kbeg, ks = 0, vs = 0;  // stages of tile t
       for (;;) {
         const int k1 = ks + 1 == 5 ? 0 : ks + 1, k2 = k1 + 1 == 5 ? 0 : k1 + 1;
@@ -643,10 +658,10 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
         dma_tile(true, k3, t0 + 3 * KT, r3);
         dma_tile(true, k4, t0 + 4 * KT, r4);
         const bool m0 = tile_masked(t0), m1 = tile_masked(t0 + KT);
-        sub_step(sa, sb, ks, 1, vs, 0, m0, ks, t0, 0);           // S(t,1)   | P(t,0) V
-        sub_step(sb, sa, k1, 0, vs, 1, m0, ks, t0, 1);           // S(t+1,0) | P(t,1) V
-        sub_step(sa, sb, k1, 1, v1, 0, m1, k1, t0 + KT, 0);      // S(t+1,1) | P(t+1,0) V
-        sub_step(sb, sa, k2, 0, v1, 1, m1, k1, t0 + KT, 1);      // S(t+2,0) | P(t+1,1) V
+        sub_step(exact_tag, sa, sb, ks, 1, vs, 0, m0, ks, t0, 0);       // S(t,1)   | P(t,0) V
+        sub_step(exact_tag, sb, sa, k1, 0, vs, 1, m0, ks, t0, 1);       // S(t+1,0) | P(t,1) V
+        sub_step(exact_tag, sa, sb, k1, 1, v1, 0, m1, k1, t0 + KT, 0);  // S(t+1,1) | P(t+1,0) V
+        sub_step(exact_tag, sb, sa, k2, 0, v1, 1, m1, k1, t0 + KT, 1);  // S(t+2,0) | P(t+1,1) V
         if (__ballot(over) != 0 && lane == 0) s_restart = gen;
         vm_wait<0>();
         __syncthreads();
@@ -656,6 +671,9 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
         ks = k2;
         vs = v2;
       }
+      };
+      if (attempt == 0) tiles(std::false_type{});
+      else tiles(std::true_type{});
     } else {
       // One tile per barrier, K stages mod 4: iteration t reads K(t) and
       // K(t+1) while K(t+2) is complete and K(t+3) arrives.  Before the
@@ -668,8 +686,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
         dma_tile(true, st3, t0 + 3 * KT, row_of(t0 + 3 * KT));
         okmask_tile(st3, t0 + 3 * KT);
         const bool m0 = tile_masked(t0);
-        sub_step(sa, sb, st, 1, 0, 0, m0, st, t0, 0);   // S(t,1)   | P(t,0)
-        sub_step(sb, sa, st1, 0, 0, 0, m0, st, t0, 1);  // S(t+1,0) | P(t,1)
+        sub_step(std::true_type{}, sa, sb, st, 1, 0, 0, m0, st, t0, 0);   // S(t,1)   | P(t,0)
+        sub_step(std::true_type{}, sb, sa, st1, 0, 0, 0, m0, st, t0, 1);  // S(t+1,0) | P(t,1)
         vm_wait<kSlots - 1>();
         __syncthreads();
         if (!more) break;
