@@ -540,6 +540,11 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
     for (int attempt = 0;; ++attempt) {
     l = 0.f;
     page_base = -64;
+    // Statistics over every key of the causal range take a fixed reference
+    // in their first attempt like the values path; after a restart, or with
+    // the visual-only domain, they keep the online maximum.
+    const bool fixed_ref = PV ? attempt == 0 : attempt == 0 && !p.vis_only;
+    if constexpr (!PV) m = kMInit;
     if constexpr (PV) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
@@ -566,7 +571,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
     }
     __syncthreads();
     f32x16 sa = scores(0, 0), sb;
-    if constexpr (PV) {
+    if (PV || fixed_ref) {
       if (tile_masked(kbeg)) mask_sub(sa, 0, kbeg, 0);
       m = fmaxf(fmaxf(sub_max(sa), m_seen), kMInit);
       m_seen = m;
@@ -579,11 +584,12 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
     // The key filter of cur comes first, so everything after it is one basic
     // block: the compiler then places the exponentials of cur among the
     // matrix products of nxt instead of sinking them past a later branch.
-    // exact_tag (values only): std::true_type tracks every sub-tile's
-    // maximum against the reference (the attempts after a restart);
-    // std::false_type, the first attempt, only checks that the sub-tile's
-    // probabilities stay below 2^kHeadroom in sum, which any sub-tile
-    // exceeding the reference by more than kHeadroom violates.
+    // exact_tag std::false_type (a first attempt with a fixed reference)
+    // only checks that the sub-tile's probabilities stay below 2^kHeadroom
+    // in sum, which any sub-tile exceeding the reference by more than
+    // kHeadroom violates.  std::true_type: with values every sub-tile's
+    // maximum is tracked against the reference (the attempts after a
+    // restart); statistics keep the online maximum.
     auto sub_step = [&](auto exact_tag, f32x16 &cur, f32x16 &nxt, int kbn, int ksub, int vst, int vsub,
                         bool cur_masked, int cbuf, int ct0, int csub) __attribute__((always_inline)) {
       constexpr bool kExact = decltype(exact_tag)::value;
@@ -596,7 +602,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
           m_seen = fmaxf(m_seen, mx);
           over = over || mx > m + kHeadroom;
         }
-      } else {
+      } else if constexpr (kExact) {
         const float mx = sub_max(cur);
         const bool grow = mx > m + kRescaleSlack;
         alpha = grow ? fast_exp2(m - mx) : 1.f;
@@ -611,8 +617,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
       float psum = 0.f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) psum += cur[v];
-      if constexpr (PV && !kExact) over = over || !(psum <= kHeadroomSum);  // inf included
-      l = PV ? l + psum : l * alpha + psum;
+      if constexpr (!kExact) over = over || !(psum <= kHeadroomSum);  // inf included
+      l = PV || !kExact ? l + psum : l * alpha + psum;
       // l is needed only after the loop; this empty statement makes it (and
       // so this sub-tile's exponentials) due here, so the compiler does not
       // sink them past the next sub-step's key filter.
@@ -672,13 +678,15 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
         vs = v2;
       }
       };
-      if (attempt == 0) tiles(std::false_type{});
+      if (fixed_ref) tiles(std::false_type{});
       else tiles(std::true_type{});
     } else {
       // One tile per barrier, K stages mod 4: iteration t reads K(t) and
       // K(t+1) while K(t+2) is complete and K(t+3) arrives.  Before the
       // barrier a wave waits until at most kSlots of its transfers are
       // outstanding: all of K(t+2)'s, so only K(t+3)'s may remain.
+      auto tiles = [&](auto exact_tag) __attribute__((always_inline)) {
+      constexpr bool kExact = decltype(exact_tag)::value;
       int t0 = kbeg, st = 0;  // K stage of tile t
       for (;;) {
         const bool more = t0 + KT < kend;
@@ -686,14 +694,21 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
         dma_tile(true, st3, t0 + 3 * KT, row_of(t0 + 3 * KT));
         okmask_tile(st3, t0 + 3 * KT);
         const bool m0 = tile_masked(t0);
-        sub_step(std::true_type{}, sa, sb, st, 1, 0, 0, m0, st, t0, 0);   // S(t,1)   | P(t,0)
-        sub_step(std::true_type{}, sb, sa, st1, 0, 0, 0, m0, st, t0, 1);  // S(t+1,0) | P(t,1)
+        sub_step(exact_tag, sa, sb, st, 1, 0, 0, m0, st, t0, 0);   // S(t,1)   | P(t,0)
+        sub_step(exact_tag, sb, sa, st1, 0, 0, 0, m0, st, t0, 1);  // S(t+1,0) | P(t,1)
+        if constexpr (!kExact) {
+          if (__ballot(over) != 0 && lane == 0) s_restart = gen;
+        }
         vm_wait<kSlots - 1>();
         __syncthreads();
-        if (!more) break;
+        if constexpr (!kExact) restart = s_restart == gen;
+        if (!more || restart) break;
         t0 += KT;
         st = st1;
       }
+      };
+      if (fixed_ref) tiles(std::false_type{});
+      else tiles(std::true_type{});
       vm_wait<0>();  // the last transfers (zero tiles) land before the stages are reused
     }
 
