@@ -44,7 +44,8 @@
  *     kernels, fp32 accumulation) or CONDUIT_F32 (fp32 throughout).  The bf16
  *     attention plans at most 4,096 blocks of (row, query head) pairs per KV
  *     head: rows * n_q_heads / n_kv_heads <= 524,288 for conduit_score and
- *     <= 1,048,576 for conduit_refresh_attn (CONDUIT_ERR_UNSUPPORTED past it).
+ *     <= 1,048,576 for conduit_refresh_attn (CONDUIT_ERR_UNSUPPORTED past it);
+ *     bf16 scoring also needs the span's queries below 2^31 bytes.
  *   - Results are bitwise reproducible run to run (no floating-point atomics).
  */
 #ifndef CONDUIT_H

@@ -14,6 +14,9 @@
 
 using namespace conduit;
 
+// bf16 scoring reads the span's queries with 32-bit byte offsets.
+constexpr int64_t kMaxSpanBytes = int64_t(1) << 31;
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -326,6 +329,9 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
     return fail(CONDUIT_ERR_UNSUPPORTED, "n_q * n_q_heads / n_kv_heads = %lld exceeds %lld",
                 (long long)n_q * (kv->n_q_heads / kv->n_kv_heads),
                 (long long)kAttnPlanMaxBlocks * attn_pairs_per_block(false));
+  if (bf16 && (int64_t)n_q * kv->n_q_heads * kv->head_dim * 2 >= kMaxSpanBytes)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "the span's queries (%lld bytes) must stay below 2^31 bytes",
+                (long long)n_q * kv->n_q_heads * kv->head_dim * 2);
   const ScoreLayout L = score_layout(kv, n_q, img->n_vis);
   st = check_ws(ws, ws_bytes, L.total);
   if (st) return st;
@@ -492,6 +498,9 @@ conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, con
     return fail(CONDUIT_ERR_UNSUPPORTED, "n_q * n_q_heads / n_kv_heads = %lld exceeds %lld",
                 (long long)n_q * (kv->n_q_heads / kv->n_kv_heads),
                 (long long)kAttnPlanMaxBlocks * attn_pairs_per_block(false));
+  if ((int64_t)n_q * kv->n_q_heads * kv->head_dim * 2 >= kMaxSpanBytes)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "the span's queries (%lld bytes) must stay below 2^31 bytes",
+                (long long)n_q * kv->n_q_heads * kv->head_dim * 2);
   const int32_t nb_max = std::min<int32_t>(n_layers, kMaxLayerBatch);
   const ScoreLayout L = score_layout(kv, n_q, img->n_vis, nb_max);
   st = check_ws(ws, ws_bytes, L.total);

@@ -171,26 +171,55 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   const u16 *Vg = static_cast<const u16 *>(v_l);
   const u16 *Qg = static_cast<const u16 *>(q_l);
 
-  // Chunk c into registers: rows past n_pair load row n_pair - 1 and are
-  // zeroed (b = +inf) when stored.
-  auto load_chunk = [&](int c, u32x4 (&qv)[CPT], float &bv) __attribute__((always_inline)) {
+  // Chunk c into registers.  Item i of a thread is pair row
+  // c * kQChunk + tid / (D/8) + i * kRowStep, i.e. span row qq[i] and head
+  // rr[i] of the group (pair = qq * G + rr), kept from chunk to chunk by
+  // adding kQChunk = q_step * G + r_step.  The loads go through a buffer
+  // resource bounded by the span's queries, so rows past n_pair read as
+  // zeros (and their b as +inf when stored).
+  constexpr int kRowStep = kColsumThreads / (D / 8);
+  const int q_step = kQChunk / G, r_step = kQChunk % G;
+  int qq[CPT], rr[CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int pr0 = tid / (D / 8) + kRowStep * i;
+    qq[i] = pr0 / G;
+    rr[i] = pr0 % G;
+  }
+  int qb = tid / G, rb = tid % G;  // statistics row of this thread (tid < kQChunk)
+  const auto q_rsrc = buffer_rsrc(Qg, p.n_q * p.n_q_heads * D * 2);
+  const auto b_rsrc = buffer_rsrc(row_b, FUSE ? 0 : p.n_q * p.n_q_heads * 4);
+  const uint32_t lane_b = (tid % (D / 8)) * 16;
+  auto next_rows = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int cidx = tid + kColsumThreads * i;
-      const int pr = min(c * kQChunk + cidx / (D / 8), n_pair - 1);
-      qv[i] = ld16(Qg + ((int64_t)(pr / G) * p.n_q_heads + kvh * G + pr % G) * D + (cidx % (D / 8)) * 8);
+      rr[i] += r_step;
+      qq[i] += q_step;
+      if (rr[i] >= G) {
+        rr[i] -= G;
+        ++qq[i];
+      }
     }
-    if (!FUSE && tid < kQChunk) {
-      const int pr = min(c * kQChunk + tid, n_pair - 1);
-      bv = row_b[(pr / G) * p.n_q_heads + kvh * G + pr % G];
+    rb += r_step;
+    qb += q_step;
+    if (rb >= G) {
+      rb -= G;
+      ++qb;
     }
+  };
+  auto load_chunk = [&](u32x4 (&qv)[CPT], float &bv) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+      qv[i] = buffer_ld16(q_rsrc, (uint32_t)((qq[i] * p.n_q_heads + kvh * G + rr[i]) * D) * 2u + lane_b);
+    if (!FUSE && tid < kQChunk)
+      bv = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                         b_rsrc, (uint32_t)(qb * p.n_q_heads + kvh * G + rb) * 4u, 0, 0));
   };
   auto store_chunk = [&](int c, int buf, const u32x4 (&qv)[CPT], float bv) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int cidx = tid + kColsumThreads * i;
-      const bool live = c * kQChunk + cidx / (D / 8) < n_pair;
-      st16(&qs[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], live ? qv[i] : u32x4{0, 0, 0, 0});
+      st16(&qs[buf][cidx / (D / 8)][(cidx % (D / 8)) * 8], qv[i]);
     }
     if (tid < kQChunk) {
       const int pr = c * kQChunk + tid;
@@ -200,7 +229,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
 
   u32x4 qv[CPT];
   float bv = kInf;
-  load_chunk(0, qv, bv);
+  load_chunk(qv, bv);
 
   image_table_to_lds(p.tbl, img, tid, kColsumThreads);
   __syncthreads();
@@ -239,17 +268,22 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     // to kLseRegSplits splits are read in one pass (indices clamped, so
     // every read is issued unconditionally) and reduced from registers.
     const int ns = p.lse_ns;
+    // split sp of a row sits sp * lse_ppb floats after split 0: a scalar
+    // offset of the load, the same for every lane
+    const auto m_rsrc = buffer_rsrc(lse_part_m, 0x7fffffff), l_rsrc = buffer_rsrc(lse_part_l, 0x7fffffff);
+    const uint32_t split_b = (uint32_t)p.lse_ppb * 4u;
     for (int pr = tid; pr < n_pair; pr += kColsumThreads) {
       const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
       const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns;
       float M = -kInf, L = 0.f;
       if (ns <= kLseRegSplits) {
         float mv[kLseRegSplits], lv[kLseRegSplits];
+        const uint32_t row_b0 = (uint32_t)(slot0 * p.lse_ppb + j) * 4u;
 #pragma unroll
         for (int sp = 0; sp < kLseRegSplits; ++sp) {
-          const int64_t idx = (slot0 + min(sp, ns - 1)) * p.lse_ppb + j;
-          mv[sp] = lse_part_m[idx];
-          lv[sp] = lse_part_l[idx];
+          const uint32_t so = (uint32_t)min(sp, ns - 1) * split_b;
+          mv[sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(m_rsrc, row_b0, so, 0));
+          lv[sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(l_rsrc, row_b0, so, 0));
         }
 #pragma unroll
         for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[sp]) : M;
@@ -277,7 +311,10 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   for (int c = 0; c < nch; ++c) {
     const int buf = c & 1;
     const bool more = c + 1 < nch;
-    if (more) load_chunk(c + 1, qv, bv);
+    if (more) {
+      next_rows();
+      load_chunk(qv, bv);
+    }
     if (c == v_chunk) load_v();
     const int rows = min(kQChunk, n_pair - c * kQChunk);
     auto row_step = [&](int r0) __attribute__((always_inline)) {

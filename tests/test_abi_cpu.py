@@ -367,3 +367,16 @@ def test_score_layers_reject_and_size():
     assert call(s_acc=None) == api.ERR_INVALID_ARG
     assert call(acc=2) == api.ERR_INVALID_ARG
     assert call(nbytes=need - 256) == api.ERR_WORKSPACE
+
+
+def test_score_rejects_span_queries_past_2_gib():
+    """bf16 scoring reads the span's queries with 32-bit byte offsets: a span
+    of 2^31 bytes or more is refused before anything is enqueued."""
+    L = api.lib()
+    big = kv(n_ctx=1 << 20, n_q_heads=256, n_kv_heads=256, k_stride=256 * 128, v_stride=256 * 128)
+    img = api.ImageTable([256], [0, 1024])
+    n_q = 32768  # 32768 * 256 heads * 128 dims * 2 bytes = 2^31
+    assert L.conduit_score(ctypes.byref(big), FAKE, n_q, 1280, ctypes.byref(img.desc), api.NORM_CAUSAL_ROW,
+                           api.AGG_MEAN, 0.1, None, None, None, FAKE, FAKE, 0, None, None, FAKE, 1 << 40,
+                           None) == api.ERR_UNSUPPORTED
+    assert b"2^31" in L.conduit_last_error()
