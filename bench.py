@@ -559,10 +559,11 @@ def other_workloads(args, dev):
     """The other workloads, each step timed on this GPU (HIP events around
     the whole step, cold caches) beside its CPU oracle timing.
 
-    A step is the refresh step of the workload: conduit_score for every
-    scored layer (layer sums accumulated), one conduit_select_topk, then the
-    merge and refresh of every layer (conduit_scatter_kv_layers +
-    conduit_refresh_attn_layers: up to 16 layers per launch, one plan).  The 28-layer
+    A step is the refresh step of the workload: the scoring of every scored
+    layer (conduit_score_layers: layer sums accumulated, up to 16 layers per
+    launch), one conduit_select_topk, then the merge and refresh of every
+    layer (conduit_scatter_kv_layers + conduit_refresh_attn_layers: up to 16
+    layers per launch, one plan).  The 28-layer
     workloads hold 28 per-layer caches, span queries and fresh rows in device
     memory; their contents are one generated layer copied into each (so the
     selection is that of one layer; every layer still reads and writes its own
