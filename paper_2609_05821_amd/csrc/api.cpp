@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <string>
 
 #include "common.h"
@@ -16,6 +17,25 @@ using namespace conduit;
 
 // bf16 scoring reads the span's queries with 32-bit byte offsets.
 constexpr int64_t kMaxSpanBytes = int64_t(1) << 31;
+
+// Epoch of a statistics launch's merge marks (never 0): a mark written
+// under another epoch counts as unset, so the workspace needs no clearing
+// between calls.
+uint32_t next_merge_epoch() {
+  static std::atomic<uint32_t> epoch{0};
+  uint32_t e;
+  do e = ++epoch;
+  while (e == 0);
+  return e;
+}
+
+// Whether the column-sum workgroups rebuild the split statistics rows
+// themselves (small spans and caches) rather than the statistics kernel
+// merging each block once.
+bool colsum_fuses_lse(int32_t lse_ns, int64_t n_pair, int32_t n_vis) {
+  return lse_ns > 1 && lse_ns <= kLseRegSplits && n_pair <= kColsumMaxLsePairs &&
+         (n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock <= kColsumFuseMaxBlocks;
+}
 
 namespace {
 
@@ -166,7 +186,7 @@ AttnPlan plan_at(void *ws, const PlanLayout &P);
 conduit_status check_layers(const conduit_kv *kvs, int32_t n_layers);
 
 struct ScoreLayout {
-  size_t row_b, colsum, vsq, done, total;
+  size_t row_b, colsum, vsq, done, merge_flag, total;
   PlanLayout plan;
 };
 
@@ -183,6 +203,7 @@ ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis, int32
   L.colsum = take((size_t)kv->n_kv_heads * n_vis * 4 * layers);
   L.vsq = take((size_t)kv->n_kv_heads * n_vis * 4 * layers);
   if (bf16) L.done = take((size_t)(n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock * 4);
+  if (bf16) L.merge_flag = take((size_t)L.plan.max_items * 4 * layers);
   L.total = off;
   return L;
 }
@@ -380,12 +401,16 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
       ap.plan = plan_at(ws, L.plan);
       ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
       ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
-      // With split rows the column-sum kernel merges the partials itself
-      // when its LDS holds every row of a KV head.
+      // split rows: merged by the column-sum workgroups, or else by the
+      // statistics kernel's last split of each block (no merge launch)
       lse_ns = attn_uniform_splits(ap, attn_pairs_per_block(false),
                                    attn_grid(false) * attn_plan_rounds(false));
-      fuse_lse = lse_ns > 1 && (int64_t)n_q * ap.group <= kColsumMaxLsePairs;
-      ap.skip_merge = fuse_lse ? 1 : 0;
+      fuse_lse = colsum_fuses_lse(lse_ns, (int64_t)n_q * ap.group, img->n_vis);
+      if (!fuse_lse) {
+        ap.merge_flag = reinterpret_cast<uint32_t *>(at(ws, L.merge_flag));
+        ap.epoch = next_merge_epoch();
+      }
+      ap.skip_merge = 1;
       ap.zero_i32 = done;
       ap.zero_n = n_done;
       e = launch_attn(ap, D, false, stream);
@@ -534,8 +559,9 @@ conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, con
   ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
   const int32_t lse_ns = attn_uniform_splits(ap, attn_pairs_per_block(false),
                                              attn_grid(false) * attn_plan_rounds(false));
-  const bool fuse_lse = lse_ns > 1 && (int64_t)n_q * ap.group <= kColsumMaxLsePairs;
-  ap.skip_merge = fuse_lse ? 1 : 0;
+  const bool fuse_lse = colsum_fuses_lse(lse_ns, (int64_t)n_q * ap.group, img->n_vis);
+  if (!fuse_lse) ap.merge_flag = reinterpret_cast<uint32_t *>(at(ws, L.merge_flag));
+  ap.skip_merge = 1;  // merged by the column sums or by the statistics kernel
   ap.zero_i32 = done;
   ap.zero_n = n_done;
 
@@ -575,7 +601,7 @@ conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, con
   fp.a_acc = a_acc;
 
   // Per batch of up to 16 layers: one statistics launch (which also clears
-  // the finalize counters) and one column-sum launch whose last workgroup per
+  // the finalize counters and merges its split rows) and one column-sum launch whose last workgroup per
   // key block finalizes the batch's layers in order onto s_acc and A.
   for (int32_t l0 = 0; l0 < n_layers; l0 += kMaxLayerBatch) {
     LayerTable lt{};
@@ -587,6 +613,7 @@ conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, con
       lt.rowb[i] = row_b + i * rows;
       lt.vnorm[i] = vnorm_in ? vnorm_in[l0 + i] : nullptr;
     }
+    if (!fuse_lse) ap.epoch = next_merge_epoch();  // each launch marks afresh
     hipError_t e = launch_attn(ap, D, false, stream, &lt);
     if (e != hipSuccess) return hip_fail(e, "row statistics");
     fp.accumulate = (l0 > 0 || accumulate) ? 1 : 0;

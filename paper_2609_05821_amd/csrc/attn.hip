@@ -47,6 +47,8 @@ constexpr float kMInit = -1e30f;  // initial running maximum (log2 units)
 // exceeds it by more than this many log2 units; probabilities stay below 2^8
 // and l is rescaled rarely.  Exact: l and the final normaliser share it.
 constexpr float kRescaleSlack = 8.f;
+// Statistics: split partials a merging workgroup loads at once per pair.
+constexpr int kMergeLoads = 16;
 
 // LDS tiles.  K rows are D + 8 elements apart (16 bytes of padding: the 16
 // lanes of an S^T operand read cover 16 rows in distinct banks); V rows are
@@ -310,6 +312,7 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
   constexpr int DT = D / 32;      // 32-row tiles of O^T
   __shared__ AttnSmem<D, PV> sm;
   __shared__ int s_restart;  // attempt id of the item being restarted (see kHeadroom)
+  __shared__ int s_last;     // statistics: this workgroup holds the last split of its block
 
   const int G = p.group;
   const int n_pairs = p.n_rows * G;
@@ -371,8 +374,9 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
     if (lidx >= n_items) break;
     const int idx = ML ? lidx % n_plan_items : lidx;  // plan item
     int64_t slot_off = 0;  // partial slots of this item's layer
+    int layer = 0;
     if constexpr (ML) {
-      const int layer = lidx / n_plan_items;
+      layer = lidx / n_plan_items;
       Kg = static_cast<const u16 *>(lt.k[layer]);
       Vg = static_cast<const u16 *>(lt.v[layer]);
       Qg = static_cast<const u16 *>(lt.q[layer]);
@@ -742,8 +746,13 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
       } else {
         const int64_t idx2 = (item.w + slot_off) * kPairs + wave * 32 + col;
         if (half == 0) {
-          p.part_m[idx2] = m;
-          p.part_l[idx2] = l_tot;
+          if (!PV && p.merge_flag) {  // read by another workgroup of this kernel
+            store_coherent(p.part_m + idx2, m);
+            store_coherent(p.part_l + idx2, l_tot);
+          } else {
+            p.part_m[idx2] = m;
+            p.part_l[idx2] = l_tot;
+          }
         }
         if constexpr (PV) {
           // the split's own attention output O_s / l_s (a convex combination
@@ -761,6 +770,71 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
                     ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 3] * inv) << 16);
               *reinterpret_cast<uint2 *>(dst + dt * 32 + 8 * g4 + 4 * half) = w;
             }
+        }
+      }
+    }
+
+    // Statistics with the closed-form plan: each split item of a block,
+    // once its partials are stored device-coherently and waited for, marks
+    // its slot with the call's epoch and then reads the marks of the block's
+    // other splits; one that finds them all set merges the block's splits in
+    // split order, b = M + log2(sum_s l_s 2^(m_s - M)), into row_b / lse_out.
+    // The last item to mark always finds them set; if two items both do,
+    // they write the same values.
+    if constexpr (!PV) {
+      if (p.merge_flag && !single) {
+        const int ns = info.z;
+        const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns + slot_off;
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores are complete
+        __syncthreads();
+        if (tid == 0)
+          __hip_atomic_store(p.merge_flag + item.w + slot_off, p.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_s_waitcnt(0);  // the mark is stored before the others are read
+        if (wave == 0) {
+          bool all = true;
+          for (int s0 = 0; s0 < ns; s0 += 64) {
+            const int sp = s0 + lane;
+            const uint32_t f = sp < ns ? __hip_atomic_load(p.merge_flag + slot0 + sp, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT)
+                                       : p.epoch;
+            all = all && __ballot(f != p.epoch) == 0;
+          }
+          if (lane == 0) s_last = all;
+        }
+        __syncthreads();
+        if (s_last) {
+          for (int j = tid; j < kPairs; j += kThreads) {
+            const int pair = pair0 + j;
+            if (pair >= n_pairs) continue;
+            const int gp = (pair / G) * p.n_q_heads + kvh * G + pair % G;
+            // kMergeLoads splits' partials are loaded at once (indices
+            // clamped, so every load is issued), then reduced in order
+            auto ld = [&](const float *a, int sp) __attribute__((always_inline)) {
+              return __hip_atomic_load(a + (slot0 + min(sp, ns - 1)) * kPairs + j, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            };
+            float mv[kMergeLoads], lv[kMergeLoads];
+            float M = kNegInf, L = 0.f;
+            for (int s0 = 0; s0 < ns; s0 += kMergeLoads) {
+#pragma unroll
+              for (int i = 0; i < kMergeLoads; ++i) mv[i] = ld(p.part_m, s0 + i);
+#pragma unroll
+              for (int i = 0; i < kMergeLoads; ++i) M = s0 + i < ns ? fmaxf(M, mv[i]) : M;
+            }
+            for (int s0 = 0; s0 < ns; s0 += kMergeLoads) {
+              if (ns > kMergeLoads) {  // else the one batch is still in registers
+#pragma unroll
+                for (int i = 0; i < kMergeLoads; ++i) mv[i] = ld(p.part_m, s0 + i);
+              }
+#pragma unroll
+              for (int i = 0; i < kMergeLoads; ++i) lv[i] = ld(p.part_l, s0 + i);
+#pragma unroll
+              for (int i = 0; i < kMergeLoads; ++i) L = s0 + i < ns ? L + fast_exp2(mv[i] - M) * lv[i] : L;
+            }
+            const float b = M + __log2f(L);
+            if (row_b) row_b[gp] = b;
+            if (lse_out) lse_out[gp] = b * kLn2;
+          }
         }
       }
     }

@@ -330,9 +330,16 @@ struct AttnParams {
   float *lse_out;           // nullable [n_rows * H_q]: natural-log log-sum-exp
   void *o_out;              // [n_rows][H_q][D] bf16 (values only)
   ImageTable tbl;           // read when vis_only
-  int32_t skip_merge;       // host side: the split partials are merged by the caller's next kernel
+  int32_t skip_merge;       // host side: no merge launch (merged in the kernel, or by the caller)
   int32_t *zero_i32;        // nullable: cleared by the kernel (counters of a later kernel)
   int32_t zero_n;
+  // Statistics with the closed-form plan (nullable): one mark per partial
+  // slot, set to the call's epoch by the item that wrote the slot; the item
+  // that finds every split of its block marked merges the block into
+  // row_b / lse_out.  Marks of another epoch count as unset, so they need no
+  // clearing.
+  uint32_t *merge_flag;
+  uint32_t epoch;
 };
 
 // Per-layer pointers of a launch that covers several layers of one request
@@ -350,6 +357,13 @@ struct LayerTable {
   const float *vnorm[kMaxLayerBatch];  // nullable: value-norm tables (column sums)
   int32_t n;
 };
+
+// Device-coherent store of a partial (written through to where every XCD
+// reads it), so that a later workgroup of the same kernel can read it with
+// device-scope loads, without a device-scope cache write-back.
+__device__ __forceinline__ void store_coherent(float *q, float v) {
+  __hip_atomic_store(q, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // Entry l of one of a LayerTable's pointer arrays, as a chain of selects.  An
 // index that is not a compile-time constant into an array of a kernel
@@ -420,8 +434,9 @@ struct ColsumParams {
   float *vsq_part;          // [n_kv_heads][n_vis]
   const float *vnorm_in;    // nullable: value norms given, V not read
   // Row log-sum-exp rebuilt from the statistics pass's split partials (its
-  // closed-form plan: lse_ns splits of lse_ppb-pair blocks) instead of read
-  // from row_b; the first key block also writes lse_out (natural log).
+  // closed-form plan: lse_ns <= kLseRegSplits splits of lse_ppb-pair blocks)
+  // instead of read from row_b; the first key block also writes lse_out
+  // (natural log).
   const float *lse_part_m;
   const float *lse_part_l;
   int32_t lse_ns;
@@ -618,7 +633,14 @@ constexpr int64_t attn_max_items(int64_t n_pb, int64_t n_kv_heads, bool with_val
 }
 constexpr int kAttnKeyTile = 64;         // keys per LDS tile
 constexpr int64_t kMaxStrideBytes = int64_t(1) << 25;  // row strides below 32 MiB: a key tile spans < 2 GiB
-constexpr int kColsumKeysPerBlock = 256;
-constexpr int kColsumMaxLsePairs = 4096;  // row LSEs a column-sum workgroup can rebuild in LDS // visual keys per workgroup
+constexpr int kColsumKeysPerBlock = 256;  // visual keys per workgroup
+// Split statistics rows are merged by every column-sum workgroup (in LDS,
+// from registers) when the span has at most kColsumMaxLsePairs pairs per KV
+// head, at most kLseRegSplits splits and at most kColsumFuseMaxBlocks key
+// blocks (so few workgroups repeat it); otherwise the statistics kernel
+// merges them once.
+constexpr int kColsumMaxLsePairs = 4096;
+constexpr int kLseRegSplits = 24;
+constexpr int kColsumFuseMaxBlocks = 64;
 
 }  // namespace conduit

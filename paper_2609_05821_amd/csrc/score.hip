@@ -30,7 +30,6 @@ constexpr int kColsumThreads = 512;   // 8 waves x 32 keys
 // tiles and exponentials run, one barrier per chunk.  The V rows for the
 // value norms are fetched during the last chunk and consumed at the end.
 constexpr int kQChunk = 256;
-constexpr int kLseRegSplits = 24;  // split partials of one row held in registers by the fused merge
 
 // Finalize of one visual token: fixed-order sum over KV heads, the mean (or
 // RMS) over rows and heads, the value norm, s = a v and the layer
@@ -61,12 +60,6 @@ __device__ __forceinline__ void finalize_token(const FinalizeParams &p, int t) {
   if (p.vnorm_out) p.vnorm_out[t] = v;
 }
 
-// Device-coherent store of a partial (written through to where every XCD
-// reads it), so that a later workgroup of the same kernel can read it without
-// a device-scope cache write-back.
-__device__ __forceinline__ void store_coherent(float *q, float v) {
-  __hip_atomic_store(q, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // The workgroups of the n_kv_heads KV heads of one key block each count
 // their arrival once their partials are stored (device-coherent stores,
@@ -264,9 +257,10 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   const int v_chunk = nch - 1;  // no chunk load (and wait) follows
   if constexpr (FUSE) {
     // b = M + log2(sum_s l_s 2^(m_s - M)) over the splits of the row's
-    // block, s ascending, exactly as the statistics merge computes it.  Up
-    // to kLseRegSplits splits are read in one pass (indices clamped, so
-    // every read is issued unconditionally) and reduced from registers.
+    // block, s ascending, exactly as the statistics merge computes it.  The
+    // host fuses only up to kLseRegSplits splits: they are read in one pass
+    // (indices clamped, so every read is issued unconditionally) and reduced
+    // from registers.
     const int ns = p.lse_ns;
     // split sp of a row sits sp * lse_ppb floats after split 0: a scalar
     // offset of the load, the same for every lane
@@ -276,28 +270,18 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
       const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
       const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns;
       float M = -kInf, L = 0.f;
-      if (ns <= kLseRegSplits) {
-        float mv[kLseRegSplits], lv[kLseRegSplits];
-        const uint32_t row_b0 = (uint32_t)(slot0 * p.lse_ppb + j) * 4u;
+      float mv[kLseRegSplits], lv[kLseRegSplits];
+      const uint32_t row_b0 = (uint32_t)(slot0 * p.lse_ppb + j) * 4u;
 #pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) {
-          const uint32_t so = (uint32_t)min(sp, ns - 1) * split_b;
-          mv[sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(m_rsrc, row_b0, so, 0));
-          lv[sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(l_rsrc, row_b0, so, 0));
-        }
-#pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[sp]) : M;
-#pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[sp] - M) * lv[sp] : L;
-      } else {
-#pragma unroll 8
-        for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, lse_part_m[(slot0 + sp) * p.lse_ppb + j]);
-#pragma unroll 8
-        for (int sp = 0; sp < ns; ++sp) {
-          const int64_t idx = (slot0 + sp) * p.lse_ppb + j;
-          L += fast_exp2(lse_part_m[idx] - M) * lse_part_l[idx];
-        }
+      for (int sp = 0; sp < kLseRegSplits; ++sp) {
+        const uint32_t so = (uint32_t)min(sp, ns - 1) * split_b;
+        mv[sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(m_rsrc, row_b0, so, 0));
+        lv[sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(l_rsrc, row_b0, so, 0));
       }
+#pragma unroll
+      for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[sp]) : M;
+#pragma unroll
+      for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[sp] - M) * lv[sp] : L;
       const float b = M + __log2f(L);
       b_all[pr] = b;
       if (blockIdx.x == 0 && lse_out) lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;

@@ -202,3 +202,15 @@ def test_score_layers_matches_oracle():
     s_ref, A_ref = O.aggregate_layers(a_l, v_l)
     assert_scores(to_f64(s), s_ref * 4, what="sum over layers of a v")
     assert_scores(to_f64(a), A_ref, what="sum over layers of a")
+
+
+def test_score_layers_statistics_merged_by_their_kernel():
+    """Eight span rows over 17k keys: each statistics block has more splits
+    than the column sums rebuild, so every layer's splits are merged by the
+    statistics kernel; 18 layers (two launches) equal the per-layer calls bit
+    for bit."""
+    w = W.custom(18, 28, 4, 128, 8, 512, [1024] * 16, 16, "bf16", n_relevant=2, seed=97)
+    layers_np = [w.layer(li, fresh=False) for li in range(18)]
+    (s_m, a_m), (s_p, a_p) = score_both(w, layers_np)
+    np.testing.assert_array_equal(bits(s_m), bits(s_p))
+    np.testing.assert_array_equal(bits(a_m), bits(a_p))

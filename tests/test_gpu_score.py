@@ -25,6 +25,10 @@ CASES = {
     # 640 x 7 = 4,480 pairs per KV head: statistics split and merged by their own kernel
     "long_span_bf16_gqa7": lambda: W.custom(1, 28, 4, 128, 640, 2000, [600, 600], 16, "bf16",
                                             n_relevant=1, seed=10),
+    # 8 span rows over 17k keys: 33 statistics splits per block, more than the
+    # column sums rebuild, so the statistics kernel merges them
+    "short_span_long_context": lambda: W.custom(1, 28, 4, 128, 8, 512, [1024] * 16, 16, "bf16",
+                                                n_relevant=2, seed=12),
 }
 
 
@@ -132,3 +136,32 @@ def test_strided_cache_rows():
     a, v, _ = O.score_layer(L.np["q"], L.np["k"], L.np["v"], w.q_pos0, w.img_pos, w.img_off)
     assert_scores(to_f64(got["a"]), a, what="a_t")
     assert_scores(to_f64(got["v"]), v, what="||V_t||")
+
+
+def test_statistics_merge_needs_no_clean_workspace():
+    """The statistics kernel's merge marks carry the call's epoch: a
+    workspace full of arbitrary bytes, and the same workspace again on the
+    next call, give the same bits as a fresh one."""
+    w = CASES["short_span_long_context"]()
+    L = Layer(w, 0)
+    img = api.ImageTable(w.img_pos, w.img_off)
+    n = api.score_workspace_bytes(L.kv, w.n_q, img)
+    f32 = dict(dtype=torch.float32, device=DEV)
+    outs = []
+    for fill in ("zeros", "random", "reuse"):
+        if fill == "zeros":
+            ws = torch.zeros(n, dtype=torch.uint8, device=DEV)
+        elif fill == "random":
+            ws = torch.randint(0, 256, (n,), dtype=torch.uint8, device=DEV,
+                               generator=torch.Generator(device=DEV).manual_seed(5))
+        s_acc, a_acc = torch.zeros(w.n_vis, **f32), torch.zeros(w.n_vis, **f32)
+        lse = torch.zeros((w.n_q, w.n_q_heads), **f32)
+        api.conduit_score(L.kv, L.q, w.q_pos0, img, s_acc, a_acc, row_lse_out=lse, ws=ws)
+        torch.cuda.synchronize()
+        outs.append((s_acc, a_acc, lse))
+    for got in outs[1:]:
+        for x, y in zip(got, outs[0]):
+            np.testing.assert_array_equal(bits(x), bits(y))
+    a, v, lse = O.score_layer(L.np["q"], L.np["k"], L.np["v"], w.q_pos0, w.img_pos, w.img_off)
+    assert_scores(to_f64(outs[0][2]), lse, what="row lse")
+    assert_scores(to_f64(outs[0][0]), a * v, what="s")
