@@ -165,3 +165,31 @@ def test_statistics_merge_needs_no_clean_workspace():
     a, v, lse = O.score_layer(L.np["q"], L.np["k"], L.np["v"], w.q_pos0, w.img_pos, w.img_off)
     assert_scores(to_f64(outs[0][2]), lse, what="row lse")
     assert_scores(to_f64(outs[0][0]), a * v, what="s")
+
+
+@pytest.mark.parametrize("boost", [400.0, 1200.0], ids=["gap_56_log2", "gap_170_log2"])
+def test_visual_only_statistics_far_below_a_text_key(boost):
+    """The first token (a text key) out-scores the visual keys by a median
+    of 56 or 170 log2 units: with visual-only normalisation its probability
+    is left out, and the visual keys' log-sum-exp and column sums must not
+    lose precision to it; with causal-row normalisation it dominates.  Some
+    rows' visual keys out-score it instead, by up to 54 log2 units.  Checked
+    against the oracle for both normalisations."""
+    w = W.custom(1, 28, 4, 128, 16, 64, [512, 512, 512], 16, "bf16", seed=14)
+    L = Layer(w, 0)
+    q = O.to_f64(L.np["q"])  # [n_q, H_q, d]
+    G = w.n_q_heads // w.n_kv_heads
+    k0 = O.to_f64(L.np["k"]).copy()
+    for h in range(w.n_kv_heads):
+        u = q[:, h * G:(h + 1) * G].reshape(-1, w.head_dim).mean(axis=0)
+        u /= np.linalg.norm(u)
+        # logit of the first token ~ boost * |q| * scale above the rest
+        k0[0, h] = boost * u
+    L.np["k"] = w._cast(k0.astype(np.float32))
+    L.k = to_dev(L.np["k"])
+    L.kv = api.kv_desc(L.k, L.v, w.n_q_heads)
+    for norm in (O.NORM_VISUAL_ONLY, O.NORM_CAUSAL_ROW):
+        got = score_one(w, L, norm)
+        a, v, lse = O.score_layer(L.np["q"], L.np["k"], L.np["v"], w.q_pos0, w.img_pos, w.img_off, norm=norm)
+        assert_scores(to_f64(got["a"]), a, what=f"a_t norm {norm}")
+        assert_scores(to_f64(got["lse"]), lse, what=f"row lse norm {norm}")
