@@ -3,9 +3,11 @@
     python bench.py [--steps K] [--warmup W] [--cfg 4] [--no-cpu]
 
 One step is the whole refresh step of one layer: the scoring pass
-(conduit_score), reweighting and global top-k (conduit_select_topk), the cache
-merge (conduit_scatter_kv) and the refresh attention of the selected rows
-(conduit_refresh_attn), all through the C ABI.  Inputs are synthetic (seeded
+(conduit_score), reweighting and global top-k (conduit_select_topk), then the
+cache merge and the refresh attention of the selected rows in one call
+(conduit_merge_refresh_attn; the per-call breakdown pass calls
+conduit_scatter_kv and conduit_refresh_attn separately), all through the C
+ABI.  Inputs are synthetic (seeded
 generator), already resident in HBM.  Before each timed step a 512 MB scrub
 buffer is written so the caches start cold; after it, the merged cache is
 restored from a pristine copy.  Both happen outside the per-step HIP events.
@@ -154,8 +156,11 @@ def main():
     out, lse = step.out[0][:k], step.lse[0][:k]
 
     def one_step(ev=None, split=False):
-        # ev: 5 events; the step's two bracket it, the three inner ones (split)
-        # separate the calls for the per-call breakdown.
+        # ev: 5 events; the step's two bracket it.  The step merges and
+        # refreshes in one call (conduit_merge_refresh_attn: the refresh plan
+        # and the merge in one launch); with split, the per-call breakdown
+        # pass calls conduit_scatter_kv and conduit_refresh_attn instead, with
+        # the three inner events separating the calls.
         if ev:
             ev[0].record(stream)
         api.conduit_score(kv, q, w.q_pos0, img, step.s_acc, step.a_acc, ws=step.ws_score)
@@ -165,10 +170,14 @@ def main():
                                 mask_out=step.mask, shat_out=step.shat, c_out=step.c, ws=step.ws_select)
         if ev and split:
             ev[2].record(stream)
-        api.conduit_scatter_kv(kv, pos, fresh["k_new"], fresh["v_new"])
-        if ev and split:
-            ev[3].record(stream)
-        api.conduit_refresh_attn(kv, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh)
+        if split:
+            api.conduit_scatter_kv(kv, pos, fresh["k_new"], fresh["v_new"])
+            if ev:
+                ev[3].record(stream)
+            api.conduit_refresh_attn(kv, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh)
+        else:
+            api.conduit_merge_refresh_attn(kv, pos, fresh["k_new"], fresh["v_new"], fresh["q_sel"], out, lse_out=lse,
+                                           ws=step.ws_refresh)
         if ev:
             ev[4].record(stream)
 
@@ -266,8 +275,8 @@ def main():
                           ws=step.ws_score)
         api.conduit_select_topk(step.s_acc, step.a_acc, 1, img, 1.0, k, step.idx, step.pos,
                                 mask_out=step.mask, shat_out=step.shat, c_out=step.c, ws=step.ws_select)
-        api.conduit_scatter_kv(kv, pos, fresh["k_new"], fresh["v_new"])
-        api.conduit_refresh_attn(kv, fresh["q_sel"], pos, out, lse_out=lse, ws=step.ws_refresh)
+        api.conduit_merge_refresh_attn(kv, pos, fresh["k_new"], fresh["v_new"], fresh["q_sel"], out, lse_out=lse,
+                                       ws=step.ws_refresh)
 
     def timed_restored(fn):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]

@@ -335,6 +335,23 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
                                     void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ *
+ * The per-layer recompute of Sec. 3 in one call: the cache merge of
+ * conduit_scatter_kv (without the copy of the stale rows) followed by
+ * conduit_refresh_attn over the merged cache, with the same arguments and
+ * results as the two calls in that order.  For bf16 the refresh's work plan
+ * and the merge run in one launch (they are independent; the attention needs
+ * both), which saves a launch and the plan's time on the critical path.
+ *
+ * Arguments as in conduit_scatter_kv and conduit_refresh_attn; ws sized by
+ * conduit_refresh_workspace_bytes(kv, k).  Errors: those of the two calls,
+ * all checked before anything is enqueued.  k = 0 enqueues nothing.
+ * ------------------------------------------------------------------------ */
+conduit_status conduit_merge_refresh_attn(const conduit_kv *kv, const int32_t *pos, int32_t k,
+                                          const void *k_new, const void *v_new, const void *q_sel,
+                                          float scale, void *o_out, float *lse_out, void *ws,
+                                          size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ *
  * The merge and the refresh attention of several layers of one request at
  * once (the recompute of Sec. 3 runs in every layer with the same selection
  * M, Algorithm 1).  The merged caches equal those of conduit_scatter_kv called

@@ -33,7 +33,7 @@ EXPORTS = [
     "conduit_profile_read", "conduit_value_norms", "conduit_residual_workspace_bytes",
     "conduit_residual_error", "conduit_score_noalloc", "conduit_scatter_kv_layers",
     "conduit_refresh_layers_workspace_bytes", "conduit_refresh_attn_layers",
-    "conduit_score_layers_workspace_bytes", "conduit_score_layers",
+    "conduit_score_layers_workspace_bytes", "conduit_score_layers", "conduit_merge_refresh_attn",
 ]
 SCORE_NOALLOC_MAX_BYTES = 16 << 20
 
@@ -100,6 +100,8 @@ def lib() -> ctypes.CDLL:
         L.conduit_refresh_workspace_bytes.restype = sz
         L.conduit_refresh_attn.argtypes = [pkv, vp, vp, i32, f32, vp, vp, vp, sz, vp]
         L.conduit_refresh_attn.restype = ctypes.c_int
+        L.conduit_merge_refresh_attn.argtypes = [pkv, vp, i32, vp, vp, vp, f32, vp, vp, vp, sz, vp]
+        L.conduit_merge_refresh_attn.restype = ctypes.c_int
         pvp = ctypes.POINTER(ctypes.c_void_p)
         L.conduit_scatter_kv_layers.argtypes = [pkv, i32, vp, i32, pvp, pvp, vp]
         L.conduit_scatter_kv_layers.restype = ctypes.c_int
@@ -391,6 +393,21 @@ def conduit_refresh_attn(kv: KV, q_sel: torch.Tensor, pos: torch.Tensor, o_out: 
                                       _stream(stream)))
 
 
+def conduit_merge_refresh_attn(kv: KV, pos: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                               q_sel: torch.Tensor, o_out: torch.Tensor, lse_out: Optional[torch.Tensor] = None,
+                               scale: Optional[float] = None, ws: Optional[torch.Tensor] = None,
+                               stream=None) -> None:
+    """Cache merge and refresh attention of the same rows in one call; see
+    conduit_merge_refresh_attn."""
+    k = pos.numel()
+    if scale is None:
+        scale = 1.0 / math.sqrt(kv.head_dim)
+    ws = _workspace(refresh_workspace_bytes(kv, k), q_sel.device, ws)
+    _check(lib().conduit_merge_refresh_attn(ctypes.byref(kv), pos.data_ptr(), k, k_new.data_ptr(), v_new.data_ptr(),
+                                            q_sel.data_ptr(), scale, o_out.data_ptr(), _ptr(lse_out), _ptr(ws),
+                                            _nbytes(ws), _stream(stream)))
+
+
 def profile_enable(enabled: bool) -> None:
     """Turn per-launch kernel timing on (clearing the record) or off, for the
     calling thread (conduit_profile_enable)."""
@@ -485,6 +502,10 @@ class RefreshStep:
                                         ws=self.ws_refresh, stream=stream)
             return
         for li, (kv, F) in enumerate(zip(self.kvs, fresh)):
+            if k_old is None and v_old is None:  # merge and refresh in one call
+                conduit_merge_refresh_attn(kv, pos, F["k_new"], F["v_new"], F["q_sel"], self.out[li][: self.k],
+                                           lse_out=self.lse[li][: self.k], ws=self.ws_refresh, stream=stream)
+                continue
             conduit_scatter_kv(kv, pos, F["k_new"], F["v_new"],
                                None if k_old is None else k_old[li],
                                None if v_old is None else v_old[li], stream=stream)

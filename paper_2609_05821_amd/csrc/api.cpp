@@ -846,17 +846,10 @@ conduit_status conduit_select_topk(const float *s_acc, const float *a_acc, int32
   return ok();
 }
 
-conduit_status conduit_scatter_kv(const conduit_kv *kv, const int32_t *pos, int32_t k, const void *k_new,
-                                  const void *v_new, void *k_old_out, void *v_old_out, hipStream_t stream) {
-  conduit_status st = check_kv(kv);
-  if (st) return st;
-  if (k < 0 || k > kv->n_ctx) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_ctx]", k);
-  if (k == 0) return ok();
-  if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
-  if (!k_new || !v_new || !aligned16(k_new) || !aligned16(v_new))
-    return fail(CONDUIT_ERR_INVALID_ARG, "k_new and v_new must be non-NULL and 16-byte aligned");
-  if ((k_old_out && !aligned16(k_old_out)) || (v_old_out && !aligned16(v_old_out)))
-    return fail(CONDUIT_ERR_INVALID_ARG, "k_old_out and v_old_out must be 16-byte aligned");
+namespace {
+
+ScatterParams scatter_params(const conduit_kv *kv, const int32_t *pos, int32_t k, const void *k_new,
+                             const void *v_new, void *k_old_out, void *v_old_out) {
   ScatterParams sp{};
   sp.k = kv->k;
   sp.v = kv->v;
@@ -871,6 +864,67 @@ conduit_status conduit_scatter_kv(const conduit_kv *kv, const int32_t *pos, int3
   sp.v_new = v_new;
   sp.k_old = k_old_out;
   sp.v_old = v_old_out;
+  return sp;
+}
+
+// Checks of a refresh of k rows (k > 0) and its workspace.
+conduit_status check_refresh(const conduit_kv *kv, const void *q_sel, const int32_t *pos, int32_t k,
+                             void *o_out, void *ws, size_t ws_bytes) {
+  if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
+  if (!q_sel || !aligned16(q_sel) || !o_out || !aligned16(o_out))
+    return fail(CONDUIT_ERR_INVALID_ARG, "q_sel and o_out must be non-NULL and 16-byte aligned");
+  if (kv->dtype == CONDUIT_BF16 && attn_blocks(k, kv->n_q_heads / kv->n_kv_heads, true) > kAttnPlanMaxBlocks)
+    return fail(CONDUIT_ERR_UNSUPPORTED, "k * n_q_heads / n_kv_heads = %lld exceeds %lld",
+                (long long)k * (kv->n_q_heads / kv->n_kv_heads),
+                (long long)kAttnPlanMaxBlocks * attn_pairs_per_block(true));
+  return check_ws(ws, ws_bytes, refresh_layout(kv, k).total);
+}
+
+// Refresh attention of the rows at pos (the plan and partials in ws for bf16).
+AttnParams refresh_params(const conduit_kv *kv, const void *q_sel, const int32_t *pos, int32_t k, float scale,
+                          void *o_out, float *lse_out, void *ws) {
+  AttnParams ap{};
+  ap.k = kv->k;
+  ap.v = kv->v;
+  ap.k_stride = kv->k_stride;
+  ap.v_stride = kv->v_stride;
+  ap.pages = pages_of(kv);
+  ap.n_kv_heads = kv->n_kv_heads;
+  ap.group = kv->n_q_heads / kv->n_kv_heads;
+  ap.n_q_heads = kv->n_q_heads;
+  ap.n_ctx = kv->n_ctx;
+  ap.q = q_sel;
+  ap.n_rows = k;
+  ap.row_pos = pos;
+  ap.q_pos0 = 0;
+  ap.vis_only = 0;
+  ap.scale_log2 = scale * kLog2e;
+  ap.lse_out = lse_out;
+  ap.o_out = o_out;
+  if (kv->dtype == CONDUIT_BF16) {
+    const RefreshLayout L = refresh_layout(kv, k);
+    ap.plan = plan_at(ws, L.plan);
+    ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
+    ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
+    ap.part_o = reinterpret_cast<u16 *>(at(ws, L.plan.part_o));
+  }
+  return ap;
+}
+
+}  // namespace
+
+conduit_status conduit_scatter_kv(const conduit_kv *kv, const int32_t *pos, int32_t k, const void *k_new,
+                                  const void *v_new, void *k_old_out, void *v_old_out, hipStream_t stream) {
+  conduit_status st = check_kv(kv);
+  if (st) return st;
+  if (k < 0 || k > kv->n_ctx) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_ctx]", k);
+  if (k == 0) return ok();
+  if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
+  if (!k_new || !v_new || !aligned16(k_new) || !aligned16(v_new))
+    return fail(CONDUIT_ERR_INVALID_ARG, "k_new and v_new must be non-NULL and 16-byte aligned");
+  if ((k_old_out && !aligned16(k_old_out)) || (v_old_out && !aligned16(v_old_out)))
+    return fail(CONDUIT_ERR_INVALID_ARG, "k_old_out and v_old_out must be 16-byte aligned");
+  const ScatterParams sp = scatter_params(kv, pos, k, k_new, v_new, k_old_out, v_old_out);
   hipError_t e = launch_scatter(sp, stream);
   if (e != hipSuccess) return hip_fail(e, "scatter");
   return ok();
@@ -890,48 +944,45 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
   if (k < 0 || k > kv->n_ctx) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_ctx]", k);
   if (!(scale > 0.f) || scale == __builtin_inff()) return fail(CONDUIT_ERR_INVALID_ARG, "scale must be finite and > 0");
   if (k == 0) return ok();
-  if (!pos) return fail(CONDUIT_ERR_INVALID_ARG, "pos is NULL");
-  if (!q_sel || !aligned16(q_sel) || !o_out || !aligned16(o_out))
-    return fail(CONDUIT_ERR_INVALID_ARG, "q_sel and o_out must be non-NULL and 16-byte aligned");
-  if (kv->dtype == CONDUIT_BF16 && attn_blocks(k, kv->n_q_heads / kv->n_kv_heads, true) > kAttnPlanMaxBlocks)
-    return fail(CONDUIT_ERR_UNSUPPORTED, "k * n_q_heads / n_kv_heads = %lld exceeds %lld",
-                (long long)k * (kv->n_q_heads / kv->n_kv_heads),
-                (long long)kAttnPlanMaxBlocks * attn_pairs_per_block(true));
-  const RefreshLayout L = refresh_layout(kv, k);
-  st = check_ws(ws, ws_bytes, L.total);
+  st = check_refresh(kv, q_sel, pos, k, o_out, ws, ws_bytes);
   if (st) return st;
-
-  AttnParams ap{};
-  ap.k = kv->k;
-  ap.v = kv->v;
-  ap.k_stride = kv->k_stride;
-  ap.v_stride = kv->v_stride;
-  ap.pages = pages_of(kv);
-  ap.n_kv_heads = kv->n_kv_heads;
-  ap.group = kv->n_q_heads / kv->n_kv_heads;
-  ap.n_q_heads = kv->n_q_heads;
-  ap.n_ctx = kv->n_ctx;
-  ap.q = q_sel;
-  ap.n_rows = k;
-  ap.row_pos = pos;
-  ap.q_pos0 = 0;
-  ap.vis_only = 0;
-  ap.scale_log2 = scale * kLog2e;
-  ap.lse_out = lse_out;
-  ap.o_out = o_out;
+  const AttnParams ap = refresh_params(kv, q_sel, pos, k, scale, o_out, lse_out, ws);
   hipError_t e;
   if (kv->dtype == CONDUIT_BF16) {
-    ap.plan = plan_at(ws, L.plan);
-    ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
-    ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
-    ap.part_o = reinterpret_cast<u16 *>(at(ws, L.plan.part_o));
     e = launch_attn(ap, kv->head_dim, true, stream);
-    if (e != hipSuccess) return hip_fail(e, "refresh attention");
   } else {
     DirectOut out{nullptr, lse_out, static_cast<float *>(o_out)};
     e = launch_attn_f32(ap, out, kv->head_dim, true, stream);
-    if (e != hipSuccess) return hip_fail(e, "refresh attention");
   }
+  if (e != hipSuccess) return hip_fail(e, "refresh attention");
+  return ok();
+}
+
+conduit_status conduit_merge_refresh_attn(const conduit_kv *kv, const int32_t *pos, int32_t k, const void *k_new,
+                                          const void *v_new, const void *q_sel, float scale, void *o_out,
+                                          float *lse_out, void *ws, size_t ws_bytes, hipStream_t stream) {
+  conduit_status st = check_kv(kv);
+  if (st) return st;
+  if (k < 0 || k > kv->n_ctx) return fail(CONDUIT_ERR_INVALID_ARG, "k = %d outside [0, n_ctx]", k);
+  if (!(scale > 0.f) || scale == __builtin_inff()) return fail(CONDUIT_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (k == 0) return ok();
+  if (!k_new || !v_new || !aligned16(k_new) || !aligned16(v_new))
+    return fail(CONDUIT_ERR_INVALID_ARG, "k_new and v_new must be non-NULL and 16-byte aligned");
+  st = check_refresh(kv, q_sel, pos, k, o_out, ws, ws_bytes);
+  if (st) return st;
+  const ScatterParams sp = scatter_params(kv, pos, k, k_new, v_new, nullptr, nullptr);
+  const AttnParams ap = refresh_params(kv, q_sel, pos, k, scale, o_out, lse_out, ws);
+  hipError_t e;
+  if (kv->dtype == CONDUIT_BF16) {
+    e = launch_merge_refresh(ap, sp, kv->head_dim, stream);
+  } else {
+    e = launch_scatter(sp, stream);
+    if (e == hipSuccess) {
+      DirectOut out{nullptr, lse_out, static_cast<float *>(o_out)};
+      e = launch_attn_f32(ap, out, kv->head_dim, true, stream);
+    }
+  }
+  if (e != hipSuccess) return hip_fail(e, "merge and refresh attention");
   return ok();
 }
 

@@ -151,7 +151,7 @@ __device__ int plan_exclusive_scan(int x, int *s_wave, int &total) {
   return before + inc - x;
 }
 
-__global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
+__device__ __forceinline__ void build_plan(const PlanArgs &a) {
   __shared__ int s_max[kAttnPlanMaxBlocks], s_min[kAttnPlanMaxBlocks];
   __shared__ int s_base[kAttnPlanMaxBlocks + 1], s_ct[kAttnPlanMaxBlocks];
   __shared__ int s_bin[kPlanBins];   // per size class: count, then base
@@ -293,6 +293,20 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) {
     a.plan.hdr[0] = min(n_items, a.plan.max_items);
     a.plan.hdr[1] = S;
   }
+}
+
+__global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanArgs a) { build_plan(a); }
+
+// The plan (workgroup 0) and the cache merge of the same rows (the other
+// workgroups, one wave per row) in one launch: they are independent, and the
+// attention that follows needs both.
+__global__ __launch_bounds__(kPlanThreads) void plan_scatter_kernel(PlanArgs a, ScatterParams sp) {
+  if (blockIdx.x == 0) {
+    build_plan(a);
+    return;
+  }
+  const int row = (blockIdx.x - 1) * kPlanWaves + (threadIdx.x >> 6);
+  if (row < sp.n_rows) scatter_row(sp, row, threadIdx.x & 63);
 }
 
 // W waves per workgroup, each owning 32 (row, head) pair columns.  With
@@ -1095,6 +1109,35 @@ int attn_uniform_splits(const AttnParams &p, int ppb, int target) {
   return ns;
 }
 
+namespace {
+
+// The plan's arguments for rows with positions (layers: the layers of one
+// launch, 0 for one).
+PlanArgs plan_args(const AttnParams &p, bool with_values, int layers) {
+  PlanArgs pa{};
+  pa.row_pos = p.row_pos;
+  pa.q_pos0 = p.q_pos0;
+  pa.n_rows = p.n_rows;
+  pa.group = p.group;
+  pa.n_kv_heads = p.n_kv_heads;
+  pa.n_ctx = p.n_ctx;
+  pa.ppb = attn_pairs_per_block(with_values);
+  // With several layers per launch every plan item runs once per layer, so
+  // when one layer's unsplit items do not fill the grid the plan needs
+  // proportionally fewer splits.  Layers that fill it on their own keep the
+  // one-layer plan: the launch then walks the layers one after the other
+  // like separate launches would (their K/V do not all fit in the last-level
+  // cache at once; unsplit items of very different lengths would spread the
+  // workgroups over several layers).
+  const int64_t one_layer = attn_plan_target(p.plan.n_pb, p.n_kv_heads, with_values);
+  pa.target_items = (int32_t)(layers > 0 && (int64_t)p.plan.n_pb * p.n_kv_heads < attn_grid(with_values)
+                                  ? std::max<int64_t>(1, one_layer / layers) : one_layer);
+  pa.plan = p.plan;
+  return pa;
+}
+
+}  // namespace
+
 hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, hipStream_t s, const LayerTable *lt,
                        bool plan_ready) {
   const LayerTable lt0 = lt ? *lt : LayerTable{};
@@ -1110,25 +1153,7 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
     p.plan.uniform_ns = 0;
     p.plan.uniform_items = 0;
   }
-  PlanArgs pa{};
-  pa.row_pos = p.row_pos;
-  pa.q_pos0 = p.q_pos0;
-  pa.n_rows = p.n_rows;
-  pa.group = p.group;
-  pa.n_kv_heads = p.n_kv_heads;
-  pa.n_ctx = p.n_ctx;
-  pa.ppb = ppb;
-  // With several layers per launch every plan item runs once per layer, so
-  // when one layer's unsplit items do not fill the grid the plan needs
-  // proportionally fewer splits.  Layers that fill it on their own keep the
-  // one-layer plan: the launch then walks the layers one after the other
-  // like separate launches would (their K/V do not all fit in the last-level
-  // cache at once; unsplit items of very different lengths would spread the
-  // workgroups over several layers).
-  const int64_t one_layer = attn_plan_target(p.plan.n_pb, p.n_kv_heads, with_values);
-  pa.target_items = (int32_t)(ml && (int64_t)p.plan.n_pb * p.n_kv_heads < attn_grid(with_values)
-                                  ? std::max<int64_t>(1, one_layer / lt0.n) : one_layer);
-  pa.plan = p.plan;
+  const PlanArgs pa = plan_args(p, with_values, lt0.n);
   hipError_t e = hipSuccess;
   if (p.plan.uniform_ns == 0 && !plan_ready) {
     ProfScope ps("attn_plan", s);
@@ -1180,6 +1205,17 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
   if (head_dim == 128) combine_kernel<128><<<blocks, 256, 0, s>>>(cp, lt0);
   else combine_kernel<64><<<blocks, 256, 0, s>>>(cp, lt0);
   return hipGetLastError();
+}
+
+hipError_t launch_merge_refresh(const AttnParams &p, const ScatterParams &sp, int head_dim, hipStream_t s) {
+  {
+    ProfScope ps("plan_scatter", s);
+    const unsigned blocks = 1u + (unsigned)((sp.n_rows + kPlanWaves - 1) / kPlanWaves);
+    plan_scatter_kernel<<<blocks, kPlanThreads, 0, s>>>(plan_args(p, true, 0), sp);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return launch_attn(p, head_dim, true, s, nullptr, /*plan_ready=*/true);
 }
 
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,

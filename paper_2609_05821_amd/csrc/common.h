@@ -504,6 +504,25 @@ struct ScatterParams {
   void *v_old;              // nullable
 };
 
+// One selected row of the cache merge, by one wave: 16-byte chunks of its K
+// and V (after copying the stale ones out, when asked).
+__device__ __forceinline__ void scatter_row(const ScatterParams &p, int row, int lane) {
+  const int64_t pos = kv_row(p.pages, min(max(p.pos[row], 0), p.n_ctx - 1));  // cache row
+  const int nch = p.row_bytes / 16;
+  char *kdst = static_cast<char *>(p.k) + pos * p.k_stride_bytes;
+  char *vdst = static_cast<char *>(p.v) + pos * p.v_stride_bytes;
+  const char *ksrc = static_cast<const char *>(p.k_new) + (int64_t)row * p.row_bytes;
+  const char *vsrc = static_cast<const char *>(p.v_new) + (int64_t)row * p.row_bytes;
+  for (int c = lane; c < nch; c += 64) {
+    const u32x4 kn = ld16(ksrc + 16 * c);
+    const u32x4 vn = ld16(vsrc + 16 * c);
+    if (p.k_old) st16(static_cast<char *>(p.k_old) + (int64_t)row * p.row_bytes + 16 * c, ld16(kdst + 16 * c));
+    if (p.v_old) st16(static_cast<char *>(p.v_old) + (int64_t)row * p.row_bytes + 16 * c, ld16(vdst + 16 * c));
+    st16(kdst + 16 * c, kn);
+    st16(vdst + 16 * c, vn);
+  }
+}
+
 // Per-layer cache and fresh-row pointers of a multi-layer merge.
 struct ScatterLayers {
   void *k[kMaxLayerBatch];
@@ -586,6 +605,9 @@ hipError_t launch_select(const SelectParams &p, const ImageTable &tbl, hipStream
 hipError_t launch_select_explicit(const SelectParams &p, const ImageTable &tbl, hipStream_t s);
 hipError_t launch_clear_u8(uint8_t *p, int64_t n, hipStream_t s);
 hipError_t launch_scatter(const ScatterParams &p, hipStream_t s);
+// Cache merge of the rows and their refresh attention (bf16): the plan and the
+// merge in one launch, then the attention and the split merge.
+hipError_t launch_merge_refresh(const AttnParams &p, const ScatterParams &sp, int head_dim, hipStream_t s);
 hipError_t launch_scatter_layers(const ScatterParams &p, const ScatterLayers &sl, hipStream_t s);
 hipError_t launch_residual(const ResidualParams &p, int head_dim, bool bf16, hipStream_t s);
 

@@ -8,23 +8,6 @@
 namespace conduit {
 namespace {
 
-__device__ __forceinline__ void scatter_row(const ScatterParams &p, int row, int lane) {
-  const int64_t pos = kv_row(p.pages, min(max(p.pos[row], 0), p.n_ctx - 1));  // cache row
-  const int nch = p.row_bytes / 16;
-  char *kdst = static_cast<char *>(p.k) + pos * p.k_stride_bytes;
-  char *vdst = static_cast<char *>(p.v) + pos * p.v_stride_bytes;
-  const char *ksrc = static_cast<const char *>(p.k_new) + (int64_t)row * p.row_bytes;
-  const char *vsrc = static_cast<const char *>(p.v_new) + (int64_t)row * p.row_bytes;
-  for (int c = lane; c < nch; c += 64) {
-    const u32x4 kn = ld16(ksrc + 16 * c);
-    const u32x4 vn = ld16(vsrc + 16 * c);
-    if (p.k_old) st16(static_cast<char *>(p.k_old) + (int64_t)row * p.row_bytes + 16 * c, ld16(kdst + 16 * c));
-    if (p.v_old) st16(static_cast<char *>(p.v_old) + (int64_t)row * p.row_bytes + 16 * c, ld16(vdst + 16 * c));
-    st16(kdst + 16 * c, kn);
-    st16(vdst + 16 * c, vn);
-  }
-}
-
 __global__ __launch_bounds__(256) void scatter_kernel(ScatterParams p) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row < p.n_rows) scatter_row(p, row, threadIdx.x & 63);

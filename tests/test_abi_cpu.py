@@ -380,3 +380,28 @@ def test_score_rejects_span_queries_past_2_gib():
                            api.AGG_MEAN, 0.1, None, None, None, FAKE, FAKE, 0, None, None, FAKE, 1 << 40,
                            None) == api.ERR_UNSUPPORTED
     assert b"2^31" in L.conduit_last_error()
+
+
+def test_merge_refresh_rejects_before_enqueueing():
+    """conduit_merge_refresh_attn checks the merge's and the refresh's
+    arguments and the workspace before anything is enqueued."""
+    L = api.lib()
+    d = kv()
+    need = L.conduit_refresh_workspace_bytes(ctypes.byref(d), 300)
+    mr = L.conduit_merge_refresh_attn
+
+    def call(kvd=d, pos=FAKE, k=300, kn=FAKE, vn=FAKE, q=FAKE, scale=0.1, o=FAKE, nbytes=need):
+        return mr(ctypes.byref(kvd) if kvd is not None else None, pos, k, kn, vn, q, scale, o, None, FAKE, nbytes,
+                  None)
+
+    assert call(kvd=None) == api.ERR_INVALID_ARG
+    assert call(k=-1) == api.ERR_INVALID_ARG
+    assert call(k=2000) == api.ERR_INVALID_ARG
+    assert call(scale=0.0) == api.ERR_INVALID_ARG
+    assert call(pos=None) == api.ERR_INVALID_ARG
+    assert call(kn=None) == api.ERR_INVALID_ARG
+    assert call(vn=FAKE + 4) == api.ERR_INVALID_ARG
+    assert call(q=None) == api.ERR_INVALID_ARG
+    assert call(o=FAKE + 8) == api.ERR_INVALID_ARG
+    assert call(nbytes=need - 256) == api.ERR_WORKSPACE
+    assert call(k=0, pos=None, kn=None, vn=None, q=None, o=None, nbytes=0) == api.OK

@@ -196,3 +196,33 @@ def test_refresh_large_logit_jumps(norms):
         L["k"][p] = w._cast((nrm * u).astype(np.float32))
     sel = np.sort(rng.choice(w.n_vis, size=240, replace=False))
     check(w, L, sel)
+
+
+@pytest.mark.parametrize("case", ["ragged_bf16_gqa7", "ragged_bf16_d64_gqa4", "cfg1_fp32_mha", "cfg4_16k"])
+def test_merge_refresh_equals_separate_calls(case):
+    """conduit_merge_refresh_attn (the plan and the merge in one launch for
+    bf16) gives the merged cache, O and the LSE of conduit_scatter_kv followed
+    by conduit_refresh_attn, bit for bit; and O matches the oracle."""
+    w = W.config(4) if case == "cfg4_16k" else CASES[case]()
+    L = w.layer(0)
+    rng = np.random.default_rng(len(case))
+    k = max(1, w.n_vis // 10)
+    sel = np.sort(rng.choice(w.n_vis, size=k, replace=False))
+    out_s, lse_s, kc_s, vc_s = run_refresh(w, L, sel)
+    P = w.vis_positions()
+    kc, vc = to_dev(L["k"]), to_dev(L["v"])
+    kv = api.kv_desc(kc, vc, w.n_q_heads)
+    pos = torch.from_numpy(P[sel].astype(np.int32)).to(DEV)
+    q_sel = to_dev(L["q_star"][sel])
+    out = torch.empty_like(out_s)
+    lse = torch.empty_like(lse_s)
+    api.conduit_merge_refresh_attn(kv, pos, to_dev(L["k_star"][sel]), to_dev(L["v_star"][sel]), q_sel, out,
+                                   lse_out=lse)
+    torch.cuda.synchronize()
+    for a, b in ((out, out_s), (lse, lse_s), (kc, kc_s), (vc, vc_s)):
+        np.testing.assert_array_equal(bits(a), bits(b))
+    rows = range(k) if case != "cfg4_16k" else range(0, k, 13)
+    _, _, o_ref, _ = oracle_refresh_rows(L["k"], L["v"], P[sel], L["k_star"][sel], L["v_star"][sel],
+                                         L["q_star"][sel], rows)
+    r = np.asarray(list(rows))
+    assert_attention(to_f64(out)[r], o_ref[r], w.dtype, what="O")
