@@ -153,6 +153,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   __shared__ alignas(16) float bs[2][kQChunk];
   __shared__ ImageLds img;
   __shared__ float b_all[FUSE ? kColsumMaxLsePairs : 1];
+  __shared__ int64_t s_row[kColsumKeysPerBlock];  // cache row of each key of the block
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, half = lane >> 5;
@@ -231,25 +232,21 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   const bool tvalid = t < p.n_vis;
   bf16x8 kreg[KS];
   {
-    const u16 *krow = Kg + kv_row(p.pages, vis_position(img, tvalid ? t : p.n_vis - 1)) * p.k_stride + kvh * D + 8 * half;
+    // the key's cache row (page lookup included), also kept for the V rows
+    const int64_t row = kv_row(p.pages, vis_position(img, tvalid ? t : p.n_vis - 1));
+    if (half == 0) s_row[wave * 32 + col] = row;
+    const u16 *krow = Kg + row * p.k_stride + kvh * D + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) kreg[ks] = as_bf16x8(ld16(krow + ks * 16));
   }
   // V rows of the block's keys for the value norms, 16 bytes per item (not
   // read when the norms are given).  They are loaded during the last Q
   // chunk, so that they do not compete with the K rows and the first chunk
-  // for memory bandwidth at the start.
-  // The rows (page lookups included) are resolved here, so that the loads
-  // inside the chunk loop wait on nothing.
+  // for memory bandwidth at the start; their addresses are formed after the
+  // first chunk is staged, from the rows the K loads resolved.
   const bool read_v = vnorm_in == nullptr;
   u32x4 vv[VPT];
   const u16 *vsrc[VPT];
-#pragma unroll
-  for (int i = 0; i < VPT; ++i) {
-    const int vi = tid + kColsumThreads * i;
-    const int tv = min(blockIdx.x * kColsumKeysPerBlock + vi / (D / 8), p.n_vis - 1);
-    vsrc[i] = Vg + kv_row(p.pages, vis_position(img, tv)) * p.v_stride + kvh * D + (vi % (D / 8)) * 8;
-  }
   auto load_v = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < VPT; ++i) vv[i] = read_v ? ld16(vsrc[i]) : u32x4{0, 0, 0, 0};
@@ -266,30 +263,48 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
     // offset of the load, the same for every lane
     const auto m_rsrc = buffer_rsrc(lse_part_m, 0x7fffffff), l_rsrc = buffer_rsrc(lse_part_l, 0x7fffffff);
     const uint32_t split_b = (uint32_t)p.lse_ppb * 4u;
-    for (int pr = tid; pr < n_pair; pr += kColsumThreads) {
-      const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
-      const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns;
-      float M = -kInf, L = 0.f;
-      float mv[kLseRegSplits], lv[kLseRegSplits];
-      const uint32_t row_b0 = (uint32_t)(slot0 * p.lse_ppb + j) * 4u;
+    // Two rows per thread and pass, both rows' reads issued before either
+    // is reduced (a second row past n_pair reads the last row instead and
+    // is not stored).
+    for (int pr0 = tid; pr0 < n_pair; pr0 += 2 * kColsumThreads) {
+      float mv[2][kLseRegSplits], lv[2][kLseRegSplits];
 #pragma unroll
-      for (int sp = 0; sp < kLseRegSplits; ++sp) {
-        const uint32_t so = (uint32_t)min(sp, ns - 1) * split_b;
-        mv[sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(m_rsrc, row_b0, so, 0));
-        lv[sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(l_rsrc, row_b0, so, 0));
+      for (int u = 0; u < 2; ++u) {
+        const int pr = min(pr0 + u * kColsumThreads, n_pair - 1);
+        const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
+        const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns;
+        const uint32_t row_b0 = (uint32_t)(slot0 * p.lse_ppb + j) * 4u;
+#pragma unroll
+        for (int sp = 0; sp < kLseRegSplits; ++sp) {
+          const uint32_t so = (uint32_t)min(sp, ns - 1) * split_b;
+          mv[u][sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(m_rsrc, row_b0, so, 0));
+          lv[u][sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(l_rsrc, row_b0, so, 0));
+        }
       }
 #pragma unroll
-      for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[sp]) : M;
+      for (int u = 0; u < 2; ++u) {
+        const int pr = pr0 + u * kColsumThreads;
+        float M = -kInf, L = 0.f;
 #pragma unroll
-      for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[sp] - M) * lv[sp] : L;
-      const float b = M + __log2f(L);
-      b_all[pr] = b;
-      if (blockIdx.x == 0 && lse_out) lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
+        for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[u][sp]) : M;
+#pragma unroll
+        for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[u][sp] - M) * lv[u][sp] : L;
+        const float b = M + __log2f(L);
+        if (pr < n_pair) {
+          b_all[pr] = b;
+          if (blockIdx.x == 0 && lse_out) lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
+        }
+      }
     }
     __syncthreads();
   }
   store_chunk(0, 0, qv, bv);
   __syncthreads();
+#pragma unroll
+  for (int i = 0; i < VPT; ++i) {
+    const int vi = tid + kColsumThreads * i;  // key vi / (D/8) of the block (rows past n_vis repeat the last)
+    vsrc[i] = Vg + s_row[vi / (D / 8)] * p.v_stride + kvh * D + (vi % (D / 8)) * 8;
+  }
 
   float colsum = 0.f;
   for (int c = 0; c < nch; ++c) {
