@@ -225,6 +225,59 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   float bv = kInf;
   load_chunk(qv, bv);
 
+  // FUSE: b = M + log2(sum_s l_s 2^(m_s - M)) over the splits of the row's
+  // block, s ascending, exactly as the statistics merge computes it.  The
+  // host fuses only up to kLseRegSplits splits: they are read in one pass
+  // (indices clamped, so every read is issued unconditionally) and reduced
+  // from registers, two rows per thread and pass (a second row past n_pair
+  // reads the last row instead and is not stored).  Split sp of a row sits
+  // sp * lse_ppb floats after split 0: a scalar offset of the load, the
+  // same for every lane.  The first pass's reads go out before the image
+  // table and the K rows: they hit in the cache the statistics kernel just
+  // wrote, and reads issued after the K rows would wait for them (the memory
+  // counter returns in order).
+  const int ns = p.lse_ns;
+  const auto m_rsrc = buffer_rsrc(lse_part_m, FUSE ? 0x7fffffff : 0);
+  const auto l_rsrc = buffer_rsrc(lse_part_l, FUSE ? 0x7fffffff : 0);
+  const uint32_t split_b = (uint32_t)p.lse_ppb * 4u;
+  float mv[FUSE ? 2 : 1][FUSE ? kLseRegSplits : 1], lv[FUSE ? 2 : 1][FUSE ? kLseRegSplits : 1];
+  auto lse_issue = [&](int pr0) __attribute__((always_inline)) {
+    if constexpr (FUSE) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int pr = min(pr0 + u * kColsumThreads, n_pair - 1);
+        const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
+        const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns;
+        const uint32_t row_b0 = (uint32_t)(slot0 * p.lse_ppb + j) * 4u;
+#pragma unroll
+        for (int sp = 0; sp < kLseRegSplits; ++sp) {
+          const uint32_t so = (uint32_t)min(sp, ns - 1) * split_b;
+          mv[u][sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(m_rsrc, row_b0, so, 0));
+          lv[u][sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(l_rsrc, row_b0, so, 0));
+        }
+      }
+    }
+  };
+  auto lse_reduce = [&](int pr0) __attribute__((always_inline)) {
+    if constexpr (FUSE) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int pr = pr0 + u * kColsumThreads;
+        float M = -kInf, L = 0.f;
+#pragma unroll
+        for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[u][sp]) : M;
+#pragma unroll
+        for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[u][sp] - M) * lv[u][sp] : L;
+        const float b = M + __log2f(L);
+        if (pr < n_pair) {
+          b_all[pr] = b;
+          if (blockIdx.x == 0 && lse_out) lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
+        }
+      }
+    }
+  };
+  if (FUSE && n_pair > 0) lse_issue(tid);
+
   image_table_to_lds(p.tbl, img, tid, kColsumThreads);
   __syncthreads();
   // This lane's key column, held as the B operand for every row tile.
@@ -253,48 +306,10 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   };
   const int v_chunk = nch - 1;  // no chunk load (and wait) follows
   if constexpr (FUSE) {
-    // b = M + log2(sum_s l_s 2^(m_s - M)) over the splits of the row's
-    // block, s ascending, exactly as the statistics merge computes it.  The
-    // host fuses only up to kLseRegSplits splits: they are read in one pass
-    // (indices clamped, so every read is issued unconditionally) and reduced
-    // from registers.
-    const int ns = p.lse_ns;
-    // split sp of a row sits sp * lse_ppb floats after split 0: a scalar
-    // offset of the load, the same for every lane
-    const auto m_rsrc = buffer_rsrc(lse_part_m, 0x7fffffff), l_rsrc = buffer_rsrc(lse_part_l, 0x7fffffff);
-    const uint32_t split_b = (uint32_t)p.lse_ppb * 4u;
-    // Two rows per thread and pass, both rows' reads issued before either
-    // is reduced (a second row past n_pair reads the last row instead and
-    // is not stored).
-    for (int pr0 = tid; pr0 < n_pair; pr0 += 2 * kColsumThreads) {
-      float mv[2][kLseRegSplits], lv[2][kLseRegSplits];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int pr = min(pr0 + u * kColsumThreads, n_pair - 1);
-        const int pb = pr / p.lse_ppb, j = pr % p.lse_ppb;
-        const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns;
-        const uint32_t row_b0 = (uint32_t)(slot0 * p.lse_ppb + j) * 4u;
-#pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) {
-          const uint32_t so = (uint32_t)min(sp, ns - 1) * split_b;
-          mv[u][sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(m_rsrc, row_b0, so, 0));
-          lv[u][sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(l_rsrc, row_b0, so, 0));
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int pr = pr0 + u * kColsumThreads;
-        float M = -kInf, L = 0.f;
-#pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[u][sp]) : M;
-#pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[u][sp] - M) * lv[u][sp] : L;
-        const float b = M + __log2f(L);
-        if (pr < n_pair) {
-          b_all[pr] = b;
-          if (blockIdx.x == 0 && lse_out) lse_out[(pr / G) * p.n_q_heads + kvh * G + pr % G] = b * kLn2;
-        }
-      }
+    if (n_pair > 0) lse_reduce(tid);
+    for (int pr0 = tid + 2 * kColsumThreads; pr0 < n_pair; pr0 += 2 * kColsumThreads) {
+      lse_issue(pr0);
+      lse_reduce(pr0);
     }
     __syncthreads();
   }
