@@ -666,7 +666,8 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
       // mod 4: the iteration reads K(t..t+2) and V(t..t+1) while K(t+3),
       // K(t+4), V(t+2) and V(t+3) arrive; they are awaited before the
       // barrier, one iteration after they were issued.  A tile t+1 past kend
-      // arrives as zeros and is masked whole.
+      // arrives as zeros and is masked whole.  The last iteration issues no
+      // transfers: only a next iteration would read them.
       // The first attempt checks the probability sums, a restart tracks the
       // maxima (below).
       auto tiles = [&](auto exact_tag) __attribute__((always_inline)) {
@@ -676,11 +677,13 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
         const int k3 = k2 + 1 == 5 ? 0 : k2 + 1, k4 = k3 + 1 == 5 ? 0 : k3 + 1;
         const int v1 = (vs + 1) & 3, v2 = (vs + 2) & 3, v3 = (vs + 3) & 3;
         const bool more2 = t0 + 2 * KT < kend;  // the next iteration exists
-        const int64_t r2 = row_of(t0 + 2 * KT), r3 = row_of(t0 + 3 * KT), r4 = row_of(t0 + 4 * KT);
-        dma_tile(false, v2, t0 + 2 * KT, r2);
-        dma_tile(false, v3, t0 + 3 * KT, r3);
-        dma_tile(true, k3, t0 + 3 * KT, r3);
-        dma_tile(true, k4, t0 + 4 * KT, r4);
+        if (more2) {
+          const int64_t r2 = row_of(t0 + 2 * KT), r3 = row_of(t0 + 3 * KT), r4 = row_of(t0 + 4 * KT);
+          dma_tile(false, v2, t0 + 2 * KT, r2);
+          dma_tile(false, v3, t0 + 3 * KT, r3);
+          dma_tile(true, k3, t0 + 3 * KT, r3);
+          dma_tile(true, k4, t0 + 4 * KT, r4);
+        }
         const bool m0 = tile_masked(t0), m1 = tile_masked(t0 + KT);
         sub_step(exact_tag, sa, sb, ks, 1, vs, 0, m0, ks, t0, 0);       // S(t,1)   | P(t,0) V
         sub_step(exact_tag, sb, sa, k1, 0, vs, 1, m0, ks, t0, 1);       // S(t+1,0) | P(t,1) V
@@ -702,22 +705,28 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
       // One tile per barrier, K stages mod 4: iteration t reads K(t) and
       // K(t+1) while K(t+2) is complete and K(t+3) arrives.  Before the
       // barrier a wave waits until at most kSlots of its transfers are
-      // outstanding: all of K(t+2)'s, so only K(t+3)'s may remain.
+      // outstanding: all of K(t+2)'s, so only K(t+3)'s may remain.  K(t+3)
+      // is issued only if iteration t+2 exists (the first to read it);
+      // otherwise the wave waits for all of its transfers.
       auto tiles = [&](auto exact_tag) __attribute__((always_inline)) {
       constexpr bool kExact = decltype(exact_tag)::value;
       int t0 = kbeg, st = 0;  // K stage of tile t
       for (;;) {
         const bool more = t0 + KT < kend;
+        const bool need3 = t0 + 2 * KT < kend;  // iteration t+2 exists
         const int st1 = (st + 1) & 3, st3 = (st + 3) & 3;
-        dma_tile(true, st3, t0 + 3 * KT, row_of(t0 + 3 * KT));
-        okmask_tile(st3, t0 + 3 * KT);
+        if (need3) {
+          dma_tile(true, st3, t0 + 3 * KT, row_of(t0 + 3 * KT));
+          okmask_tile(st3, t0 + 3 * KT);
+        }
         const bool m0 = tile_masked(t0);
         sub_step(exact_tag, sa, sb, st, 1, 0, 0, m0, st, t0, 0);   // S(t,1)   | P(t,0)
         sub_step(exact_tag, sb, sa, st1, 0, 0, 0, m0, st, t0, 1);  // S(t+1,0) | P(t,1)
         if constexpr (!kExact) {
           if (__ballot(over) != 0 && lane == 0) s_restart = gen;
         }
-        vm_wait<kSlots - 1>();
+        if (need3) vm_wait<kSlots - 1>();
+        else vm_wait<0>();
         __syncthreads();
         if constexpr (!kExact) restart = s_restart == gen;
         if (!more || restart) break;
