@@ -751,21 +751,6 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
           if (row_b) row_b[gpair] = b;
           if (lse_out) lse_out[gpair] = b * kLn2;
         }
-        if constexpr (PV) {
-          const float inv = 1.f / l_tot;
-          u16 *dst = static_cast<u16 *>(o_out) + (int64_t)gpair * D;
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-              uint2 w;
-              w.x = (uint32_t)f32_to_bf16(o[dt][4 * g4] * inv) |
-                    ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 1] * inv) << 16);
-              w.y = (uint32_t)f32_to_bf16(o[dt][4 * g4 + 2] * inv) |
-                    ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 3] * inv) << 16);
-              *reinterpret_cast<uint2 *>(dst + dt * 32 + 8 * g4 + 4 * half) = w;
-            }
-        }
       } else {
         const int64_t idx2 = (item.w + slot_off) * kPairs + wave * 32 + col;
         if (half == 0) {
@@ -777,24 +762,43 @@ __global__ __launch_bounds__(W * 64, 8 / W) void attn_bf16_kernel(AttnParams p, 
             p.part_l[idx2] = l_tot;
           }
         }
-        if constexpr (PV) {
-          // the split's own attention output O_s / l_s (a convex combination
-          // of V rows) in bf16; l = 0 (no visible key in the split) gives 0
-          const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-          u16 *dst = p.part_o + idx2 * D;
+      }
+    }
+    if constexpr (PV) {
+      // O / l of a single-split block, else the split's own output O_s / l_s
+      // (a convex combination of V rows; l = 0, no visible key in the split,
+      // gives 0), in bf16.  A lane holds 4-dim pieces of its pair column, so
+      // the rows are assembled in LDS (pair-major, the K stages: no tile is
+      // read any more) and written out 16 bytes per lane, each pair's row
+      // contiguous.
+      static_assert(kPairs * Geo::kPitch <= (int)(sizeof(sm.k) / 2), "output rows fit the K stages");
+      u16 *orow = &sm.k[0][0][0];
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
+      for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-              uint2 w;
-              w.x = (uint32_t)f32_to_bf16(o[dt][4 * g4] * inv) |
-                    ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 1] * inv) << 16);
-              w.y = (uint32_t)f32_to_bf16(o[dt][4 * g4 + 2] * inv) |
-                    ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 3] * inv) << 16);
-              *reinterpret_cast<uint2 *>(dst + dt * 32 + 8 * g4 + 4 * half) = w;
-            }
+        for (int g4 = 0; g4 < 4; ++g4) {
+          uint2 w;
+          w.x = (uint32_t)f32_to_bf16(o[dt][4 * g4] * inv) | ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 1] * inv) << 16);
+          w.y = (uint32_t)f32_to_bf16(o[dt][4 * g4 + 2] * inv) | ((uint32_t)f32_to_bf16(o[dt][4 * g4 + 3] * inv) << 16);
+          *reinterpret_cast<uint2 *>(orow + (wave * 32 + col) * Geo::kPitch + dt * 32 + 8 * g4 + 4 * half) = w;
+        }
+      __syncthreads();
+      constexpr int kChunks = D / 8;  // 16-byte pieces of a row
+      // rows of the item's pairs: O rows (row, head) or consecutive partial rows
+      u16 *const obase = single ? static_cast<u16 *>(o_out) : p.part_o + (item.w + slot_off) * kPairs * D;
+#pragma unroll 2
+      for (int i = 0; i < kPairs * kChunks / kThreads; ++i) {
+        const int c = tid + kThreads * i;
+        const int pl = c / kChunks, ch = c % kChunks;
+        const int pr = pair0 + pl;
+        if (pr < n_pairs) {
+          const u32x4 v = *reinterpret_cast<const u32x4 *>(orow + pl * Geo::kPitch + ch * 8);
+          const int64_t row = single ? (int64_t)(pr / G) * p.n_q_heads + kvh * G + pr % G : pl;
+          *reinterpret_cast<u32x4 *>(obase + row * D + ch * 8) = v;
         }
       }
+      __syncthreads();  // the next item's transfers overwrite these rows
     }
 
     // Statistics with the closed-form plan: each split item of a block,
