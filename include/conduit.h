@@ -211,7 +211,10 @@ conduit_status conduit_score_noalloc(const conduit_kv *kv, const void *q, int32_
  * the scored layers L of Algorithm 1): conduit_score of every layer in turn,
  * accumulating into s_acc and a_acc, with the layers' work in a few launches
  * (up to 16 layers in each).  The results equal those of the per-layer calls
- * bit for bit (the same arithmetic, layers added in order).
+ * up to rounding: the layers are added in order with the same arithmetic,
+ * but a launch of several layers may cut each layer's row statistics into
+ * fewer key splits (the grid is filled by the layers instead), which changes
+ * the rounding of the row log-sum-exps (relative differences near 1e-7).
  *
  * kvs       HOST [n_layers] descriptors shaped alike (see the multi-layer
  *           merge below); q: HOST [n_layers] span queries, each as q above.

@@ -403,8 +403,7 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
       ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
       // split rows: merged by the column-sum workgroups, or else by the
       // statistics kernel's last split of each block (no merge launch)
-      lse_ns = attn_uniform_splits(ap, attn_pairs_per_block(false),
-                                   attn_grid(false) * attn_plan_rounds(false));
+      lse_ns = attn_span_splits(ap, attn_pairs_per_block(false), 1);
       fuse_lse = colsum_fuses_lse(lse_ns, (int64_t)n_q * ap.group, img->n_vis);
       if (!fuse_lse) {
         ap.merge_flag = reinterpret_cast<uint32_t *>(at(ws, L.merge_flag));
@@ -557,11 +556,7 @@ conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, con
   ap.plan = plan_at(ws, L.plan);
   ap.part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
   ap.part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));
-  const int32_t lse_ns = attn_uniform_splits(ap, attn_pairs_per_block(false),
-                                             attn_grid(false) * attn_plan_rounds(false));
-  const bool fuse_lse = colsum_fuses_lse(lse_ns, (int64_t)n_q * ap.group, img->n_vis);
-  if (!fuse_lse) ap.merge_flag = reinterpret_cast<uint32_t *>(at(ws, L.merge_flag));
-  ap.skip_merge = 1;  // merged by the column sums or by the statistics kernel
+  ap.skip_merge = 1;  // merged by the column sums or by the statistics kernel (split count per launch, below)
   ap.zero_i32 = done;
   ap.zero_n = n_done;
 
@@ -582,13 +577,6 @@ conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, con
   cs.scale_log2 = scale_log2;
   cs.colsum_part = reinterpret_cast<float *>(at(ws, L.colsum));
   cs.vsq_part = reinterpret_cast<float *>(at(ws, L.vsq));
-  if (fuse_lse) {
-    cs.lse_part_m = ap.part_m;
-    cs.lse_part_l = ap.part_l;
-    cs.lse_ns = lse_ns;
-    cs.lse_ppb = attn_pairs_per_block(false);
-    cs.lse_layer_stride = (int64_t)L.plan.max_items * attn_pairs_per_block(false);
-  }
   cs.done = done;
   FinalizeParams fp{};
   fp.colsum_part = cs.colsum_part;
@@ -613,7 +601,18 @@ conduit_status conduit_score_layers(const conduit_kv *kvs, int32_t n_layers, con
       lt.rowb[i] = row_b + i * rows;
       lt.vnorm[i] = vnorm_in ? vnorm_in[l0 + i] : nullptr;
     }
-    if (!fuse_lse) ap.epoch = next_merge_epoch();  // each launch marks afresh
+    // The statistics' split count depends on the launch's layer count; the
+    // column sums rebuild the split rows themselves when they can, otherwise
+    // the statistics kernel merges them (each launch marks afresh).
+    const int32_t lse_ns = attn_span_splits(ap, attn_pairs_per_block(false), lt.n);
+    const bool fuse_lse = colsum_fuses_lse(lse_ns, (int64_t)n_q * ap.group, img->n_vis);
+    ap.merge_flag = fuse_lse ? nullptr : reinterpret_cast<uint32_t *>(at(ws, L.merge_flag));
+    if (!fuse_lse) ap.epoch = next_merge_epoch();
+    cs.lse_part_m = fuse_lse ? ap.part_m : nullptr;
+    cs.lse_part_l = fuse_lse ? ap.part_l : nullptr;
+    cs.lse_ns = fuse_lse ? lse_ns : 0;
+    cs.lse_ppb = fuse_lse ? attn_pairs_per_block(false) : 0;
+    cs.lse_layer_stride = fuse_lse ? (int64_t)L.plan.max_items * attn_pairs_per_block(false) : 0;
     hipError_t e = launch_attn(ap, D, false, stream, &lt);
     if (e != hipSuccess) return hip_fail(e, "row statistics");
     fp.accumulate = (l0 > 0 || accumulate) ? 1 : 0;

@@ -1122,6 +1122,47 @@ int attn_uniform_splits(const AttnParams &p, int ppb, int target) {
   return ns;
 }
 
+// Split count of the scoring span's statistics with `layers` layers in one
+// launch.  One layer takes attn_uniform_splits' count.  With several, every
+// split count multiplies into layers * blocks * KV heads items, so fewer
+// splits fill the grid: among the counts up to the one-layer count that
+// leave no split empty, the one with the least estimated time, i.e. grid
+// rounds times (tiles per split + kSpanItemTiles, an item's fixed start and
+// end in tiles), the smaller count on ties.
+int attn_span_splits(const AttnParams &p, int ppb, int layers) {
+  const int ns1 = attn_uniform_splits(p, ppb, attn_grid(false) * attn_plan_rounds(false));
+  if (layers <= 1) return ns1;
+  constexpr int kSpanItemTiles = 4;
+  const int64_t n_pairs = (int64_t)p.n_rows * p.group;
+  const int64_t n_pb = (n_pairs + ppb - 1) / ppb;
+  auto tiles_of = [&](int64_t b) {
+    const int64_t last = std::min<int64_t>((b + 1) * ppb, n_pairs) - 1;
+    const int maxpos = std::min(p.q_pos0 + (int)(last / p.group), p.n_ctx - 1);
+    return maxpos / KT + 1;
+  };
+  const int max_tiles = tiles_of(n_pb - 1);  // positions grow with the row
+  auto all_nonempty = [&](int n) {
+    for (int64_t b = 0; b < n_pb; ++b) {
+      const int t = tiles_of(b);
+      if ((int64_t)((t + n - 1) / n) * (n - 1) >= t) return false;
+    }
+    return true;
+  };
+  int best = ns1;
+  int64_t best_cost = INT64_MAX;
+  for (int ns = 1; ns <= ns1; ++ns) {
+    if (ns > 1 && !all_nonempty(ns)) continue;
+    const int64_t items = (int64_t)layers * n_pb * p.n_kv_heads * ns;
+    const int64_t rounds = (items + attn_grid(false) - 1) / attn_grid(false);
+    const int64_t cost = rounds * ((max_tiles + ns - 1) / ns + kSpanItemTiles);
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = ns;
+    }
+  }
+  return best;
+}
+
 namespace {
 
 // The plan's arguments for rows with positions (layers: the layers of one
@@ -1158,7 +1199,7 @@ hipError_t launch_attn(const AttnParams &p_in, int head_dim, bool with_values, h
   const int ppb = attn_pairs_per_block(with_values);
   AttnParams p = p_in;
   if (!p.row_pos && !with_values) {  // the scoring span: closed-form plan, no plan launch
-    const int ns = attn_uniform_splits(p, ppb, attn_grid(with_values) * attn_plan_rounds(with_values));
+    const int ns = attn_span_splits(p, ppb, ml ? lt0.n : 1);
     const int64_t n_pb = ((int64_t)p.n_rows * p.group + ppb - 1) / ppb;
     p.plan.uniform_ns = ns;
     p.plan.uniform_items = (int32_t)(n_pb * p.n_kv_heads * ns);

@@ -595,6 +595,9 @@ hipError_t launch_lse_to_b(const float *lse_in, float *row_b, int32_t n, int32_t
 // Split count of the closed-form plan the statistics pass uses for rows at
 // q_pos0 + r (pairs per block ppb), as launch_attn picks it.
 int attn_uniform_splits(const AttnParams &p, int ppb, int target);
+// Split count of the scoring span's statistics for `layers` layers in one
+// launch (attn_uniform_splits' count for one).
+int attn_span_splits(const AttnParams &p, int ppb, int layers);
 // lt (nullable, bf16 only): several layers in one launch (grid z = layer).
 hipError_t launch_colsum(const ColsumParams &p, int head_dim, bool bf16, bool rms, hipStream_t s,
                          const LayerTable *lt = nullptr);

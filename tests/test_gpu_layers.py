@@ -1,8 +1,9 @@
 """The multi-layer calls on the GPU: the merge and refresh
 (conduit_scatter_kv_layers, conduit_refresh_attn_layers) against the CPU
 oracle layer by layer, the same selection M refreshed in every layer (Sec. 3,
-Algorithm 1); the scoring (conduit_score_layers) bit for bit against the
-per-layer calls and against the oracle's layer sums (Eq. 7)."""
+Algorithm 1); the scoring (conduit_score_layers) against the per-layer calls
+(equal up to the rounding of the row statistics, which a launch of several
+layers may split differently) and against the oracle's layer sums (Eq. 7)."""
 import numpy as np
 import pytest
 import torch
@@ -159,16 +160,22 @@ def score_both(w, layers_np, norm=api.NORM_CAUSAL_ROW, agg=api.AGG_MEAN, tables=
     return (s_m, a_m), (s_p, a_p)
 
 
+def assert_same_sums(m, per_layer):
+    """The multi-layer sums against the per-layer calls: the same arithmetic
+    up to the rounding of the row log-sum-exps (relative 1e-7 in 2^(c z - b)),
+    so well inside 1e-5 relative."""
+    for x, y, what in zip(m, per_layer, ("s", "A")):
+        assert_scores(to_f64(x), to_f64(y), rtol=1e-5, what=f"{what} multi-layer vs per-layer")
+
+
 @pytest.mark.parametrize("n_layers", [2, 17])
 @pytest.mark.parametrize("norm", [api.NORM_CAUSAL_ROW, api.NORM_VISUAL_ONLY], ids=["causal", "visual"])
 def test_score_layers_equal_per_layer_calls(n_layers, norm):
-    """Bit for bit the per-layer calls with the layer sums accumulated in
-    order; 17 layers cross the 16-layer launch batch."""
+    """The per-layer calls with the layer sums accumulated in order; 17
+    layers cross the 16-layer launch batch."""
     w = small(n_layers, seed=90 + n_layers)
     layers_np = [w.layer(li, fresh=False) for li in range(n_layers)]
-    (s_m, a_m), (s_p, a_p) = score_both(w, layers_np, norm=norm)
-    np.testing.assert_array_equal(bits(s_m), bits(s_p))
-    np.testing.assert_array_equal(bits(a_m), bits(a_p))
+    assert_same_sums(*score_both(w, layers_np, norm=norm))
 
 
 @pytest.mark.parametrize("case", ["rms", "tables", "accumulate"])
@@ -176,9 +183,31 @@ def test_score_layers_variants(case):
     w = small(3, seed=95)
     layers_np = [w.layer(li, fresh=False) for li in range(3)]
     kw = {"rms": dict(agg=api.AGG_RMS), "tables": dict(tables=True), "accumulate": dict(accumulate=True)}[case]
-    (s_m, a_m), (s_p, a_p) = score_both(w, layers_np, **kw)
-    np.testing.assert_array_equal(bits(s_m), bits(s_p))
-    np.testing.assert_array_equal(bits(a_m), bits(a_p))
+    assert_same_sums(*score_both(w, layers_np, **kw))
+
+
+def test_score_layers_fewer_splits_match_oracle():
+    """The 28-layer multi-image shape with 16 layers in one launch, where each
+    layer's row statistics take fewer key splits than a one-layer call:
+    every layer's contribution summed against the oracle (Eq. 7)."""
+    from oracle import conduit_oracle as O
+    w = W.config(3, n_layers=16)
+    layers_np = [w.layer(li, fresh=False) for li in range(16)]
+    caches = [(to_dev(L["k"]), to_dev(L["v"])) for L in layers_np]
+    kvs = [api.kv_desc(kc, vc, w.n_q_heads) for kc, vc in caches]
+    img = api.ImageTable(w.img_pos, w.img_off)
+    s = torch.zeros(w.n_vis, device=DEV)
+    a = torch.zeros(w.n_vis, device=DEV)
+    api.conduit_score_layers(kvs, [to_dev(L["q"]) for L in layers_np], w.q_pos0, img, s, a)
+    torch.cuda.synchronize()
+    a_l, v_l = [], []
+    for L in layers_np:
+        a_o, v_o, _ = O.score_layer(L["q"], L["k"], L["v"], w.q_pos0, w.img_pos, w.img_off)
+        a_l.append(a_o)
+        v_l.append(v_o)
+    s_ref, A_ref = O.aggregate_layers(a_l, v_l)
+    assert_scores(to_f64(s), s_ref * 16, what="sum over layers of a v")
+    assert_scores(to_f64(a), A_ref, what="sum over layers of a")
 
 
 def test_score_layers_matches_oracle():
@@ -207,10 +236,7 @@ def test_score_layers_matches_oracle():
 def test_score_layers_statistics_merged_by_their_kernel():
     """Eight span rows over 17k keys: each statistics block has more splits
     than the column sums rebuild, so every layer's splits are merged by the
-    statistics kernel; 18 layers (two launches) equal the per-layer calls bit
-    for bit."""
+    statistics kernel; 18 layers (two launches) equal the per-layer calls."""
     w = W.custom(18, 28, 4, 128, 8, 512, [1024] * 16, 16, "bf16", n_relevant=2, seed=97)
     layers_np = [w.layer(li, fresh=False) for li in range(18)]
-    (s_m, a_m), (s_p, a_p) = score_both(w, layers_np)
-    np.testing.assert_array_equal(bits(s_m), bits(s_p))
-    np.testing.assert_array_equal(bits(a_m), bits(a_p))
+    assert_same_sums(*score_both(w, layers_np))
