@@ -241,7 +241,12 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   const auto l_rsrc = buffer_rsrc(lse_part_l, FUSE ? 0x7fffffff : 0);
   const uint32_t split_b = (uint32_t)p.lse_ppb * 4u;
   float mv[FUSE ? 2 : 1][FUSE ? kLseRegSplits : 1], lv[FUSE ? 2 : 1][FUSE ? kLseRegSplits : 1];
-  auto lse_issue = [&](int pr0) __attribute__((always_inline)) {
+  // Spans of at most kLseFewSplits splits read only that many (the tag
+  // gives the count read); the rest read all kLseRegSplits, clamped.
+  constexpr int kLseFewSplits = 8;
+  const bool few_splits = ns <= kLseFewSplits;
+  auto lse_issue = [&](int pr0, auto nsm_tag) __attribute__((always_inline)) {
+    constexpr int NSM = decltype(nsm_tag)::value;
     if constexpr (FUSE) {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -250,7 +255,7 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
         const int64_t slot0 = ((int64_t)pb * p.n_kv_heads + kvh) * ns;
         const uint32_t row_b0 = (uint32_t)(slot0 * p.lse_ppb + j) * 4u;
 #pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) {
+        for (int sp = 0; sp < NSM; ++sp) {
           const uint32_t so = (uint32_t)min(sp, ns - 1) * split_b;
           mv[u][sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(m_rsrc, row_b0, so, 0));
           lv[u][sp] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(l_rsrc, row_b0, so, 0));
@@ -258,16 +263,17 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
       }
     }
   };
-  auto lse_reduce = [&](int pr0) __attribute__((always_inline)) {
+  auto lse_reduce = [&](int pr0, auto nsm_tag) __attribute__((always_inline)) {
+    constexpr int NSM = decltype(nsm_tag)::value;
     if constexpr (FUSE) {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int pr = pr0 + u * kColsumThreads;
         float M = -kInf, L = 0.f;
 #pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) M = sp < ns ? fmaxf(M, mv[u][sp]) : M;
+        for (int sp = 0; sp < NSM; ++sp) M = sp < ns ? fmaxf(M, mv[u][sp]) : M;
 #pragma unroll
-        for (int sp = 0; sp < kLseRegSplits; ++sp) L = sp < ns ? L + fast_exp2(mv[u][sp] - M) * lv[u][sp] : L;
+        for (int sp = 0; sp < NSM; ++sp) L = sp < ns ? L + fast_exp2(mv[u][sp] - M) * lv[u][sp] : L;
         const float b = M + __log2f(L);
         if (pr < n_pair) {
           b_all[pr] = b;
@@ -276,7 +282,12 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
       }
     }
   };
-  if (FUSE && n_pair > 0) lse_issue(tid);
+  using FewTag = std::integral_constant<int, kLseFewSplits>;
+  using AllTag = std::integral_constant<int, kLseRegSplits>;
+  if (FUSE && n_pair > 0) {
+    if (few_splits) lse_issue(tid, FewTag{});
+    else lse_issue(tid, AllTag{});
+  }
 
   image_table_to_lds(p.tbl, img, tid, kColsumThreads);
   __syncthreads();
@@ -306,10 +317,18 @@ __global__ __launch_bounds__(kColsumThreads) void colsum_bf16_kernel(ColsumParam
   };
   const int v_chunk = nch - 1;  // no chunk load (and wait) follows
   if constexpr (FUSE) {
-    if (n_pair > 0) lse_reduce(tid);
-    for (int pr0 = tid + 2 * kColsumThreads; pr0 < n_pair; pr0 += 2 * kColsumThreads) {
-      lse_issue(pr0);
-      lse_reduce(pr0);
+    if (few_splits) {
+      if (n_pair > 0) lse_reduce(tid, FewTag{});
+      for (int pr0 = tid + 2 * kColsumThreads; pr0 < n_pair; pr0 += 2 * kColsumThreads) {
+        lse_issue(pr0, FewTag{});
+        lse_reduce(pr0, FewTag{});
+      }
+    } else {
+      if (n_pair > 0) lse_reduce(tid, AllTag{});
+      for (int pr0 = tid + 2 * kColsumThreads; pr0 < n_pair; pr0 += 2 * kColsumThreads) {
+        lse_issue(pr0, AllTag{});
+        lse_reduce(pr0, AllTag{});
+      }
     }
     __syncthreads();
   }
