@@ -186,7 +186,7 @@ AttnPlan plan_at(void *ws, const PlanLayout &P);
 conduit_status check_layers(const conduit_kv *kvs, int32_t n_layers);
 
 struct ScoreLayout {
-  size_t row_b, colsum, vsq, done, merge_flag, total;
+  size_t row_b, colsum, vsq, done, merge_flag, f32_ml, total;
   PlanLayout plan;
 };
 
@@ -204,24 +204,54 @@ ScoreLayout score_layout(const conduit_kv *kv, int32_t n_q, int32_t n_vis, int32
   L.vsq = take((size_t)kv->n_kv_heads * n_vis * 4 * layers);
   if (bf16) L.done = take((size_t)(n_vis + kColsumKeysPerBlock - 1) / kColsumKeysPerBlock * 4);
   if (bf16) L.merge_flag = take((size_t)L.plan.max_items * 4 * layers);
+  if (!bf16) {  // the fp32 statistics' key splits
+    const int32_t ns = f32_attn_splits(n_q, kv->n_q_heads, kv->n_ctx);
+    L.f32_ml = ns > 1 ? take((size_t)ns * rows * 8) : 0;
+  }
   L.total = off;
   return L;
 }
 
 struct RefreshLayout {
-  size_t total;
+  size_t f32_ml, f32_o, total;
   PlanLayout plan;
 };
 
 // layers: the layers one attention launch covers (the multi-layer refresh).
+// fp32: the key splits' partials, if the rows are split.
 RefreshLayout refresh_layout(const conduit_kv *kv, int32_t k, int32_t layers = 1) {
   RefreshLayout L{};
-  if (kv->dtype != CONDUIT_BF16 || k <= 0) return L;
+  if (k <= 0) return L;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, 256); return at; };
-  L.plan = plan_layout(kv, k, true, take, layers);
+  if (kv->dtype == CONDUIT_BF16) {
+    L.plan = plan_layout(kv, k, true, take, layers);
+  } else {
+    const int32_t ns = f32_attn_splits(k, kv->n_q_heads, kv->n_ctx);
+    if (ns > 1) {
+      const size_t pairs = (size_t)k * kv->n_q_heads;
+      L.f32_ml = take(ns * pairs * 8);
+      L.f32_o = take(ns * pairs * kv->head_dim * 4);
+    }
+  }
   L.total = off;
   return L;
+}
+
+// The fp32 attention's outputs, with the key splits' partials in ws when
+// f32_attn_splits cuts the rows' keys (ml_off / o_off: their workspace offsets).
+DirectOut f32_out(const conduit_kv *kv, int64_t n_rows, float *row_b, float *lse_out, void *o_out, void *ws,
+                  size_t ml_off, size_t o_off) {
+  DirectOut out{row_b, lse_out, static_cast<float *>(o_out), 1, 0, nullptr, nullptr};
+  const int32_t ns = f32_attn_splits(n_rows, kv->n_q_heads, kv->n_ctx);
+  if (ns > 1) {
+    const int32_t tiles = (kv->n_ctx + 63) / 64;
+    out.n_split = ns;
+    out.chunk = (tiles + ns - 1) / ns * 64;
+    out.part_ml = reinterpret_cast<float2 *>(static_cast<char *>(ws) + ml_off);
+    out.part_o = o_out ? reinterpret_cast<float *>(static_cast<char *>(ws) + o_off) : nullptr;
+  }
+  return out;
 }
 
 conduit_status check_ws(const void *ws, size_t ws_bytes, size_t need) {
@@ -415,7 +445,7 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
       e = launch_attn(ap, D, false, stream);
       if (e != hipSuccess) return hip_fail(e, "row statistics");
     } else {
-      DirectOut out{row_b, row_lse_out, nullptr};
+      const DirectOut out = f32_out(kv, n_q, row_b, row_lse_out, nullptr, ws, L.f32_ml, 0);
       e = launch_attn_f32(ap, out, D, false, stream);
       if (e != hipSuccess) return hip_fail(e, "row statistics");
     }
@@ -950,7 +980,8 @@ conduit_status conduit_refresh_attn(const conduit_kv *kv, const void *q_sel, con
   if (kv->dtype == CONDUIT_BF16) {
     e = launch_attn(ap, kv->head_dim, true, stream);
   } else {
-    DirectOut out{nullptr, lse_out, static_cast<float *>(o_out)};
+    const RefreshLayout L = refresh_layout(kv, k);
+    const DirectOut out = f32_out(kv, k, nullptr, lse_out, o_out, ws, L.f32_ml, L.f32_o);
     e = launch_attn_f32(ap, out, kv->head_dim, true, stream);
   }
   if (e != hipSuccess) return hip_fail(e, "refresh attention");
@@ -977,7 +1008,8 @@ conduit_status conduit_merge_refresh_attn(const conduit_kv *kv, const int32_t *p
   } else {
     e = launch_scatter(sp, stream);
     if (e == hipSuccess) {
-      DirectOut out{nullptr, lse_out, static_cast<float *>(o_out)};
+      const RefreshLayout L = refresh_layout(kv, k);
+      const DirectOut out = f32_out(kv, k, nullptr, lse_out, o_out, ws, L.f32_ml, L.f32_o);
       e = launch_attn_f32(ap, out, kv->head_dim, true, stream);
     }
   }
@@ -1083,7 +1115,7 @@ conduit_status conduit_refresh_attn_layers(const conduit_kv *kvs, int32_t n_laye
   const RefreshLayout L = refresh_layout(kv, k, std::min<int32_t>(n_layers, kMaxLayerBatch));
   st = check_ws(ws, ws_bytes, L.total);
   if (st) return st;
-  if (kv->dtype != CONDUIT_BF16) {  // fp32: the per-layer kernel, which needs no workspace
+  if (kv->dtype != CONDUIT_BF16) {  // fp32: the per-layer calls, one after the other on the workspace
     for (int32_t l = 0; l < n_layers; ++l) {
       st = conduit_refresh_attn(&kvs[l], q_sel[l], pos, k, scale, o_out[l], lse_out ? lse_out[l] : nullptr, ws,
                                 ws_bytes, stream);

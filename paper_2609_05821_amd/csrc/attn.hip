@@ -984,7 +984,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p, LayerTabl
 // the current one is used, and the queries sit in LDS (read as broadcasts).
 // Online softmax in the log2 domain, fp32 throughout; the final outputs are
 // written directly (no splits).
-constexpr int kF32Rows = 4;
+constexpr int kF32Rows = kF32RowsPerBlock;
 template <int D, bool PV>
 __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, DirectOut out) {
   constexpr int KP = D + 4;
@@ -1028,11 +1028,15 @@ __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, D
   };
   __syncthreads();
   const int maxpos = s_maxpos;
+  // this workgroup's keys: split blockIdx.z of the range, or all of it
+  const bool split = out.n_split > 1;
+  const int kb = split ? (int)blockIdx.z * out.chunk : 0;
+  const int kend = split ? min(maxpos + 1, kb + out.chunk) : maxpos + 1;
   float m = kNegInf, l = 0.f, o[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) o[i] = 0.f;
-  load_tile(0);
-  for (int t0 = 0; t0 <= maxpos; t0 += KT) {
+  if (kb < kend) load_tile(kb);
+  for (int t0 = kb; t0 < kend; t0 += KT) {
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int cidx = tid + kF32Rows * 64 * i;
@@ -1041,9 +1045,9 @@ __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, D
       if constexpr (PV) *reinterpret_cast<f32x4 *>(&vsm[row][4 * c4]) = vq[i];
     }
     __syncthreads();
-    if (t0 + KT <= maxpos) load_tile(t0 + KT);
+    if (t0 + KT < kend) load_tile(t0 + KT);
     const int key = t0 + lane;
-    const bool vis = key <= rpos && (!p.vis_only || is_visual(img, key));
+    const bool vis = key <= rpos && key < kend && (!p.vis_only || is_visual(img, key));
     float d4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int e = 0; e < D; e += 4) {
@@ -1074,6 +1078,15 @@ __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, D
     __syncthreads();
   }
   if (!valid) return;
+  if (split) {  // the split's (m, l) and unnormalised output, merged below
+    const int64_t idx = (int64_t)blockIdx.z * p.n_rows * p.n_q_heads + gp;
+    if (lane == 0) out.part_ml[idx] = make_float2(m, l);
+    if constexpr (PV) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) out.part_o[idx * D + lane + 64 * i] = o[i];
+    }
+    return;
+  }
   const float b = m + __log2f(l);
   if (lane == 0) {
     if (out.row_b) out.row_b[gp] = b;
@@ -1085,6 +1098,33 @@ __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, D
 #pragma unroll
     for (int i = 0; i < PER; ++i) dst[lane + 64 * i] = o[i] * inv;
   }
+}
+
+// Merge of the fp32 key splits, in split order: M = max m_s,
+// L = sum l_s 2^(m_s - M), O = sum o_s 2^(m_s - M) / L (o_s unnormalised,
+// relative to m_s).  One thread per (pair, output dim), or per pair without
+// values.  Every pair sees at least one key, so M is finite.
+template <int D, bool PV>
+__global__ __launch_bounds__(256) void attn_f32_merge_kernel(int64_t n_gp, DirectOut out) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t gp = PV ? gid / D : gid;
+  const int d = PV ? (int)(gid % D) : 0;
+  if (gp >= n_gp) return;
+  float M = kNegInf;
+  for (int sp = 0; sp < out.n_split; ++sp) M = fmaxf(M, out.part_ml[sp * n_gp + gp].x);
+  float L = 0.f, acc = 0.f;
+  for (int sp = 0; sp < out.n_split; ++sp) {
+    const float2 ml = out.part_ml[sp * n_gp + gp];
+    const float w = ml.y > 0.f ? fast_exp2(ml.x - M) : 0.f;  // an empty split adds nothing
+    L = fmaf(w, ml.y, L);
+    if constexpr (PV) acc = fmaf(w, out.part_o[(sp * n_gp + gp) * D + d], acc);
+  }
+  const float b = M + __log2f(L);
+  if (d == 0) {
+    if (out.row_b) out.row_b[gp] = b;
+    if (out.lse_out) out.lse_out[gp] = b * kLn2;
+  }
+  if constexpr (PV) out.o_out[gp * D + d] = acc / L;
 }
 
 __global__ void lse_to_b_kernel(const float *lse, float *b, int n, int32_t *zero_i32, int zero_n) {
@@ -1274,14 +1314,30 @@ hipError_t launch_merge_refresh(const AttnParams &p, const ScatterParams &sp, in
 
 hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_dim,
                            bool with_values, hipStream_t s) {
-  ProfScope ps("attn_f32", s);
-  const dim3 grid((p.n_rows + kF32Rows - 1) / kF32Rows, p.n_q_heads);
+  const int ns = out.n_split > 1 ? out.n_split : 1;
+  {
+    ProfScope ps("attn_f32", s);
+    const dim3 grid((p.n_rows + kF32Rows - 1) / kF32Rows, p.n_q_heads, ns);
+    if (head_dim == 128) {
+      if (with_values) attn_f32_kernel<128, true><<<grid, kF32Rows * 64, 0, s>>>(p, out);
+      else attn_f32_kernel<128, false><<<grid, kF32Rows * 64, 0, s>>>(p, out);
+    } else {
+      if (with_values) attn_f32_kernel<64, true><<<grid, kF32Rows * 64, 0, s>>>(p, out);
+      else attn_f32_kernel<64, false><<<grid, kF32Rows * 64, 0, s>>>(p, out);
+    }
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || ns == 1) return e;
+  ProfScope ps("attn_f32_merge", s);
+  const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
+  const int64_t n = with_values ? n_gp * head_dim : n_gp;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
   if (head_dim == 128) {
-    if (with_values) attn_f32_kernel<128, true><<<grid, kF32Rows * 64, 0, s>>>(p, out);
-    else attn_f32_kernel<128, false><<<grid, kF32Rows * 64, 0, s>>>(p, out);
+    if (with_values) attn_f32_merge_kernel<128, true><<<blocks, 256, 0, s>>>(n_gp, out);
+    else attn_f32_merge_kernel<128, false><<<blocks, 256, 0, s>>>(n_gp, out);
   } else {
-    if (with_values) attn_f32_kernel<64, true><<<grid, kF32Rows * 64, 0, s>>>(p, out);
-    else attn_f32_kernel<64, false><<<grid, kF32Rows * 64, 0, s>>>(p, out);
+    if (with_values) attn_f32_merge_kernel<64, true><<<blocks, 256, 0, s>>>(n_gp, out);
+    else attn_f32_merge_kernel<64, false><<<blocks, 256, 0, s>>>(n_gp, out);
   }
   return hipGetLastError();
 }

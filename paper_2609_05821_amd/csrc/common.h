@@ -392,12 +392,32 @@ struct CombineParams {
   void *o_out;              // nullable [n_rows][H_q][D] bf16
 };
 
-// Inputs of the fp32 path, which writes its final outputs directly.
+// Outputs of the fp32 path.  With n_split > 1 each (row, head) pair's key
+// range is cut into n_split ranges of `chunk` keys (whole tiles), processed by
+// separate workgroups that write partials (part_ml: [n_split][pairs] of
+// {m, l}; part_o: [n_split][pairs][D], unnormalised), merged by a second
+// launch into the outputs.
 struct DirectOut {
   float *row_b;
   float *lse_out;
   float *o_out;
+  int32_t n_split;
+  int32_t chunk;
+  float2 *part_ml;
+  float *part_o;
 };
+// Key splits of the fp32 attention for n_rows rows of n_q_heads heads over a
+// cache of n_ctx keys: enough workgroups to cover the chip about twice (four
+// rows per workgroup), at least two tiles per split, at most 8 splits.
+constexpr int kF32RowsPerBlock = 4;
+inline int32_t f32_attn_splits(int64_t n_rows, int32_t n_q_heads, int32_t n_ctx) {
+  const int64_t blocks = (n_rows + kF32RowsPerBlock - 1) / kF32RowsPerBlock * n_q_heads;
+  const int64_t tiles = ((int64_t)n_ctx + 63) / 64;
+  int64_t ns = (512 + blocks - 1) / blocks;
+  ns = ns < 8 ? ns : 8;
+  ns = ns < tiles / 2 ? ns : tiles / 2;
+  return (int32_t)(ns > 1 ? ns : 1);
+}
 
 
 struct FinalizeParams {

@@ -154,7 +154,14 @@ def test_refresh_rejects_and_sizes():
     kvd = kv()
     need = L.conduit_refresh_workspace_bytes(ctypes.byref(kvd), 102)
     assert need > 0
+    # fp32 needs a workspace only when the rows' keys are split over several
+    # workgroups (few rows): then it holds every split's (m, l) and output
     assert L.conduit_refresh_workspace_bytes(ctypes.byref(kv(dtype=api.F32)), 102) == 0
+    small = kv(dtype=api.F32, n_ctx=672, n_q_heads=8, n_kv_heads=8, head_dim=64, k_stride=512, v_stride=512)
+    f32_need = L.conduit_refresh_workspace_bytes(ctypes.byref(small), 57)
+    assert f32_need >= 2 * 57 * 8 * (64 * 4 + 8) and f32_need % 256 == 0
+    assert L.conduit_refresh_attn(ctypes.byref(small), FAKE, FAKE, 57, 0.125, FAKE, None, FAKE, f32_need - 256,
+                                  None) == api.ERR_WORKSPACE
     args = lambda **o: dict(dict(q=FAKE, pos=FAKE, k=102, scale=0.088, o=FAKE, ws=FAKE, wsb=need), **o)
     def call(a):
         return L.conduit_refresh_attn(ctypes.byref(kvd), a["q"], a["pos"], a["k"], a["scale"], a["o"],
