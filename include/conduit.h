@@ -329,6 +329,9 @@ conduit_status conduit_scatter_kv(const conduit_kv *kv, const int32_t *pos, int3
  * o_out   device [k][n_q_heads][head_dim], kv->dtype (bf16 rounded to nearest
  *         even from fp32 accumulation).
  * lse_out nullable device [k][n_q_heads] fp32: natural-log log-sum-exp.
+ * ws      conduit_refresh_workspace_bytes(kv, k) bytes, 256-byte aligned: the
+ *         work plan and split partials (bf16), or the key splits' partials
+ *         when an fp32 call has few rows (0 bytes otherwise).
  * k = 0 enqueues nothing.
  * ------------------------------------------------------------------------ */
 size_t conduit_refresh_workspace_bytes(const conduit_kv *kv, int32_t k);
