@@ -242,7 +242,7 @@ RefreshLayout refresh_layout(const conduit_kv *kv, int32_t k, int32_t layers = 1
 // f32_attn_splits cuts the rows' keys (ml_off / o_off: their workspace offsets).
 DirectOut f32_out(const conduit_kv *kv, int64_t n_rows, float *row_b, float *lse_out, void *o_out, void *ws,
                   size_t ml_off, size_t o_off) {
-  DirectOut out{row_b, lse_out, static_cast<float *>(o_out), 1, 0, nullptr, nullptr};
+  DirectOut out{row_b, lse_out, static_cast<float *>(o_out), 1, 0, nullptr, nullptr, 1};
   const int32_t ns = f32_attn_splits(n_rows, kv->n_q_heads, kv->n_ctx);
   if (ns > 1) {
     const int32_t tiles = (kv->n_ctx + 63) / 64;
@@ -394,6 +394,7 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
 
   int32_t lse_ns = 0;
   bool fuse_lse = false;
+  DirectOut f32_stats{};  // fp32: the statistics' outputs (key splits merged by the column sums)
   hipError_t e;
   // bf16: the column-sum workgroups count their arrivals per key block and
   // the last one finalizes it; the kernel before them clears the counters.
@@ -445,8 +446,10 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
       e = launch_attn(ap, D, false, stream);
       if (e != hipSuccess) return hip_fail(e, "row statistics");
     } else {
-      const DirectOut out = f32_out(kv, n_q, row_b, row_lse_out, nullptr, ws, L.f32_ml, 0);
-      e = launch_attn_f32(ap, out, D, false, stream);
+      // split rows are merged by the column sums (below), not by a launch
+      f32_stats = f32_out(kv, n_q, row_b, row_lse_out, nullptr, ws, L.f32_ml, 0);
+      f32_stats.merge = 0;
+      e = launch_attn_f32(ap, f32_stats, D, false, stream);
       if (e != hipSuccess) return hip_fail(e, "row statistics");
     }
   }
@@ -484,6 +487,11 @@ conduit_status conduit_score(const conduit_kv *kv, const void *q, int32_t n_q, i
   fp.a_out = a_out;
   fp.vnorm_out = vnorm_out;
 
+  if (f32_stats.n_split > 1) {
+    cs.f32_ml = f32_stats.part_ml;
+    cs.lse_ns = f32_stats.n_split;
+    cs.lse_out = row_lse_out;
+  }
   if (fuse_lse) {
     cs.lse_part_m = reinterpret_cast<float *>(at(ws, L.plan.part_m));
     cs.lse_part_l = reinterpret_cast<float *>(at(ws, L.plan.part_l));

@@ -1327,7 +1327,7 @@ hipError_t launch_attn_f32(const AttnParams &p, const DirectOut &out, int head_d
     }
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || ns == 1) return e;
+  if (e != hipSuccess || ns == 1 || !out.merge) return e;
   ProfScope ps("attn_f32_merge", s);
   const int64_t n_gp = (int64_t)p.n_rows * p.n_q_heads;
   const int64_t n = with_values ? n_gp * head_dim : n_gp;

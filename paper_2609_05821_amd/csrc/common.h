@@ -405,6 +405,7 @@ struct DirectOut {
   int32_t chunk;
   float2 *part_ml;
   float *part_o;
+  int32_t merge;  // 0: the partials are merged by the caller's next kernel
 };
 // Key splits of the fp32 attention for n_rows rows of n_q_heads heads over a
 // cache of n_ctx keys: enough workgroups to cover the chip about twice (four
@@ -463,6 +464,10 @@ struct ColsumParams {
   int32_t lse_ppb;
   float *lse_out;
   int64_t lse_layer_stride;  // several layers: statistics partial slots per layer
+  // fp32: the statistics' key splits ({m, l} per pair, lse_ns of them),
+  // merged here instead of read from row_b (the first key block writes
+  // lse_out).
+  const float2 *f32_ml;
   // nullable: arrival counters, one per key block, cleared beforehand; the
   // last KV head's workgroup of a key block finalizes its keys (fin).
   int32_t *done;

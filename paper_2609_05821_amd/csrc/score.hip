@@ -462,7 +462,25 @@ __global__ __launch_bounds__(64) void colsum_f32_kernel(ColsumParams p, bool rms
     }
     if (lane < rows) {
       const int pr = c0 + lane;
-      bs[lane] = p.row_b[(int64_t)(pr / G) * p.n_q_heads + kvh * G + pr % G];
+      const int64_t gq = (int64_t)(pr / G) * p.n_q_heads + kvh * G + pr % G;
+      if (p.f32_ml) {
+        // the statistics' key splits, merged as their merge launch would:
+        // b = M + log2(sum_s l_s 2^(m_s - M)), splits in order
+        const int64_t n_gp = (int64_t)p.n_q * p.n_q_heads;
+        float M = -kInf;
+        for (int sp = 0; sp < p.lse_ns; ++sp) M = fmaxf(M, p.f32_ml[sp * n_gp + gq].x);
+        float L = 0.f;
+        for (int sp = 0; sp < p.lse_ns; ++sp) {
+          const float2 ml = p.f32_ml[sp * n_gp + gq];
+          const float w = ml.y > 0.f ? fast_exp2(ml.x - M) : 0.f;
+          L = fmaf(w, ml.y, L);
+        }
+        const float b = M + __log2f(L);
+        if (blockIdx.x == 0 && p.lse_out) p.lse_out[gq] = b * kLn2;
+        bs[lane] = b;
+      } else {
+        bs[lane] = p.row_b[gq];
+      }
     }
     __syncthreads();
     for (int rr = 0; rr < rows; ++rr) {
