@@ -982,8 +982,11 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineParams p, LayerTabl
 // through LDS, so that lane e accumulates output dims e, e + 64, ... over the
 // tile's V rows.  The next tile's K/V chunks are loaded into registers while
 // the current one is used, and the queries sit in LDS (read as broadcasts).
-// Online softmax in the log2 domain, fp32 throughout; the final outputs are
-// written directly (no splits).
+// Online softmax in the log2 domain, fp32 throughout.  With few rows the
+// key range is cut into splits of whole tiles (blockIdx.z; see
+// f32_attn_splits): each writes its (m, l) and unnormalised output, merged in
+// split order by attn_f32_merge_kernel (or, for the statistics, by the fp32
+// column sums).  Otherwise the final outputs are written directly.
 constexpr int kF32Rows = kF32RowsPerBlock;
 template <int D, bool PV>
 __global__ __launch_bounds__(kF32Rows * 64) void attn_f32_kernel(AttnParams p, DirectOut out) {
